@@ -1,0 +1,181 @@
+"""CPU oracle for CoFiE's NGFF and QER stages (test infrastructure only).
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the benchmark's
+``cpu_baseline`` leg may import this package.  It wraps the plain C oracle in
+``cofie_oracle.c`` (built with gcc by :func:`build`) and shares nothing with
+the HIP implementation in ``paper_2609_03675_amd``.
+
+Paper sections followed: Sec. 3.2 (NGFF: histogram, total-variation distance,
+Eqs. 2-5 and the gap-aware safeguards) and Sec. 3.3 (QER: Eqs. 6-8).
+
+Parity status: every function here is pinned by the CPU tests under
+``tests/test_oracle_*.py`` (closed forms, invariants, brute force, library
+routines, the paper's printed drop-ratio compositions).  The retention-target
+calibration (``ngff_calibrate``) is not in the paper; it is pinned by a brute
+force over every integer threshold on small inputs.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cofie_oracle.c")
+_LIB = os.path.join(_HERE, "libcofie_oracle.so")
+
+GRAY, PER_CHANNEL, JOINT3D = 0, 1, 2
+F32, BF16 = 0, 1
+LOGIT, SOFTMAX = 0, 1
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (-O2, OpenMP).  Returns the library path."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build(force=False)
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, f32, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+    lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_nbins.argtypes = [i32, i32]
+    lib.orc_nbins.restype = i64
+    lib.orc_mass.argtypes = [i32, i32, i32]
+    lib.orc_mass.restype = i64
+    lib.orc_histogram.argtypes = [P, i64, i32, i32, i32, i32, i32, P]
+    lib.orc_histogram.restype = ctypes.c_int
+    lib.orc_l1.argtypes = [P, P, i64]
+    lib.orc_l1.restype = i64
+    lib.orc_ngff_select.argtypes = [P, i64, i64, i64, P, i64, i32, i32, i64, P, P, P]
+    lib.orc_ngff_select.restype = ctypes.c_int
+    lib.orc_ngff_calibrate.argtypes = [P, i64, i64, i64, i32, i32, i64, i64, P, P]
+    lib.orc_ngff_calibrate.restype = ctypes.c_int
+    lib.orc_qer_scores.argtypes = [P, P, i32, P, i32, i32, i32, i32, i32, i32, i32, f64, P]
+    lib.orc_qer_scores.restype = ctypes.c_int
+    lib.orc_topk.argtypes = [P, i32, i32, P]
+    lib.orc_topk.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle uses."""
+    return int(_load().orc_num_threads())
+
+
+def nbins(mode: int, bins: int) -> int:
+    return int(_load().orc_nbins(mode, bins))
+
+
+def mass(mode: int, H: int, W: int) -> int:
+    """Histogram mass M (count total); h_t = counts / M sums to 1."""
+    return int(_load().orc_mass(mode, H, W))
+
+
+def histogram(frames: np.ndarray, bins: int, mode: int) -> np.ndarray:
+    """Counts [n][nbins] uint32 for uint8 frames [n][H][W][C] (Sec. 3.2)."""
+    f = np.ascontiguousarray(frames, dtype=np.uint8)
+    if f.ndim == 3:
+        f = f[..., None]
+    n, H, W, C = f.shape
+    out = np.zeros((n, nbins(mode, bins)), dtype=np.uint32)
+    rc = _load().orc_histogram(_ptr(f), n, H, W, C, bins, mode, _ptr(out))
+    if rc != 0:
+        raise ValueError(f"oracle histogram rejected C={C} mode={mode}")
+    return out
+
+
+def l1(ci: np.ndarray, cj: np.ndarray) -> int:
+    """Exact integer sum_b |c_i[b]-c_j[b]| = 2M * d(h_i, h_j) (Eq. 2)."""
+    a = np.ascontiguousarray(ci, dtype=np.uint32)
+    b = np.ascontiguousarray(cj, dtype=np.uint32)
+    return int(_load().orc_l1(_ptr(a), _ptr(b), a.size))
+
+
+def ngff_select(counts: np.ndarray, mass_: int, tau, L_max: int = 30, M_min: int = 4,
+                seg_len: int = 0):
+    """Keep rule (Eqs. 3-5 and safeguards) over histograms [n][nbins].
+
+    ``tau`` is one float (all streams) or one per stream of ``seg_len`` frames.
+    Returns (scores fp32 [n], mask uint8 [n], kept count per stream int64)."""
+    c = np.ascontiguousarray(counts, dtype=np.uint32)
+    n, nb = c.shape
+    taus = np.atleast_1d(np.asarray(tau, dtype=np.float32))
+    seg = seg_len if 0 < seg_len <= n else max(n, 1)
+    nseg = (n + seg - 1) // seg if n > 0 else 0
+    scores = np.zeros(n, dtype=np.float32)
+    mask = np.zeros(n, dtype=np.uint8)
+    kept = np.zeros(max(nseg, 1), dtype=np.int64)
+    rc = _load().orc_ngff_select(_ptr(c), n, nb, mass_, _ptr(taus), taus.size, L_max, M_min,
+                                 seg_len, _ptr(scores), _ptr(mask), _ptr(kept))
+    assert rc == 0
+    return scores, mask, kept[:nseg]
+
+
+def ngff_calibrate(counts: np.ndarray, mass_: int, target: int, L_max: int = 30, M_min: int = 4,
+                   seg_len: int = 0):
+    """Smallest candidate threshold keeping at most ``target`` frames per stream.
+
+    Returns (theta int64 [nseg], tau fp32 [nseg]) with tau = fl32(theta)/fl32(2M)."""
+    c = np.ascontiguousarray(counts, dtype=np.uint32)
+    n, nb = c.shape
+    seg = seg_len if 0 < seg_len <= n else max(n, 1)
+    nseg = (n + seg - 1) // seg if n > 0 else 0
+    theta = np.zeros(max(nseg, 1), dtype=np.int64)
+    tau = np.zeros(max(nseg, 1), dtype=np.float32)
+    rc = _load().orc_ngff_calibrate(_ptr(c), n, nb, mass_, L_max, M_min, seg_len, target,
+                                    _ptr(theta), _ptr(tau))
+    if rc != 0:
+        raise ValueError("oracle calibration needs L_max >= 1")
+    return theta[:nseg], tau[:nseg]
+
+
+def qer_scores(Q: np.ndarray, K: np.ndarray, frame_offsets: np.ndarray, H_q: int, H_kv: int,
+               d: int, mode: int = LOGIT, scale: float = 0.0) -> np.ndarray:
+    """w_f in fp64 (Eqs. 6-7).  Q [n_q][H_q][d], K [n_vis][H_kv][d], either
+    float32 or bf16 bit patterns stored as uint16."""
+    Q = np.ascontiguousarray(Q)
+    K = np.ascontiguousarray(K)
+    if Q.dtype == np.float32 and K.dtype == np.float32:
+        dt = F32
+    elif Q.dtype == np.uint16 and K.dtype == np.uint16:
+        dt = BF16
+    else:
+        raise TypeError("Q and K must both be float32 or both bf16 bits (uint16)")
+    n_q = Q.size // (H_q * d)
+    n_vis = K.size // (H_kv * d)
+    offs = np.ascontiguousarray(frame_offsets, dtype=np.int32)
+    n_frames = offs.size - 1
+    w = np.zeros(max(n_frames, 1), dtype=np.float64)
+    rc = _load().orc_qer_scores(_ptr(Q), _ptr(K), dt, _ptr(offs), n_frames, n_q, n_vis, H_q, H_kv,
+                                d, mode, float(scale), _ptr(w))
+    assert rc == 0
+    return w[:n_frames]
+
+
+def topk(w: np.ndarray, k_top: int) -> np.ndarray:
+    """S_e (Eq. 8): k best by (score desc, index asc), chronological, -1 padded."""
+    a = np.ascontiguousarray(w, dtype=np.float64)
+    idx = np.full(max(k_top, 1), -1, dtype=np.int32)
+    rc = _load().orc_topk(_ptr(a), a.size, k_top, _ptr(idx))
+    assert rc == 0
+    return idx[:k_top]
