@@ -1,0 +1,233 @@
+/*
+ * cofie.h -- C ABI of libcofie: CoFiE evidence selection on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * CoFiE selects evidence frames for a video LLM in two stages:
+ *   NGFF  Novelty-Guided Frame Filtering (Sec. 3.2): per-frame histograms of
+ *         raw uint8 frames, a total-variation novelty score against the
+ *         previous frame and the last kept frame, and a gap-aware keep rule,
+ *         run before any vision encoder.
+ *   QER   Query-Specific Evidence Refinement (Sec. 3.3): head-averaged
+ *         text-to-visual scaled dot products at prefill, max over text tokens,
+ *         mean over each frame's visual tokens, top-k frames.
+ *
+ * Conventions shared by every entry point
+ *   - Return value: COFIE_OK (0) or a negative COFIE_E* status.  On error,
+ *     cofie_last_error() returns a message for the calling thread.  Nothing
+ *     throws across this boundary.
+ *   - "device" pointers are HIP device memory (for example from PyTorch on
+ *     ROCm); "host" pointers are read during the call only.  The library never
+ *     keeps a pointer past the call and never frees caller memory.
+ *   - Every argument is validated on the host before any work is enqueued;
+ *     a rejected call enqueues nothing.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  All work is
+ *     enqueued on it asynchronously; outputs are valid once the caller has
+ *     synchronised the stream.
+ *   - Scratch memory: a caller may pass a device workspace of at least the
+ *     size the matching *_workspace_bytes() function reports.  With a NULL
+ *     workspace the library allocates and frees scratch with stream-ordered
+ *     hipMallocAsync / hipFreeAsync on `stream`.
+ *   - Results are deterministic: the same inputs give the same output bits.
+ */
+#ifndef COFIE_H_
+#define COFIE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define COFIE_OK 0
+#define COFIE_EINVAL (-1)       /* invalid argument (null pointer, bad size or enum) */
+#define COFIE_EUNSUPPORTED (-2) /* valid but outside what this build implements */
+#define COFIE_EHIP (-3)         /* a HIP runtime call or kernel launch failed */
+#define COFIE_ENOMEM (-4)       /* scratch allocation failed or workspace too small */
+
+/* ---- enums -------------------------------------------------------------- */
+/* Histogram of a frame (Sec. 3.2).  B = `bins` (a power of two).  Intensity v
+ * falls in bin floor(v * B / 256), i.e. B equal bins over the normalised range.
+ *   GRAY         B bins of the BT.601 luma (299 R + 587 G + 114 B + 500) div 1000
+ *                (C = 3) or of the single channel (C = 1).  The paper's default
+ *                (32 bins).  Mass M = H*W.
+ *   PER_CHANNEL  3B bins: R, G and B histograms side by side.  Mass M = 3*H*W;
+ *                the total-variation distance is then the mean of the three
+ *                per-channel distances.  C = 3.
+ *   JOINT3D      B^3 bins indexed (bin(R)*B + bin(G))*B + bin(B).  Mass M = H*W.
+ *                C = 3, B^3 <= 4096.                                          */
+enum cofie_hist_mode { COFIE_HIST_GRAY = 0, COFIE_HIST_PER_CHANNEL = 1, COFIE_HIST_JOINT3D = 2 };
+
+/* Element type of Q and K. */
+enum cofie_dtype { COFIE_F32 = 0, COFIE_BF16 = 1 };
+
+/* Text-to-visual association a_ij aggregated by QER.
+ *   LOGIT    the paper's Eq. 6: head mean of scaled dot products.
+ *   SOFTMAX  head mean of softmax-normalised scaled dot products, each softmax
+ *            taken over all n_vis visual keys passed in (not over the model's
+ *            full key set).                                                  */
+enum cofie_score_mode { COFIE_SCORE_LOGIT = 0, COFIE_SCORE_SOFTMAX = 1 };
+
+/* ---- NGFF --------------------------------------------------------------- */
+
+/* Keep rule of NGFF (Sec. 3.2, Eqs. 3-5 and the gap-aware safeguards).
+ * For each independent stream of T frames:
+ *   s_t = max(d(h_t, h_{t-1}), d(h_t, h_{r(t)})), d = total variation of the
+ *         normalised histograms, computed as the exact integer L1 distance D of
+ *         the counts divided once, in IEEE fp32, by 2M; s_0 = 1.
+ *   r(t) = the most recent frame kept by the rule below (top-up frames excluded).
+ *   Frame 0 and frame T-1 are kept; frame 0 < t < T-1 is kept when
+ *   s_t >= tau or (L_max > 0 and t - r(t) >= L_max).  If fewer than M_min
+ *   frames are kept (M_min >= 2), the frames floor(i (T-1) / (M_min-1)),
+ *   i = 0..M_min-1, are added.                                                 */
+typedef struct cofie_keep_rule {
+  int32_t hist_mode;             /* enum cofie_hist_mode (paper default: GRAY)      */
+  float tau_h;                   /* novelty threshold tau (paper default 0.30);      */
+                                 /*   any non-NaN value: < 0 keeps every frame,     */
+                                 /*   > 1 keeps only the forced frames              */
+  const float* tau_per_segment;  /* optional device [n_segments]: one tau per       */
+                                 /*   stream, overrides tau_h (e.g. the output of   */
+                                 /*   cofie_ngff_calibrate)                         */
+  int32_t L_max;                 /* forced-retention gap in frames (default 30);    */
+                                 /*   <= 0 disables the gap rule                    */
+  int32_t M_min;                 /* minimum kept frames per stream (default 4)      */
+  int64_t segment_len;           /* frames per independent stream; 0 = the whole   */
+                                 /*   batch is one stream; the last may be shorter  */
+  uint32_t* out_hist;            /* optional device [n][nbins] histogram counts     */
+  int32_t* out_count;            /* optional device [n_segments] kept frames         */
+  void* workspace;               /* optional device scratch (see header comment)    */
+  size_t workspace_bytes;
+} cofie_keep_rule;
+
+/* Fill *rule with the paper's defaults: GRAY histogram, tau_h = 0.30,
+ * L_max = 30, M_min = 4 (Sec. 3.2; Table 7's middle row), one stream, no
+ * optional outputs, library-managed scratch. */
+void cofie_keep_rule_default(cofie_keep_rule* rule);
+
+/* Number of histogram bins for a mode and `bins` (B, 3B or B^3); 0 if invalid. */
+int64_t cofie_ngff_nbins(int32_t hist_mode, int32_t bins);
+
+/* Bytes of device scratch cofie_ngff_filter / cofie_ngff_calibrate need for
+ * these arguments (0 for invalid arguments). */
+size_t cofie_ngff_workspace_bytes(int64_t n, int32_t H, int32_t W, int32_t C, int32_t bins,
+                                  const cofie_keep_rule* rule);
+
+/* Per-frame histogram counts of NGFF (Sec. 3.2, the normalised B-bin
+ * histogram h_t = counts / M).
+ *   frames    device uint8 [n][H][W][C], C-order, channels interleaved (RGB)
+ *   n         frames (n = 0: nothing to do)
+ *   H, W, C   frame shape; C = 3, or C = 1 with GRAY
+ *   bins      B, a power of two in [2, 256]
+ *   out_hist  device uint32 [n][nbins], fully overwritten
+ * Errors: EINVAL for null pointers, negative/zero sizes, bad enums or C;
+ * EUNSUPPORTED for B not a power of two, B^3 > 4096, or 2M >= 2^24.       */
+int cofie_ngff_histogram(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                         int32_t bins, int32_t hist_mode, uint32_t* out_hist, void* stream);
+
+/* NGFF end to end (Sec. 3.2, Eqs. 2-5 and safeguards): histograms, novelty
+ * scores and the keep rule of `keep_rule` (host struct).
+ *   out_scores  device float [n]: s_t (s = 1 for each stream's first frame)
+ *   out_mask    device uint8 [n]: 1 = frame is a candidate (in S_c), else 0
+ * Same frame arguments and errors as cofie_ngff_histogram; also EINVAL for
+ * a NULL keep_rule, a NaN tau_h, M_min < 0 or segment_len < 0; ENOMEM if the
+ * caller's workspace is smaller than cofie_ngff_workspace_bytes(). */
+int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                      int32_t bins, const cofie_keep_rule* keep_rule, float* out_scores,
+                      uint8_t* out_mask, void* stream);
+
+/* Threshold calibration for a retention target (the paper fixes tau_h; a
+ * target kept count per stream is an extension).  Per stream, among the
+ * candidate integer thresholds theta in {0, 2M+1} and every distance
+ * D(t, t-k), 1 <= k <= L_max, the smallest one whose keep rule (with
+ * tau = fl32(theta)/fl32(2M), top-up included) keeps at most
+ * `target_per_segment` frames; 2M+1 if none does.  Writes that tau to
+ * out_tau (device float [n_segments]), ready for tau_per_segment.  Uses
+ * hist_mode, L_max (>= 1 required, else EUNSUPPORTED), M_min, segment_len and
+ * the workspace of keep_rule; tau_h, tau_per_segment, out_hist and out_count
+ * are ignored. */
+int cofie_ngff_calibrate(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                         int32_t bins, const cofie_keep_rule* keep_rule,
+                         int64_t target_per_segment, float* out_tau, void* stream);
+
+/* ---- QER ---------------------------------------------------------------- */
+
+typedef struct cofie_qer_desc {
+  int32_t n_q;        /* text (query) tokens used for scoring, >= 1                 */
+  int32_t n_vis;      /* visual tokens (rows of K), >= 0                            */
+  int32_t n_frames;   /* frames (CSR segments of the visual tokens), >= 0           */
+  int32_t H_q;        /* query heads                                                */
+  int32_t H_kv;       /* key heads; H_q % H_kv == 0; query head h reads key head    */
+                      /*   h / (H_q / H_kv) (contiguous groups)                     */
+  int32_t d;          /* head dimension, a multiple of 16                           */
+  int32_t dtype;      /* enum cofie_dtype of Q and K                                */
+  int32_t score_mode; /* enum cofie_score_mode                                      */
+  float scale;        /* dot-product scale; <= 0 selects 1/sqrt(d)                  */
+  void* workspace;    /* optional device scratch (see header comment)               */
+  size_t workspace_bytes;
+} cofie_qer_desc;
+
+/* Bytes of device scratch cofie_qer_rank needs (0 for invalid arguments). */
+size_t cofie_qer_workspace_bytes(const cofie_qer_desc* heads, int32_t k_top);
+
+/* QER frame ranking (Sec. 3.3, Eqs. 6-8):
+ *   a_ij = (1/H_q) sum_h scale * <q_i^h, k_j^h>          (LOGIT; Eq. 6)
+ *   w_f  = (1/|V_f|) sum_{j in V_f} max_i a_ij           (Eq. 7; -inf if V_f empty)
+ *   S_e  = the k_top frames of largest w_f               (Eq. 8)
+ *   Q              device [n_q][H_q][d] of dtype, row-major (post-RoPE queries)
+ *   K              device [n_vis][H_kv][d] of dtype, row-major (post-RoPE keys)
+ *   frame_offsets  device int32 [n_frames+1], CSR: V_f = [off[f], off[f+1]);
+ *                  values are clamped to [0, n_vis] and an inverted range is an
+ *                  empty frame, so malformed offsets never read out of bounds
+ *   heads          host descriptor
+ *   k_top          frames to keep (>= 0); more than n_frames keeps all
+ *   out_scores     device float [n_frames]: w_f
+ *   out_idx        device int32 [k_top] (may be NULL if k_top == 0): the winners
+ *                  ordered by score descending, ties to the lower frame index,
+ *                  NaN ranked as -inf, returned in ascending (chronological)
+ *                  frame order and padded with -1.
+ * bf16 inputs are multiplied on MFMA with fp32 accumulation; fp32 inputs use
+ * the fp32 MFMA.  Errors: EINVAL for null pointers, sizes or enums out of
+ * range or H_q % H_kv != 0; EUNSUPPORTED for d % 16 != 0; ENOMEM for a short
+ * workspace. */
+int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
+                   const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
+                   int32_t* out_idx, void* stream);
+
+/* ---- host helpers ------------------------------------------------------- */
+
+/* k = max(1, round(rho * n_candidates)) (Eq. 8), rounding half to even;
+ * 0 if n_candidates <= 0; -1 if rho is NaN or negative. */
+int64_t cofie_qer_k_from_ratio(double rho, int64_t n_candidates);
+
+/* Total drop ratio of the two stages, 1 - (1 - d_ngff)(1 - d_qer) (Sec. 4.1, Eq. 9). */
+double cofie_drop_total(double d_ngff, double d_qer);
+
+/* Message describing the calling thread's last error ("" if none). */
+const char* cofie_last_error(void);
+
+/* Library version string. */
+const char* cofie_version(void);
+
+/* ---- measurement -------------------------------------------------------- */
+
+/* Kernel timing: when enabled, every kernel the library enqueues is bracketed
+ * by a pair of HIP events on its stream, so per-kernel durations are measured
+ * on the GPU's own clock.  cofie_profiler_read synchronises those events and
+ * returns, for kernels whose name contains `name_substr`, the summed duration
+ * (ms) and the number of launches.  Process-wide state; not for concurrent
+ * use from several host threads. */
+int cofie_profiler_enable(int on);
+int cofie_profiler_reset(void);
+int cofie_profiler_read(const char* name_substr, double* total_ms, int64_t* launches);
+
+/* Streaming copy of `bytes` device bytes (16-byte aligned pointers): a plain
+ * HBM read+write kernel used as a bandwidth and hardware-counter reference
+ * for the measurement of the kernels above. */
+int cofie_diag_stream_copy(const void* src, void* dst, size_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COFIE_H_ */

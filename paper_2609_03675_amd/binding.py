@@ -1,0 +1,292 @@
+"""Thin Python binding of libcofie's C ABI (include/cofie.h).
+
+Argument marshalling only: every step runs in the HIP kernels of libcofie.so.
+Functions carry the C entry points' names and take torch tensors that live on
+the GPU; the library enqueues work on the current torch stream (or the one
+passed) and never synchronises.  There is no CPU fallback: if the library is
+missing or the tensors are not on the GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libcofie.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "cofie.h")
+
+COFIE_OK, COFIE_EINVAL, COFIE_EUNSUPPORTED, COFIE_EHIP, COFIE_ENOMEM = 0, -1, -2, -3, -4
+GRAY, PER_CHANNEL, JOINT3D = 0, 1, 2
+F32, BF16 = 0, 1
+LOGIT, SOFTMAX = 0, 1
+HIST_MODES = {"gray": GRAY, "per_channel": PER_CHANNEL, "joint3d": JOINT3D}
+
+
+class CofieError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"cofie error {code}: {msg}")
+        self.code = code
+
+
+class KeepRule(ctypes.Structure):
+    _fields_ = [
+        ("hist_mode", ctypes.c_int32),
+        ("tau_h", ctypes.c_float),
+        ("tau_per_segment", ctypes.c_void_p),
+        ("L_max", ctypes.c_int32),
+        ("M_min", ctypes.c_int32),
+        ("segment_len", ctypes.c_int64),
+        ("out_hist", ctypes.c_void_p),
+        ("out_count", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+class QerDesc(ctypes.Structure):
+    _fields_ = [
+        ("n_q", ctypes.c_int32),
+        ("n_vis", ctypes.c_int32),
+        ("n_frames", ctypes.c_int32),
+        ("H_q", ctypes.c_int32),
+        ("H_kv", ctypes.c_int32),
+        ("d", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("score_mode", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def declared_functions() -> list:
+    """Names of the functions include/cofie.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cofie_\w+)\s*\(", text)))
+
+
+def lib() -> ctypes.CDLL:
+    """Load libcofie.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2609_03675_amd.build`")
+    try:  # share torch's HIP runtime (same soname) when torch is present
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover
+        pass
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32, f64, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                 ctypes.c_double, ctypes.c_size_t)
+    sig = {
+        "cofie_keep_rule_default": (None, [ctypes.POINTER(KeepRule)]),
+        "cofie_ngff_nbins": (i64, [i32, i32]),
+        "cofie_ngff_workspace_bytes": (sz, [i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule)]),
+        "cofie_ngff_histogram": (ctypes.c_int, [P, i64, i32, i32, i32, i32, i32, P, P]),
+        "cofie_ngff_filter": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), P, P, P]),
+        "cofie_ngff_calibrate": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), i64, P, P]),
+        "cofie_qer_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32]),
+        "cofie_qer_rank": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
+        "cofie_qer_k_from_ratio": (i64, [f64, i64]),
+        "cofie_drop_total": (f64, [f64, f64]),
+        "cofie_last_error": (ctypes.c_char_p, []),
+        "cofie_version": (ctypes.c_char_p, []),
+        "cofie_profiler_enable": (ctypes.c_int, [ctypes.c_int]),
+        "cofie_profiler_reset": (ctypes.c_int, []),
+        "cofie_profiler_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(f64), ctypes.POINTER(i64)]),
+        "cofie_diag_stream_copy": (ctypes.c_int, [P, P, sz, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != COFIE_OK:
+        raise CofieError(rc, lib().cofie_last_error().decode())
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _dev(t, name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _mode(m) -> int:
+    return HIST_MODES[m] if isinstance(m, str) else int(m)
+
+
+# ---- host helpers ----------------------------------------------------------------
+
+def cofie_qer_k_from_ratio(rho: float, n_candidates: int) -> int:
+    return int(lib().cofie_qer_k_from_ratio(rho, n_candidates))
+
+
+def cofie_drop_total(d_ngff: float, d_qer: float) -> float:
+    return float(lib().cofie_drop_total(d_ngff, d_qer))
+
+
+def cofie_ngff_nbins(hist_mode, bins: int) -> int:
+    return int(lib().cofie_ngff_nbins(_mode(hist_mode), bins))
+
+
+def keep_rule(hist_mode="gray", tau_h: float = 0.30, L_max: int = 30, M_min: int = 4,
+              segment_len: int = 0, tau_per_segment=None, out_hist=None, out_count=None,
+              workspace=None) -> KeepRule:
+    r = KeepRule()
+    lib().cofie_keep_rule_default(ctypes.byref(r))
+    r.hist_mode = _mode(hist_mode)
+    r.tau_h = tau_h
+    r.L_max = L_max
+    r.M_min = M_min
+    r.segment_len = segment_len
+    r.tau_per_segment = _dev(tau_per_segment, "tau_per_segment")
+    r.out_hist = _dev(out_hist, "out_hist")
+    r.out_count = _dev(out_count, "out_count")
+    if workspace is not None:
+        r.workspace = _dev(workspace, "workspace")
+        r.workspace_bytes = workspace.numel() * workspace.element_size()
+    return r
+
+
+# ---- NGFF ---------------------------------------------------------------------------
+
+def _frame_shape(frames):
+    if frames.dim() == 3:
+        n, H, W = frames.shape
+        return n, H, W, 1
+    n, H, W, C = frames.shape
+    return n, H, W, C
+
+
+def cofie_ngff_histogram(frames, bins: int, hist_mode="gray", out=None, stream=None):
+    """Histogram counts uint32 [n][nbins] (returned as int32 bits) of uint8 frames [n][H][W][C]."""
+    import torch
+    n, H, W, C = _frame_shape(frames)
+    nb = cofie_ngff_nbins(hist_mode, bins)
+    if out is None:
+        out = torch.empty((n, max(nb, 1)), dtype=torch.int32, device=frames.device)
+    _check(lib().cofie_ngff_histogram(_dev(frames, "frames"), n, H, W, C, bins, _mode(hist_mode),
+                                      _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def cofie_ngff_filter(frames, bins: int, rule: KeepRule, out_scores=None, out_mask=None,
+                      stream=None):
+    """NGFF scores (float32 [n]) and candidate mask (uint8 [n])."""
+    import torch
+    n, H, W, C = _frame_shape(frames)
+    if out_scores is None:
+        out_scores = torch.empty(n, dtype=torch.float32, device=frames.device)
+    if out_mask is None:
+        out_mask = torch.empty(n, dtype=torch.uint8, device=frames.device)
+    _check(lib().cofie_ngff_filter(_dev(frames, "frames"), n, H, W, C, bins, ctypes.byref(rule),
+                                   _dev(out_scores, "out_scores"), _dev(out_mask, "out_mask"),
+                                   _stream(stream)))
+    return out_scores, out_mask
+
+
+def cofie_ngff_calibrate(frames, bins: int, rule: KeepRule, target_per_segment: int, out_tau=None,
+                         stream=None):
+    """Per-stream tau keeping at most `target_per_segment` frames (float32 [n_segments])."""
+    import torch
+    n, H, W, C = _frame_shape(frames)
+    seg = rule.segment_len if 0 < rule.segment_len <= n else max(n, 1)
+    nseg = (n + seg - 1) // seg if n > 0 else 0
+    if out_tau is None:
+        out_tau = torch.empty(max(nseg, 1), dtype=torch.float32, device=frames.device)
+    _check(lib().cofie_ngff_calibrate(_dev(frames, "frames"), n, H, W, C, bins, ctypes.byref(rule),
+                                      target_per_segment, _dev(out_tau, "out_tau"), _stream(stream)))
+    return out_tau[:nseg]
+
+
+def ngff_workspace_bytes(n: int, H: int, W: int, C: int, bins: int, rule: KeepRule) -> int:
+    return int(lib().cofie_ngff_workspace_bytes(n, H, W, C, bins, ctypes.byref(rule)))
+
+
+# ---- QER ------------------------------------------------------------------------------
+
+def qer_desc(n_q: int, n_vis: int, n_frames: int, H_q: int, H_kv: int, d: int, dtype=BF16,
+             score_mode=LOGIT, scale: float = 0.0, workspace=None) -> QerDesc:
+    h = QerDesc(n_q, n_vis, n_frames, H_q, H_kv, d, dtype, score_mode, scale, None, 0)
+    if workspace is not None:
+        h.workspace = _dev(workspace, "workspace")
+        h.workspace_bytes = workspace.numel() * workspace.element_size()
+    return h
+
+
+def qer_workspace_bytes(desc: QerDesc, k_top: int) -> int:
+    return int(lib().cofie_qer_workspace_bytes(ctypes.byref(desc), k_top))
+
+
+def cofie_qer_rank(Q, K, frame_offsets, k_top: int, score_mode=LOGIT, scale: float = 0.0,
+                   out_scores=None, out_idx=None, workspace=None, stream=None):
+    """QER frame scores w_f (float32 [n_frames]) and chronological top-k (int32 [k_top]).
+
+    Q: [n_q][H_q][d], K: [n_vis][H_kv][d], both torch.bfloat16 or torch.float32."""
+    import torch
+    n_q, H_q, d = Q.shape
+    n_vis, H_kv, d2 = K.shape
+    if d2 != d:
+        raise ValueError("Q and K head dimensions differ")
+    if Q.dtype != K.dtype or Q.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("Q and K must both be bfloat16 or both float32")
+    dtype = BF16 if Q.dtype == torch.bfloat16 else F32
+    n_frames = frame_offsets.numel() - 1
+    if out_scores is None:
+        out_scores = torch.empty(max(n_frames, 1), dtype=torch.float32, device=Q.device)
+    if out_idx is None:
+        out_idx = torch.empty(max(k_top, 1), dtype=torch.int32, device=Q.device)
+    desc = qer_desc(n_q, n_vis, n_frames, H_q, H_kv, d, dtype, score_mode, scale, workspace)
+    _check(lib().cofie_qer_rank(_dev(Q, "Q"), _dev(K, "K") if n_vis > 0 else None,
+                                _dev(frame_offsets, "frame_offsets"), ctypes.byref(desc), k_top,
+                                _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
+                                _stream(stream)))
+    return out_scores[:n_frames], out_idx[:k_top]
+
+
+# ---- measurement ----------------------------------------------------------------------
+
+def cofie_profiler_enable(on: bool = True) -> None:
+    _check(lib().cofie_profiler_enable(1 if on else 0))
+
+
+def cofie_profiler_reset() -> None:
+    _check(lib().cofie_profiler_reset())
+
+
+def cofie_profiler_read(name_substr: str = ""):
+    """(summed ms, launches) of the kernels whose name contains name_substr."""
+    ms = ctypes.c_double()
+    cnt = ctypes.c_int64()
+    _check(lib().cofie_profiler_read(name_substr.encode(), ctypes.byref(ms), ctypes.byref(cnt)))
+    return ms.value, cnt.value
+
+
+def cofie_diag_stream_copy(src, dst, stream=None) -> None:
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    _check(lib().cofie_diag_stream_copy(_dev(src, "src"), _dev(dst, "dst"), nbytes, _stream(stream)))

@@ -1,0 +1,873 @@
+// NGFF -- Novelty-Guided Frame Filtering (Sec. 3.2) on gfx950.
+//
+// Pipeline of one cofie_ngff_filter call (all on the caller's stream):
+//   [fill]   zero the histogram when several workgroups share a frame
+//   hist     streaming histogram: 12-byte coalesced loads (64 lanes x 12 B =
+//            768 contiguous bytes per wave instruction), byte -> bin in
+//            registers, increments into 64 lane-private LDS copies laid out
+//            bin-major ([bin][lane]) so that the lanes of one instruction
+//            always hit 64 distinct banks; one merge per workgroup
+//   band     exact integer L1 distances D(t, t-k), 1 <= k <= L_max, from
+//            histogram rows staged in LDS
+//   next     for every frame r, the frame the keep rule would keep next if r
+//            were the last kept frame (depends only on the band and theta)
+//   select   one workgroup per stream follows the next[] chain from frame 0,
+//            applies the M_min top-up and writes scores, mask and counts
+// Novelty comparisons run on integers: s >= tau  <=>  max(D) >= theta with
+// theta = min{D : fl32(D)/fl32(2M) >= tau}, exact because fl32(D)/fl32(2M) is
+// strictly increasing in D for 2M < 2^24.  Scores are fl32(D)/fl32(2M), one
+// IEEE division, so they are bit-identical to any correct implementation.
+#include "common.h"
+
+namespace cofie {
+namespace {
+
+constexpr int kUnitBytes = 768;  // one wave-wide load: 64 lanes x 12 bytes
+constexpr int kUnroll = 8;       // units in flight per wave
+
+enum HistKind { K_PC = 0, K_GRAY1 = 1, K_GRAY3 = 2, K_JOINT = 3 };
+
+struct HistArgs {
+  const uint8_t* frames;
+  int64_t frame_bytes;
+  int64_t npix;
+  uint32_t* hist;
+  int32_t nbins;
+  int32_t B;
+  int32_t shift;  // 8 - log2(B): bin = v >> shift
+  int32_t logB;
+  int32_t splits; // workgroups per frame
+  int32_t units;  // whole 768-byte units covered by the vector path
+  int32_t atomic; // 1: several workgroups per frame add into a zeroed histogram
+};
+
+struct __attribute__((packed, aligned(4))) U3 {
+  uint32_t x, y, z;
+};
+
+__device__ __forceinline__ uint32_t luma_bt601(uint32_t r, uint32_t g, uint32_t b) {
+  return (299u * r + 587u * g + 114u * b + 500u) / 1000u;
+}
+
+// Bin of one pixel for the pixel-wise kinds (GRAY of RGB, JOINT3D).
+template <int KIND, int BC>
+__device__ __forceinline__ uint32_t pixel_bin(uint32_t r, uint32_t g, uint32_t b, const HistArgs& a) {
+  const int shift = BC ? (8 - __builtin_ctz(BC)) : a.shift;
+  const int logB = BC ? __builtin_ctz(BC) : a.logB;
+  if constexpr (KIND == K_GRAY3) {
+    return luma_bt601(r, g, b) >> shift;
+  } else {
+    return ((r >> shift) << (2 * logB)) | ((g >> shift) << logB) | (b >> shift);
+  }
+}
+
+// Count the 12 bytes one lane loaded (4 RGB pixels, or 12 gray pixels).
+template <int KIND, int P, int BC>
+__device__ __forceinline__ void count12(uint32_t* cnt, const U3& v, uint32_t lane, const HistArgs& a) {
+  const uint32_t w[3] = {v.x, v.y, v.z};
+  const uint32_t copy = lane & (P - 1);
+  if constexpr (KIND == K_PC || KIND == K_GRAY1) {
+    if constexpr (P == 64 && BC != 0) {
+      // bins of 4 bytes at once, then byte-permute each bin into bits 8..15 of
+      // an LDS byte address whose low byte is lane*4: bin*256 + lane*4.  The
+      // channel (byte position mod 3, fixed because lanes read 12-byte pixel-
+      // aligned chunks) becomes a constant offset of c*B rows.
+      constexpr int shift = 8 - __builtin_ctz(BC);
+      constexpr uint32_t m4 = (uint32_t)(BC - 1) * 0x01010101u;
+      const uint32_t lane4 = lane * 4u;
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+        const uint32_t tb = (w[j] >> shift) & m4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          constexpr int dummy = 0;
+          (void)dummy;
+          const int c = (KIND == K_PC) ? ((4 * j + i) % 3) : 0;
+          const uint32_t addr = __builtin_amdgcn_perm(tb, lane4, 0x0C0C0000u | ((4u + i) << 8));
+          atomicAdd(reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(cnt) + addr) + c * BC * 64, 1u);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int c = (KIND == K_PC) ? ((4 * j + i) % 3) : 0;
+          const uint32_t bin = ((w[j] >> (8 * i)) & 0xFFu) >> a.shift;
+          atomicAdd(cnt + (bin + (uint32_t)(c * a.B)) * P + copy, 1u);
+        }
+      }
+    }
+  } else {
+    uint32_t byte[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) byte[k] = (w[k >> 2] >> (8 * (k & 3))) & 0xFFu;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t bin = pixel_bin<KIND, BC>(byte[3 * p], byte[3 * p + 1], byte[3 * p + 2], a);
+      atomicAdd(cnt + bin * P + copy, 1u);
+    }
+  }
+}
+
+// One pixel read byte by byte (ragged tails and unaligned frames).
+template <int KIND, int P, int BC>
+__device__ __forceinline__ void count_pixel(uint32_t* cnt, const uint8_t* px, uint32_t lane,
+                                            const HistArgs& a) {
+  const uint32_t copy = lane & (P - 1);
+  if constexpr (KIND == K_GRAY1) {
+    atomicAdd(cnt + (uint32_t)(px[0] >> a.shift) * P + copy, 1u);
+  } else if constexpr (KIND == K_PC) {
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+      atomicAdd(cnt + ((uint32_t)(px[c] >> a.shift) + (uint32_t)(c * a.B)) * P + copy, 1u);
+  } else {
+    atomicAdd(cnt + pixel_bin<KIND, BC>(px[0], px[1], px[2], a) * P + copy, 1u);
+  }
+}
+
+// grid: n * splits workgroups; workgroup (t, s) counts its share of frame t.
+template <int KIND, int P, int BC>
+__global__ __launch_bounds__(1024) void ngff_hist_kernel(HistArgs a) {
+  extern __shared__ uint32_t cnt[];  // [nbins][P]
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const uint32_t lane = tid & 63;
+  const int wave = tid >> 6, nw = nthr >> 6;
+  const int64_t t = blockIdx.x / a.splits;
+  const int s = (int)(blockIdx.x - t * a.splits);
+  const int ncnt = a.nbins * P;
+  for (int i = tid; i < ncnt; i += nthr) cnt[i] = 0;
+  __syncthreads();
+
+  const uint8_t* f = a.frames + t * a.frame_bytes;
+  const int G = a.splits * nw;  // waves sharing this frame
+  const int g = s * nw + wave;
+  for (int u0 = g; u0 < a.units; u0 += G * kUnroll) {
+    U3 v[kUnroll];
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      const int u = u0 + j * G;
+      if (u < a.units)
+        v[j] = *reinterpret_cast<const U3*>(f + (int64_t)u * kUnitBytes + lane * 12);
+    }
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      const int u = u0 + j * G;
+      if (u < a.units) count12<KIND, P, BC>(cnt, v[j], lane, a);
+    }
+  }
+  // pixels after the whole units (or every pixel of an unaligned frame)
+  const int C = (KIND == K_GRAY1) ? 1 : 3;
+  const int64_t p0 = (int64_t)a.units * (kUnitBytes / C);
+  for (int64_t p = p0 + (int64_t)g * 64 + lane; p < a.npix; p += (int64_t)G * 64)
+    count_pixel<KIND, P, BC>(cnt, f + p * C, lane, a);
+  __syncthreads();
+
+  uint32_t* out = a.hist + t * a.nbins;
+  for (int b = tid; b < a.nbins; b += nthr) {
+    uint32_t sum = 0;
+    for (int l = 0; l < P; ++l) sum += cnt[b * P + ((l + b) & (P - 1))];
+    if (a.atomic) {
+      if (sum) atomicAdd(out + b, sum);
+    } else {
+      out[b] = sum;
+    }
+  }
+}
+
+__global__ void fill_u32_kernel(uint32_t* p, uint32_t v, int64_t count) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// ---- band of distances ----------------------------------------------------------
+struct BandArgs {
+  const uint32_t* hist;
+  int64_t n;
+  int32_t nbins;
+  int32_t L;       // band width (>= 1)
+  int64_t seg_len; // frames per stream
+  int32_t TB;      // frames per workgroup
+  int32_t stride;  // LDS row stride in words (nbins + 1), 0 = read global memory
+  int32_t* band;   // [n][L]: band[t*L + k-1] = D(t, t-k), 0 if t-k precedes the stream
+};
+
+__global__ __launch_bounds__(256) void ngff_band_kernel(BandArgs a) {
+  extern __shared__ uint32_t rows[];
+  const int64_t t0 = (int64_t)blockIdx.x * a.TB;
+  const int64_t r0 = t0 - a.L > 0 ? t0 - a.L : 0;
+  const int64_t r1 = t0 + a.TB < a.n ? t0 + a.TB : a.n;
+  if (a.stride) {
+    const int64_t nrows = r1 - r0;
+    for (int64_t i = threadIdx.x; i < nrows * a.nbins; i += blockDim.x) {
+      const int64_t r = i / a.nbins, b = i - r * a.nbins;
+      rows[r * a.stride + b] = a.hist[(r0 + r) * a.nbins + b];
+    }
+    __syncthreads();
+  }
+  for (int p = threadIdx.x; p < a.TB * a.L; p += blockDim.x) {
+    const int64_t t = t0 + p / a.L;
+    const int k = p % a.L + 1;
+    if (t >= a.n) continue;
+    const int64_t seg0 = (t / a.seg_len) * a.seg_len;
+    int32_t D = 0;
+    if (t - k >= seg0) {
+      const uint32_t* x;
+      const uint32_t* y;
+      if (a.stride) {
+        x = rows + (t - r0) * a.stride;
+        y = rows + (t - k - r0) * a.stride;
+      } else {
+        x = a.hist + t * a.nbins;
+        y = a.hist + (t - k) * a.nbins;
+      }
+      uint32_t acc = 0;
+      for (int b = 0; b < a.nbins; ++b) {
+        const uint32_t u = x[b], v = y[b];
+        acc += u > v ? u - v : v - u;
+      }
+      D = (int32_t)acc;
+    }
+    a.band[t * a.L + (k - 1)] = D;
+  }
+}
+
+// Smallest integer D in [0, 2M+1] with fl32(D)/fl32(2M) >= tau, or 2M+2 if
+// none (NaN tau).  The quotient is strictly increasing in D, so a binary search
+// over the exact IEEE predicate finds it.
+__device__ int64_t theta_of(float tau, int64_t twoM) {
+  const float den = (float)twoM;
+  int64_t lo = 0, hi = twoM + 2;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (mid <= twoM + 1 && (float)mid / den >= tau)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  return lo;
+}
+
+struct RuleArgs {
+  const int32_t* band;
+  int64_t n;
+  int64_t seg_len;
+  int32_t L;
+  int32_t M_min;
+  int64_t twoM;
+  float tau;
+  const float* tau_seg;  // device, may be null
+};
+
+__device__ __forceinline__ float tau_of_segment(const RuleArgs& a, int64_t seg) {
+  return a.tau_seg ? a.tau_seg[seg] : a.tau;
+}
+
+// next[r] (segment-relative): first u in (r, r+L] that the rule keeps when r is
+// the last kept frame: u is the stream's last frame, or u - r >= L, or
+// max(D(u,u-1), D(u,r)) >= theta.  The stream's last frame gets T.
+__global__ void ngff_next_kernel(RuleArgs a, int32_t* next) {
+  const int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (r >= a.n) return;
+  const int64_t seg = r / a.seg_len, s0 = seg * a.seg_len;
+  const int64_t T = a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len;
+  const int64_t rr = r - s0;
+  if (rr == T - 1) {
+    next[r] = (int32_t)T;
+    return;
+  }
+  const int64_t theta = theta_of(tau_of_segment(a, seg), a.twoM);
+  int64_t u = rr + 1;
+  for (int k = 1;; ++k, ++u) {
+    if (u == T - 1 || k >= a.L) break;
+    const int32_t* row = a.band + (s0 + u) * a.L;
+    const int32_t Dadj = row[0], Dref = row[k - 1];
+    if ((Dadj > Dref ? Dadj : Dref) >= theta) break;
+  }
+  next[r] = (int32_t)u;
+}
+
+// Is t one of the uniformly spaced top-up frames floor(i (T-1)/(m-1)), 0 <= i < m?
+__device__ __forceinline__ bool is_uniform(int64_t t, int64_t T, int64_t m) {
+  if (T <= 1) return t == 0;
+  const int64_t i = (t * (m - 1) + (T - 2)) / (T - 1);  // ceil(t (m-1) / (T-1))
+  return i < m && (i * (T - 1)) / (m - 1) == t;
+}
+
+// Block-wide sum of v (blockDim.x a multiple of 64, <= 1024).
+__device__ int64_t block_sum(int64_t v, int64_t* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  int64_t s = 0;
+  for (int i = 0; i < nw; ++i) s += red[i];
+  __syncthreads();
+  return s;
+}
+
+// One workgroup per stream: follow next[] from frame 0, top up, score, mask.
+// flags: 1 = kept by the rule, 2 = added by the top-up.  next/flags live in LDS
+// when USE_LDS, else in the global scratch slices.
+template <bool USE_LDS>
+__global__ __launch_bounds__(1024) void ngff_select_kernel(RuleArgs a, const int32_t* next_g,
+                                                           uint8_t* flag_g, float* scores,
+                                                           uint8_t* mask, int32_t* count) {
+  extern __shared__ int32_t lds_i[];
+  __shared__ int64_t red[16];
+  __shared__ int64_t kept_sh;
+  const int64_t seg = blockIdx.x, s0 = seg * a.seg_len;
+  const int64_t T = a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len;
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int32_t* nx;
+  uint8_t* fl;
+  if constexpr (USE_LDS) {
+    int32_t* nxl = lds_i;
+    fl = reinterpret_cast<uint8_t*>(lds_i + T);
+    for (int64_t i = tid; i < T; i += nthr) {
+      nxl[i] = next_g[s0 + i];
+      fl[i] = 0;
+    }
+    nx = nxl;
+  } else {
+    nx = next_g + s0;
+    fl = flag_g + s0;
+    for (int64_t i = tid; i < T; i += nthr) fl[i] = 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t r = 0, kept = 1;
+    fl[0] = 1;
+    while (r < T - 1) {
+      r = nx[r];
+      fl[r] = 1;
+      ++kept;
+    }
+    kept_sh = kept;
+  }
+  __syncthreads();
+  const int64_t kept = kept_sh;
+  if (a.M_min >= 2 && kept < a.M_min) {
+    for (int64_t i = tid; i < a.M_min; i += nthr) {
+      const int64_t u = (i * (T - 1)) / (a.M_min - 1);
+      if (fl[u] == 0) fl[u] = 2;
+    }
+  }
+  __syncthreads();
+  const float den = (float)a.twoM;
+  int64_t local = 0;
+  for (int64_t t = tid; t < T; t += nthr) {
+    const uint8_t f = fl[t];
+    local += f != 0;
+    mask[s0 + t] = f != 0;
+    float s = 1.0f;
+    if (t > 0) {
+      int64_t r = t - 1;
+      while (!(fl[r] & 1)) --r;  // last rule-kept frame before t (t - r <= L)
+      const int32_t* row = a.band + (s0 + t) * a.L;
+      const int32_t Dadj = row[0], Dref = row[t - r - 1];
+      s = (float)(Dadj > Dref ? Dadj : Dref) / den;
+    }
+    scores[s0 + t] = s;
+  }
+  const int64_t total = block_sum(local, red);
+  if (count && tid == 0) count[seg] = (int32_t)total;
+}
+
+// L_max <= 0: no gap rule, so r(t) can lie arbitrarily far back.  One
+// workgroup per stream walks t sequentially and measures D(t, r) from the
+// histograms with a block reduction.
+__global__ __launch_bounds__(256) void ngff_select_seq_kernel(RuleArgs a, const uint32_t* hist,
+                                                              int32_t nbins, uint8_t* flag_g,
+                                                              float* scores, uint8_t* mask,
+                                                              int32_t* count) {
+  __shared__ int64_t red[16];
+  const int64_t seg = blockIdx.x, s0 = seg * a.seg_len;
+  const int64_t T = a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len;
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  uint8_t* fl = flag_g + s0;
+  for (int64_t i = tid; i < T; i += nthr) fl[i] = 0;
+  const int64_t theta = theta_of(tau_of_segment(a, seg), a.twoM);
+  const float den = (float)a.twoM;
+  __syncthreads();
+  if (tid == 0) {
+    fl[0] = 1;
+    scores[s0] = 1.0f;
+  }
+  int64_t r = 0, kept = 1;
+  for (int64_t t = 1; t < T; ++t) {
+    const uint32_t* x = hist + (s0 + t) * nbins;
+    const uint32_t* y = hist + (s0 + r) * nbins;
+    int64_t part = 0;
+    for (int b = tid; b < nbins; b += nthr) {
+      const uint32_t u = x[b], v = y[b];
+      part += u > v ? u - v : v - u;
+    }
+    const int64_t Dref = block_sum(part, red);
+    const int32_t Dadj = a.band[(s0 + t) * a.L];  // band of width 1
+    const int64_t D = Dadj > Dref ? Dadj : Dref;
+    const bool keep = (t == T - 1) || D >= theta;
+    if (tid == 0) {
+      scores[s0 + t] = (float)D / den;
+      fl[t] = keep ? 1 : 0;
+    }
+    if (keep) {
+      r = t;
+      ++kept;
+    }
+  }
+  __syncthreads();
+  if (a.M_min >= 2 && kept < a.M_min) {
+    for (int64_t i = tid; i < a.M_min; i += nthr) {
+      const int64_t u = (i * (T - 1)) / (a.M_min - 1);
+      if (fl[u] == 0) fl[u] = 2;
+    }
+  }
+  __syncthreads();
+  int64_t local = 0;
+  for (int64_t t = tid; t < T; t += nthr) {
+    local += fl[t] != 0;
+    mask[s0 + t] = fl[t] != 0;
+  }
+  const int64_t total = block_sum(local, red);
+  if (count && tid == 0) count[seg] = (int32_t)total;
+}
+
+// ---- threshold calibration ---------------------------------------------------------
+__global__ void calib_init_kernel(int32_t* best, int64_t nseg, int64_t twoM) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < nseg) best[i] = (int32_t)(twoM + 1);
+}
+
+// Kept count (top-up included) of one stream under integer threshold theta.
+__device__ int64_t kept_count(const RuleArgs& a, int64_t s0, int64_t T, int64_t theta) {
+  int64_t r = 0, kept = 1;
+  while (r < T - 1) {
+    int64_t u = r + 1;
+    for (int k = 1;; ++k, ++u) {
+      if (u == T - 1 || k >= a.L) break;
+      const int32_t* row = a.band + (s0 + u) * a.L;
+      const int32_t Dadj = row[0], Dref = row[k - 1];
+      if ((Dadj > Dref ? Dadj : Dref) >= theta) break;
+    }
+    r = u;
+    ++kept;
+  }
+  if (a.M_min >= 2 && kept < a.M_min) {
+    // add the distinct uniform frames missing from the (short) kept chain
+    int64_t prev = -1;
+    for (int64_t i = 0; i < a.M_min; ++i) {
+      const int64_t u = (i * (T - 1)) / (a.M_min - 1);
+      if (u == prev) continue;
+      prev = u;
+      bool in_chain = false;
+      int64_t c = 0;
+      while (true) {  // walk the chain again: it has fewer than M_min frames
+        if (c == u) {
+          in_chain = true;
+          break;
+        }
+        if (c > u || c >= T - 1) break;
+        int64_t v = c + 1;
+        for (int k = 1;; ++k, ++v) {
+          if (v == T - 1 || k >= a.L) break;
+          const int32_t* row = a.band + (s0 + v) * a.L;
+          const int32_t Dadj = row[0], Dref = row[k - 1];
+          if ((Dadj > Dref ? Dadj : Dref) >= theta) break;
+        }
+        c = v;
+      }
+      if (!in_chain) ++kept;
+    }
+  }
+  return kept;
+}
+
+// One thread per candidate threshold: every band entry of a stream, plus 0 and
+// 2M+1 per stream.  Satisfying candidates race with atomicMin.
+__global__ void calib_kernel(RuleArgs a, int64_t nseg, int64_t target, int32_t* best) {
+  const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int64_t nband = a.n * a.L;
+  int64_t seg, theta;
+  if (c < nband) {
+    const int64_t t = c / a.L;
+    const int k = (int)(c - t * a.L) + 1;
+    seg = t / a.seg_len;
+    if (t - k < seg * a.seg_len) return;
+    theta = a.band[c];
+  } else if (c < nband + 2 * nseg) {
+    const int64_t e = c - nband;
+    seg = e >> 1;
+    theta = (e & 1) ? a.twoM + 1 : 0;
+  } else {
+    return;
+  }
+  if (theta >= __hip_atomic_load(best + seg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+  const int64_t s0 = seg * a.seg_len;
+  const int64_t T = a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len;
+  if (kept_count(a, s0, T, theta) <= target) atomicMin(best + seg, (int32_t)theta);
+}
+
+__global__ void calib_final_kernel(const int32_t* best, int64_t nseg, int64_t twoM, float* tau) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < nseg) tau[i] = (float)best[i] / (float)twoM;
+}
+
+// ---- host side ------------------------------------------------------------------------
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+struct NgffShape {
+  int64_t n;
+  int32_t H, W, C, B, mode;
+  int64_t nbins, npix, frame_bytes, mass;
+};
+
+int validate_frames(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C, int32_t bins,
+                    int32_t mode, NgffShape* sh) {
+  if (n < 0) return set_error(COFIE_EINVAL, "n = %lld is negative", (long long)n);
+  if (n > 0 && !frames) return set_error(COFIE_EINVAL, "frames is NULL");
+  if (H <= 0 || W <= 0) return set_error(COFIE_EINVAL, "H = %d, W = %d must be positive", H, W);
+  if (C != 1 && C != 3) return set_error(COFIE_EINVAL, "C = %d must be 1 or 3", C);
+  if (mode != COFIE_HIST_GRAY && mode != COFIE_HIST_PER_CHANNEL && mode != COFIE_HIST_JOINT3D)
+    return set_error(COFIE_EINVAL, "unknown hist_mode %d", mode);
+  if (C == 1 && mode != COFIE_HIST_GRAY)
+    return set_error(COFIE_EINVAL, "C = 1 frames support only the GRAY histogram");
+  if (bins < 2 || bins > 256) return set_error(COFIE_EINVAL, "bins = %d outside [2, 256]", bins);
+  if (!is_pow2(bins))
+    return set_error(COFIE_EUNSUPPORTED, "bins = %d is not a power of two", bins);
+  const int64_t nbins = cofie_ngff_nbins(mode, bins);
+  if (nbins > 4096)
+    return set_error(COFIE_EUNSUPPORTED, "%lld bins exceed 4096", (long long)nbins);
+  const int64_t npix = (int64_t)H * W;
+  const int64_t mass = mode == COFIE_HIST_PER_CHANNEL ? 3 * npix : npix;
+  if (2 * mass >= (int64_t(1) << 24))
+    return set_error(COFIE_EUNSUPPORTED,
+                     "2M = %lld >= 2^24: distances would not be exact in fp32", (long long)(2 * mass));
+  sh->n = n;
+  sh->H = H;
+  sh->W = W;
+  sh->C = C;
+  sh->B = bins;
+  sh->mode = mode;
+  sh->nbins = nbins;
+  sh->npix = npix;
+  sh->frame_bytes = npix * C;
+  sh->mass = mass;
+  return COFIE_OK;
+}
+
+// Histogram launch geometry.
+struct HistPlan {
+  int kind, P, threads, splits, units;
+  size_t lds;
+};
+
+HistPlan plan_hist(const NgffShape& sh, const uint8_t* frames) {
+  HistPlan p;
+  if (sh.mode == COFIE_HIST_PER_CHANNEL)
+    p.kind = K_PC;
+  else if (sh.mode == COFIE_HIST_JOINT3D)
+    p.kind = K_JOINT;
+  else
+    p.kind = sh.C == 1 ? K_GRAY1 : K_GRAY3;
+  p.P = 64;
+  while ((size_t)sh.nbins * p.P * 4 > 160 * 1024) p.P >>= 1;
+  p.lds = (size_t)sh.nbins * p.P * 4;
+  p.threads = p.lds <= 40 * 1024 ? 256 : (p.lds <= 80 * 1024 ? 512 : 1024);
+  // the vector path needs 4-byte aligned frames
+  const bool aligned = (reinterpret_cast<uintptr_t>(frames) % 4 == 0) && (sh.frame_bytes % 4 == 0);
+  p.units = aligned ? (int)(sh.frame_bytes / kUnitBytes) : 0;
+  const int nw = p.threads / 64;
+  const int64_t target = 8LL * device_cu_count();
+  int64_t splits = (target + sh.n - 1) / (sh.n > 0 ? sh.n : 1);
+  const int64_t by_units = p.units / (nw * kUnroll);
+  if (splits > by_units) splits = by_units;
+  if (splits < 1) splits = 1;
+  p.splits = (int)splits;
+  return p;
+}
+
+template <int KIND, int P, int BC>
+int launch_hist_t(const HistArgs& args, const HistPlan& p, int64_t n, hipStream_t s) {
+  auto k = ngff_hist_kernel<KIND, P, BC>;
+  int rc = allow_lds(k, p.lds);
+  if (rc) return rc;
+  return launch("ngff_hist", k, dim3((unsigned)(n * p.splits)), dim3(p.threads), p.lds, s, args);
+}
+
+template <int KIND>
+int launch_hist_kind(const HistArgs& args, const HistPlan& p, int64_t n, hipStream_t s) {
+  switch (p.P) {
+    case 64:
+      if (args.B == 32) return launch_hist_t<KIND, 64, 32>(args, p, n, s);
+      if (args.B == 16) return launch_hist_t<KIND, 64, 16>(args, p, n, s);
+      if (KIND == K_JOINT && args.B == 8) return launch_hist_t<KIND, 64, 8>(args, p, n, s);
+      return launch_hist_t<KIND, 64, 0>(args, p, n, s);
+    case 32:
+      return launch_hist_t<KIND, 32, 0>(args, p, n, s);
+    case 16:
+      return launch_hist_t<KIND, 16, 0>(args, p, n, s);
+    default:
+      return launch_hist_t<KIND, 8, 0>(args, p, n, s);
+  }
+}
+
+int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hipStream_t s) {
+  if (sh.n == 0) return COFIE_OK;
+  const HistPlan p = plan_hist(sh, frames);
+  HistArgs a;
+  a.frames = frames;
+  a.frame_bytes = sh.frame_bytes;
+  a.npix = sh.npix;
+  a.hist = hist;
+  a.nbins = (int32_t)sh.nbins;
+  a.B = sh.B;
+  a.logB = __builtin_ctz(sh.B);
+  a.shift = 8 - a.logB;
+  a.splits = p.splits;
+  a.units = p.units;
+  a.atomic = p.splits > 1;
+  if (a.atomic) {
+    const int64_t cnt = sh.n * sh.nbins;
+    int rc = launch("ngff_fill", fill_u32_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(cnt, 256), 4096)),
+                    dim3(256), 0, s, hist, 0u, cnt);
+    if (rc) return rc;
+  }
+  switch (p.kind) {
+    case K_PC: return launch_hist_kind<K_PC>(a, p, sh.n, s);
+    case K_GRAY1: return launch_hist_kind<K_GRAY1>(a, p, sh.n, s);
+    case K_GRAY3: return launch_hist_kind<K_GRAY3>(a, p, sh.n, s);
+    default: return launch_hist_kind<K_JOINT>(a, p, sh.n, s);
+  }
+}
+
+struct RulePlan {
+  int64_t seg_len, nseg;
+  int32_t L;          // band width (>= 1)
+  bool gap_rule;      // L_max >= 1
+};
+
+RulePlan plan_rule(const NgffShape& sh, const cofie_keep_rule* r) {
+  RulePlan p;
+  p.seg_len = (r->segment_len <= 0 || r->segment_len > sh.n) ? (sh.n > 0 ? sh.n : 1) : r->segment_len;
+  p.nseg = sh.n > 0 ? (sh.n + p.seg_len - 1) / p.seg_len : 0;
+  p.gap_rule = r->L_max >= 1;
+  p.L = p.gap_rule ? r->L_max : 1;
+  return p;
+}
+
+// Scratch layout of filter/calibrate (same sequence sizes and carves).
+struct NgffScratch {
+  uint32_t* hist;
+  int32_t* band;
+  int32_t* next;
+  uint8_t* flags;
+  int32_t* best;
+};
+
+NgffScratch carve(Arena& ar, const NgffShape& sh, const RulePlan& rp, bool need_hist) {
+  NgffScratch w;
+  w.hist = need_hist ? ar.take<uint32_t>((size_t)(sh.n * sh.nbins)) : nullptr;
+  w.band = ar.take<int32_t>((size_t)(sh.n * rp.L));
+  w.next = ar.take<int32_t>((size_t)sh.n);
+  w.flags = ar.take<uint8_t>((size_t)sh.n);
+  w.best = ar.take<int32_t>((size_t)(rp.nseg > 0 ? rp.nseg : 1));
+  return w;
+}
+
+int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int32_t* band,
+             hipStream_t s) {
+  BandArgs b;
+  b.hist = hist;
+  b.n = sh.n;
+  b.nbins = (int32_t)sh.nbins;
+  b.L = rp.L;
+  b.seg_len = rp.seg_len;
+  const size_t budget = 64 * 1024;
+  const size_t row = (size_t)(sh.nbins + 1) * 4;
+  int TB = 64;
+  while (TB > 1 && (size_t)(TB + rp.L) * row > budget) TB >>= 1;
+  size_t lds = (size_t)(TB + rp.L) * row;
+  b.TB = TB;
+  b.stride = (int32_t)(sh.nbins + 1);
+  if (lds > budget) {  // rows too wide for LDS: read the histogram from global memory
+    b.stride = 0;
+    lds = 0;
+  }
+  b.band = band;
+  int rc = allow_lds(ngff_band_kernel, lds);
+  if (rc) return rc;
+  return launch("ngff_band", ngff_band_kernel, dim3((unsigned)ceil_div(sh.n, TB)), dim3(256), lds, s, b);
+}
+
+RuleArgs rule_args(const NgffShape& sh, const RulePlan& rp, const cofie_keep_rule* r,
+                   const int32_t* band) {
+  RuleArgs a;
+  a.band = band;
+  a.n = sh.n;
+  a.seg_len = rp.seg_len;
+  a.L = rp.L;
+  a.M_min = r->M_min;
+  a.twoM = 2 * sh.mass;
+  a.tau = r->tau_h;
+  a.tau_seg = r->tau_per_segment;
+  return a;
+}
+
+int validate_rule(const cofie_keep_rule* r) {
+  if (!r) return set_error(COFIE_EINVAL, "keep_rule is NULL");
+  if (r->segment_len < 0) return set_error(COFIE_EINVAL, "segment_len is negative");
+  if (r->M_min < 0) return set_error(COFIE_EINVAL, "M_min is negative");
+  if (!r->tau_per_segment && r->tau_h != r->tau_h) return set_error(COFIE_EINVAL, "tau_h is NaN");
+  return COFIE_OK;
+}
+
+}  // namespace
+}  // namespace cofie
+
+using namespace cofie;
+
+extern "C" {
+
+void cofie_keep_rule_default(cofie_keep_rule* r) {
+  if (!r) return;
+  r->hist_mode = COFIE_HIST_GRAY;
+  r->tau_h = 0.30f;
+  r->tau_per_segment = nullptr;
+  r->L_max = 30;
+  r->M_min = 4;
+  r->segment_len = 0;
+  r->out_hist = nullptr;
+  r->out_count = nullptr;
+  r->workspace = nullptr;
+  r->workspace_bytes = 0;
+}
+
+int64_t cofie_ngff_nbins(int32_t mode, int32_t bins) {
+  if (bins < 1) return 0;
+  if (mode == COFIE_HIST_GRAY) return bins;
+  if (mode == COFIE_HIST_PER_CHANNEL) return 3 * (int64_t)bins;
+  if (mode == COFIE_HIST_JOINT3D) return (int64_t)bins * bins * bins;
+  return 0;
+}
+
+size_t cofie_ngff_workspace_bytes(int64_t n, int32_t H, int32_t W, int32_t C, int32_t bins,
+                                  const cofie_keep_rule* rule) {
+  NgffShape sh;
+  static const uint8_t dummy = 0;
+  if (!rule || validate_frames(n > 0 ? &dummy : nullptr, n, H, W, C, bins, rule->hist_mode, &sh))
+    return 0;
+  const RulePlan rp = plan_rule(sh, rule);
+  Arena ar;
+  carve(ar, sh, rp, true);
+  return ar.bytes();
+}
+
+int cofie_ngff_histogram(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                         int32_t bins, int32_t hist_mode, uint32_t* out_hist, void* stream) {
+  clear_error();
+  NgffShape sh;
+  int rc = validate_frames(frames, n, H, W, C, bins, hist_mode, &sh);
+  if (rc) return rc;
+  if (n > 0 && !out_hist) return set_error(COFIE_EINVAL, "out_hist is NULL");
+  return run_histogram(frames, sh, out_hist, static_cast<hipStream_t>(stream));
+}
+
+int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                      int32_t bins, const cofie_keep_rule* keep_rule, float* out_scores,
+                      uint8_t* out_mask, void* stream) {
+  clear_error();
+  int rc = validate_rule(keep_rule);
+  if (rc) return rc;
+  NgffShape sh;
+  rc = validate_frames(frames, n, H, W, C, bins, keep_rule->hist_mode, &sh);
+  if (rc) return rc;
+  if (n > 0 && (!out_scores || !out_mask))
+    return set_error(COFIE_EINVAL, "out_scores / out_mask is NULL");
+  if (n == 0) return COFIE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const RulePlan rp = plan_rule(sh, keep_rule);
+  const bool need_hist = keep_rule->out_hist == nullptr;
+  Arena plan;
+  carve(plan, sh, rp, need_hist);
+  Scratch scratch;
+  rc = scratch.acquire(keep_rule->workspace, keep_rule->workspace_bytes, plan.bytes(), s);
+  if (rc) return rc;
+  Arena ar;
+  ar.base = scratch.ptr();
+  NgffScratch w = carve(ar, sh, rp, need_hist);
+  uint32_t* hist = need_hist ? w.hist : keep_rule->out_hist;
+
+  rc = run_histogram(frames, sh, hist, s);
+  if (rc) return rc;
+  rc = run_band(hist, sh, rp, w.band, s);
+  if (rc) return rc;
+  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
+  if (rp.gap_rule) {
+    rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0, s,
+                ra, w.next);
+    if (rc) return rc;
+    const size_t lds = (size_t)rp.seg_len * 5 + 16;
+    if (lds <= 96 * 1024) {
+      rc = allow_lds(ngff_select_kernel<true>, lds);
+      if (rc) return rc;
+      rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(1024), lds,
+                  s, ra, (const int32_t*)w.next, w.flags, out_scores, out_mask, keep_rule->out_count);
+    } else {
+      rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(1024), 0, s,
+                  ra, (const int32_t*)w.next, w.flags, out_scores, out_mask, keep_rule->out_count);
+    }
+  } else {
+    rc = launch("ngff_select_seq", ngff_select_seq_kernel, dim3((unsigned)rp.nseg), dim3(256), 0, s,
+                ra, (const uint32_t*)hist, (int32_t)sh.nbins, w.flags, out_scores, out_mask,
+                keep_rule->out_count);
+  }
+  return rc;
+}
+
+int cofie_ngff_calibrate(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
+                         int32_t bins, const cofie_keep_rule* keep_rule,
+                         int64_t target_per_segment, float* out_tau, void* stream) {
+  clear_error();
+  if (!keep_rule) return set_error(COFIE_EINVAL, "keep_rule is NULL");
+  if (keep_rule->segment_len < 0) return set_error(COFIE_EINVAL, "segment_len is negative");
+  if (keep_rule->M_min < 0) return set_error(COFIE_EINVAL, "M_min is negative");
+  NgffShape sh;
+  int rc = validate_frames(frames, n, H, W, C, bins, keep_rule->hist_mode, &sh);
+  if (rc) return rc;
+  if (keep_rule->L_max < 1)
+    return set_error(COFIE_EUNSUPPORTED, "calibration needs L_max >= 1");
+  if (target_per_segment < 0) return set_error(COFIE_EINVAL, "negative target");
+  if (n > 0 && !out_tau) return set_error(COFIE_EINVAL, "out_tau is NULL");
+  if (n == 0) return COFIE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const RulePlan rp = plan_rule(sh, keep_rule);
+  Arena plan;
+  carve(plan, sh, rp, true);
+  Scratch scratch;
+  rc = scratch.acquire(keep_rule->workspace, keep_rule->workspace_bytes, plan.bytes(), s);
+  if (rc) return rc;
+  Arena ar;
+  ar.base = scratch.ptr();
+  NgffScratch w = carve(ar, sh, rp, true);
+  rc = run_histogram(frames, sh, w.hist, s);
+  if (rc) return rc;
+  rc = run_band(w.hist, sh, rp, w.band, s);
+  if (rc) return rc;
+  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
+  const int64_t twoM = 2 * sh.mass;
+  rc = launch("ngff_calib_init", calib_init_kernel, dim3((unsigned)ceil_div(rp.nseg, 256)), dim3(256),
+              0, s, w.best, rp.nseg, twoM);
+  if (rc) return rc;
+  const int64_t ncand = sh.n * rp.L + 2 * rp.nseg;
+  rc = launch("ngff_calib", calib_kernel, dim3((unsigned)ceil_div(ncand, 256)), dim3(256), 0, s, ra,
+              rp.nseg, target_per_segment, w.best);
+  if (rc) return rc;
+  return launch("ngff_calib_final", calib_final_kernel, dim3((unsigned)ceil_div(rp.nseg, 256)),
+                dim3(256), 0, s, (const int32_t*)w.best, rp.nseg, twoM, out_tau);
+}
+
+}  // extern "C"

@@ -1,0 +1,176 @@
+// Host runtime of libcofie: thread-local error strings, the event-based kernel
+// timer, the scratch arena and device queries.
+#include <cstdarg>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace cofie {
+
+// ---- errors -------------------------------------------------------------------
+static thread_local char g_err[512] = "";
+
+int set_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+void clear_error() { g_err[0] = '\0'; }
+
+// ---- kernel timing ------------------------------------------------------------
+namespace {
+struct Record {
+  std::string name;
+  hipEvent_t start, stop;
+};
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<Record> recs;        // events recorded since the last reset
+  std::vector<hipEvent_t> spare;   // events kept for reuse
+  hipEvent_t get() {
+    if (!spare.empty()) {
+      hipEvent_t e = spare.back();
+      spare.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Profiler& prof() {
+  static Profiler* p = new Profiler();  // never destroyed: events outlive static teardown
+  return *p;
+}
+}  // namespace
+
+int prof_begin(const char* name, hipStream_t s) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  if (!p.on) return -1;
+  hipEvent_t a = p.get(), b = p.get();
+  if (!a || !b) return -1;
+  if (hipEventRecord(a, s) != hipSuccess) {
+    p.spare.push_back(a);
+    p.spare.push_back(b);
+    return -1;
+  }
+  p.recs.push_back({name, a, b});
+  return (int)p.recs.size() - 1;
+}
+
+void prof_end(int slot, hipStream_t s) {
+  if (slot < 0) return;
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  if (slot < (int)p.recs.size()) (void)hipEventRecord(p.recs[slot].stop, s);
+}
+
+// ---- scratch ------------------------------------------------------------------
+static void raise_pool_threshold(hipStream_t) {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return;
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) != hipSuccess) return;
+    uint64_t keep = ~uint64_t(0);  // keep freed blocks in the pool between calls
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  });
+}
+
+int Scratch::acquire(void* ws, size_t ws_bytes, size_t need, hipStream_t s) {
+  if (ws) {
+    if (ws_bytes < need)
+      return set_error(COFIE_ENOMEM, "workspace of %zu bytes is smaller than the %zu required",
+                       ws_bytes, need);
+    base_ = static_cast<char*>(ws);
+    return COFIE_OK;
+  }
+  if (need == 0) return COFIE_OK;
+  raise_pool_threshold(s);
+  void* p = nullptr;
+  hipError_t e = hipMallocAsync(&p, need, s);
+  if (e != hipSuccess || !p)
+    return set_error(COFIE_ENOMEM, "hipMallocAsync(%zu) failed: %s", need, hipGetErrorString(e));
+  base_ = static_cast<char*>(p);
+  owned_ = true;
+  stream_ = s;
+  return COFIE_OK;
+}
+
+Scratch::~Scratch() {
+  if (owned_ && base_) (void)hipFreeAsync(base_, stream_);
+}
+
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
+
+}  // namespace cofie
+
+// ---- exported profiler / error API ------------------------------------------------
+extern "C" {
+
+const char* cofie_last_error(void) { return cofie::g_err; }
+
+const char* cofie_version(void) { return "cofie-mi355x 0.1.0 (gfx950)"; }
+
+int cofie_profiler_enable(int on) {
+  auto& p = cofie::prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  p.on = on != 0;
+  return COFIE_OK;
+}
+
+int cofie_profiler_reset(void) {
+  auto& p = cofie::prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  for (auto& r : p.recs) {
+    (void)hipEventSynchronize(r.stop);
+    p.spare.push_back(r.start);
+    p.spare.push_back(r.stop);
+  }
+  p.recs.clear();
+  return COFIE_OK;
+}
+
+int cofie_profiler_read(const char* name_substr, double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return cofie::set_error(COFIE_EINVAL, "null output pointer");
+  auto& p = cofie::prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  double sum = 0;
+  int64_t cnt = 0;
+  for (auto& r : p.recs) {
+    if (name_substr && !strstr(r.name.c_str(), name_substr)) continue;
+    if (hipEventSynchronize(r.stop) != hipSuccess)
+      return cofie::set_error(COFIE_EHIP, "event synchronisation failed");
+    float ms = 0;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+      return cofie::set_error(COFIE_EHIP, "hipEventElapsedTime failed");
+    sum += ms;
+    ++cnt;
+  }
+  *total_ms = sum;
+  *launches = cnt;
+  return COFIE_OK;
+}
+
+}  // extern "C"

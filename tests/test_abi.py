@@ -1,0 +1,168 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, its host helpers match the paper's printed values, and every
+host-side validation error is reported before any GPU work."""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+
+from paper_2609_03675_amd import binding as B
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:  # pragma: no cover
+        return True
+
+
+@pytest.fixture(scope="module")
+def L():
+    return B.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = B.declared_functions()
+    assert len(names) >= 16
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version(L):
+    assert b"gfx950" in L.cofie_version()
+
+
+def test_drop_ratio_compositions_printed_in_paper():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "drop_ratio_compositions.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 12
+    for r in rows:
+        dn, dq, printed = float(r[0]) / 100, float(r[1]) / 100, float(r[2])
+        total = 100 * B.cofie_drop_total(dn, dq)
+        assert abs(total - printed) <= 0.5 + 1e-9, r
+    assert B.cofie_drop_total(0.2, 0.375) == pytest.approx(0.5, abs=1e-15)
+
+
+def test_paper_defaults(L):
+    vals = {l.split()[0]: l.split()[1] for l in open(os.path.join(GOLDEN, "paper_defaults.txt"))
+            if l.strip() and not l.startswith("#")}
+    r = B.KeepRule()
+    L.cofie_keep_rule_default(ctypes.byref(r))
+    assert r.M_min == int(vals["M_min"]) and r.L_max == int(vals["L_max"])
+    assert r.tau_h == np.float32(float(vals["tau_h"]))
+    assert r.hist_mode == B.GRAY and r.segment_len == 0
+    assert B.cofie_ngff_nbins("gray", int(vals["bins"])) == 32
+
+
+def test_k_from_ratio_eq8():
+    """k = max(1, round(rho |S_c|)) (Eq. 8), half to even."""
+    assert B.cofie_qer_k_from_ratio(0.5, 256) == 128
+    assert B.cofie_qer_k_from_ratio(0.3, 1024) == 307
+    assert B.cofie_qer_k_from_ratio(0.01, 10) == 1
+    assert B.cofie_qer_k_from_ratio(0.5, 5) == 2     # 2.5 -> 2
+    assert B.cofie_qer_k_from_ratio(0.5, 7) == 4     # 3.5 -> 4
+    assert B.cofie_qer_k_from_ratio(0.4, 0) == 0
+    assert B.cofie_qer_k_from_ratio(-0.1, 10) == -1
+
+
+def test_nbins():
+    assert B.cofie_ngff_nbins("per_channel", 32) == 96
+    assert B.cofie_ngff_nbins("joint3d", 8) == 512
+    assert B.cofie_ngff_nbins("gray", 32) == 32
+    assert B.cofie_ngff_nbins(7, 32) == 0
+
+
+def test_workspace_sizes_are_host_only():
+    r = B.keep_rule("per_channel", L_max=30, segment_len=512)
+    ws = B.ngff_workspace_bytes(16384, 448, 448, 3, 32, r)
+    assert ws >= 16384 * (96 + 30 + 1) * 4  # hist + band + next
+    assert B.ngff_workspace_bytes(16, 448, 448, 3, 33, r) == 0   # invalid bins
+    d = B.qer_desc(32, 32768, 128, 28, 28, 128)
+    assert B.qer_workspace_bytes(d, 16) >= 32768 * 4
+    g = B.qer_desc(48, 58800, 300, 28, 4, 128)
+    assert B.qer_workspace_bytes(g, 24) >= 58800 * 4 + 3 * 48 * 512 * 2
+    assert B.qer_workspace_bytes(B.qer_desc(32, 10, 2, 28, 5, 128), 4) == 0  # H_q % H_kv
+
+
+# Every case below is rejected by host validation before any HIP call; the
+# fake pointer is never dereferenced.  Skipped where a GPU exists so that a
+# validation bug can never turn into a device access.
+FAKE = 0x1000
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+@pytest.mark.parametrize("args,code", [
+    ((None, 4, 8, 8, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),        # frames NULL
+    ((FAKE, -1, 8, 8, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),       # n < 0
+    ((FAKE, 4, 0, 8, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),        # H = 0
+    ((FAKE, 4, 8, 8, 2, 32, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),        # C = 2
+    ((FAKE, 4, 8, 8, 1, 32, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),        # C = 1 needs GRAY
+    ((FAKE, 4, 8, 8, 3, 32, 9, FAKE), B.COFIE_EINVAL),                     # bad mode
+    ((FAKE, 4, 8, 8, 3, 1, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),         # bins < 2
+    ((FAKE, 4, 8, 8, 3, 512, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),       # bins > 256
+    ((FAKE, 4, 8, 8, 3, 24, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # not a power of two
+    ((FAKE, 4, 8, 8, 3, 32, B.JOINT3D, FAKE), B.COFIE_EUNSUPPORTED),      # 32^3 bins
+    ((FAKE, 4, 2000, 2000, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # 2M >= 2^24
+    ((FAKE, 4, 8, 8, 3, 32, B.PER_CHANNEL, None), B.COFIE_EINVAL),        # out NULL
+])
+def test_histogram_validation(L, args, code):
+    assert L.cofie_ngff_histogram(*args, None) == code
+    assert L.cofie_last_error()
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+def test_filter_validation(L):
+    r = B.KeepRule()
+    L.cofie_keep_rule_default(ctypes.byref(r))
+    assert L.cofie_ngff_filter(FAKE, 4, 8, 8, 3, 32, None, FAKE, FAKE, None) == B.COFIE_EINVAL
+    r.tau_h = float("nan")
+    assert L.cofie_ngff_filter(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), FAKE, FAKE, None) == B.COFIE_EINVAL
+    r.tau_h = 0.3
+    r.M_min = -1
+    assert L.cofie_ngff_filter(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), FAKE, FAKE, None) == B.COFIE_EINVAL
+    r.M_min = 4
+    r.segment_len = -5
+    assert L.cofie_ngff_filter(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), FAKE, FAKE, None) == B.COFIE_EINVAL
+    r.segment_len = 0
+    assert L.cofie_ngff_filter(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), None, FAKE, None) == B.COFIE_EINVAL
+    # n = 0 is a valid no-op that touches nothing
+    assert L.cofie_ngff_filter(None, 0, 8, 8, 3, 32, ctypes.byref(r), None, None, None) == B.COFIE_OK
+    r.L_max = 0
+    assert L.cofie_ngff_calibrate(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), 2, FAKE, None) == B.COFIE_EUNSUPPORTED
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+@pytest.mark.parametrize("field,value,code", [
+    ("n_q", 0, B.COFIE_EINVAL),
+    ("n_vis", -1, B.COFIE_EINVAL),
+    ("H_kv", 3, B.COFIE_EINVAL),          # 28 % 3
+    ("d", 24, B.COFIE_EUNSUPPORTED),      # not a multiple of 16
+    ("dtype", 5, B.COFIE_EINVAL),
+    ("score_mode", 7, B.COFIE_EINVAL),
+])
+def test_qer_validation(L, field, value, code):
+    d = B.qer_desc(32, 64, 4, 28, 28, 128)
+    setattr(d, field, value)
+    assert L.cofie_qer_rank(FAKE, FAKE, FAKE, ctypes.byref(d), 2, FAKE, FAKE, None) == code
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+def test_qer_null_and_alignment_validation(L):
+    d = B.qer_desc(32, 64, 4, 28, 28, 128)
+    assert L.cofie_qer_rank(None, FAKE, FAKE, ctypes.byref(d), 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE, None, FAKE, ctypes.byref(d), 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE, FAKE, None, ctypes.byref(d), 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE, FAKE, FAKE, ctypes.byref(d), 2, FAKE, None, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE, FAKE, FAKE, ctypes.byref(d), -1, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE + 4, FAKE, FAKE, ctypes.byref(d), 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank(FAKE, FAKE, FAKE, None, 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+
+
+def test_diag_copy_validation(L):
+    assert L.cofie_diag_stream_copy(FAKE, FAKE, 0, None) == B.COFIE_OK
+    if _no_gpu():
+        assert L.cofie_diag_stream_copy(FAKE, FAKE + 8, 32, None) == B.COFIE_EINVAL

@@ -1,0 +1,224 @@
+"""GPU parity of NGFF (Sec. 3.2) against the CPU oracle through the C ABI:
+histogram counts, keep masks, scores, kept counts and calibrated thresholds
+must be bit-identical."""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_03675_amd import binding as B
+from paper_2609_03675_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import hist_np, require_gpu, to_dev  # noqa: E402
+
+MODES = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    B.lib()
+
+
+def gpu_hist(frames, bins, mode):
+    h = B.cofie_ngff_histogram(to_dev(frames), bins, mode)
+    torch.cuda.synchronize()
+    return hist_np(h)
+
+
+# ---------------------------------------------------------------- histogram --
+
+@pytest.mark.parametrize("shape", [(3, 64, 64, 3),     # whole 768-byte units only
+                                   (2, 40, 40, 3),     # units + pixel tail
+                                   (3, 37, 53, 3),     # frame bytes not a multiple of 4
+                                   (5, 448, 448, 3),   # several workgroups per frame
+                                   (1, 1, 1, 3)])
+@pytest.mark.parametrize("mode,bins", [("per_channel", 32), ("per_channel", 16), ("per_channel", 64),
+                                       ("per_channel", 2), ("joint3d", 8), ("joint3d", 4),
+                                       ("joint3d", 16), ("gray", 32), ("gray", 256)])
+def test_histogram_bit_exact(shape, mode, bins):
+    print(f"hist shape={shape} mode={mode} bins={bins}", flush=True)
+    f = synth.random_frames(zlib.crc32(repr((shape, mode, bins)).encode()) % 1000, *shape)
+    assert np.array_equal(gpu_hist(f, bins, mode), oracle.histogram(f, bins, MODES[mode]))
+
+
+@pytest.mark.parametrize("shape", [(4, 64, 64), (3, 37, 53), (2, 448, 448)])
+@pytest.mark.parametrize("bins", [32, 256, 8])
+def test_histogram_gray_single_channel(shape, bins):
+    f = synth.random_frames(7, *shape, C=1)[..., 0]
+    assert np.array_equal(gpu_hist(f, bins, "gray"), oracle.histogram(f, bins, oracle.GRAY))
+
+
+def test_histogram_extreme_values():
+    """All-0 and all-255 frames, and every byte value, land in the edge bins."""
+    f = np.zeros((3, 16, 48, 3), dtype=np.uint8)
+    f[1] = 255
+    f[2] = np.arange(16 * 48 * 3).reshape(16, 48, 3) % 256
+    for mode, bins in [("per_channel", 32), ("joint3d", 8), ("gray", 32)]:
+        assert np.array_equal(gpu_hist(f, bins, mode), oracle.histogram(f, bins, MODES[mode]))
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_histogram_workloads(cfg):
+    wl = synth.WORKLOADS[cfg]
+    f = synth.frames(cfg)
+    assert np.array_equal(gpu_hist(f, wl.bins, wl.hist_mode),
+                          oracle.histogram(f, wl.bins, MODES[wl.hist_mode]))
+
+
+def test_histogram_empty_batch():
+    out = torch.zeros((1, 96), dtype=torch.int32, device="cuda")
+    B.cofie_ngff_histogram(torch.zeros((0, 8, 8, 3), dtype=torch.uint8, device="cuda"), 32,
+                           "per_channel", out=out)
+    torch.cuda.synchronize()
+    assert int(out.abs().sum()) == 0
+
+
+def test_histogram_deterministic():
+    f = to_dev(synth.frames(2, 0, 0, 16))
+    a = hist_np(B.cofie_ngff_histogram(f, 32, "per_channel"))
+    b = hist_np(B.cofie_ngff_histogram(f, 32, "per_channel"))
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------------------ filter --
+
+def run_filter(frames, bins, mode, tau, L_max=30, M_min=4, seg_len=0, tau_per_segment=None):
+    n = frames.shape[0]
+    nseg = 1 if seg_len <= 0 else (n + seg_len - 1) // seg_len
+    fd = to_dev(frames)
+    nb = B.cofie_ngff_nbins(mode, bins)
+    hist = torch.empty((n, nb), dtype=torch.int32, device="cuda")
+    count = torch.empty(nseg, dtype=torch.int32, device="cuda")
+    tps = to_dev(np.asarray(tau_per_segment, dtype=np.float32)) if tau_per_segment is not None else None
+    rule = B.keep_rule(mode, tau, L_max, M_min, seg_len, tau_per_segment=tps, out_hist=hist,
+                       out_count=count)
+    s, m = B.cofie_ngff_filter(fd, bins, rule)
+    torch.cuda.synchronize()
+    return s.cpu().numpy(), m.cpu().numpy(), hist_np(hist), count.cpu().numpy()
+
+
+def oracle_filter(frames, bins, mode, tau, L_max=30, M_min=4, seg_len=0):
+    h = oracle.histogram(frames, bins, MODES[mode])
+    H, W = frames.shape[1:3]
+    M = oracle.mass(MODES[mode], H, W)
+    s, m, k = oracle.ngff_select(h, M, tau, L_max, M_min, seg_len)
+    return s, m, h, k
+
+
+def assert_filter_equal(g, o):
+    s, m, h, c = g
+    so, mo, ho, ko = o
+    assert np.array_equal(h, ho), "histograms differ"
+    assert np.array_equal(m, mo), f"masks differ at {np.flatnonzero(m != mo)[:10]}"
+    assert np.array_equal(s.view(np.uint32), so.view(np.uint32)), \
+        f"scores differ at {np.flatnonzero(s != so)[:10]}"
+    assert np.array_equal(c, ko.astype(np.int32))
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_filter_workload_calibrated(cfg):
+    """Workload streams with the retention threshold the oracle calibrates."""
+    wl = synth.WORKLOADS[cfg]
+    f = synth.frames(cfg)
+    h = oracle.histogram(f, wl.bins, MODES[wl.hist_mode])
+    M = oracle.mass(MODES[wl.hist_mode], wl.H, wl.W)
+    theta, tau = oracle.ngff_calibrate(h, M, wl.target, 30, 4)
+    g = run_filter(f, wl.bins, wl.hist_mode, float(tau[0]))
+    o = oracle_filter(f, wl.bins, wl.hist_mode, tau[0])
+    assert_filter_equal(g, o)
+    assert g[3][0] <= wl.target
+
+
+@pytest.mark.parametrize("tau", [0.0, 0.05, 0.3, 0.9, 1.5, -1.0])
+@pytest.mark.parametrize("L_max,M_min", [(30, 4), (1, 4), (7, 0), (0, 4), (0, 0), (200, 50)])
+def test_filter_rule_edges(tau, L_max, M_min):
+    f = synth.random_frames(21, 70, 12, 16, scenes=9)
+    assert_filter_equal(run_filter(f, 16, "per_channel", tau, L_max, M_min),
+                        oracle_filter(f, 16, "per_channel", np.float32(tau), L_max, M_min))
+
+
+@pytest.mark.parametrize("T", [1, 2, 3])
+def test_filter_short_streams(T):
+    f = synth.random_frames(22, T, 8, 8)
+    assert_filter_equal(run_filter(f, 32, "per_channel", 0.3),
+                        oracle_filter(f, 32, "per_channel", np.float32(0.3)))
+
+
+def test_filter_static_and_alternating():
+    static = np.full((100, 8, 8, 3), 77, dtype=np.uint8)
+    g = run_filter(static, 32, "gray", 0.3)
+    assert np.flatnonzero(g[1]).tolist() == [0, 30, 60, 90, 99]
+    assert_filter_equal(g, oracle_filter(static, 32, "gray", np.float32(0.3)))
+    alt = np.zeros((20, 8, 8, 3), dtype=np.uint8)
+    alt[1::2] = 255
+    g = run_filter(alt, 32, "per_channel", 1.0)
+    assert g[1].all()
+
+
+@pytest.mark.parametrize("seg_len,n", [(40, 160), (40, 150), (512, 1100)])
+def test_filter_segments_per_stream_tau(seg_len, n):
+    f = synth.random_frames(23, n, 6, 10, scenes=12)
+    nseg = (n + seg_len - 1) // seg_len
+    taus = np.linspace(0.05, 0.6, nseg).astype(np.float32)
+    g = run_filter(f, 16, "per_channel", 0.3, L_max=9, M_min=3, seg_len=seg_len, tau_per_segment=taus)
+    o = oracle_filter(f, 16, "per_channel", taus, L_max=9, M_min=3, seg_len=seg_len)
+    assert_filter_equal(g, o)
+
+
+@pytest.mark.parametrize("mode,bins", [("joint3d", 8), ("gray", 32), ("per_channel", 32)])
+def test_filter_modes(mode, bins):
+    f = synth.random_frames(24, 50, 30, 20, scenes=7)
+    assert_filter_equal(run_filter(f, bins, mode, 0.2, L_max=12),
+                        oracle_filter(f, bins, mode, np.float32(0.2), L_max=12))
+
+
+def test_filter_long_segment_global_scratch_path():
+    """A stream too long for the select kernel's LDS copy (next[] in global memory)."""
+    f = synth.random_frames(25, 24000, 2, 2, scenes=60)
+    assert_filter_equal(run_filter(f, 8, "per_channel", 0.4, L_max=5),
+                        oracle_filter(f, 8, "per_channel", np.float32(0.4), L_max=5))
+
+
+def test_filter_deterministic_and_workspace():
+    f = synth.frames(2, 0, 0, 64)
+    fd = to_dev(f)
+    rule = B.keep_rule("per_channel", 0.2, 30, 4)
+    nbytes = B.ngff_workspace_bytes(64, 448, 448, 3, 32, rule)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    rule2 = B.keep_rule("per_channel", 0.2, 30, 4, workspace=ws)
+    s1, m1 = B.cofie_ngff_filter(fd, 32, rule)
+    s2, m2 = B.cofie_ngff_filter(fd, 32, rule2)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(m1, m2)
+    small = torch.empty(max(nbytes // 2, 1), dtype=torch.uint8, device="cuda")
+    with pytest.raises(B.CofieError) as e:
+        B.cofie_ngff_filter(fd, 32, B.keep_rule("per_channel", 0.2, 30, 4, workspace=small))
+    assert e.value.code == B.COFIE_ENOMEM
+
+
+# ------------------------------------------------------------- calibration --
+
+@pytest.mark.parametrize("case", ["tiny", "random", "segments", "1fps"])
+def test_calibration_matches_oracle(case):
+    if case == "tiny":
+        wl = synth.WORKLOADS[1]
+        f, bins, mode, target, seg, L = synth.frames(1), wl.bins, wl.hist_mode, wl.target, 0, 30
+    elif case == "1fps":
+        wl = synth.WORKLOADS[2]
+        f, bins, mode, target, seg, L = synth.frames(2), wl.bins, wl.hist_mode, wl.target, 0, 30
+    elif case == "random":
+        f, bins, mode, target, seg, L = synth.random_frames(31, 90, 6, 6, scenes=20), 8, "per_channel", 30, 0, 6
+    else:
+        f, bins, mode, target, seg, L = synth.random_frames(32, 200, 6, 6, scenes=40), 16, "joint3d", 12, 50, 8
+    n, H, W = f.shape[:3]
+    h = oracle.histogram(f, bins, MODES[mode])
+    M = oracle.mass(MODES[mode], H, W)
+    theta, tau_o = oracle.ngff_calibrate(h, M, target, L, 4, seg)
+    rule = B.keep_rule(mode, 0.3, L, 4, seg)
+    tau_g = B.cofie_ngff_calibrate(to_dev(f), bins, rule, target).cpu().numpy()
+    assert np.array_equal(tau_g.view(np.uint32), tau_o.view(np.uint32))

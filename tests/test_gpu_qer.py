@@ -1,0 +1,127 @@
+"""GPU parity of QER (Sec. 3.3, Eqs. 6-8) against the fp64 CPU oracle through
+the C ABI.  Frame scores within 1e-5 relative (fp32 inputs) or 2e-2 relative
+(bf16 MFMA path); top-k index sets identical except inside a group of
+reference scores tied within 1e-6."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_03675_amd import binding as B
+from paper_2609_03675_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import check_topk, qk_dev, rel_err, require_gpu, to_dev  # noqa: E402
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    B.lib()
+
+
+def run_case(Q, K, offs, H_q, H_kv, d, k_top, mode=B.LOGIT, scale=0.0, dtype="bf16"):
+    print(f"qer n_q={Q.shape[0]} n_vis={K.shape[0]} frames={len(offs)-1} H={H_q}/{H_kv} d={d} "
+          f"k={k_top} mode={mode} {dtype}", flush=True)
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs.astype(np.int32)), k_top,
+                              score_mode=mode, scale=scale)
+    torch.cuda.synchronize()
+    w = w.cpu().numpy()
+    idx = idx.cpu().numpy()
+    ref = oracle.qer_scores(Q, K, offs, H_q, H_kv, d, mode, scale)
+    err = rel_err(w, ref)
+    print(f"  max rel err {err:.3e}", flush=True)
+    assert err <= TOL[dtype], err
+    assert np.array_equal(np.isneginf(w), np.isneginf(ref)), "empty-frame scores differ"
+    check_topk(idx, ref, k_top)
+    return w, idx, ref
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_workload_scores_and_topk(cfg):
+    wl = synth.WORKLOADS[cfg]
+    Q, K, offs = synth.qer_inputs(cfg)
+    run_case(Q, K, offs, wl.H_q, wl.H_kv, wl.d, wl.k_top, dtype=wl.qk_dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_q,H_q,H_kv,d", [(20, 4, 4, 32),     # query rows not a multiple of 16
+                                            (80, 2, 2, 64),     # two query chunks (> 64 rows)
+                                            (16, 8, 2, 32),     # GQA fold
+                                            (48, 28, 4, 128),   # GQA, high-res workload heads
+                                            (3, 1, 1, 16),      # single head, d = 16
+                                            (33, 28, 28, 128)]) # long contraction (k-split)
+def test_shapes(dtype, n_q, H_q, H_kv, d):
+    tokens = [17, 0, 40, 1, 33, 64, 5, 0, 29]
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(n_q * 7 + d, n_q, int(offs[-1]), H_q, H_kv, d, dtype)
+    for k in (0, 1, 4, 9, 12):
+        run_case(Q, K, offs, H_q, H_kv, d, k, dtype=dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_q,H_q,H_kv,d", [(8, 4, 4, 32), (40, 4, 2, 16), (70, 2, 2, 32)])
+def test_softmax_mode(dtype, n_q, H_q, H_kv, d):
+    offs = synth.frame_offsets([12, 30, 0, 7, 64, 19])
+    Q, K = synth.random_qk(n_q + 3 * d, n_q, int(offs[-1]), H_q, H_kv, d, dtype)
+    run_case(Q, K, offs, H_q, H_kv, d, 3, mode=B.SOFTMAX, dtype=dtype)
+
+
+def test_explicit_scale():
+    offs = synth.frame_offsets([16] * 6)
+    Q, K = synth.random_qk(5, 16, 96, 4, 4, 32, "bf16")
+    run_case(Q, K, offs, 4, 4, 32, 2, scale=0.25)
+    run_case(Q, K, offs, 4, 4, 32, 2, mode=B.SOFTMAX, scale=0.25)
+
+
+def test_planted_frame_and_ties():
+    """A frame whose keys align with the mean query ranks first; identical
+    frames tie and resolve to the lower index."""
+    d, H = 32, 4
+    Q, K = synth.random_qk(9, 16, 160, H, H, d, "f32")
+    qbar = Q.mean(axis=0)
+    K[48:64] = 3.0 * qbar / np.linalg.norm(qbar, axis=-1, keepdims=True)
+    K[96:112] = K[0:16]  # frames 6 and 0 identical
+    offs = synth.frame_offsets([16] * 10)
+    w, idx, ref = run_case(Q, K, offs, H, H, d, 1, dtype="f32")
+    assert idx.tolist() == [3]
+    assert w[6] == w[0]
+
+
+def test_no_frames_no_tokens():
+    Q, K = synth.random_qk(1, 4, 8, 2, 2, 16, "bf16")
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(np.zeros(1, np.int32)), 3)
+    torch.cuda.synchronize()
+    assert idx.cpu().tolist() == [-1, -1, -1]
+    offs = np.array([0, 0, 0], np.int32)
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K[:0]), to_dev(offs), 1)
+    torch.cuda.synchronize()
+    assert np.isneginf(w.cpu().numpy()).all() and idx.cpu().tolist() == [0]
+
+
+def test_malformed_offsets_are_clamped():
+    """Offsets outside [0, n_vis] or inverted ranges read nothing out of bounds:
+    frame f covers [clamp(off[f]), max(that, clamp(off[f+1])))."""
+    Q, K = synth.random_qk(2, 4, 40, 2, 2, 16, "bf16")
+    offs = np.array([-5, 10, 4, 40, 1000], np.int32)
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs), 4)
+    torch.cuda.synchronize()
+    w = w.cpu().numpy()
+    spans = [(0, 10), (10, 10), (4, 40), (40, 40)]
+    ref = np.array([oracle.qer_scores(Q, K, np.array(sp, np.int32), 2, 2, 16)[0] for sp in spans])
+    assert rel_err(w, ref) <= 2e-2 and np.isneginf(w[1]) and np.isneginf(w[3])
+    check_topk(idx.cpu().numpy(), ref, 4)
+
+
+def test_deterministic_and_workspace():
+    Q, K, offs = synth.qer_inputs(2)
+    Qd, Kd, od = qk_dev(Q), qk_dev(K), to_dev(offs)
+    w1, i1 = B.cofie_qer_rank(Qd, Kd, od, 16)
+    desc = B.qer_desc(32, K.shape[0], 128, 28, 28, 128)
+    ws = torch.empty(B.qer_workspace_bytes(desc, 16), dtype=torch.uint8, device="cuda")
+    w2, i2 = B.cofie_qer_rank(Qd, Kd, od, 16, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(w1, w2) and torch.equal(i1, i2)
