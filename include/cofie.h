@@ -226,6 +226,12 @@ int cofie_profiler_read(const char* name_substr, double* total_ms, int64_t* laun
  * for the measurement of the kernels above. */
 int cofie_diag_stream_copy(const void* src, void* dst, size_t bytes, void* stream);
 
+/* Streaming read of `bytes` device bytes (16-byte aligned): the attainable
+ * read bandwidth, the ceiling of the read-dominated kernels above.  `sink`
+ * (device, sink_words >= 256 words) receives per-thread XORs of the data. */
+int cofie_diag_stream_read(const void* src, size_t bytes, uint32_t* sink, size_t sink_words,
+                           void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -103,6 +103,7 @@ def lib() -> ctypes.CDLL:
         "cofie_profiler_reset": (ctypes.c_int, []),
         "cofie_profiler_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(f64), ctypes.POINTER(i64)]),
         "cofie_diag_stream_copy": (ctypes.c_int, [P, P, sz, P]),
+        "cofie_diag_stream_read": (ctypes.c_int, [P, sz, P, sz, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -290,3 +291,9 @@ def cofie_diag_stream_copy(src, dst, stream=None) -> None:
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
     _check(lib().cofie_diag_stream_copy(_dev(src, "src"), _dev(dst, "dst"), nbytes, _stream(stream)))
+
+
+def cofie_diag_stream_read(src, sink, stream=None) -> None:
+    nbytes = src.numel() * src.element_size()
+    _check(lib().cofie_diag_stream_read(_dev(src, "src"), nbytes, _dev(sink, "sink"), sink.numel(),
+                                        _stream(stream)))

@@ -47,14 +47,21 @@ int launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, si
 }
 
 // Allow a kernel more than the default dynamic LDS (gfx950 has 160 KiB per CU).
+// The attribute is set once per kernel and size, so later calls (including
+// ones made while a stream is being captured into a graph) make no runtime call.
+bool lds_attr_done(const void* kernel, size_t bytes);
+void lds_attr_mark(const void* kernel, size_t bytes);
+
 template <typename... KArgs>
 int allow_lds(void (*kernel)(KArgs...), size_t bytes) {
   if (bytes <= 65536) return COFIE_OK;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  const void* k = reinterpret_cast<const void*>(kernel);
+  if (lds_attr_done(k, bytes)) return COFIE_OK;
+  hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   if (e != hipSuccess)
     return set_error(COFIE_EHIP, "hipFuncSetAttribute(LDS=%zu) failed: %s", bytes,
                      hipGetErrorString(e));
+  lds_attr_mark(k, bytes);
   return COFIE_OK;
 }
 

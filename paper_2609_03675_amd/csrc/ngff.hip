@@ -1,18 +1,20 @@
 // NGFF -- Novelty-Guided Frame Filtering (Sec. 3.2) on gfx950.
 //
 // Pipeline of one cofie_ngff_filter call (all on the caller's stream):
-//   [fill]   zero the histogram when several workgroups share a frame
-//   hist     streaming histogram: 12-byte coalesced loads (64 lanes x 12 B =
-//            768 contiguous bytes per wave instruction), byte -> bin in
-//            registers, increments into 64 lane-private LDS copies laid out
-//            bin-major ([bin][lane]) so that the lanes of one instruction
-//            always hit 64 distinct banks; one merge per workgroup
-//   band     exact integer L1 distances D(t, t-k), 1 <= k <= L_max, from
-//            histogram rows staged in LDS
-//   next     for every frame r, the frame the keep rule would keep next if r
-//            were the last kept frame (depends only on the band and theta)
-//   select   one workgroup per stream follows the next[] chain from frame 0,
-//            applies the M_min top-up and writes scores, mask and counts
+//   [fill]     zero the histogram when several workgroups share a frame
+//   hist       streaming histogram: 12-byte coalesced loads (64 lanes x 12 B =
+//              768 contiguous bytes per wave instruction), byte -> bin in
+//              registers, increments into 64 lane-private LDS copies laid out
+//              bin-major ([bin][lane]) so that the lanes of one instruction
+//              always hit 64 distinct banks; one merge per workgroup
+//   band_next  exact integer L1 distances D(t, t-k), 1 <= k <= L_max, from
+//              histogram rows staged in LDS, and for every frame r the frame
+//              the keep rule would keep next if r were the last kept frame
+//              (that depends only on the band and theta)
+//   select     one workgroup per stream follows the next[] chain from frame 0,
+//              applies the M_min top-up and writes scores, mask and counts
+// Without the gap rule (L_max <= 0) a sequential kernel per stream measures
+// D(t, r(t)) directly.
 // Novelty comparisons run on integers: s >= tau  <=>  max(D) >= theta with
 // theta = min{D : fl32(D)/fl32(2M) >= tau}, exact because fl32(D)/fl32(2M) is
 // strictly increasing in D for 2M < 2^24.  Scores are fl32(D)/fl32(2M), one
@@ -80,8 +82,6 @@ __device__ __forceinline__ void count12(uint32_t* cnt, const U3& v, uint32_t lan
         const uint32_t tb = (w[j] >> shift) & m4;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          constexpr int dummy = 0;
-          (void)dummy;
           const int c = (KIND == K_PC) ? ((4 * j + i) % 3) : 0;
           const uint32_t addr = __builtin_amdgcn_perm(tb, lane4, 0x0C0C0000u | ((4u + i) << 8));
           atomicAdd(reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(cnt) + addr) + c * BC * 64, 1u);
@@ -163,14 +163,28 @@ __global__ __launch_bounds__(1024) void ngff_hist_kernel(HistArgs a) {
     count_pixel<KIND, P, BC>(cnt, f + p * C, lane, a);
   __syncthreads();
 
+  // merge the P lane copies: J threads per bin each add P/J copies (rotated by
+  // the bin so that the lanes of a wave hit distinct banks), then combine
+  constexpr int J = P >= 8 ? 8 : P;
+  constexpr int PER = P / J;
   uint32_t* out = a.hist + t * a.nbins;
-  for (int b = tid; b < a.nbins; b += nthr) {
+  const int bins_per_pass = nthr / J;
+  const int j = tid % J;
+  for (int b0 = 0; b0 < a.nbins; b0 += bins_per_pass) {
+    const int b = b0 + tid / J;
     uint32_t sum = 0;
-    for (int l = 0; l < P; ++l) sum += cnt[b * P + ((l + b) & (P - 1))];
-    if (a.atomic) {
-      if (sum) atomicAdd(out + b, sum);
-    } else {
-      out[b] = sum;
+    if (b < a.nbins) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) sum += cnt[b * P + ((j * PER + i + b) & (P - 1))];
+    }
+#pragma unroll
+    for (int o = J / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, J);
+    if (j == 0 && b < a.nbins) {
+      if (a.atomic) {
+        if (sum) atomicAdd(out + b, sum);
+      } else {
+        out[b] = sum;
+      }
     }
   }
 }
@@ -234,19 +248,21 @@ __global__ __launch_bounds__(256) void ngff_band_kernel(BandArgs a) {
 }
 
 // Smallest integer D in [0, 2M+1] with fl32(D)/fl32(2M) >= tau, or 2M+2 if
-// none (NaN tau).  The quotient is strictly increasing in D, so a binary search
-// over the exact IEEE predicate finds it.
+// none (NaN tau, or tau above fl32(2M+1)/fl32(2M)).  With y = tau * 2M (exact
+// in fp64: a 24-bit mantissa times an integer below 2^24) every D >= y passes
+// and, because 1/2M exceeds half an fp32 ulp of tau, every D <= y - 1 fails;
+// so the answer is ceil(y) or ceil(y) - 1 and one exact IEEE test decides.
+// Straight-line code: no data-dependent loop for the compiler to expand.
 __device__ int64_t theta_of(float tau, int64_t twoM) {
   const float den = (float)twoM;
-  int64_t lo = 0, hi = twoM + 2;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (mid <= twoM + 1 && (float)mid / den >= tau)
-      hi = mid;
-    else
-      lo = mid + 1;
-  }
-  return lo;
+  if (!(tau == tau)) return twoM + 2;
+  if (tau <= 0.f) return 0;
+  const double y = (double)tau * (double)twoM;
+  if (y > (double)(twoM + 1))
+    return ((float)(int32_t)(twoM + 1) / den >= tau) ? twoM + 1 : twoM + 2;
+  const int64_t x = (int64_t)ceil(y);
+  if (x >= 1 && (float)(int32_t)(x - 1) / den >= tau) return x - 1;
+  return x;
 }
 
 struct RuleArgs {
@@ -288,6 +304,124 @@ __global__ void ngff_next_kernel(RuleArgs a, int32_t* next) {
   next[r] = (int32_t)u;
 }
 
+// Band and next[] in one pass.  A workgroup owns frames [t0, t0+TB): it stages
+// histogram rows [t0-L, t0+TB+L) in LDS, computes the band rows
+// [t0, t0+TB+L) there (the extra L rows are the look-ahead next[] needs),
+// writes its own band rows and next[r] for r in [t0, t0+TB).
+struct BandNextArgs {
+  const uint32_t* hist;
+  int64_t n;
+  int32_t nbins;
+  int32_t stride;  // LDS row stride in words (multiple of 4, >= nbins)
+  int32_t TB;
+  RuleArgs rule;   // band pointer = output band
+  int32_t* band;
+  int32_t* next;
+};
+
+__global__ __launch_bounds__(1024) void ngff_band_next_kernel(BandNextArgs a) {
+  extern __shared__ uint32_t sm[];
+  __shared__ int64_t theta_sh;
+  const int L = a.rule.L;
+  const int n = (int)a.n;
+  const int seg_len = (int)a.rule.seg_len;
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
+  const int t0 = blockIdx.x * a.TB;
+  const int r0 = t0 - L > 0 ? t0 - L : 0;
+  const int r1 = t0 + a.TB + L < n ? t0 + a.TB + L : n;  // histogram rows [r0, r1)
+  // histogram rows transposed in LDS: rows[b * RS + (r - r0)], so lanes that
+  // read consecutive frames of one bin touch consecutive words
+  const int RS = a.stride;
+  uint32_t* rows = sm;
+  int32_t* bl = reinterpret_cast<int32_t*>(sm + (size_t)a.nbins * RS);
+  {
+    // rows [r0, r1) are contiguous in global memory; all loads are issued
+    // before any store (indices past the end are clamped to 0 and rewrite
+    // element 0 with its own value)
+    const int total = (r1 - r0) * a.nbins;
+    const uint32_t* src = a.hist + (int64_t)r0 * a.nbins;
+    constexpr int V = 8;
+    for (int i0 = tid; i0 < total; i0 += V * nthr) {
+      uint32_t v[V];
+      int idx[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int i = i0 + j * nthr;
+        idx[j] = i < total ? i : 0;
+        v[j] = src[idx[j]];
+      }
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int r = idx[j] / a.nbins, b = idx[j] - r * a.nbins;
+        rows[b * RS + r] = v[j];
+      }
+    }
+  }
+  if (tid == 0) theta_sh = theta_of(tau_of_segment(a.rule, t0 / seg_len), a.rule.twoM);
+  __syncthreads();
+  // band rows [t0, r1): one wave per row; LPP lanes share one lag k, each
+  // adding a slice of the bins, combined with shuffles
+  int LPP = 1;
+  while (LPP < 16 && 2 * LPP * L <= 64) LPP <<= 1;
+  const int per_pass = 64 / LPP;  // lags per wave pass
+  const int sub = lane % LPP, kl = lane / LPP;
+  const int blo = (a.nbins * sub) / LPP, bhi = (a.nbins * (sub + 1)) / LPP;
+  for (int t = t0 + wave; t < r1; t += nw) {
+    const int seg0 = (t / seg_len) * seg_len;
+    const uint32_t* x = rows + (t - r0);
+    for (int kb = 0; kb < L; kb += per_pass) {
+      const int k = kb + kl + 1;
+      uint32_t D = 0;
+      if (k <= L && t - k >= seg0) {
+        const uint32_t* y = rows + (t - k - r0);
+#pragma unroll 8
+        for (int b = blo; b < bhi; ++b) {
+          const uint32_t u = x[b * RS], v = y[b * RS];
+          D += u > v ? u - v : v - u;
+        }
+      }
+      for (int o = 1; o < LPP; o <<= 1) D += __shfl_xor(D, o, LPP);
+      if (sub == 0 && k <= L) {
+        bl[(t - t0) * L + (k - 1)] = (int32_t)D;
+        if (t < t0 + a.TB) a.band[(int64_t)t * L + (k - 1)] = (int32_t)D;
+      }
+    }
+  }
+  __syncthreads();
+  // next[r]: one wave per r, lane k tests frame r+k, the first hit wins
+  const int tend = t0 + a.TB < n ? t0 + a.TB : n;
+  for (int r = t0 + wave; r < tend; r += nw) {
+    const int seg = r / seg_len, s0 = seg * seg_len;
+    const int T = n - s0 < seg_len ? n - s0 : seg_len;
+    const int rr = r - s0;
+    int nxt = T;
+    if (rr < T - 1) {
+      const int64_t theta = (seg == t0 / seg_len) ? theta_sh
+                                                   : theta_of(tau_of_segment(a.rule, seg), a.rule.twoM);
+      // the rule keeps frame rr + kmax at the latest (gap rule or last frame)
+      const int kmax = L < T - 1 - rr ? L : T - 1 - rr;
+      int found = kmax;
+      for (int kb = 1; kb <= kmax; kb += 64) {
+        const int k = kb + lane;
+        bool hit = false;
+        if (k < kmax) {
+          const int32_t* row = bl + (r + k - t0) * L;
+          const int32_t Dadj = row[0], Dref = row[k - 1];
+          hit = (Dadj > Dref ? Dadj : Dref) >= theta;
+        }
+        const uint64_t m = __ballot(hit);
+        if (m) {
+          found = kb + (int)__builtin_ctzll(m);
+          break;
+        }
+      }
+      nxt = rr + found;
+    }
+    if (lane == 0) a.next[r] = nxt;
+  }
+}
+
 // Is t one of the uniformly spaced top-up frames floor(i (T-1)/(m-1)), 0 <= i < m?
 __device__ __forceinline__ bool is_uniform(int64_t t, int64_t T, int64_t m) {
   if (T <= 1) return t == 0;
@@ -308,47 +442,94 @@ __device__ int64_t block_sum(int64_t v, int64_t* red) {
   return s;
 }
 
-// One workgroup per stream: follow next[] from frame 0, top up, score, mask.
-// flags: 1 = kept by the rule, 2 = added by the top-up.  next/flags live in LDS
-// when USE_LDS, else in the global scratch slices.
+// Block-wide inclusive prefix maximum (blockDim a multiple of 64, <= 1024).
+__device__ int block_inclusive_max(int v, int* wtmp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x = x > y ? x : y;
+  }
+  if (lane == 63) wtmp[wave] = x;
+  __syncthreads();
+  int before = -1;
+  for (int i = 0; i < wave; ++i) before = before > wtmp[i] ? before : wtmp[i];
+  __syncthreads();
+  return x > before ? x : before;
+}
+
+// One workgroup per stream.  The frames the rule keeps are the chain
+// 0 -> next[0] -> next[next[0]] -> ... -> T-1; it is marked by pointer
+// doubling: with J = next^(2^j), every marked frame also marks J of itself,
+// then J <- J o J, so after ceil(log2 T) + 1 rounds the whole chain is marked
+// (marks made early within a round are chain frames too).  r(t) is then a
+// prefix maximum of kept indices, and every frame's score is formed in
+// parallel.  next/J/flags/r live in LDS when USE_LDS, else in global scratch.
 template <bool USE_LDS>
 __global__ __launch_bounds__(1024) void ngff_select_kernel(RuleArgs a, const int32_t* next_g,
-                                                           uint8_t* flag_g, float* scores,
+                                                           uint8_t* flag_g, int32_t* jump_g,
+                                                           int32_t* rprev_g, float* scores,
                                                            uint8_t* mask, int32_t* count) {
   extern __shared__ int32_t lds_i[];
   __shared__ int64_t red[16];
-  __shared__ int64_t kept_sh;
+  __shared__ int wtmp[16];
   const int64_t seg = blockIdx.x, s0 = seg * a.seg_len;
-  const int64_t T = a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len;
+  const int T = (int)(a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len);
   const int tid = threadIdx.x, nthr = blockDim.x;
-  const int32_t* nx;
+  int32_t *J0, *J1, *rp;
   uint8_t* fl;
   if constexpr (USE_LDS) {
-    int32_t* nxl = lds_i;
-    fl = reinterpret_cast<uint8_t*>(lds_i + T);
-    for (int64_t i = tid; i < T; i += nthr) {
-      nxl[i] = next_g[s0 + i];
-      fl[i] = 0;
-    }
-    nx = nxl;
+    J0 = lds_i;
+    J1 = lds_i + T;
+    rp = lds_i + 2 * T;
+    fl = reinterpret_cast<uint8_t*>(lds_i + 3 * T);
   } else {
-    nx = next_g + s0;
+    J0 = rprev_g + s0;  // rp reuses J0's slice once the chain is marked
+    J1 = jump_g + s0;
+    rp = rprev_g + s0;
     fl = flag_g + s0;
-    for (int64_t i = tid; i < T; i += nthr) fl[i] = 0;
+  }
+  const float den = (float)a.twoM;
+  for (int t = tid; t < T; t += nthr) {
+    J0[t] = next_g[s0 + t];
+    fl[t] = t == 0;
   }
   __syncthreads();
-  if (tid == 0) {
-    int64_t r = 0, kept = 1;
-    fl[0] = 1;
-    while (r < T - 1) {
-      r = nx[r];
-      fl[r] = 1;
-      ++kept;
+  for (int span = 1; span < 2 * T; span <<= 1) {
+    for (int t = tid; t < T; t += nthr)
+      if (fl[t]) {
+        const int j = J0[t];
+        if (j < T) fl[j] = 1;
+      }
+    __syncthreads();
+    for (int t = tid; t < T; t += nthr) {
+      const int j = J0[t];
+      J1[t] = j < T ? J0[j] : T;
     }
-    kept_sh = kept;
+    __syncthreads();
+    int32_t* tmp = J0;
+    J0 = J1;
+    J1 = tmp;
   }
+  // r(t) = last kept frame before t: exclusive prefix max over chunks
+  const int chunk = (T + nthr - 1) / nthr;
+  const int c0 = tid * chunk, c1 = c0 + chunk < T ? c0 + chunk : T;
+  int last = -1;
+  for (int t = c0; t < c1; ++t)
+    if (fl[t]) last = t;
+  __shared__ int incl_sh[1024];
+  incl_sh[tid] = block_inclusive_max(last, wtmp);
   __syncthreads();
-  const int64_t kept = kept_sh;
+  int run = tid > 0 ? incl_sh[tid - 1] : -1;  // max over the chunks before this one
+  for (int t = c0; t < c1; ++t) {
+    rp[t] = run;
+    if (fl[t]) run = t;
+  }
+  // top-up when the rule kept fewer than M_min frames
+  int64_t local = 0;
+  for (int t = tid; t < T; t += nthr) local += fl[t] != 0;
+  const int64_t kept = block_sum(local, red);
   if (a.M_min >= 2 && kept < a.M_min) {
     for (int64_t i = tid; i < a.M_min; i += nthr) {
       const int64_t u = (i * (T - 1)) / (a.M_min - 1);
@@ -356,21 +537,19 @@ __global__ __launch_bounds__(1024) void ngff_select_kernel(RuleArgs a, const int
     }
   }
   __syncthreads();
-  const float den = (float)a.twoM;
-  int64_t local = 0;
-  for (int64_t t = tid; t < T; t += nthr) {
+  local = 0;
+  for (int t = tid; t < T; t += nthr) {
     const uint8_t f = fl[t];
     local += f != 0;
     mask[s0 + t] = f != 0;
-    float s = 1.0f;
+    float sc = 1.0f;
     if (t > 0) {
-      int64_t r = t - 1;
-      while (!(fl[r] & 1)) --r;  // last rule-kept frame before t (t - r <= L)
+      const int r = rp[t];  // t - r <= L: the gap rule bounds every jump
       const int32_t* row = a.band + (s0 + t) * a.L;
       const int32_t Dadj = row[0], Dref = row[t - r - 1];
-      s = (float)(Dadj > Dref ? Dadj : Dref) / den;
+      sc = (float)(Dadj > Dref ? Dadj : Dref) / den;
     }
-    scores[s0 + t] = s;
+    scores[s0 + t] = sc;
   }
   const int64_t total = block_sum(local, red);
   if (count && tid == 0) count[seg] = (int32_t)total;
@@ -576,13 +755,15 @@ HistPlan plan_hist(const NgffShape& sh, const uint8_t* frames) {
   p.P = 64;
   while ((size_t)sh.nbins * p.P * 4 > 160 * 1024) p.P >>= 1;
   p.lds = (size_t)sh.nbins * p.P * 4;
-  p.threads = p.lds <= 40 * 1024 ? 256 : (p.lds <= 80 * 1024 ? 512 : 1024);
+  p.threads = 1024;
   // the vector path needs 4-byte aligned frames
   const bool aligned = (reinterpret_cast<uintptr_t>(frames) % 4 == 0) && (sh.frame_bytes % 4 == 0);
   p.units = aligned ? (int)(sh.frame_bytes / kUnitBytes) : 0;
   const int nw = p.threads / 64;
-  const int64_t target = 8LL * device_cu_count();
-  int64_t splits = (target + sh.n - 1) / (sh.n > 0 ? sh.n : 1);
+  // one workgroup per frame when there are at least as many frames as CUs,
+  // otherwise split frames so that every CU streams
+  const int64_t cus = device_cu_count();
+  int64_t splits = sh.n >= cus ? 1 : (cus + sh.n - 1) / (sh.n > 0 ? sh.n : 1);
   const int64_t by_units = p.units / (nw * kUnroll);
   if (splits > by_units) splits = by_units;
   if (splits < 1) splits = 1;
@@ -664,6 +845,8 @@ struct NgffScratch {
   uint32_t* hist;
   int32_t* band;
   int32_t* next;
+  int32_t* rprev;
+  int32_t* jump;
   uint8_t* flags;
   int32_t* best;
 };
@@ -673,11 +856,14 @@ NgffScratch carve(Arena& ar, const NgffShape& sh, const RulePlan& rp, bool need_
   w.hist = need_hist ? ar.take<uint32_t>((size_t)(sh.n * sh.nbins)) : nullptr;
   w.band = ar.take<int32_t>((size_t)(sh.n * rp.L));
   w.next = ar.take<int32_t>((size_t)sh.n);
+  w.rprev = ar.take<int32_t>((size_t)sh.n);
+  w.jump = ar.take<int32_t>((size_t)sh.n);
   w.flags = ar.take<uint8_t>((size_t)sh.n);
   w.best = ar.take<int32_t>((size_t)(rp.nseg > 0 ? rp.nseg : 1));
   return w;
 }
 
+// Separate band kernel (rows read from global memory when they do not fit LDS).
 int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int32_t* band,
              hipStream_t s) {
   BandArgs b;
@@ -701,6 +887,13 @@ int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int3
   int rc = allow_lds(ngff_band_kernel, lds);
   if (rc) return rc;
   return launch("ngff_band", ngff_band_kernel, dim3((unsigned)ceil_div(sh.n, TB)), dim3(256), lds, s, b);
+}
+
+// LDS bytes of the fused band/next kernel for a tile of TB frames: the
+// transposed histogram rows (nbins x RS words, RS >= TB + 2L) and the band
+// rows of the tile plus look-ahead ((TB + L) x L words).
+size_t band_next_lds(const NgffShape& sh, int L, int TB, int RS) {
+  return (size_t)sh.nbins * RS * 4 + (size_t)(TB + L) * L * 4;
 }
 
 RuleArgs rule_args(const NgffShape& sh, const RulePlan& rp, const cofie_keep_rule* r,
@@ -803,24 +996,49 @@ int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, in
 
   rc = run_histogram(frames, sh, hist, s);
   if (rc) return rc;
-  rc = run_band(hist, sh, rp, w.band, s);
-  if (rc) return rc;
   RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
   if (rp.gap_rule) {
-    rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0, s,
-                ra, w.next);
+    int TB = 8;
+    auto rs_of = [&](int tb) { return tb + 2 * rp.L; };
+    while (TB > 1 && band_next_lds(sh, rp.L, TB, rs_of(TB)) > 150 * 1024) TB >>= 1;
+    const int stride = rs_of(TB);
+    const size_t lds_bn = band_next_lds(sh, rp.L, TB, stride);
+    if (lds_bn <= 150 * 1024) {
+      BandNextArgs bn;
+      bn.hist = hist;
+      bn.n = sh.n;
+      bn.nbins = (int32_t)sh.nbins;
+      bn.stride = stride;
+      bn.TB = TB;
+      bn.rule = ra;
+      bn.band = w.band;
+      bn.next = w.next;
+      rc = allow_lds(ngff_band_next_kernel, lds_bn);
+      if (rc) return rc;
+      rc = launch("ngff_band_next", ngff_band_next_kernel, dim3((unsigned)ceil_div(sh.n, TB)),
+                  dim3(1024), lds_bn, s, bn);
+    } else {
+      rc = run_band(hist, sh, rp, w.band, s);
+      if (rc) return rc;
+      rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0,
+                  s, ra, w.next);
+    }
     if (rc) return rc;
-    const size_t lds = (size_t)rp.seg_len * 5 + 16;
+    const size_t lds = (size_t)rp.seg_len * 13 + 16;
     if (lds <= 96 * 1024) {
       rc = allow_lds(ngff_select_kernel<true>, lds);
       if (rc) return rc;
       rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(1024), lds,
-                  s, ra, (const int32_t*)w.next, w.flags, out_scores, out_mask, keep_rule->out_count);
+                  s, ra, (const int32_t*)w.next, w.flags, w.jump, w.rprev, out_scores, out_mask,
+                  keep_rule->out_count);
     } else {
       rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(1024), 0, s,
-                  ra, (const int32_t*)w.next, w.flags, out_scores, out_mask, keep_rule->out_count);
+                  ra, (const int32_t*)w.next, w.flags, w.jump, w.rprev, out_scores, out_mask,
+                  keep_rule->out_count);
     }
   } else {
+    rc = run_band(hist, sh, rp, w.band, s);
+    if (rc) return rc;
     rc = launch("ngff_select_seq", ngff_select_seq_kernel, dim3((unsigned)rp.nseg), dim3(256), 0, s,
                 ra, (const uint32_t*)hist, (int32_t)sh.nbins, w.flags, out_scores, out_mask,
                 keep_rule->out_count);

@@ -14,9 +14,10 @@
 //   (KS) and add the partial tiles through LDS.  The epilogue takes the max
 //   over query rows (registers, then 16-lane shuffles) and writes
 //   m_j = scale * max_i S_ij: the text-by-vision matrix is never stored.
-// qer_rank: one workgroup: wave-per-frame fp64 means of m over V_f (Eq. 7),
-//   then a radix select of the top k by (score desc, frame asc) on
-//   order-preserving 32-bit keys, written in chronological order (Eq. 8).
+// qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7).
+// qer_topk: one workgroup ranks the frames by (score desc, frame asc) on
+//   order-preserving 32-bit keys (counting ranks in LDS, or a radix select for
+//   very many frames) and writes the top k in chronological order (Eq. 8).
 // SOFTMAX mode: per-(head, query) row statistics over all visual keys, merged
 //   across workgroups, then a second pass forming the head mean of the
 //   normalised probabilities and its max over query rows.
@@ -78,10 +79,45 @@ struct ScoreArgs {
   int32_t accumulate; // take the max with the m already stored (later query chunks)
 };
 
+// Loads of one batch of U macro steps starting at macro step `ms`.  Row
+// pointers are clamped to valid rows, so every load is unconditional; rows past
+// n_vis and query columns past n_q only produce tile entries that are never
+// stored.  A partial last macro step (Lc % KPS != 0) is handled separately.
+template <typename T, int NB, int P, int U>
+__device__ __forceinline__ void score_load(uint4 (&fa)[U][kMB], uint4 (&fb)[U][P][NB],
+                                           const uint4* const (&kp)[kMB],
+                                           const uint4* const (&qp)[P][NB], int ms) {
+  constexpr int STEP = Mma<T>::KPS * (int)sizeof(T) / 16;  // uint4 per macro step (= 4)
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb) fa[u][mb] = kp[mb][(ms + u) * STEP];
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) fb[u][p][nb] = qp[p][nb][(ms + u) * STEP];
+  }
+}
+
+template <typename T, int NB, int P, int U>
+__device__ __forceinline__ void score_mac(f32x4 (&acc)[kMB][NB], const uint4 (&fa)[U][kMB],
+                                          const uint4 (&fb)[U][P][NB]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+#pragma unroll
+      for (int mb = 0; mb < kMB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) Mma<T>::mac(acc[mb][nb], fa[u][mb], fb[u][p][nb]);
+}
+
 template <typename T, int NB, int P>
 __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
   using M = Mma<T>;
-  constexpr int U = (P * NB > 4) ? 2 : 4;  // macro steps in flight
+  // macro steps per batch: two batches of at most 8 loads stay within 128
+  // VGPRs, so four waves fit per SIMD
+  constexpr int U = (kMB + P * NB) <= 4 ? 2 : 1;
   __shared__ f32x4 part[4][kMB * NB][64];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -91,15 +127,14 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
   const int64_t tokbase = ((int64_t)blockIdx.x * TG + tg) * (kMB * 16);
   const int64_t rowbytes = (int64_t)a.Lc * sizeof(T);
 
-  const uint8_t* krow[kMB];
-  bool kok[kMB];
+  // lane's 16-byte column (g4) of its clamped rows
+  const uint4* kp[kMB];
 #pragma unroll
   for (int mb = 0; mb < kMB; ++mb) {
     const int64_t tok = tokbase + mb * 16 + r16;
-    kok[mb] = tok < a.n_vis;
-    krow[mb] = a.K + (kok[mb] ? tok : 0) * rowbytes;
+    kp[mb] = reinterpret_cast<const uint4*>(a.K + (tok < a.n_vis ? tok : 0) * rowbytes) + g4;
   }
-  const uint8_t* qrow[P][NB];
+  const uint4* qp[P][NB];
   bool qok[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -107,7 +142,8 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
     qok[nb] = q < a.n_q;
 #pragma unroll
     for (int p = 0; p < P; ++p)
-      qrow[p][nb] = a.Qp + ((int64_t)p * a.nq_total + a.q0 + (qok[nb] ? q : 0)) * rowbytes;
+      qp[p][nb] = reinterpret_cast<const uint4*>(
+                      a.Qp + ((int64_t)p * a.nq_total + a.q0 + (qok[nb] ? q : 0)) * rowbytes) + g4;
   }
 
   f32x4 acc[kMB][NB];
@@ -116,35 +152,59 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // this wave's macro steps [ms0, ms1); whole steps first, then the partial one
+  const int full = a.Lc / M::KPS;
   const int ms0 = ks * a.per_split;
   const int ms1 = ms0 + a.per_split < a.ksteps ? ms0 + a.per_split : a.ksteps;
-  const uint4 zero = {0u, 0u, 0u, 0u};
-  for (int ms = ms0; ms < ms1; ms += U) {
-    uint4 fa[U][kMB];
-    uint4 fb[U][P][NB];
+  const int msf = ms1 < full ? ms1 : full;
+  int ms = ms0;
+  if (ms + U <= msf) {
+    // software pipeline: batch i+1 is in flight while batch i is multiplied
+    uint4 fa[U][kMB], fb[U][P][NB];
+    score_load<T, NB, P, U>(fa, fb, kp, qp, ms);
+    for (; ms + 2 * U <= msf; ms += U) {
+      uint4 ga[U][kMB], gb[U][P][NB];
+      score_load<T, NB, P, U>(ga, gb, kp, qp, ms + U);
+      score_mac<T, NB, P, U>(acc, fa, fb);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int s = ms + u;
-      const int kk = s * M::KPS + g4 * M::EPL;
-      const bool kin = (s < ms1) && (kk < a.Lc);
-      const int64_t off = (int64_t)kk * sizeof(T);
+      for (int u = 0; u < U; ++u) {
 #pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
-        fa[u][mb] = (kin && kok[mb]) ? *reinterpret_cast<const uint4*>(krow[mb] + off) : zero;
+        for (int mb = 0; mb < kMB; ++mb) fa[u][mb] = ga[u][mb];
 #pragma unroll
-      for (int p = 0; p < P; ++p)
+        for (int p = 0; p < P; ++p)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          fb[u][p][nb] = (kin && qok[nb]) ? *reinterpret_cast<const uint4*>(qrow[p][nb] + off) : zero;
+          for (int nb = 0; nb < NB; ++nb) fb[u][p][nb] = gb[u][p][nb];
+      }
+    }
+    score_mac<T, NB, P, U>(acc, fa, fb);
+    ms += U;
+  }
+  for (; ms < msf; ++ms) {
+    uint4 fa[1][kMB], fb[1][P][NB];
+    score_load<T, NB, P, 1>(fa, fb, kp, qp, ms);
+    score_mac<T, NB, P, 1>(acc, fa, fb);
+  }
+  if (ms < ms1) {
+    // partial macro step (bf16 with Lc % 32 == 16): lane groups past Lc read the
+    // previous 16 bytes of their row and contribute zero
+    const bool in = ms * M::KPS + g4 * M::EPL < a.Lc;
+    const int back = in ? 0 : -2;  // uint4 offset back into the row
+    const uint4 zero = {0u, 0u, 0u, 0u};
+    constexpr int STEP = M::KPS * (int)sizeof(T) / 16;
+    uint4 fa[1][kMB], fb[1][P][NB];
+#pragma unroll
+    for (int mb = 0; mb < kMB; ++mb) {
+      const uint4 v = kp[mb][ms * STEP + back];
+      fa[0][mb] = in ? v : zero;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int p = 0; p < P; ++p)
 #pragma unroll
-      for (int p = 0; p < P; ++p)
-#pragma unroll
-        for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) M::mac(acc[mb][nb], fa[u][mb], fb[u][p][nb]);
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint4 v = qp[p][nb][ms * STEP + back];
+        fb[0][p][nb] = in ? v : zero;
+      }
+    score_mac<T, NB, P, 1>(acc, fa, fb);
   }
 
   if (a.KS > 1) {
@@ -237,8 +297,8 @@ __device__ __forceinline__ uint32_t order_key(float w) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exclusive prefix sum over the block (1024 threads = 16 waves); returns the
-// block total in *total.
+// Exclusive prefix sum over the block (blockDim a multiple of 64, <= 1024);
+// returns the block total in *total.
 __device__ int block_exscan(int v, int* total, int* wsum) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int x = v;
@@ -259,78 +319,116 @@ __device__ int block_exscan(int v, int* total, int* wsum) {
   return before + x - v;
 }
 
-__global__ __launch_bounds__(1024) void qer_rank_kernel(const float* m, int32_t n_vis,
-                                                        const int32_t* offs, int32_t n_frames,
-                                                        int32_t k_top, float* out_scores,
-                                                        int32_t* out_idx, uint32_t* keys) {
+// Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
+// fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
+__global__ __launch_bounds__(256) void qer_frame_mean_kernel(const float* m, int32_t n_vis,
+                                                             const int32_t* offs, int32_t n_frames,
+                                                             float* out_scores, uint32_t* keys) {
+  const int lane = threadIdx.x & 63;
+  const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (f >= n_frames) return;
+  int lo = offs[f], hi = offs[f + 1];
+  lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
+  hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
+  // four loads in flight per lane (clamped indices, masked adds)
+  double s = 0.0;
+  for (int j0 = lo + lane; j0 < hi; j0 += 256) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = j0 + 64 * u;
+      v[u] = m[j < hi ? j : lo];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s += (j0 + 64 * u < hi) ? (double)v[u] : 0.0;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) {
+    const float w = hi > lo ? (float)(s / (double)(hi - lo)) : -INFINITY;
+    out_scores[f] = w;
+    keys[f] = order_key(w);
+  }
+}
+
+constexpr int kRankMax = 4096;  // frames ranked by counting in LDS
+
+// Eq. 8: the k frames of largest score (ties to the lower index), written in
+// chronological order and padded with -1.  Up to kRankMax frames, every frame's
+// rank is counted against all keys held in LDS; above that, a radix select
+// finds the k-th key (8 bits per pass).
+__global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_frames,
+                                                        int32_t k_top, int32_t* out_idx) {
+  __shared__ uint32_t keys[kRankMax];
   __shared__ int hist[256];
   __shared__ int wsum[16];
   __shared__ uint32_t sh_prefix;
   __shared__ int sh_remaining;
-  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
-
-  // Eq. 7: w_f = mean over the frame's visual tokens of m_j (fp64 sum, fixed order)
-  for (int f = wave; f < n_frames; f += nw) {
-    int lo = offs[f], hi = offs[f + 1];
-    lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
-    hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
-    double s = 0.0;
-    for (int j = lo + lane; j < hi; j += 64) s += (double)m[j];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    if (lane == 0) {
-      const float w = hi > lo ? (float)(s / (double)(hi - lo)) : -INFINITY;
-      out_scores[f] = w;
-      keys[f] = order_key(w);
-    }
-  }
-  __syncthreads();
+  const int tid = threadIdx.x, nthr = blockDim.x;
   const int k = k_top < n_frames ? k_top : n_frames;
   if (k > 0) {
-    // radix select of the k-th largest key, 8 bits per pass
-    if (tid == 0) {
-      sh_prefix = 0;
-      sh_remaining = k;
-    }
-    uint32_t mask = 0;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += nthr) hist[i] = 0;
+    uint32_t kth = 0;
+    int take_eq = 0;
+    const bool small = n_frames <= kRankMax;
+    if (small) {
+      for (int f = tid; f < n_frames; f += nthr) keys[f] = keys_g[f];
       __syncthreads();
-      const uint32_t prefix = sh_prefix;
-      for (int f = tid; f < n_frames; f += nthr) {
-        const uint32_t key = keys[f];
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-      }
-      __syncthreads();
+    } else {
       if (tid == 0) {
-        int need = sh_remaining, cum = 0;
-        for (int dgt = 255; dgt >= 0; --dgt) {
-          if (cum + hist[dgt] >= need) {
-            sh_prefix = prefix | ((uint32_t)dgt << shift);
-            sh_remaining = need - cum;
-            break;
-          }
-          cum += hist[dgt];
-        }
+        sh_prefix = 0;
+        sh_remaining = k;
       }
-      mask |= 255u << shift;
-      __syncthreads();
+      uint32_t mask = 0;
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += nthr) hist[i] = 0;
+        __syncthreads();
+        const uint32_t prefix = sh_prefix;
+        const int need = sh_remaining;
+        for (int f = tid; f < n_frames; f += nthr) {
+          const uint32_t key = keys_g[f];
+          if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+        }
+        __syncthreads();
+        // the digit d with (count of digits > d) < need <= (count of digits >= d)
+        if (tid < 256) {
+          int above = 0;
+          for (int e = 255; e > tid; --e) above += hist[e];
+          if (above < need && above + hist[tid] >= need) {
+            sh_prefix = prefix | ((uint32_t)tid << shift);
+            sh_remaining = need - above;
+          }
+        }
+        mask |= 255u << shift;
+        __syncthreads();
+      }
+      kth = sh_prefix;
+      take_eq = sh_remaining;
     }
-    const uint32_t kth = sh_prefix;   // key of the k-th best frame
-    const int take_eq = sh_remaining; // frames with that key to take, lowest index first
-    // chronological output: frames with key > kth, plus the first take_eq with key == kth
     int eq_base = 0, out_base = 0;
     for (int f0 = 0; f0 < n_frames; f0 += nthr) {
       const int f = f0 + tid;
-      const uint32_t key = f < n_frames ? keys[f] : 0u;
-      const int is_eq = (f < n_frames && key == kth) ? 1 : 0;
-      int eq_total;
-      const int eq_rank = eq_base + block_exscan(is_eq, &eq_total, wsum);
-      const int sel = (f < n_frames) && (key > kth || (is_eq && eq_rank < take_eq)) ? 1 : 0;
+      int sel = 0;
+      if (small) {
+        if (f < n_frames) {
+          const uint32_t kf = keys[f];
+          int rank = 0;
+          for (int g = 0; g < n_frames; ++g) {
+            const uint32_t kg = keys[g];
+            rank += (kg > kf) || (kg == kf && g < f);
+          }
+          sel = rank < k;
+        }
+      } else {
+        const uint32_t key = f < n_frames ? keys_g[f] : 0u;
+        const int is_eq = (f < n_frames && key == kth) ? 1 : 0;
+        int eq_total;
+        const int eq_rank = eq_base + block_exscan(is_eq, &eq_total, wsum);
+        sel = (f < n_frames) && (key > kth || (is_eq && eq_rank < take_eq)) ? 1 : 0;
+        eq_base += eq_total;
+      }
       int sel_total;
       const int pos = out_base + block_exscan(sel, &sel_total, wsum);
       if (sel) out_idx[pos] = f;
-      eq_base += eq_total;
       out_base += sel_total;
     }
   }
@@ -708,9 +806,15 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
       }
     }
   }
-  if (h.n_frames == 0 && k_top == 0) return COFIE_OK;
-  return launch("qer_rank", qer_rank_kernel, dim3(1), dim3(1024), 0, s, (const float*)w.m, h.n_vis,
-                frame_offsets, h.n_frames, k_top, out_scores, out_idx, w.keys);
+  if (h.n_frames > 0) {
+    rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4)),
+                dim3(256), 0, s, (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores,
+                w.keys);
+    if (rc) return rc;
+  }
+  if (k_top == 0) return COFIE_OK;
+  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)w.keys,
+                h.n_frames, k_top, out_idx);
 }
 
 int64_t cofie_qer_k_from_ratio(double rho, int64_t n) {

@@ -2,6 +2,7 @@
 // timer, the scratch arena and device queries.
 #include <cstdarg>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -71,6 +72,27 @@ void prof_end(int slot, hipStream_t s) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> lk(p.mu);
   if (slot < (int)p.recs.size()) (void)hipEventRecord(p.recs[slot].stop, s);
+}
+
+// ---- LDS attribute cache ----------------------------------------------------------
+namespace {
+std::mutex g_lds_mu;
+std::map<const void*, size_t>& lds_sizes() {
+  static auto* m = new std::map<const void*, size_t>();
+  return *m;
+}
+}  // namespace
+
+bool lds_attr_done(const void* kernel, size_t bytes) {
+  std::lock_guard<std::mutex> lk(g_lds_mu);
+  auto it = lds_sizes().find(kernel);
+  return it != lds_sizes().end() && it->second >= bytes;
+}
+
+void lds_attr_mark(const void* kernel, size_t bytes) {
+  std::lock_guard<std::mutex> lk(g_lds_mu);
+  size_t& v = lds_sizes()[kernel];
+  if (bytes > v) v = bytes;
 }
 
 // ---- scratch ------------------------------------------------------------------
