@@ -83,15 +83,15 @@ struct ScoreArgs {
 // pointers are clamped to valid rows, so every load is unconditional; rows past
 // n_vis and query columns past n_q only produce tile entries that are never
 // stored.  A partial last macro step (Lc % KPS != 0) is handled separately.
-template <typename T, int NB, int P, int U>
-__device__ __forceinline__ void score_load(uint4 (&fa)[U][kMB], uint4 (&fb)[U][P][NB],
-                                           const uint4* const (&kp)[kMB],
+template <typename T, int MB, int NB, int P, int U>
+__device__ __forceinline__ void score_load(uint4 (&fa)[U][MB], uint4 (&fb)[U][P][NB],
+                                           const uint4* const (&kp)[MB],
                                            const uint4* const (&qp)[P][NB], int ms) {
   constexpr int STEP = Mma<T>::KPS * (int)sizeof(T) / 16;  // uint4 per macro step (= 4)
 #pragma unroll
   for (int u = 0; u < U; ++u) {
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb) fa[u][mb] = kp[mb][(ms + u) * STEP];
+    for (int mb = 0; mb < MB; ++mb) fa[u][mb] = kp[mb][(ms + u) * STEP];
 #pragma unroll
     for (int p = 0; p < P; ++p)
 #pragma unroll
@@ -99,38 +99,37 @@ __device__ __forceinline__ void score_load(uint4 (&fa)[U][kMB], uint4 (&fb)[U][P
   }
 }
 
-template <typename T, int NB, int P, int U>
-__device__ __forceinline__ void score_mac(f32x4 (&acc)[kMB][NB], const uint4 (&fa)[U][kMB],
+template <typename T, int MB, int NB, int P, int U>
+__device__ __forceinline__ void score_mac(f32x4 (&acc)[MB][NB], const uint4 (&fa)[U][MB],
                                           const uint4 (&fb)[U][P][NB]) {
 #pragma unroll
   for (int u = 0; u < U; ++u)
 #pragma unroll
     for (int p = 0; p < P; ++p)
 #pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) Mma<T>::mac(acc[mb][nb], fa[u][mb], fb[u][p][nb]);
 }
 
-template <typename T, int NB, int P>
+template <typename T, int MB, int NB, int P>
 __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
   using M = Mma<T>;
-  // macro steps per batch: two batches of at most 8 loads stay within 128
-  // VGPRs, so four waves fit per SIMD
-  constexpr int U = (kMB + P * NB) <= 4 ? 2 : 1;
-  __shared__ f32x4 part[4][kMB * NB][64];
+  // macro steps per batch: two batches of at most 12 loads in flight
+  constexpr int U = (MB + P * NB) <= 6 ? 2 : 1;
+  __shared__ f32x4 part[4][MB * NB][64];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int TG = 4 / a.KS;
   const int tg = wave / a.KS, ks = wave - tg * a.KS;
-  const int64_t tokbase = ((int64_t)blockIdx.x * TG + tg) * (kMB * 16);
+  const int64_t tokbase = ((int64_t)blockIdx.x * TG + tg) * (MB * 16);
   const int64_t rowbytes = (int64_t)a.Lc * sizeof(T);
 
   // lane's 16-byte column (g4) of its clamped rows
-  const uint4* kp[kMB];
+  const uint4* kp[MB];
 #pragma unroll
-  for (int mb = 0; mb < kMB; ++mb) {
+  for (int mb = 0; mb < MB; ++mb) {
     const int64_t tok = tokbase + mb * 16 + r16;
     kp[mb] = reinterpret_cast<const uint4*>(a.K + (tok < a.n_vis ? tok : 0) * rowbytes) + g4;
   }
@@ -146,9 +145,9 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
                       a.Qp + ((int64_t)p * a.nq_total + a.q0 + (qok[nb] ? q : 0)) * rowbytes) + g4;
   }
 
-  f32x4 acc[kMB][NB];
+  f32x4 acc[MB][NB];
 #pragma unroll
-  for (int mb = 0; mb < kMB; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -160,29 +159,29 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
   int ms = ms0;
   if (ms + U <= msf) {
     // software pipeline: batch i+1 is in flight while batch i is multiplied
-    uint4 fa[U][kMB], fb[U][P][NB];
-    score_load<T, NB, P, U>(fa, fb, kp, qp, ms);
+    uint4 fa[U][MB], fb[U][P][NB];
+    score_load<T, MB, NB, P, U>(fa, fb, kp, qp, ms);
     for (; ms + 2 * U <= msf; ms += U) {
-      uint4 ga[U][kMB], gb[U][P][NB];
-      score_load<T, NB, P, U>(ga, gb, kp, qp, ms + U);
-      score_mac<T, NB, P, U>(acc, fa, fb);
+      uint4 ga[U][MB], gb[U][P][NB];
+      score_load<T, MB, NB, P, U>(ga, gb, kp, qp, ms + U);
+      score_mac<T, MB, NB, P, U>(acc, fa, fb);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
 #pragma unroll
-        for (int mb = 0; mb < kMB; ++mb) fa[u][mb] = ga[u][mb];
+        for (int mb = 0; mb < MB; ++mb) fa[u][mb] = ga[u][mb];
 #pragma unroll
         for (int p = 0; p < P; ++p)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) fb[u][p][nb] = gb[u][p][nb];
       }
     }
-    score_mac<T, NB, P, U>(acc, fa, fb);
+    score_mac<T, MB, NB, P, U>(acc, fa, fb);
     ms += U;
   }
   for (; ms < msf; ++ms) {
-    uint4 fa[1][kMB], fb[1][P][NB];
-    score_load<T, NB, P, 1>(fa, fb, kp, qp, ms);
-    score_mac<T, NB, P, 1>(acc, fa, fb);
+    uint4 fa[1][MB], fb[1][P][NB];
+    score_load<T, MB, NB, P, 1>(fa, fb, kp, qp, ms);
+    score_mac<T, MB, NB, P, 1>(acc, fa, fb);
   }
   if (ms < ms1) {
     // partial macro step (bf16 with Lc % 32 == 16): lane groups past Lc read the
@@ -191,9 +190,9 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
     const int back = in ? 0 : -2;  // uint4 offset back into the row
     const uint4 zero = {0u, 0u, 0u, 0u};
     constexpr int STEP = M::KPS * (int)sizeof(T) / 16;
-    uint4 fa[1][kMB], fb[1][P][NB];
+    uint4 fa[1][MB], fb[1][P][NB];
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb) {
+    for (int mb = 0; mb < MB; ++mb) {
       const uint4 v = kp[mb][ms * STEP + back];
       fa[0][mb] = in ? v : zero;
     }
@@ -204,13 +203,13 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
         const uint4 v = qp[p][nb][ms * STEP + back];
         fb[0][p][nb] = in ? v : zero;
       }
-    score_mac<T, NB, P, 1>(acc, fa, fb);
+    score_mac<T, MB, NB, P, 1>(acc, fa, fb);
   }
 
   if (a.KS > 1) {
     if (ks > 0) {
 #pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) part[wave][mb * NB + nb][lane] = acc[mb][nb];
     }
@@ -218,7 +217,7 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
     if (ks == 0) {
       for (int j = 1; j < a.KS; ++j)
 #pragma unroll
-        for (int mb = 0; mb < kMB; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) acc[mb][nb] += part[wave + j][mb * NB + nb][lane];
     }
@@ -227,7 +226,7 @@ __global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
 
   // max over query rows: registers over nb, then the 16 lanes of a row group.
 #pragma unroll
-  for (int mb = 0; mb < kMB; ++mb) {
+  for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float v = -INFINITY;
@@ -664,18 +663,28 @@ int validate_qer(const void* Q, const void* K, const int32_t* offs, const cofie_
   return COFIE_OK;
 }
 
-template <typename T, int NB, int P>
+template <typename T, int MB, int NB, int P>
 int launch_score_t(const ScoreArgs& sa, unsigned grid, hipStream_t s) {
-  return launch("qer_score", qer_score_kernel<T, NB, P>, dim3(grid), dim3(256), 0, s, sa);
+  return launch("qer_score", qer_score_kernel<T, MB, NB, P>, dim3(grid), dim3(256), 0, s, sa);
 }
 
+// Tokens per wave: 64 (MB = 4) halves the L2 traffic of the query fragments
+// relative to the streamed keys; 32 (MB = 2) when the query side is wide.
 template <typename T, int P>
-int launch_score_p(const ScoreArgs& sa, int NB, unsigned grid, hipStream_t s) {
+int launch_score_p(const ScoreArgs& sa, int MB, int NB, unsigned grid, hipStream_t s) {
+  if (MB == 4) {
+    switch (NB) {
+      case 1: return launch_score_t<T, 4, 1, P>(sa, grid, s);
+      case 2: return launch_score_t<T, 4, 2, P>(sa, grid, s);
+      case 3: return launch_score_t<T, 4, 3, P>(sa, grid, s);
+      default: return launch_score_t<T, 4, 4, P>(sa, grid, s);
+    }
+  }
   switch (NB) {
-    case 1: return launch_score_t<T, 1, P>(sa, grid, s);
-    case 2: return launch_score_t<T, 2, P>(sa, grid, s);
-    case 3: return launch_score_t<T, 3, P>(sa, grid, s);
-    default: return launch_score_t<T, 4, P>(sa, grid, s);
+    case 1: return launch_score_t<T, 2, 1, P>(sa, grid, s);
+    case 2: return launch_score_t<T, 2, 2, P>(sa, grid, s);
+    case 3: return launch_score_t<T, 2, 3, P>(sa, grid, s);
+    default: return launch_score_t<T, 2, 4, P>(sa, grid, s);
   }
 }
 
@@ -759,7 +768,8 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
       sa.per_split = (sa.ksteps + sa.KS - 1) / sa.KS;
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
-      const int tokens_per_wg = (4 / sa.KS) * kMB * 16;
+      const int MB = (p.P == 1) ? 4 : 2;
+      const int tokens_per_wg = (4 / sa.KS) * MB * 16;
       const unsigned grid = (unsigned)ceil_div(h.n_vis, tokens_per_wg);
       for (int q0 = 0; q0 < h.n_q; q0 += 64) {
         sa.q0 = q0;
@@ -767,9 +777,10 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
         sa.accumulate = q0 > 0;
         const int NB = (sa.n_q + 15) / 16;
         if (bf16)
-          rc = p.P == 3 ? launch_score_p<bf16_t, 3>(sa, NB, grid, s) : launch_score_p<bf16_t, 1>(sa, NB, grid, s);
+          rc = p.P == 3 ? launch_score_p<bf16_t, 3>(sa, MB, NB, grid, s)
+                        : launch_score_p<bf16_t, 1>(sa, MB, NB, grid, s);
         else
-          rc = launch_score_p<float, 1>(sa, NB, grid, s);
+          rc = launch_score_p<float, 1>(sa, MB, NB, grid, s);
         if (rc) return rc;
       }
     } else {
