@@ -1,0 +1,124 @@
+"""Full-size parity on the hour-long stream, high-resolution and multi-stream
+workloads, in the launch configuration the benchmark uses: thresholds
+calibrated on the GPU for each stream's retention target, then the filter
+with those per-stream thresholds and a caller workspace; QER on the
+workload's candidate frames.  Histograms, thresholds, masks, scores and kept
+counts must match the CPU oracle bit for bit; QER scores within 2e-2
+relative (bf16 MFMA path) and top-k sets exactly (outside 1e-6 ties)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_03675_amd import binding as B
+from paper_2609_03675_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import bf16_dev, check_topk, hist_np, rel_err, require_gpu, to_dev  # noqa: E402
+
+MODES = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
+CHUNK = 128  # frames generated, uploaded and histogrammed on the host at a time
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    B.lib()
+
+
+def upload_workload(cfg):
+    """All frames of a workload on the GPU, plus the oracle histograms, built
+    chunk by chunk so that host memory stays bounded."""
+    wl = synth.WORKLOADS[cfg]
+    mode = MODES[wl.hist_mode]
+    frames = torch.empty((wl.n, wl.H, wl.W, 3), dtype=torch.uint8, device="cuda")
+    hists = []
+    for s in range(wl.n_streams):
+        plan = synth.StreamPlan(cfg, s)
+        for t0 in range(0, wl.T, CHUNK):
+            c = min(CHUNK, wl.T - t0)
+            host = plan.frames(t0, c)
+            frames[s * wl.T + t0:s * wl.T + t0 + c].copy_(torch.from_numpy(host))
+            hists.append(oracle.histogram(host, wl.bins, mode))
+    print(f"workload {cfg}: {wl.n} frames uploaded", flush=True)
+    return frames, np.concatenate(hists)
+
+
+@pytest.mark.parametrize("cfg", [3, 4, 5])
+def test_ngff_full_size(cfg):
+    wl = synth.WORKLOADS[cfg]
+    mode = MODES[wl.hist_mode]
+    frames, h_o = upload_workload(cfg)
+    seg = wl.T if wl.n_streams > 1 else 0
+    M = oracle.mass(mode, wl.H, wl.W)
+    theta_o, tau_o = oracle.ngff_calibrate(h_o, M, wl.target, 30, 4, seg)
+    print(f"oracle calibrated: theta {theta_o[:4]}...", flush=True)
+
+    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, seg)
+    tau_g = B.cofie_ngff_calibrate(frames, wl.bins, rule, wl.target)
+    nseg = wl.n_streams
+    nb = B.cofie_ngff_nbins(wl.hist_mode, wl.bins)
+    hist = torch.empty((wl.n, nb), dtype=torch.int32, device="cuda")
+    count = torch.empty(nseg, dtype=torch.int32, device="cuda")
+    ws = torch.empty(B.ngff_workspace_bytes(wl.n, wl.H, wl.W, 3, wl.bins, rule), dtype=torch.uint8,
+                     device="cuda")
+    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, seg, tau_per_segment=tau_g, out_hist=hist,
+                       out_count=count, workspace=ws)
+    s, m = B.cofie_ngff_filter(frames, wl.bins, rule)
+    torch.cuda.synchronize()
+    assert np.array_equal(tau_g.cpu().numpy().view(np.uint32), tau_o.view(np.uint32))
+    assert np.array_equal(hist_np(hist), h_o)
+    so, mo, ko = oracle.ngff_select(h_o, M, tau_o, 30, 4, seg)
+    m = m.cpu().numpy()
+    assert np.array_equal(m, mo), f"masks differ at {np.flatnonzero(m != mo)[:10]}"
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), so.view(np.uint32))
+    assert np.array_equal(count.cpu().numpy(), ko.astype(np.int32))
+    assert np.all(ko <= wl.target)
+    print(f"kept per stream {ko[:8]}... (target {wl.target})", flush=True)
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_qer_full_size(cfg):
+    wl = synth.WORKLOADS[cfg]
+    Q, K, offs = synth.qer_inputs(cfg)
+    w, idx = B.cofie_qer_rank(bf16_dev(Q), bf16_dev(K), to_dev(offs), wl.k_top)
+    torch.cuda.synchronize()
+    ref = oracle.qer_scores(Q, K, offs, wl.H_q, wl.H_kv, wl.d)
+    w = w.cpu().numpy()
+    err = rel_err(w, ref)
+    print(f"workload {cfg}: QER max rel err {err:.3e}", flush=True)
+    assert err <= 2e-2
+    check_topk(idx.cpu().numpy(), ref, wl.k_top)
+
+
+@pytest.mark.parametrize("streams", [(0, 1, 2, 3), (17, 31)])
+def test_qer_multistream_queries(streams):
+    """Each stream's queries rank that stream's NGFF candidates up to the query
+    timestamp (one call per query; the stream's keys are shared by its queries)."""
+    cfg = 5
+    wl = synth.WORKLOADS[cfg]
+    mode = MODES[wl.hist_mode]
+    M = oracle.mass(mode, wl.H, wl.W)
+    for s in streams:
+        plan = synth.StreamPlan(cfg, s)
+        h = oracle.histogram(plan.frames(), wl.bins, mode)
+        _, tau = oracle.ngff_calibrate(h, M, wl.target, 30, 4)
+        _, mask, _ = oracle.ngff_select(h, M, tau[0], 30, 4)
+        kept = np.flatnonzero(mask)
+        stamps = synth.multistream_queries(cfg, s)
+        last = kept[kept <= stamps.max()]
+        K_all = synth.multistream_k(cfg, s, last)
+        Kd = bf16_dev(K_all)
+        for qi, ts in enumerate(stamps):
+            cand = kept[kept <= ts]
+            nc = cand.size
+            Q = synth.multistream_q(cfg, s, qi)
+            offs = synth.frame_offsets(np.full(nc, wl.tokens))
+            k = min(wl.k_top, nc)
+            w, idx = B.cofie_qer_rank(bf16_dev(Q), Kd[:nc * wl.tokens], to_dev(offs), k)
+            torch.cuda.synchronize()
+            ref = oracle.qer_scores(Q, K_all[:nc * wl.tokens], offs, wl.H_q, wl.H_kv, wl.d)
+            assert rel_err(w.cpu().numpy(), ref) <= 2e-2
+            check_topk(idx.cpu().numpy(), ref, k)
+        print(f"stream {s}: {len(stamps)} queries over {last.size} candidates ok", flush=True)
