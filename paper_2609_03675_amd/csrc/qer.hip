@@ -8,12 +8,13 @@
 // carried as three bf16 terms hi + mid + lo that reproduce the fp32 value, so
 // the bf16 MFMA still multiplies exact operands.
 //
-// qer_score: each wave owns MB x 16 visual tokens and all (<= 64) query rows
-//   of one chunk; K rows stream from HBM exactly once in 16-byte lane loads, Q
-//   comes from L2.  Workgroups of 4 waves split long contractions over waves
-//   (KS) and add the partial tiles through LDS.  The epilogue takes the max
-//   over query rows (registers, then 16-lane shuffles) and writes
-//   m_j = scale * max_i S_ij: the text-by-vision matrix is never stored.
+// qer_score: one 8-wave workgroup per CU; each wave owns MB x 16 visual tokens
+//   and all (<= 64) query rows of one chunk, over the whole contraction.  K
+//   rows stream from HBM exactly once, in 128-byte row segments that a lane
+//   select and a DPP swap turn into MFMA operands; the query fragments are
+//   staged in LDS phase by phase.  The epilogue takes the max over query rows
+//   (registers, then 16-lane shuffles) and writes m_j = scale * max_i S_ij:
+//   the text-by-vision matrix is never stored.
 // qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7).
 // qer_topk: one workgroup ranks the frames by (score desc, frame asc) on
 //   order-preserving 32-bit keys (counting ranks in LDS, or a radix select for
@@ -63,182 +64,311 @@ struct Mma<float> {
   }
 };
 
-struct ScoreArgs {
+// ---- LDS-staged query fragments -------------------------------------------------------
+// One workgroup of 8 waves per CU.  Each wave keeps the whole contraction of
+// its MB tiles of 16 tokens in registers; vector memory carries only the key
+// stream and, once per phase, the query fragments of the phase.
+//
+// Key loads.  An MFMA operand holds 16 rows x 64 bytes per register, and a
+// load instruction in that shape (16 rows, 64 bytes each) streams at roughly
+// half the per-CU rate of one that takes 128 or 256 contiguous bytes from each
+// of 8 or 4 rows.  The contraction order is free as long as keys and queries
+// agree, so each row is read in segments of SEGC = 64/R 16-byte chunks with
+// R rows per load: per segment and tile, load q (q < VPS = 16/R) covers rows
+// R q .. R q + R-1, lane s taking row R q + s%R and chunk
+// VPS*(s/16) + ((s%16)/R - q) mod VPS.  Lane l then finds chunk VPS*g + k
+// (g = l/16) of its own row l%16 in load ((l%16)/R - k) mod VPS ... of lane
+// l + R k within its 16-lane row: a per-lane register select and one DPP row
+// rotation make operand k.  Segment m so yields VPS operands, "virtual steps"
+// VPS m + k, whose lane group g covers 16-byte chunk SEGC m + VPS g + k.  A
+// contraction tail shorter than a segment is read in plain MFMA shape.
+//
+// Query fragments.  The contraction is cut into phases of S virtual steps; a
+// phase's query fragments sit in LDS in MFMA operand order ([step][term]
+// [16-query block][lane], 16 bytes per lane, read by every wave with
+// conflict-free 16-byte LDS loads), double buffered: the fragments of phase
+// i+1 are fetched into registers at the start of phase i and written to LDS
+// one batch later.
+struct ScoreLdsArgs {
   const uint8_t* K;   // [n_vis][Lc] elements
   const uint8_t* Qp;  // [P][nq_total][Lc] elements
   int32_t n_vis;
   int32_t n_q;        // query rows in this chunk (<= 64)
-  int32_t q0;         // first query row of the chunk
+  int32_t q0;
   int32_t nq_total;
   int32_t Lc;
-  int32_t ksteps;     // macro steps over Lc
-  int32_t KS;         // waves splitting one token group's contraction (1, 2, 4)
-  int32_t per_split;  // macro steps per splitting wave
+  int32_t nseg;       // whole segments per row
+  int32_t ksteps;     // virtual steps: VPS nseg + tail steps
+  int32_t S;          // virtual steps per phase (a multiple of the batch length)
+  int32_t nphase;
+  int32_t tiles;      // 16-token tiles
+  int32_t nwg;        // workgroups
   float scale;
-  float* m;           // [n_vis]
-  int32_t accumulate; // take the max with the m already stored (later query chunks)
+  float* m;
+  int32_t accumulate;
 };
 
-// Loads of one batch of U macro steps starting at macro step `ms`.  Row
-// pointers are clamped to valid rows, so every load is unconditional; rows past
-// n_vis and query columns past n_q only produce tile entries that are never
-// stored.  A partial last macro step (Lc % KPS != 0) is handled separately.
-template <typename T, int MB, int NB, int P, int U>
-__device__ __forceinline__ void score_load(uint4 (&fa)[U][MB], uint4 (&fb)[U][P][NB],
-                                           const uint4* const (&kp)[MB],
-                                           const uint4* const (&qp)[P][NB], int ms) {
-  constexpr int STEP = Mma<T>::KPS * (int)sizeof(T) / 16;  // uint4 per macro step (= 4)
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) fa[u][mb] = kp[mb][(ms + u) * STEP];
-#pragma unroll
-    for (int p = 0; p < P; ++p)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fb[u][p][nb] = qp[p][nb][(ms + u) * STEP];
-  }
+constexpr int kLdsWaves = 8;
+constexpr int kLdsThreads = kLdsWaves * 64;
+constexpr int kQRegs = 8;               // uint4 per thread per phase fill
+constexpr int kPhaseU4 = kQRegs * kLdsThreads;  // uint4 per phase buffer (64 KiB)
+
+// virtual steps per batch: 8 key loads per batch and wave (two batches in
+// flight), fewer where the query fragments and accumulators of wide query
+// blocks take the registers; at least one segment (16/R steps)
+__host__ __device__ constexpr int lds_batch(int MB, int PNB, int R) {
+  const int u = MB == 1 ? (PNB <= 4 ? 8 : 4) : (PNB <= 2 ? 4 : 2);
+  return u > 16 / R ? u : 16 / R;
 }
 
-template <typename T, int MB, int NB, int P, int U>
-__device__ __forceinline__ void score_mac(f32x4 (&acc)[MB][NB], const uint4 (&fa)[U][MB],
-                                          const uint4 (&fb)[U][P][NB]) {
-#pragma unroll
-  for (int u = 0; u < U; ++u)
-#pragma unroll
-    for (int p = 0; p < P; ++p)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) Mma<T>::mac(acc[mb][nb], fa[u][mb], fb[u][p][nb]);
+template <int N>
+__device__ __forceinline__ uint32_t row_ror(uint32_t v) {  // lane i <- lane (i - N) mod 16 of its row
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x120 + N, 0xF, 0xF, false);
 }
+template <int N>
+__device__ __forceinline__ uint4 row_ror4(const uint4& v) {
+  if constexpr (N == 0) return v;
+  else return uint4{row_ror<N>(v.x), row_ror<N>(v.y), row_ror<N>(v.z), row_ror<N>(v.w)};
+}
+
+// rows per key load.  8 (128-byte segments) measured faster than 4 (256-byte
+// segments) in this kernel on the 1 fps stream workload (48.9 vs 51.1 us).
+__host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 
 template <typename T, int MB, int NB, int P>
-__global__ __launch_bounds__(256) void qer_score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) {
   using M = Mma<T>;
-  // macro steps per batch: two batches of at most 12 loads in flight
-  constexpr int U = (MB + P * NB) <= 6 ? 2 : 1;
-  __shared__ f32x4 part[4][MB * NB][64];
+  constexpr int R = lds_rows(MB, P * NB);
+  constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
+  constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
+  constexpr int U = lds_batch(MB, P * NB, R);
+  constexpr int FPS = P * NB;   // fragments per virtual step
+  static_assert(U % VPS == 0, "batches hold whole segments");
+  extern __shared__ uint4 qs[];  // [2][kPhaseU4]: [S][P][NB][64] each
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int TG = 4 / a.KS;
-  const int tg = wave / a.KS, ks = wave - tg * a.KS;
-  const int64_t tokbase = ((int64_t)blockIdx.x * TG + tg) * (MB * 16);
-  const int64_t rowbytes = (int64_t)a.Lc * sizeof(T);
+  const int qs_lane = r16 / R;  // load index holding this lane's own row
+  const int pfull = VPS * a.nseg;
+  const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
+  const uint4* Kq = reinterpret_cast<const uint4*>(a.K);
+  const uint4* Qq = reinterpret_cast<const uint4*>(a.Qp);
+  const int t_begin = (int)((int64_t)a.tiles * blockIdx.x / a.nwg);
+  const int t_end = (int)((int64_t)a.tiles * (blockIdx.x + 1) / a.nwg);
 
-  // lane's 16-byte column (g4) of its clamped rows
-  const uint4* kp[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int64_t tok = tokbase + mb * 16 + r16;
-    kp[mb] = reinterpret_cast<const uint4*>(a.K + (tok < a.n_vis ? tok : 0) * rowbytes) + g4;
-  }
-  const uint4* qp[P][NB];
   bool qok[NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int q = nb * 16 + r16;
-    qok[nb] = q < a.n_q;
-#pragma unroll
-    for (int p = 0; p < P; ++p)
-      qp[p][nb] = reinterpret_cast<const uint4*>(
-                      a.Qp + ((int64_t)p * a.nq_total + a.q0 + (qok[nb] ? q : 0)) * rowbytes) + g4;
-  }
+  for (int nb = 0; nb < NB; ++nb) qok[nb] = nb * 16 + r16 < a.n_q;
 
-  f32x4 acc[MB][NB];
+  // fragments of phase ph: element e = tid + kLdsThreads * i of the buffer;
+  // rows past n_q, columns past Lc and steps past the phase are zero.  Loads
+  // are unconditional (clamped addresses); the zeroing is a select made when
+  // the registers are stored, so that issuing the loads never waits for them.
+  uint32_t qmask = 0;
+  auto q_load = [&](int ph, uint4 (&qr)[kQRegs]) __attribute__((always_inline)) {
+    const int nstep = min(a.S, a.ksteps - ph * a.S);
+    qmask = 0;
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+    for (int i = 0; i < kQRegs; ++i) {
+      const int e = tid + kLdsThreads * i;
+      const int frag = e >> 6, ln = e & 63;
+      const int ls = frag / FPS, rem = frag - ls * FPS;
+      const int p = rem / NB, nb = rem - p * NB;
+      const int q = nb * 16 + (ln & 15);
+      const int v = ph * a.S + ls, g = ln >> 4;
+      const int col = v < pfull ? SEGC * (v / VPS) + VPS * g + v % VPS : 4 * v + g;
+      const bool ok = ls < nstep && q < a.n_q && col * M::EPL < a.Lc;
+      const int64_t row = (int64_t)p * a.nq_total + a.q0 + (ok ? q : 0);
+      qr[i] = Qq[row * row_u4 + (ok ? col : 0)];
+      qmask |= ok ? 1u << i : 0u;
+    }
+  };
+  auto q_store = [&](int ph, const uint4 (&qr)[kQRegs]) __attribute__((always_inline)) {
+    uint4* dst = qs + (ph & 1) * kPhaseU4 + tid;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < kQRegs; ++i) {
+      const bool ok = (qmask >> i) & 1u;
+      dst[kLdsThreads * i] = uint4{ok ? qr[i].x : 0u, ok ? qr[i].y : 0u, ok ? qr[i].z : 0u, ok ? qr[i].w : 0u};
+    }
+  };
+  auto barrier_lds = []() __attribute__((always_inline)) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
 
-  // this wave's macro steps [ms0, ms1); whole steps first, then the partial one
-  const int full = a.Lc / M::KPS;
-  const int ms0 = ks * a.per_split;
-  const int ms1 = ms0 + a.per_split < a.ksteps ? ms0 + a.per_split : a.ksteps;
-  const int msf = ms1 < full ? ms1 : full;
-  int ms = ms0;
-  if (ms + U <= msf) {
-    // software pipeline: batch i+1 is in flight while batch i is multiplied
-    uint4 fa[U][MB], fb[U][P][NB];
-    score_load<T, MB, NB, P, U>(fa, fb, kp, qp, ms);
-    for (; ms + 2 * U <= msf; ms += U) {
-      uint4 ga[U][MB], gb[U][P][NB];
-      score_load<T, MB, NB, P, U>(ga, gb, kp, qp, ms + U);
-      score_mac<T, MB, NB, P, U>(acc, fa, fb);
+  for (int rb = t_begin; rb < t_end; rb += kLdsWaves * MB) {
+    // this wave's tiles: rb + wave + 8 j.  Missing ones repeat tile rb (the
+    // first tile of wave 0 in this round): their loads hit the cache and their
+    // results are never stored.
+    int nmb = 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
+    for (int j = 0; j < MB; ++j) nmb += (rb + wave + kLdsWaves * j < t_end) ? 1 : 0;
+    const uint4* kq[MB][VPS];
+    const uint4* k16[MB];
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) fa[u][mb] = ga[u][mb];
+    for (int j = 0; j < MB; ++j) {
+      const int64_t t0 = (int64_t)(j < nmb ? rb + wave + kLdsWaves * j : rb) * 16;
+      const int64_t last = a.n_vis - 1;
 #pragma unroll
-        for (int p = 0; p < P; ++p)
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) fb[u][p][nb] = gb[u][p][nb];
+      for (int q = 0; q < VPS; ++q) {
+        const int64_t tok = min(t0 + R * q + (lane % R), last);
+        const int chunk = VPS * g4 + ((((lane & 15) / R) - q) & (VPS - 1));
+        kq[j][q] = Kq + tok * row_u4 + chunk;
       }
+      k16[j] = Kq + min(t0 + r16, last) * row_u4 + g4;
     }
-    score_mac<T, MB, NB, P, U>(acc, fa, fb);
-    ms += U;
-  }
-  for (; ms < msf; ++ms) {
-    uint4 fa[1][MB], fb[1][P][NB];
-    score_load<T, MB, NB, P, 1>(fa, fb, kp, qp, ms);
-    score_mac<T, MB, NB, P, 1>(acc, fa, fb);
-  }
-  if (ms < ms1) {
-    // partial macro step (bf16 with Lc % 32 == 16): lane groups past Lc read the
-    // previous 16 bytes of their row and contribute zero
-    const bool in = ms * M::KPS + g4 * M::EPL < a.Lc;
-    const int back = in ? 0 : -2;  // uint4 offset back into the row
-    const uint4 zero = {0u, 0u, 0u, 0u};
-    constexpr int STEP = M::KPS * (int)sizeof(T) / 16;
-    uint4 fa[1][MB], fb[1][P][NB];
+    f32x4 acc[MB][NB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const uint4 v = kp[mb][ms * STEP + back];
-      fa[0][mb] = in ? v : zero;
-    }
+    for (int j = 0; j < MB; ++j)
 #pragma unroll
-    for (int p = 0; p < P; ++p)
+      for (int nb = 0; nb < NB; ++nb) acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // loads of the U virtual steps from ms (U/VPS segments, VPS loads each)
+    auto k_load = [&](uint4 (&f)[U][MB], int ms) __attribute__((always_inline)) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const uint4 v = qp[p][nb][ms * STEP + back];
-        fb[0][p][nb] = in ? v : zero;
+      for (int h = 0; h < U / VPS; ++h) {
+        const int seg = min(ms / VPS + h, a.nseg - 1);
+#pragma unroll
+        for (int q = 0; q < VPS; ++q)
+#pragma unroll
+          for (int j = 0; j < MB; ++j) f[VPS * h + q][j] = kq[j][q][SEGC * seg];
       }
-    score_mac<T, MB, NB, P, 1>(acc, fa, fb);
-  }
+    };
 
-  if (a.KS > 1) {
-    if (ks > 0) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) part[wave][mb * NB + nb][lane] = acc[mb][nb];
-    }
-    __syncthreads();
-    if (ks == 0) {
-      for (int j = 1; j < a.KS; ++j)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] += part[wave + j][mb * NB + nb][lane];
-    }
-  }
-  if (ks != 0) return;
+    uint4 fa[U][MB], fb[U][MB];
+    if (a.nseg > 0) k_load(fa, 0);
+    if (rb != t_begin) barrier_lds();  // previous round's readers are done
+    uint4 qr[kQRegs];
+    q_load(0, qr);
+    q_store(0, qr);
+    bool pending = a.nphase > 1;
+    if (pending) q_load(1, qr);
+    barrier_lds();
 
-  // max over query rows: registers over nb, then the 16 lanes of a row group.
+    // one batch: prefetch the next batch into `nxt`, multiply `cur`, and at a
+    // phase end publish the next phase's fragments
+    int ph = 0;
+    auto batch = [&](int ms, const uint4 (&cur)[U][MB], uint4 (&nxt)[U][MB], bool guard) __attribute__((always_inline)) {
+      k_load(nxt, ms + U);
+      if (pending && ms > ph * a.S) {
+        q_store(ph + 1, qr);
+        pending = false;
+      }
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (ms - ph * a.S) * FPS * 64 + lane;
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
+      for (int h = 0; h < U / VPS; ++h) {
+        if (!guard || ms + VPS * h < pfull) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float v = -INFINITY;
+          for (int k = 0; k < VPS; ++k) {
+            // operand k: the load ((l%16)/R - k) mod VPS of lane l + R k
+            // the register choice is a bit-mask blend: a select between
+            // array elements would be folded into an indexed (stack) load
+            uint32_t pick[VPS];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        if (qok[nb]) v = fmaxf(v, acc[mb][nb][r]);
+            for (int q = 0; q < VPS; ++q) pick[q] = ((qs_lane - k) & (VPS - 1)) == q ? ~0u : 0u;
+            uint4 fk[MB];
 #pragma unroll
-      for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
-      const int64_t tok = tokbase + mb * 16 + g4 * 4 + r;
-      if (r16 == 0 && tok < a.n_vis) {
-        const float x = v * a.scale;
-        a.m[tok] = a.accumulate ? fmaxf(a.m[tok], x) : x;
+            for (int j = 0; j < MB; ++j) {
+              uint4 send = {0u, 0u, 0u, 0u};
+#pragma unroll
+              for (int q = 0; q < VPS; ++q) {
+                const uint4 c = cur[VPS * h + q][j];
+                send.x |= c.x & pick[q];
+                send.y |= c.y & pick[q];
+                send.z |= c.z & pick[q];
+                send.w |= c.w & pick[q];
+              }
+              if constexpr (VPS == 2) {
+                fk[j] = k == 0 ? send : row_ror4<8>(send);
+              } else {
+                fk[j] = k == 0 ? send : (k == 1 ? row_ror4<12>(send) : (k == 2 ? row_ror4<8>(send) : row_ror4<4>(send)));
+              }
+            }
+            uint4 qf[FPS];
+#pragma unroll
+            for (int f = 0; f < FPS; ++f) qf[f] = qb[((VPS * h + k) * FPS + f) * 64];
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+#pragma unroll
+              for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int j = 0; j < MB; ++j) M::mac(acc[j][nb], fk[j], qf[p * NB + nb]);
+          }
+        }
+      }
+      if (ms + U == (ph + 1) * a.S && ph + 1 < a.nphase) {
+        if (pending) {
+          q_store(ph + 1, qr);
+          pending = false;
+        }
+        barrier_lds();
+        ++ph;
+        if (ph + 1 < a.nphase) {
+          q_load(ph + 1, qr);
+          pending = true;
+        }
+      }
+    };
+    // pairs of whole batches (the two register sets alternate without copies),
+    // then at most two guarded batches
+    int ms = 0;
+    for (; ms + 2 * U <= pfull; ms += 2 * U) {
+      batch(ms, fa, fb, false);
+      batch(ms + U, fb, fa, false);
+    }
+    if (ms < pfull) {
+      batch(ms, fa, fb, true);
+      if (ms + U < pfull) batch(ms + U, fb, fa, true);
+    }
+
+    // tail steps in plain MFMA shape; lane groups past Lc re-read the previous
+    // 32 bytes of their row and contribute zero (the query side is zero too)
+    if (pfull < a.ksteps && pending) {  // a last phase holding only the tail
+      q_store(ph + 1, qr);
+      barrier_lds();
+      ++ph;
+    }
+    for (int v = pfull; v < a.ksteps; ++v) {
+      const int col = SEGC * a.nseg + 4 * (v - pfull);  // 16-byte column of lane group 0
+      const bool in = (col + g4) * M::EPL < a.Lc;
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (v - ph * a.S) * FPS * 64 + lane;
+      uint4 kf[MB];
+#pragma unroll
+      for (int j = 0; j < MB; ++j) {
+        const uint4 x = k16[j][col + (in ? 0 : -2)];
+        kf[j] = in ? x : uint4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const uint4 qf = qb[(p * NB + nb) * 64];
+#pragma unroll
+          for (int j = 0; j < MB; ++j) M::mac(acc[j][nb], kf[j], qf);
+        }
+    }
+
+    // m_j = scale * max over the query rows: registers over nb, then the 16
+    // lanes of a row group
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      if (j < nmb) {
+        const int64_t tile = rb + wave + kLdsWaves * j;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            if (qok[nb]) v = fmaxf(v, acc[j][nb][r]);
+#pragma unroll
+          for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
+          const int64_t tok = tile * 16 + g4 * 4 + r;
+          if (r16 == 0 && tok < a.n_vis) {
+            const float x = v * a.scale;
+            a.m[tok] = a.accumulate ? fmaxf(a.m[tok], x) : x;
+          }
+        }
       }
     }
   }
@@ -358,7 +488,7 @@ constexpr int kRankMax = 4096;  // frames ranked by counting in LDS
 // finds the k-th key (8 bits per pass).
 __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_frames,
                                                         int32_t k_top, int32_t* out_idx) {
-  __shared__ uint32_t keys[kRankMax];
+  __shared__ __align__(16) uint32_t keys[kRankMax];
   __shared__ int hist[256];
   __shared__ int wsum[16];
   __shared__ uint32_t sh_prefix;
@@ -370,7 +500,10 @@ __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, 
     int take_eq = 0;
     const bool small = n_frames <= kRankMax;
     if (small) {
-      for (int f = tid; f < n_frames; f += nthr) keys[f] = keys_g[f];
+      // order keys are >= 0x007FFFFF (the key of -inf), so padding with 0 is
+      // never counted as beating a frame
+      const int padded = (n_frames + 3) & ~3;
+      for (int f = tid; f < padded; f += nthr) keys[f] = f < n_frames ? keys_g[f] : 0u;
       __syncthreads();
     } else {
       if (tid == 0) {
@@ -409,11 +542,20 @@ __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, 
       int sel = 0;
       if (small) {
         if (f < n_frames) {
+          // rank = frames that beat f; keys are read four at a time (the LDS
+          // copy is padded with zero keys, which never beat anything)
           const uint32_t kf = keys[f];
           int rank = 0;
-          for (int g = 0; g < n_frames; ++g) {
-            const uint32_t kg = keys[g];
-            rank += (kg > kf) || (kg == kf && g < f);
+          const uint4* k4 = reinterpret_cast<const uint4*>(keys);
+          const int nq = (n_frames + 3) >> 2;
+#pragma unroll 4
+          for (int q = 0; q < nq; ++q) {
+            const uint4 v = k4[q];
+            const int g = 4 * q;
+            rank += (v.x > kf) || (v.x == kf && g < f);
+            rank += (v.y > kf) || (v.y == kf && g + 1 < f);
+            rank += (v.z > kf) || (v.z == kf && g + 2 < f);
+            rank += (v.w > kf) || (v.w == kf && g + 3 < f);
           }
           sel = rank < k;
         }
@@ -663,29 +805,54 @@ int validate_qer(const void* Q, const void* K, const int32_t* offs, const cofie_
   return COFIE_OK;
 }
 
-template <typename T, int MB, int NB, int P>
-int launch_score_t(const ScoreArgs& sa, unsigned grid, hipStream_t s) {
-  return launch("qer_score", qer_score_kernel<T, MB, NB, P>, dim3(grid), dim3(256), 0, s, sa);
+// Work split of the LDS-staged score kernel: one workgroup per CU (fewer for
+// small inputs), tiles of 16 tokens spread evenly over the workgroups, 1 or 2
+// tiles per wave per round, 4-row key segments unless the batch is too short
+// to hold one, phases as long as a 64 KiB buffer allows.
+struct LdsPlan {
+  int MB, R, nwg, S, nphase, nseg, ksteps;
+  size_t lds;
+};
+
+LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int PNB, int cus) {
+  LdsPlan L;
+  const int64_t tiles = ceil_div(n_vis, 16);
+  L.nwg = (int)std::min<int64_t>(cus, ceil_div(tiles, kLdsWaves));
+  const int64_t tpw = ceil_div(tiles, L.nwg);
+  L.MB = tpw > kLdsWaves ? 2 : 1;
+  L.R = lds_rows(L.MB, PNB);
+  const int U = lds_batch(L.MB, PNB, L.R);
+  const int64_t kps = 64 / (int64_t)esize;             // elements per plain MFMA step
+  const int64_t seg_el = (1024 / L.R) / (int64_t)esize;  // elements per segment
+  L.nseg = (int)(Lc / seg_el);
+  L.ksteps = (int)((16 / L.R) * L.nseg + ceil_div(Lc % seg_el, kps));
+  L.S = (int)std::min<int64_t>((kPhaseU4 / 64) / PNB / U * U, ceil_div(L.ksteps, U) * U);
+  L.nphase = (int)ceil_div(L.ksteps, L.S);
+  L.lds = (size_t)(L.nphase > 1 ? 2 : 1) * kPhaseU4 * sizeof(uint4);
+  return L;
 }
 
-// Tokens per wave: 64 (MB = 4) halves the L2 traffic of the query fragments
-// relative to the streamed keys; 32 (MB = 2) when the query side is wide.
-template <typename T, int P>
-int launch_score_p(const ScoreArgs& sa, int MB, int NB, unsigned grid, hipStream_t s) {
-  if (MB == 4) {
-    switch (NB) {
-      case 1: return launch_score_t<T, 4, 1, P>(sa, grid, s);
-      case 2: return launch_score_t<T, 4, 2, P>(sa, grid, s);
-      case 3: return launch_score_t<T, 4, 3, P>(sa, grid, s);
-      default: return launch_score_t<T, 4, 4, P>(sa, grid, s);
-    }
-  }
+template <typename T, int MB, int NB, int P>
+int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, hipStream_t s) {
+  auto k = qer_score_kernel<T, MB, NB, P>;
+  int rc = allow_lds(k, L.lds);
+  if (rc) return rc;
+  return launch("qer_score", k, dim3((unsigned)L.nwg), dim3(kLdsThreads), L.lds, s, sa);
+}
+
+template <typename T, int MB, int P>
+int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
   switch (NB) {
-    case 1: return launch_score_t<T, 2, 1, P>(sa, grid, s);
-    case 2: return launch_score_t<T, 2, 2, P>(sa, grid, s);
-    case 3: return launch_score_t<T, 2, 3, P>(sa, grid, s);
-    default: return launch_score_t<T, 2, 4, P>(sa, grid, s);
+    case 1: return launch_lds_t<T, MB, 1, P>(sa, L, s);
+    case 2: return launch_lds_t<T, MB, 2, P>(sa, L, s);
+    case 3: return launch_lds_t<T, MB, 3, P>(sa, L, s);
+    default: return launch_lds_t<T, MB, 4, P>(sa, L, s);
   }
+}
+
+template <typename T, int P>
+int launch_lds(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
+  return L.MB == 1 ? launch_lds_nb<T, 1, P>(sa, L, NB, s) : launch_lds_nb<T, 2, P>(sa, L, NB, s);
 }
 
 template <typename T, int NB>
@@ -756,31 +923,32 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
         if (rc) return rc;
         qp = w.qp;
       }
-      ScoreArgs sa;
+      ScoreLdsArgs sa;
       sa.K = static_cast<const uint8_t*>(K);
       sa.Qp = qp;
       sa.n_vis = h.n_vis;
       sa.nq_total = h.n_q;
       sa.Lc = (int32_t)p.Lc;
       const int kps = bf16 ? Mma<bf16_t>::KPS : Mma<float>::KPS;
-      sa.ksteps = (int32_t)((p.Lc + kps - 1) / kps);
-      sa.KS = sa.ksteps >= 32 ? 4 : (sa.ksteps >= 8 ? 2 : 1);
-      sa.per_split = (sa.ksteps + sa.KS - 1) / sa.KS;
+      sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
-      const int MB = (p.P == 1) ? 4 : 2;
-      const int tokens_per_wg = (4 / sa.KS) * MB * 16;
-      const unsigned grid = (unsigned)ceil_div(h.n_vis, tokens_per_wg);
+      const int cus = device_cu_count();
       for (int q0 = 0; q0 < h.n_q; q0 += 64) {
         sa.q0 = q0;
         sa.n_q = std::min(64, h.n_q - q0);
         sa.accumulate = q0 > 0;
         const int NB = (sa.n_q + 15) / 16;
+        const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P * NB, cus);
+        sa.nseg = L.nseg;
+        sa.ksteps = L.ksteps;
+        sa.S = L.S;
+        sa.nphase = L.nphase;
+        sa.nwg = L.nwg;
         if (bf16)
-          rc = p.P == 3 ? launch_score_p<bf16_t, 3>(sa, MB, NB, grid, s)
-                        : launch_score_p<bf16_t, 1>(sa, MB, NB, grid, s);
+          rc = p.P == 3 ? launch_lds<bf16_t, 3>(sa, L, NB, s) : launch_lds<bf16_t, 1>(sa, L, NB, s);
         else
-          rc = launch_score_p<float, 1>(sa, MB, NB, grid, s);
+          rc = launch_lds<float, 1>(sa, L, NB, s);
         if (rc) return rc;
       }
     } else {

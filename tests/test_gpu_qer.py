@@ -53,6 +53,10 @@ def test_workload_scores_and_topk(cfg):
                                             (16, 8, 2, 32),     # GQA fold
                                             (48, 28, 4, 128),   # GQA, high-res workload heads
                                             (3, 1, 1, 16),      # single head, d = 16
+                                            (5, 3, 3, 16),      # contraction 48: tail only
+                                            (7, 5, 5, 16),      # 80: one segment + 16 tail
+                                            (9, 2, 2, 48),      # 96: one segment + 32 tail
+                                            (10, 7, 7, 16),     # 112: one segment + 48 tail
                                             (33, 28, 28, 128)]) # long contraction (k-split)
 def test_shapes(dtype, n_q, H_q, H_kv, d):
     tokens = [17, 0, 40, 1, 33, 64, 5, 0, 29]
@@ -125,3 +129,14 @@ def test_deterministic_and_workspace():
     w2, i2 = B.cofie_qer_rank(Qd, Kd, od, 16, workspace=ws)
     torch.cuda.synchronize()
     assert torch.equal(w1, w2) and torch.equal(i1, i2)
+
+
+def test_many_tokens_per_workgroup():
+    """More 16-token tiles than one pass of a workgroup's waves covers (the
+    score kernel loops over rounds of tiles, refilling the query phases), with
+    a contraction of several query phases."""
+    n_q, H, d = 4, 32, 128
+    tokens = [10000] * 7
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(4242, n_q, int(offs[-1]), H, H, d, "bf16")
+    run_case(Q, K, offs, H, H, d, 3)
