@@ -135,10 +135,6 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
   const int wave = tid >> 6, nw = nthr >> 6;
   const int64_t t = blockIdx.x / a.splits;
   const int s = (int)(blockIdx.x - t * a.splits);
-  const int ncnt = a.nbins * P;
-  for (int i = tid; i < ncnt; i += nthr) cnt[i] = 0;
-  __syncthreads();
-
   const uint8_t* f = a.frames + t * a.frame_bytes;
   const int G = a.splits * nw;  // waves sharing this frame
   const int g = s * nw + wave;
@@ -160,9 +156,16 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
     for (int j = 0; j < kUnroll; ++j)
       if (g + (b * kUnroll + j) * G < a.units) count12<KIND, P, BC>(cnt, v[j], lane, a);
   };
+  // the first batch is issued before the counters are cleared; the barrier
+  // orders LDS only, so it does not wait for those loads
+  U3 va[kUnroll], vb[kUnroll];
+  if (nbatch > 0) load_batch(va, 0);
+  const int ncnt = a.nbins * P;
+  for (int i = tid; i < ncnt; i += nthr) cnt[i] = 0;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   if (nbatch > 0) {
-    U3 va[kUnroll], vb[kUnroll];
-    load_batch(va, 0);
     int b = 0;
     for (; b + 2 <= nbatch; b += 2) {
       load_batch(vb, b + 1);
