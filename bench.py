@@ -45,6 +45,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="target wall time of the CPU oracle sample")
+    ap.add_argument("--configs", default="",
+                    help="comma-separated workload ids (1-5): print a per-workload stage report "
+                         "(one JSON line each) instead of the headline step")
+    ap.add_argument("--report", default="", help="with --configs: also write a markdown table here")
+    ap.add_argument("--ms-streams", type=int, default=8,
+                    help="with --configs 5: streams whose queries are ranked (of 32)")
     return ap.parse_args()
 
 
@@ -64,6 +70,9 @@ def main():
         raise RuntimeError("bench.py needs a GPU")
     torch.cuda.set_device(0)
     B.lib()
+    if args.configs:
+        config_report(args, [int(c) for c in args.configs.split(",")])
+        return
     cfg = 2
     wl = synth.WORKLOADS[cfg]
     n, H, W, C = wl.T, wl.H, wl.W, 3
@@ -281,6 +290,269 @@ def measured_traffic(kernel: str):
                 return None
             return int(parts[2]) if digest == parts[4] else None
     return None
+
+
+def read_probe_gbs(torch, B) -> float:
+    """Plain streaming read of 1 GiB (the attainable HBM read rate)."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(1 << 20, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        B.cofie_diag_stream_read(src, sink)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        B.cofie_diag_stream_read(src, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    return (1 << 30) / (e0.elapsed_time(e1) * 1e-3 / 10) / 1e9
+
+
+def median_call_us(torch, fn, reps: int, warmup: int = 3) -> float:
+    """Median over `reps` calls of fn(i), each bracketed by its own HIP events."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for i, (a, b) in enumerate(ev):
+        a.record()
+        fn(i)
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+
+
+def profiled_kernels(torch, B, fn, reps: int) -> dict:
+    """Average duration (us) of every library kernel over `reps` calls of fn(i)."""
+    B.cofie_profiler_reset()
+    B.cofie_profiler_enable(True)
+    for i in range(reps):
+        fn(i)
+    torch.cuda.synchronize()
+    B.cofie_profiler_enable(False)
+    out = {}
+    # names are matched as substrings: these are the kernels of the paths used
+    for name in ("ngff_fill", "ngff_hist", "ngff_band_next", "ngff_select", "qer_fold", "qer_score",
+                 "qer_frame_mean", "qer_topk"):
+        ms, cnt = B.cofie_profiler_read(name)
+        if cnt:
+            out[name] = round(1e3 * ms / cnt, 2)
+    B.cofie_profiler_reset()
+    return out
+
+
+def config_report(args, cfgs):
+    """Per-workload stage figures: NGFF frames/s and histogram GB/s against the
+    HBM peak and the measured read ceiling, the retention reached, QER
+    candidates/s, K GB/s and MFMA utilisation, and the CPU oracle's time on the
+    same host bytes."""
+    import torch
+    import oracle
+    from paper_2609_03675_amd import binding as B
+    from paper_2609_03675_amd import synth
+
+    probe = read_probe_gbs(torch, B)
+    modes = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
+    rows = []
+    for cfg in cfgs:
+        wl = synth.WORKLOADS[cfg]
+        n, H, W = wl.n, wl.H, wl.W
+        frame_bytes = H * W * 3
+        mode = modes[wl.hist_mode]
+        M = oracle.mass(mode, H, W)
+        seg = wl.T if wl.n_streams > 1 else 0
+        # frames, generated stream by stream; the oracle's histograms are timed
+        # on the same host bytes as they go by
+        frames = torch.empty((n, H, W, 3), dtype=torch.uint8, device="cuda")
+        cpu_hist_s = 0.0
+        hists = []
+        for st in range(wl.n_streams):
+            plan = synth.StreamPlan(cfg, st)
+            hs = []
+            for c0 in range(0, wl.T, 128):
+                c = min(128, wl.T - c0)
+                host = plan.frames(c0, c)
+                frames[st * wl.T + c0:st * wl.T + c0 + c].copy_(torch.from_numpy(host))
+                t0 = time.perf_counter()
+                hs.append(oracle.histogram(host, wl.bins, mode))
+                cpu_hist_s += time.perf_counter() - t0
+            hists.append(np.concatenate(hs))
+            del host
+        copies = [frames]
+        if n * frame_bytes * 3 < (1 << 30):  # small inputs: rotate copies past the 256 MiB cache
+            copies += [frames.clone() for _ in range(2)]
+        rule0 = B.keep_rule(wl.hist_mode, 0.3, 30, 4, seg)
+        tau = B.cofie_ngff_calibrate(frames, wl.bins, rule0, wl.target)
+        tau_np = tau.cpu().numpy()
+        t0 = time.perf_counter()
+        for st in range(wl.n_streams):
+            oracle.ngff_select(hists[st], M, float(tau_np[st]), 30, 4)
+        cpu_sel_s = time.perf_counter() - t0
+        del hists
+        count = torch.empty(wl.n_streams, dtype=torch.int32, device="cuda")
+        mask = torch.empty(n, dtype=torch.uint8, device="cuda")
+        scores = torch.empty(n, dtype=torch.float32, device="cuda")
+        ws = torch.empty(B.ngff_workspace_bytes(n, H, W, 3, wl.bins, rule0), dtype=torch.uint8,
+                         device="cuda")
+        rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, seg, tau_per_segment=tau, out_count=count,
+                           workspace=ws)
+
+        def ngff_call(i):
+            B.cofie_ngff_filter(copies[i % len(copies)], wl.bins, rule, out_scores=scores, out_mask=mask)
+
+        reps = 30 if n * frame_bytes < (1 << 30) else 10
+        ngff_us = median_call_us(torch, ngff_call, reps)
+        nk = profiled_kernels(torch, B, ngff_call, reps)
+        kept = int(count.sum().item())
+        hist_gbs = n * frame_bytes / (nk["ngff_hist"] * 1e-6) / 1e9
+        row = {"workload": wl.name, "config": cfg,
+               "ngff": {"frames": n, "us_per_call": round(ngff_us, 2),
+                        "frames_per_s": round(n / (ngff_us * 1e-6), 1),
+                        "call_GBps": round(n * frame_bytes / (ngff_us * 1e-6) / 1e9, 1),
+                        "hist_GBps": round(hist_gbs, 1), "hist_frac_hbm": round(hist_gbs / HBM_PEAK_GBS, 4),
+                        "hist_frac_read_probe": round(hist_gbs / probe, 4),
+                        "kept": kept, "retention": round(kept / n, 4), "target_retention": wl.retain,
+                        "kernels_us": nk, "oracle_s": round(cpu_hist_s + cpu_sel_s, 3),
+                        "oracle_cores": oracle.num_threads()}}
+        mask_np = mask.cpu().numpy()
+        del copies, frames, ws
+        torch.cuda.empty_cache()
+
+        if cfg != 5:
+            row["qer"] = qer_single(torch, B, oracle, synth, wl, cfg, probe)
+        else:
+            row["qer"] = qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, args.ms_streams)
+        row["read_probe_GBps"] = round(probe, 1)
+        print(json.dumps(row), flush=True)
+        rows.append(row)
+    if args.report:
+        write_report(args, rows, probe)
+
+
+def qer_figures(calls, n_cand, total_us, kbytes, score_us, flops, flops_head, kernels, cpu_s, probe):
+    gbs = kbytes / (score_us * 1e-6) / 1e9
+    return {"calls": calls, "candidates": n_cand, "us_total": round(total_us, 2),
+            "candidates_per_s": round(n_cand / (total_us * 1e-6), 1),
+            "score_GBps": round(gbs, 1), "score_frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+            "score_frac_read_probe": round(gbs / probe, 4),
+            "mfma_util_computed": round(flops / (score_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "per_head_TFLOPs": round(flops_head / (score_us * 1e-6) / 1e12, 1),
+            "kernels_us_per_call": kernels, "oracle_s": round(cpu_s, 3)}
+
+
+def qer_single(torch, B, oracle, synth, wl, cfg, probe):
+    """One ranking call over the workload's candidates; K rotated over enough
+    copies to exceed 512 MiB (at most 8)."""
+    Q, K, offs = synth.qer_inputs(cfg)
+    bf16 = wl.qk_dtype == "bf16"
+
+    def dev(x):
+        return torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) if bf16 else torch.from_numpy(x).cuda()
+
+    Qd = dev(Q)
+    Kc = [dev(K)]
+    ncopy = min(8, max(2, -(-(512 << 20) // K.nbytes)))
+    Kc += [Kc[0].clone() for _ in range(ncopy - 1)]
+    offs_d = torch.from_numpy(offs).cuda()
+    desc = B.qer_desc(wl.n_q, K.shape[0], wl.n_frames, wl.H_q, wl.H_kv, wl.d, dtype=B.BF16 if bf16 else B.F32)
+    qws = torch.empty(B.qer_workspace_bytes(desc, wl.k_top), dtype=torch.uint8, device="cuda")
+    w_out = torch.empty(wl.n_frames, dtype=torch.float32, device="cuda")
+    idx = torch.empty(wl.k_top, dtype=torch.int32, device="cuda")
+
+    def call(i):
+        B.cofie_qer_rank(Qd, Kc[i % len(Kc)], offs_d, wl.k_top, out_scores=w_out, out_idx=idx, workspace=qws)
+
+    us = median_call_us(torch, call, 30)
+    kern = profiled_kernels(torch, B, call, 30)
+    t0 = time.perf_counter()
+    oracle.topk(oracle.qer_scores(Q, K, offs, wl.H_q, wl.H_kv, wl.d), wl.k_top)
+    cpu_s = time.perf_counter() - t0
+    terms = 3 if (wl.H_q != wl.H_kv and bf16) else 1   # folded GQA carries q^ as three bf16 terms
+    flops = 2.0 * wl.n_q * K.shape[0] * wl.H_kv * wl.d * terms
+    flops_head = 2.0 * wl.n_q * K.shape[0] * wl.H_q * wl.d
+    return qer_figures(1, wl.n_frames, us, K.nbytes + Q.nbytes, kern["qer_score"], flops, flops_head, kern,
+                       cpu_s, probe)
+
+
+def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams):
+    """Each query of the first n_streams streams ranks that stream's NGFF-kept
+    frames up to the query time (its own call, K shared by the stream's queries)."""
+    total_us = cpu_s = score_us = flops = 0.0
+    n_cand = calls = kbytes = 0
+    acc = {}
+    for st in range(min(n_streams, wl.n_streams)):
+        kept = np.flatnonzero(mask_np[st * wl.T:(st + 1) * wl.T])
+        stamps = synth.multistream_queries(cfg, st)
+        last = kept[kept <= stamps.max()]
+        K_all = synth.multistream_k(cfg, st, last)
+        Kd = torch.from_numpy(K_all.view(np.int16)).cuda().view(torch.bfloat16)
+        for qi, ts in enumerate(stamps):
+            nc = int((kept <= ts).sum())
+            if nc == 0:
+                continue
+            Q = synth.multistream_q(cfg, st, qi)
+            Qd = torch.from_numpy(Q.view(np.int16)).cuda().view(torch.bfloat16)
+            offs = synth.frame_offsets(np.full(nc, wl.tokens))
+            offs_d = torch.from_numpy(offs).cuda()
+            k = min(wl.k_top, nc)
+            Ksl = Kd[:nc * wl.tokens]
+
+            def call(i, Qd=Qd, Ksl=Ksl, offs_d=offs_d, k=k):
+                B.cofie_qer_rank(Qd, Ksl, offs_d, k)
+
+            total_us += median_call_us(torch, call, 10)
+            kern = profiled_kernels(torch, B, call, 10)
+            for name, v in kern.items():
+                acc[name] = acc.get(name, 0.0) + v
+            score_us += kern["qer_score"]
+            t0 = time.perf_counter()
+            oracle.topk(oracle.qer_scores(Q, K_all[:nc * wl.tokens], offs, wl.H_q, wl.H_kv, wl.d), k)
+            cpu_s += time.perf_counter() - t0
+            n_cand += nc
+            calls += 1
+            kbytes += nc * wl.tokens * wl.H_kv * wl.d * 2 + Q.nbytes
+            flops += 2.0 * wl.n_q * nc * wl.tokens * wl.H_kv * wl.d
+        del Kd
+    kern = {name: round(v / max(calls, 1), 2) for name, v in acc.items()}
+    return qer_figures(calls, n_cand, total_us, kbytes, score_us, flops, flops, kern, cpu_s, probe)
+
+
+def write_report(args, rows, probe):
+    cmd = f"python bench.py --configs {args.configs} --report {args.report}"
+    lines = ["# Per-workload stage throughput (NGFF and QER) on one MI355X", "",
+             "Command (from the repository root):", "", "```", cmd, "```", "",
+             f"Read-probe ceiling (plain 1 GiB streaming read): {probe:.0f} GB/s.  HBM peak 8000 GB/s.  "
+             "Call times are medians of per-call HIP-event brackets; kernel times are averages of the "
+             "library's per-kernel HIP-event profiler.  NGFF inputs under 1 GiB are rotated over three "
+             "copies and K over enough copies to exceed 512 MiB, so the 256 MiB last-level cache cannot "
+             "serve a call from the previous one.  The oracle columns time the CPU oracle on the same host "
+             "bytes (all host cores).", "", "## NGFF", "",
+             "| workload | frames | µs / call | frames/s | hist GB/s | % of 8 TB/s | % of read probe | "
+             "kept (retention; target) | oracle s (threads) |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        g = r["ngff"]
+        lines.append(f"| {r['workload']} | {g['frames']} | {g['us_per_call']:.1f} | {g['frames_per_s']:,.0f} | "
+                     f"{g['hist_GBps']:.0f} | {100 * g['hist_frac_hbm']:.1f} | "
+                     f"{100 * g['hist_frac_read_probe']:.1f} | {g['kept']} ({g['retention']:.3f}; "
+                     f"{g['target_retention']}) | {g['oracle_s']:.2f} ({g['oracle_cores']}) |")
+    lines += ["", "## QER", "",
+              "| workload | calls | candidates | µs total | candidates/s | score GB/s | % of 8 TB/s | "
+              "% of read probe | MFMA util | per-head TFLOP/s | oracle s |",
+              "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        q = r["qer"]
+        lines.append(f"| {r['workload']} | {q['calls']} | {q['candidates']} | {q['us_total']:.1f} | "
+                     f"{q['candidates_per_s']:,.0f} | {q['score_GBps']:.0f} | {100 * q['score_frac_hbm']:.1f} | "
+                     f"{100 * q['score_frac_read_probe']:.1f} | {100 * q['mfma_util_computed']:.2f} % | "
+                     f"{q['per_head_TFLOPs']:.1f} | {q['oracle_s']:.2f} |")
+    lines += ["", "MFMA utilisation = MFMA flops issued (the folded contraction; three bf16 query terms for "
+              "grouped-query attention) / score-kernel time / 2.5 PFLOP/s.  Per-head TFLOP/s counts the "
+              "per-head form 2·n_q·n_vis·H_q·d.", "", "Kernel times (µs per call):", ""]
+    for r in rows:
+        lines.append(f"- {r['workload']}: NGFF {r['ngff']['kernels_us']}; QER {r['qer']['kernels_us_per_call']}")
+    with open(args.report, "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def cpu_baseline(wl, frames_np, Q_np, K_np, offs_np, tau, target_s):

@@ -17,8 +17,8 @@
 //   the text-by-vision matrix is never stored.
 // qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7).
 // qer_topk: one workgroup ranks the frames by (score desc, frame asc) on
-//   order-preserving 32-bit keys (counting ranks in LDS, or a radix select for
-//   very many frames) and writes the top k in chronological order (Eq. 8).
+//   order-preserving 32-bit keys (a 4-pass radix select) and writes the top k
+//   in chronological order (Eq. 8).
 // SOFTMAX mode: per-(head, query) row statistics over all visual keys, merged
 //   across workgroups, then a second pass forming the head mean of the
 //   normalised probabilities and its max over query rows.
@@ -480,97 +480,119 @@ __global__ __launch_bounds__(256) void qer_frame_mean_kernel(const float* m, int
   }
 }
 
-constexpr int kRankMax = 4096;  // frames ranked by counting in LDS
+constexpr int kTopkCount = 128;   // up to this many frames: ranks by counting
+constexpr int kTopkStage = 8192;  // up to this many frames: keys staged in LDS
 
 // Eq. 8: the k frames of largest score (ties to the lower index), written in
-// chronological order and padded with -1.  Up to kRankMax frames, every frame's
-// rank is counted against all keys held in LDS; above that, a radix select
-// finds the k-th key (8 bits per pass).
+// chronological order and padded with -1.  One workgroup.  Up to kTopkCount
+// frames each frame's rank is counted against every key.  Beyond, a radix
+// select on the order-preserving 32-bit keys finds the k-th largest key (8
+// bits per pass, the digit located by a suffix scan of the 256 digit counts)
+// and how many keys equal to it are taken; a scan over the frames in index
+// order then writes the selected indices, each thread owning a contiguous
+// chunk of frames.
 __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_frames,
                                                         int32_t k_top, int32_t* out_idx) {
-  __shared__ __align__(16) uint32_t keys[kRankMax];
+  __shared__ __align__(16) uint32_t keys_sh[kTopkStage];
   __shared__ int hist[256];
   __shared__ int wsum[16];
   __shared__ uint32_t sh_prefix;
-  __shared__ int sh_remaining;
-  const int tid = threadIdx.x, nthr = blockDim.x;
+  __shared__ int sh_need;
+  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6;
   const int k = k_top < n_frames ? k_top : n_frames;
-  if (k > 0) {
-    uint32_t kth = 0;
-    int take_eq = 0;
-    const bool small = n_frames <= kRankMax;
-    if (small) {
-      // order keys are >= 0x007FFFFF (the key of -inf), so padding with 0 is
-      // never counted as beating a frame
-      const int padded = (n_frames + 3) & ~3;
-      for (int f = tid; f < padded; f += nthr) keys[f] = f < n_frames ? keys_g[f] : 0u;
-      __syncthreads();
-    } else {
-      if (tid == 0) {
-        sh_prefix = 0;
-        sh_remaining = k;
-      }
-      uint32_t mask = 0;
-      for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = tid; i < 256; i += nthr) hist[i] = 0;
-        __syncthreads();
-        const uint32_t prefix = sh_prefix;
-        const int need = sh_remaining;
-        for (int f = tid; f < n_frames; f += nthr) {
-          const uint32_t key = keys_g[f];
-          if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-        }
-        __syncthreads();
-        // the digit d with (count of digits > d) < need <= (count of digits >= d)
-        if (tid < 256) {
-          int above = 0;
-          for (int e = 255; e > tid; --e) above += hist[e];
-          if (above < need && above + hist[tid] >= need) {
-            sh_prefix = prefix | ((uint32_t)tid << shift);
-            sh_remaining = need - above;
-          }
-        }
-        mask |= 255u << shift;
-        __syncthreads();
-      }
-      kth = sh_prefix;
-      take_eq = sh_remaining;
-    }
-    int eq_base = 0, out_base = 0;
-    for (int f0 = 0; f0 < n_frames; f0 += nthr) {
-      const int f = f0 + tid;
-      int sel = 0;
-      if (small) {
-        if (f < n_frames) {
-          // rank = frames that beat f; keys are read four at a time (the LDS
-          // copy is padded with zero keys, which never beat anything)
-          const uint32_t kf = keys[f];
-          int rank = 0;
-          const uint4* k4 = reinterpret_cast<const uint4*>(keys);
-          const int nq = (n_frames + 3) >> 2;
+  if (k > 0 && n_frames <= kTopkCount) {
+    // rank = frames that beat f; keys are read four at a time (the LDS copy is
+    // padded with zero keys, which never beat anything: a key is >= the key
+    // of -inf, 0x007FFFFF)
+    const int padded = (n_frames + 3) & ~3;
+    for (int f = tid; f < padded; f += nthr) keys_sh[f] = f < n_frames ? keys_g[f] : 0u;
+    __syncthreads();
+    int sel = 0;
+    if (tid < n_frames) {
+      const uint32_t kf = keys_sh[tid];
+      const uint4* k4 = reinterpret_cast<const uint4*>(keys_sh);
+      int rank = 0;
 #pragma unroll 4
-          for (int q = 0; q < nq; ++q) {
-            const uint4 v = k4[q];
-            const int g = 4 * q;
-            rank += (v.x > kf) || (v.x == kf && g < f);
-            rank += (v.y > kf) || (v.y == kf && g + 1 < f);
-            rank += (v.z > kf) || (v.z == kf && g + 2 < f);
-            rank += (v.w > kf) || (v.w == kf && g + 3 < f);
-          }
-          sel = rank < k;
-        }
-      } else {
-        const uint32_t key = f < n_frames ? keys_g[f] : 0u;
-        const int is_eq = (f < n_frames && key == kth) ? 1 : 0;
-        int eq_total;
-        const int eq_rank = eq_base + block_exscan(is_eq, &eq_total, wsum);
-        sel = (f < n_frames) && (key > kth || (is_eq && eq_rank < take_eq)) ? 1 : 0;
-        eq_base += eq_total;
+      for (int q = 0; q < padded / 4; ++q) {
+        const uint4 v = k4[q];
+        const int g = 4 * q;
+        rank += (v.x > kf) || (v.x == kf && g < tid);
+        rank += (v.y > kf) || (v.y == kf && g + 1 < tid);
+        rank += (v.z > kf) || (v.z == kf && g + 2 < tid);
+        rank += (v.w > kf) || (v.w == kf && g + 3 < tid);
       }
-      int sel_total;
-      const int pos = out_base + block_exscan(sel, &sel_total, wsum);
-      if (sel) out_idx[pos] = f;
-      out_base += sel_total;
+      sel = rank < k ? 1 : 0;
+    }
+    int total;
+    const int pos = block_exscan(sel, &total, wsum);
+    if (sel) out_idx[pos] = tid;
+  } else if (k > 0) {
+    const bool staged = n_frames <= kTopkStage;
+    const uint32_t* keys = staged ? keys_sh : keys_g;
+    if (staged) {
+      for (int f = tid; f < n_frames; f += nthr) keys_sh[f] = keys_g[f];
+    }
+    const int chunk = (n_frames + nthr - 1) / nthr;
+    const int f_lo = tid * chunk < n_frames ? tid * chunk : n_frames;
+    const int f_hi = f_lo + chunk < n_frames ? f_lo + chunk : n_frames;
+    uint32_t prefix = 0, mask = 0;
+    int need = k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (tid < 256) hist[tid] = 0;
+      __syncthreads();
+      for (int f = f_lo; f < f_hi; ++f) {
+        const uint32_t key = keys[f];
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+      }
+      __syncthreads();
+      // thread t < 256 takes digit d = 255 - t; an inclusive scan over t gives
+      // the count of keys with digit >= d, so exactly one d has
+      // (count > d) < need <= (count >= d)
+      int ge = 0, cnt = 0;
+      if (tid < 256) {
+        cnt = hist[255 - tid];
+        ge = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(ge, o);
+          if (lane >= o) ge += y;
+        }
+        if (lane == 63) wsum[wave] = ge;
+      }
+      __syncthreads();
+      if (tid < 256) {
+        for (int i = 0; i < wave; ++i) ge += wsum[i];
+        const int above = ge - cnt;
+        if (above < need && need <= ge) {
+          sh_prefix = prefix | ((uint32_t)(255 - tid) << shift);
+          sh_need = need - above;
+        }
+      }
+      __syncthreads();
+      prefix = sh_prefix;
+      need = sh_need;
+      mask |= 255u << shift;
+    }
+    // prefix = the k-th largest key; `need` keys equal to it are taken, the
+    // lowest frame indices first
+    int n_eq = 0;
+    for (int f = f_lo; f < f_hi; ++f) n_eq += keys[f] == prefix ? 1 : 0;
+    int total;
+    int eq_rank = block_exscan(n_eq, &total, wsum);
+    int n_sel = 0;
+    for (int f = f_lo; f < f_hi; ++f) {
+      const uint32_t key = keys[f];
+      const bool eq = key == prefix;
+      n_sel += (key > prefix || (eq && eq_rank < need)) ? 1 : 0;
+      eq_rank += eq ? 1 : 0;
+    }
+    int pos = block_exscan(n_sel, &total, wsum);
+    eq_rank -= n_eq;
+    for (int f = f_lo; f < f_hi; ++f) {
+      const uint32_t key = keys[f];
+      const bool eq = key == prefix;
+      if (key > prefix || (eq && eq_rank < need)) out_idx[pos++] = f;
+      eq_rank += eq ? 1 : 0;
     }
   }
   for (int i = k + tid; i < k_top; i += nthr) out_idx[i] = -1;

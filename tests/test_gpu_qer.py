@@ -140,3 +140,24 @@ def test_many_tokens_per_workgroup():
     offs = synth.frame_offsets(tokens)
     Q, K = synth.random_qk(4242, n_q, int(offs[-1]), H, H, d, "bf16")
     run_case(Q, K, offs, H, H, d, 3)
+
+
+@pytest.mark.parametrize("n_frames", [1, 7, 128, 129, 1000, 8192, 8193, 20000])
+@pytest.mark.parametrize("k", [1, 16, 300])
+def test_topk_selection_exact(n_frames, k):
+    """The selection itself, bit for bit: the GPU's top-k indices equal the
+    oracle's top-k of the GPU's own frame scores.  One token per frame drawn
+    from 5 distinct key rows, so scores tie exactly in large groups, and every
+    13th frame is empty (score -inf); covers the counting path (<= 128 frames),
+    the radix select on LDS-staged keys (<= 8192) and on keys in memory."""
+    H, d, n_q = 1, 16, 4
+    Q, base = synth.random_qk(77, n_q, 5, H, H, d, "bf16")
+    tokens = np.where(np.arange(n_frames) % 13 == 12, 0, 1)
+    rows = (np.flatnonzero(tokens) * 7919) % 5
+    K = base[rows]
+    offs = synth.frame_offsets(tokens)
+    print(f"topk n_frames={n_frames} k={k}", flush=True)
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs), k)
+    torch.cuda.synchronize()
+    w = w.cpu().numpy()
+    assert np.array_equal(idx.cpu().numpy(), oracle.topk(w.astype(np.float64), k))
