@@ -110,8 +110,11 @@ struct ScoreLdsArgs {
 
 constexpr int kLdsWaves = 8;
 constexpr int kLdsThreads = kLdsWaves * 64;
-constexpr int kQRegs = 8;               // uint4 per thread per phase fill
-constexpr int kPhaseU4 = kQRegs * kLdsThreads;  // uint4 per phase buffer (64 KiB)
+// uint4 per thread per phase fill (a phase buffer holds q_regs * 512 uint4):
+// 32 KiB phases when the query side is narrow (fewer registers held, a shorter
+// first fill: 1 fps stream 47.2 vs 48.8 us), 64 KiB otherwise (fewer phases:
+// high-res 20.4 vs 23.1 us)
+__host__ __device__ constexpr int lds_q_regs(int PNB) { return PNB <= 2 ? 4 : 8; }
 
 // virtual steps per batch: 8 key loads per batch and wave (two batches in
 // flight), fewer where the query fragments and accumulators of wide query
@@ -143,6 +146,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
   constexpr int U = lds_batch(MB, P * NB, R);
   constexpr int FPS = P * NB;   // fragments per virtual step
+  constexpr int kQRegs = lds_q_regs(FPS);
+  constexpr int kPhaseU4 = kQRegs * kLdsThreads;
   static_assert(U % VPS == 0, "batches hold whole segments");
   extern __shared__ uint4 qs[];  // [2][kPhaseU4]: [S][P][NB][64] each
 
@@ -262,8 +267,9 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
           for (int k = 0; k < VPS; ++k) {
             // operand k: the load ((l%16)/R - k) mod VPS of lane l + R k
-            // the register choice is a bit-mask blend: a select between
-            // array elements would be folded into an indexed (stack) load
+            // the register choice: a select of two loaded values, or for 4
+            // loads a bit-mask blend (a select chain between array elements
+            // would be folded into an indexed stack load)
             uint32_t pick[VPS];
 #pragma unroll
             for (int q = 0; q < VPS; ++q) pick[q] = ((qs_lane - k) & (VPS - 1)) == q ? ~0u : 0u;
@@ -271,13 +277,18 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
             for (int j = 0; j < MB; ++j) {
               uint4 send = {0u, 0u, 0u, 0u};
+              if constexpr (VPS == 2) {
+                const uint4 c0 = cur[VPS * h][j], c1 = cur[VPS * h + 1][j];
+                send = pick[0] ? c0 : c1;
+              } else {
 #pragma unroll
-              for (int q = 0; q < VPS; ++q) {
-                const uint4 c = cur[VPS * h + q][j];
-                send.x |= c.x & pick[q];
-                send.y |= c.y & pick[q];
-                send.z |= c.z & pick[q];
-                send.w |= c.w & pick[q];
+                for (int q = 0; q < VPS; ++q) {
+                  const uint4 c = cur[VPS * h + q][j];
+                  send.x |= c.x & pick[q];
+                  send.y |= c.y & pick[q];
+                  send.z |= c.z & pick[q];
+                  send.w |= c.w & pick[q];
+                }
               }
               if constexpr (VPS == 2) {
                 fk[j] = k == 0 ? send : row_ror4<8>(send);
@@ -848,9 +859,10 @@ LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int PNB, int cus
   const int64_t seg_el = (1024 / L.R) / (int64_t)esize;  // elements per segment
   L.nseg = (int)(Lc / seg_el);
   L.ksteps = (int)((16 / L.R) * L.nseg + ceil_div(Lc % seg_el, kps));
-  L.S = (int)std::min<int64_t>((kPhaseU4 / 64) / PNB / U * U, ceil_div(L.ksteps, U) * U);
+  const int phase_u4 = lds_q_regs(PNB) * kLdsThreads;
+  L.S = (int)std::min<int64_t>((phase_u4 / 64) / PNB / U * U, ceil_div(L.ksteps, U) * U);
   L.nphase = (int)ceil_div(L.ksteps, L.S);
-  L.lds = (size_t)(L.nphase > 1 ? 2 : 1) * kPhaseU4 * sizeof(uint4);
+  L.lds = (size_t)(L.nphase > 1 ? 2 : 1) * phase_u4 * sizeof(uint4);
   return L;
 }
 
