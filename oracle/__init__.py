@@ -6,13 +6,17 @@ Only the test-suite, ``__graft_entry__.smoke()`` and the benchmark's
 the HIP implementation in ``paper_2609_03675_amd``.
 
 Paper sections followed: Sec. 3.2 (NGFF: histogram, total-variation distance,
-Eqs. 2-5 and the gap-aware safeguards) and Sec. 3.3 (QER: Eqs. 6-8).
+Eqs. 2-5 and the gap-aware safeguards), Sec. 3.3 (QER: Eqs. 6-8) and the glue
+between them (the candidate set S_c as frame indices, Sec. 3.1-3.2; removal of
+the frames outside S_e from a token sequence, chronological, Sec. 3.3).
 
 Parity status: every function here is pinned by the CPU tests under
 ``tests/test_oracle_*.py`` (closed forms, invariants, brute force, library
 routines, the paper's printed drop-ratio compositions).  The retention-target
 calibration (``ngff_calibrate``) is not in the paper; it is pinned by a brute
-force over every integer threshold on small inputs.
+force over every integer threshold on small inputs.  The glue functions are
+pinned by hand-built cases, numpy's flatnonzero and a row-by-row brute force
+(``tests/test_oracle_glue.py``).
 """
 from __future__ import annotations
 
@@ -69,6 +73,10 @@ def _load():
     lib.orc_qer_scores.restype = ctypes.c_int
     lib.orc_topk.argtypes = [P, i32, i32, P]
     lib.orc_topk.restype = ctypes.c_int
+    lib.orc_mask_compact.argtypes = [P, i64, i64, P, P]
+    lib.orc_mask_compact.restype = i64
+    lib.orc_gather_frames.argtypes = [P, i64, i64, P, i32, P, i32, P, i64, P, P]
+    lib.orc_gather_frames.restype = i64
     _lib = lib
     return lib
 
@@ -179,3 +187,43 @@ def topk(w: np.ndarray, k_top: int) -> np.ndarray:
     rc = _load().orc_topk(_ptr(a), a.size, k_top, _ptr(idx))
     assert rc == 0
     return idx[:k_top]
+
+
+def mask_compact(mask: np.ndarray, seg_len: int = 0):
+    """S_c as frame indices (increasing) and per-segment starts [nseg+1]."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    n = m.size
+    nseg = -(-n // seg_len) if seg_len > 0 else 1
+    idx = np.full(max(n, 1), -1, dtype=np.int32)
+    seg_start = np.zeros(nseg + 1, dtype=np.int32)
+    total = _load().orc_mask_compact(_ptr(m), n, seg_len, _ptr(idx), _ptr(seg_start))
+    return idx[:total], seg_start
+
+
+def gather_frames(src: np.ndarray, frame_offsets: np.ndarray, sel: np.ndarray, capacity: int = -1):
+    """Rows of the selected frames, in the order of ``sel`` (Sec. 3.3 frame
+    refinement).  ``src`` is [n_rows][...] (any dtype; rows are byte blocks).
+    Returns (dst [min(total, capacity)][...], out_offs int32 [k+1],
+    out_rows int32 [min(total, capacity)])."""
+    s = np.ascontiguousarray(src)
+    n_rows = s.shape[0]
+    row_bytes = s.nbytes // n_rows if n_rows else (s.itemsize * int(np.prod(s.shape[1:])))
+    offs = np.ascontiguousarray(frame_offsets, dtype=np.int32)
+    sel_ = np.ascontiguousarray(sel, dtype=np.int32)
+    k = sel_.size
+    lengths = []
+    for f in sel_:
+        if 0 <= f < offs.size - 1:
+            lo = min(max(int(offs[f]), 0), n_rows)
+            hi = max(lo, min(max(int(offs[f + 1]), 0), n_rows))
+            lengths.append(hi - lo)
+    total = int(sum(lengths))
+    cap = total if capacity < 0 else capacity
+    dst = np.zeros((max(min(total, cap), 1),) + s.shape[1:], dtype=s.dtype)
+    out_offs = np.zeros(k + 1, dtype=np.int32)
+    out_rows = np.full(max(min(total, cap), 1), -1, dtype=np.int32)
+    got = _load().orc_gather_frames(_ptr(s), n_rows, row_bytes, _ptr(offs), offs.size - 1, _ptr(sel_), k,
+                                    _ptr(dst), cap, _ptr(out_offs), _ptr(out_rows))
+    assert got == total
+    m = min(total, cap)
+    return dst[:m], out_offs, out_rows[:m]

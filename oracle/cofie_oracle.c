@@ -417,3 +417,60 @@ int orc_topk(const double* w, int32_t n, int32_t k_top, int32_t* idx) {
   free(taken);
   return 0;
 }
+
+/* ---- coarse-to-fine glue ------------------------------------------------- */
+
+/* The candidate set S_c that NGFF hands to the visual encoder (Sec. 3.1,
+ * Sec. 3.2): the indices of the nonzero entries of mask[n], in increasing
+ * (chronological) order, written to idx; and for each stream segment of
+ * seg_len frames (seg_len = 0: one segment; the last may be shorter), the
+ * number of candidates in the segments before it, seg_start[0..nseg], with
+ * seg_start[nseg] the total.  Returns the total.                            */
+int64_t orc_mask_compact(const uint8_t* mask, int64_t n, int64_t seg_len, int32_t* idx,
+                         int32_t* seg_start) {
+  const int64_t nseg = seg_len > 0 ? (n + seg_len - 1) / seg_len : 1;
+  int64_t c = 0;
+  for (int64_t s = 0; s < nseg; ++s) {
+    seg_start[s] = (int32_t)c;
+    const int64_t lo = seg_len > 0 ? s * seg_len : 0;
+    const int64_t hi = seg_len > 0 && lo + seg_len < n ? lo + seg_len : n;
+    for (int64_t t = lo; t < hi; ++t)
+      if (mask[t]) idx[c++] = (int32_t)t;
+  }
+  seg_start[nseg] = (int32_t)c;
+  return c;
+}
+
+/* Frame refinement (Sec. 3.3): frames outside S_e are removed from the token
+ * sequence (hidden states, cached keys/values, positions) and the kept frames
+ * stay in chronological order.  src holds n_rows rows of row_bytes bytes;
+ * frame f owns rows [lo, hi) with lo = clamp(offs[f], 0, n_rows) and
+ * hi = max(lo, clamp(offs[f+1], 0, n_rows)).  For i = 0..k-1 the rows of frame
+ * sel[i] (none when sel[i] is outside [0, n_frames), e.g. the -1 padding of a
+ * top-k) are appended to dst, at most dst_capacity rows being written;
+ * out_offs[0..k] is the CSR of the appended rows (counted in full, so a total
+ * beyond the capacity shows the shortfall) and out_rows[r] the source row of
+ * dst row r (r < capacity).  Returns the total row count.                   */
+int64_t orc_gather_frames(const uint8_t* src, int64_t n_rows, int64_t row_bytes, const int32_t* offs,
+                          int32_t n_frames, const int32_t* sel, int32_t k, uint8_t* dst,
+                          int64_t dst_capacity, int32_t* out_offs, int32_t* out_rows) {
+  int64_t pos = 0;
+  out_offs[0] = 0;
+  for (int32_t i = 0; i < k; ++i) {
+    const int32_t f = sel[i];
+    if (f >= 0 && f < n_frames) {
+      int64_t lo = offs[f], hi = offs[f + 1];
+      lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
+      hi = hi < 0 ? 0 : (hi > n_rows ? n_rows : hi);
+      if (hi < lo) hi = lo;
+      for (int64_t r = lo; r < hi; ++r, ++pos) {
+        if (pos < dst_capacity) {
+          memcpy(dst + pos * row_bytes, src + r * row_bytes, (size_t)row_bytes);
+          out_rows[pos] = (int32_t)r;
+        }
+      }
+    }
+    out_offs[i + 1] = (int32_t)pos;
+  }
+  return pos;
+}
