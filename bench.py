@@ -309,17 +309,22 @@ def read_probe_gbs(torch, B) -> float:
 
 
 def median_call_us(torch, fn, reps: int, warmup: int = 3) -> float:
-    """Median over `reps` calls of fn(i), each bracketed by its own HIP events."""
+    """GPU time per call of fn(i): `reps` calls enqueued back to back between two
+    HIP events, three such runs, the median of their means (the host's launch
+    latency stays outside, as in a pipeline that keeps the GPU fed)."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    for i, (a, b) in enumerate(ev):
+    runs = []
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        fn(i)
+        for i in range(reps):
+            fn(i)
         b.record()
-    torch.cuda.synchronize()
-    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+        torch.cuda.synchronize()
+        runs.append(a.elapsed_time(b) * 1e3 / reps)
+    return float(np.median(runs))
 
 
 def profiled_kernels(torch, B, fn, reps: int) -> dict:
@@ -352,6 +357,7 @@ def config_report(args, cfgs):
     from paper_2609_03675_amd import synth
 
     probe = read_probe_gbs(torch, B)
+    copy_probe = copy_probe_gbs(torch, B)
     modes = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
     rows = []
     for cfg in cfgs:
@@ -415,13 +421,19 @@ def config_report(args, cfgs):
                         "kernels_us": nk, "oracle_s": round(cpu_hist_s + cpu_sel_s, 3),
                         "oracle_cores": oracle.num_threads()}}
         mask_np = mask.cpu().numpy()
+        seg_len = wl.T if wl.n_streams > 1 else 0
+        cidx, cseg = B.cofie_mask_compact(mask, seg_len)
+        compact_us = median_call_us(torch, lambda i: B.cofie_mask_compact(mask, seg_len, out_idx=cidx,
+                                                                          out_seg_start=cseg), 30)
         del copies, frames, ws
         torch.cuda.empty_cache()
 
         if cfg != 5:
-            row["qer"] = qer_single(torch, B, oracle, synth, wl, cfg, probe)
+            row["qer"], gather = qer_single(torch, B, oracle, synth, wl, cfg, probe, copy_probe)
         else:
             row["qer"] = qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, args.ms_streams)
+            gather = None
+        row["glue"] = {"compact_us": round(compact_us, 2), "gather": gather}
         row["read_probe_GBps"] = round(probe, 1)
         print(json.dumps(row), flush=True)
         rows.append(row)
@@ -440,9 +452,19 @@ def qer_figures(calls, n_cand, total_us, kbytes, score_us, flops, flops_head, ke
             "kernels_us_per_call": kernels, "oracle_s": round(cpu_s, 3)}
 
 
-def qer_single(torch, B, oracle, synth, wl, cfg, probe):
+def copy_probe_gbs(torch, B) -> float:
+    """Plain streaming copy of 1 GiB, bytes read + written per second."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    us = median_call_us(torch, lambda i: B.cofie_diag_stream_copy(src, dst), 10)
+    return 2 * (1 << 30) / (us * 1e-6) / 1e9
+
+
+def qer_single(torch, B, oracle, synth, wl, cfg, probe, copy_probe):
     """One ranking call over the workload's candidates; K rotated over enough
-    copies to exceed 512 MiB (at most 8)."""
+    copies to exceed 512 MiB (at most 8).  Then the glue after it: the keys of
+    the selected frames gathered in chronological order (the shortened key
+    sequence of Sec. 3.3), timed against the plain copy."""
     Q, K, offs = synth.qer_inputs(cfg)
     bf16 = wl.qk_dtype == "bf16"
 
@@ -470,8 +492,24 @@ def qer_single(torch, B, oracle, synth, wl, cfg, probe):
     terms = 3 if (wl.H_q != wl.H_kv and bf16) else 1   # folded GQA carries q^ as three bf16 terms
     flops = 2.0 * wl.n_q * K.shape[0] * wl.H_kv * wl.d * terms
     flops_head = 2.0 * wl.n_q * K.shape[0] * wl.H_q * wl.d
-    return qer_figures(1, wl.n_frames, us, K.nbytes + Q.nbytes, kern["qer_score"], flops, flops_head, kern,
-                       cpu_s, probe)
+    fig = qer_figures(1, wl.n_frames, us, K.nbytes + Q.nbytes, kern["qer_score"], flops, flops_head, kern,
+                      cpu_s, probe)
+
+    cap = K.shape[0]
+    dst = torch.empty_like(Kc[0])
+    goffs = torch.empty(wl.k_top + 1, dtype=torch.int32, device="cuda")
+    grows = torch.empty(cap, dtype=torch.int32, device="cuda")
+
+    def gather(i):
+        B.cofie_gather_frames(Kc[i % len(Kc)], offs_d, idx, dst=dst, out_offsets=goffs, out_rows=grows)
+
+    gus = median_call_us(torch, gather, 30)
+    rows = int(goffs[-1].item())
+    moved = 2 * rows * (K.nbytes // K.shape[0])
+    gbs = moved / (gus * 1e-6) / 1e9
+    g = {"frames": int((idx >= 0).sum().item()), "rows": rows, "us": round(gus, 2), "GBps": round(gbs, 1),
+         "frac_copy_probe": round(gbs / copy_probe, 4), "copy_probe_GBps": round(copy_probe, 1)}
+    return fig, g
 
 
 def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams):
@@ -522,7 +560,7 @@ def write_report(args, rows, probe):
     lines = ["# Per-workload stage throughput (NGFF and QER) on one MI355X", "",
              "Command (from the repository root):", "", "```", cmd, "```", "",
              f"Read-probe ceiling (plain 1 GiB streaming read): {probe:.0f} GB/s.  HBM peak 8000 GB/s.  "
-             "Call times are medians of per-call HIP-event brackets; kernel times are averages of the "
+             "Call times: calls enqueued back to back between two HIP events (median of three runs); kernel times are averages of the "
              "library's per-kernel HIP-event profiler.  NGFF inputs under 1 GiB are rotated over three "
              "copies and K over enough copies to exceed 512 MiB, so the 256 MiB last-level cache cannot "
              "serve a call from the previous one.  The oracle columns time the CPU oracle on the same host "
@@ -546,6 +584,19 @@ def write_report(args, rows, probe):
                      f"{q['candidates_per_s']:,.0f} | {q['score_GBps']:.0f} | {100 * q['score_frac_hbm']:.1f} | "
                      f"{100 * q['score_frac_read_probe']:.1f} | {100 * q['mfma_util_computed']:.2f} % | "
                      f"{q['per_head_TFLOPs']:.1f} | {q['oracle_s']:.2f} |")
+    lines += ["", "## Glue", "",
+              "| workload | compaction µs | gathered frames | rows | gather µs | gather GB/s (read + write) | "
+              "% of copy probe |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        g = r["glue"]
+        ga = g["gather"]
+        if ga:
+            lines.append(f"| {r['workload']} | {g['compact_us']:.1f} | {ga['frames']} | {ga['rows']} | {ga['us']:.1f} | "
+                         f"{ga['GBps']:.0f} | {100 * ga['frac_copy_probe']:.1f} |")
+        else:
+            lines.append(f"| {r['workload']} | {g['compact_us']:.1f} | | | | | |")
+    lines += ["", "Compaction: `cofie_mask_compact` of the NGFF mask.  Gather: `cofie_gather_frames` of the keys "
+              "of the QER-selected frames (chronological), bytes read + written.", ""]
     lines += ["", "MFMA utilisation = MFMA flops issued (the folded contraction; three bf16 query terms for "
               "grouped-query attention) / score-kernel time / 2.5 PFLOP/s.  Per-head TFLOP/s counts the "
               "per-head form 2·n_q·n_vis·H_q·d.", "", "Kernel times (µs per call):", ""]

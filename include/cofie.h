@@ -194,6 +194,49 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
                    const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
                    int32_t* out_idx, void* stream);
 
+/* ---- coarse-to-fine glue ------------------------------------------------ */
+
+/* The NGFF candidate set S_c as frame indices (Sec. 3.1-3.2: the candidates
+ * are the frames the visual encoder runs on).
+ *   mask           device uint8 [n]; nonzero = candidate (e.g. the out_mask of
+ *                  cofie_ngff_filter)
+ *   n              frames, 0 <= n < 2^31
+ *   segment_len    frames per stream as in cofie_keep_rule (0 = one stream;
+ *                  n_segments = ceil(n / segment_len), the last may be shorter)
+ *   out_idx        device int32 [n] (may be NULL if n == 0): the candidate
+ *                  indices in increasing (chronological) order; entries past
+ *                  the candidate count are left untouched
+ *   out_seg_start  device int32 [n_segments + 1]: candidates in the streams
+ *                  before each stream; the last entry is the candidate count
+ * Errors: EINVAL for a NULL pointer, n out of range or segment_len < 0. */
+int cofie_mask_compact(const uint8_t* mask, int64_t n, int64_t segment_len, int32_t* out_idx,
+                       int32_t* out_seg_start, void* stream);
+
+/* Frame refinement (Sec. 3.3): the frames outside S_e are removed from a token
+ * sequence (hidden states, cached keys or values, positions) and the kept
+ * frames stay in chronological order.
+ *   src                device [n_rows][row_bytes] bytes (any row type)
+ *   frame_offsets      device int32 [n_frames+1], CSR of the frames' rows,
+ *                      clamped as in cofie_qer_rank (an inverted range is empty)
+ *   sel, k             device int32 [k]: the frames to keep, in output order
+ *                      (the out_idx of cofie_qer_rank is chronological); entries
+ *                      outside [0, n_frames), such as its -1 padding, keep nothing
+ *   dst                device [dst_capacity_rows][row_bytes]: the kept rows,
+ *                      appended frame by frame; rows beyond the capacity are not
+ *                      written
+ *   out_offsets        device int32 [k+1]: CSR of the kept rows per entry of
+ *                      sel, counted in full (out_offsets[k] > capacity reports
+ *                      a short dst); the total must stay below 2^31
+ *   out_rows           optional device int32 [dst_capacity_rows]: the source
+ *                      row of every written dst row (e.g. to gather positions)
+ * 16-byte accesses when src, dst and row_bytes are 16-byte aligned.  Errors:
+ * EINVAL for NULL pointers, n_rows outside [0, 2^31), row_bytes <= 0 or a
+ * negative n_frames, k or capacity. */
+int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, const int32_t* frame_offsets,
+                        int32_t n_frames, const int32_t* sel, int32_t k, void* dst,
+                        int64_t dst_capacity_rows, int32_t* out_offsets, int32_t* out_rows,
+                        void* stream);
+
 /* ---- host helpers ------------------------------------------------------- */
 
 /* k = max(1, round(rho * n_candidates)) (Eq. 8), rounding half to even;

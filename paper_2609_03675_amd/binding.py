@@ -95,6 +95,8 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_calibrate": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), i64, P, P]),
         "cofie_qer_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32]),
         "cofie_qer_rank": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
+        "cofie_mask_compact": (ctypes.c_int, [P, i64, i64, P, P, P]),
+        "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
         "cofie_drop_total": (f64, [f64, f64]),
         "cofie_last_error": (ctypes.c_char_p, []),
@@ -297,3 +299,45 @@ def cofie_diag_stream_read(src, sink, stream=None) -> None:
     nbytes = src.numel() * src.element_size()
     _check(lib().cofie_diag_stream_read(_dev(src, "src"), nbytes, _dev(sink, "sink"), sink.numel(),
                                         _stream(stream)))
+
+
+def cofie_mask_compact(mask, segment_len: int = 0, out_idx=None, out_seg_start=None, stream=None):
+    """S_c as frame indices: (idx int32 [n], whose first seg_start[-1] entries are
+    the candidates in increasing order; seg_start int32 [n_segments+1])."""
+    import torch
+    n = mask.numel()
+    nseg = -(-n // segment_len) if segment_len > 0 else 1
+    if out_idx is None:
+        out_idx = torch.empty(max(n, 1), dtype=torch.int32, device=mask.device)
+    if out_seg_start is None:
+        out_seg_start = torch.empty(nseg + 1, dtype=torch.int32, device=mask.device)
+    _check(lib().cofie_mask_compact(_dev(mask, "mask") if n else None, n, segment_len,
+                                    _dev(out_idx, "out_idx"), _dev(out_seg_start, "out_seg_start"),
+                                    _stream(stream)))
+    return out_idx, out_seg_start
+
+
+def cofie_gather_frames(src, frame_offsets, sel, dst=None, capacity: Optional[int] = None,
+                        out_offsets=None, out_rows=None, with_rows: bool = True, stream=None):
+    """Rows of the selected frames of ``src`` ([n_rows, ...] on the GPU), in the
+    order of ``sel`` (Sec. 3.3 frame refinement).  Returns (dst, out_offsets
+    int32 [k+1], out_rows int32 or None); ``capacity`` (rows) defaults to
+    n_rows."""
+    import torch
+    n_rows = src.shape[0]
+    row_bytes = src.numel() * src.element_size() // n_rows if n_rows else src.element_size()
+    k = sel.numel()
+    if capacity is None:
+        capacity = dst.shape[0] if dst is not None else n_rows
+    if dst is None:
+        dst = torch.empty((max(capacity, 1),) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    if out_offsets is None:
+        out_offsets = torch.empty(k + 1, dtype=torch.int32, device=src.device)
+    if out_rows is None and with_rows:
+        out_rows = torch.empty(max(capacity, 1), dtype=torch.int32, device=src.device)
+    _check(lib().cofie_gather_frames(
+        _dev(src, "src") if n_rows else None, n_rows, row_bytes, _dev(frame_offsets, "frame_offsets"),
+        frame_offsets.numel() - 1, _dev(sel, "sel") if k else None, k,
+        _dev(dst, "dst") if capacity else None, capacity, _dev(out_offsets, "out_offsets"),
+        _dev(out_rows, "out_rows") if out_rows is not None else None, _stream(stream)))
+    return dst, out_offsets, out_rows
