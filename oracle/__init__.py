@@ -16,7 +16,11 @@ routines, the paper's printed drop-ratio compositions).  The retention-target
 calibration (``ngff_calibrate``) is not in the paper; it is pinned by a brute
 force over every integer threshold on small inputs.  The glue functions are
 pinned by hand-built cases, numpy's flatnonzero and a row-by-row brute force
-(``tests/test_oracle_glue.py``).
+(``tests/test_oracle_glue.py``).  The online reading of the keep rule
+(``ngff_scan_open`` / ``ngff_finish``: decisions as frames arrive, the two
+end-of-stream safeguards when the stream ends) is pinned by a hand-computed
+stream, causality, and equality with the one-shot rule
+(``tests/test_oracle_ngff_stream.py``).
 """
 from __future__ import annotations
 
@@ -73,6 +77,10 @@ def _load():
     lib.orc_qer_scores.restype = ctypes.c_int
     lib.orc_topk.argtypes = [P, i32, i32, P]
     lib.orc_topk.restype = ctypes.c_int
+    lib.orc_ngff_scan_open.argtypes = [P, i64, i64, i64, f32, i32, P, P, P]
+    lib.orc_ngff_scan_open.restype = i64
+    lib.orc_ngff_finish.argtypes = [P, i64, i32, P]
+    lib.orc_ngff_finish.restype = i64
     lib.orc_mask_compact.argtypes = [P, i64, i64, P, P]
     lib.orc_mask_compact.restype = i64
     lib.orc_gather_frames.argtypes = [P, i64, i64, P, i32, P, i32, P, i64, P, P]
@@ -227,3 +235,24 @@ def gather_frames(src: np.ndarray, frame_offsets: np.ndarray, sel: np.ndarray, c
     assert got == total
     m = min(total, cap)
     return dst[:m], out_offs, out_rows[:m]
+
+
+def ngff_scan_open(counts: np.ndarray, mass_: int, tau: float, L_max: int = 30):
+    """The keep rule as frames arrive (one stream so far, no end-of-stream
+    safeguards).  Returns (scores fp32 [T], mask uint8 [T], last kept r)."""
+    c = np.ascontiguousarray(counts, dtype=np.uint32)
+    T, nb = c.shape
+    scores = np.zeros(max(T, 1), dtype=np.float32)
+    mask = np.zeros(max(T, 1), dtype=np.uint8)
+    r = ctypes.c_int64(0)
+    _load().orc_ngff_scan_open(_ptr(c), T, nb, mass_, float(np.float32(tau)), L_max, _ptr(scores),
+                               _ptr(mask), ctypes.byref(r))
+    return scores[:T], mask[:T], int(r.value)
+
+
+def ngff_finish(mask: np.ndarray, M_min: int = 4):
+    """End-of-stream safeguards on an open mask: (mask, frames added [M_min+1] -1 padded)."""
+    m = np.array(mask, dtype=np.uint8, copy=True)
+    added = np.full(max(M_min, 0) + 1, -1, dtype=np.int32)
+    _load().orc_ngff_finish(_ptr(m), m.size, M_min, _ptr(added))
+    return m, added

@@ -474,3 +474,66 @@ int64_t orc_gather_frames(const uint8_t* src, int64_t n_rows, int64_t row_bytes,
   }
   return pos;
 }
+
+/* ---- NGFF as frames arrive ---------------------------------------------- */
+
+/* The keep rule applied online (a reading of Sec. 3.2 for the streaming
+ * setting of Sec. 3.1, where the video prefix grows): each frame is decided
+ * when it arrives, by the rule of scan_stream except its two end-of-stream
+ * safeguards (keep the last frame, the M_min top-up), which need the stream's
+ * end and are applied by orc_ngff_finish.  One stream of T frames so far.
+ * Returns the kept count; *r_out = the last kept frame.                     */
+int64_t orc_ngff_scan_open(const uint32_t* h, int64_t T, int64_t nbins, int64_t mass, float tau_h,
+                           int32_t L_max, float* scores, uint8_t* keep, int64_t* r_out) {
+  int64_t r = 0, kept = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    int k;
+    if (t == 0) {
+      scores[0] = 1.0f;
+      k = 1;
+    } else {
+      const float s_adj = tv_of(orc_l1(h + t * nbins, h + (t - 1) * nbins, nbins), mass);
+      const float s_ref = tv_of(orc_l1(h + t * nbins, h + r * nbins, nbins), mass);
+      const float s = s_adj > s_ref ? s_adj : s_ref;
+      scores[t] = s;
+      k = (s >= tau_h) || (L_max > 0 && t - r >= L_max);
+    }
+    keep[t] = (uint8_t)k;
+    if (k) {
+      r = t;
+      ++kept;
+    }
+  }
+  if (r_out) *r_out = r;
+  return kept;
+}
+
+/* End of a stream of T frames decided by orc_ngff_scan_open: the last frame
+ * is kept, then, if fewer than M_min frames are kept (M_min >= 2), the frames
+ * floor(i (T-1) / (M_min-1)) are added.  The frames this adds are written to
+ * added[0..M_min] in increasing order, -1 padded.  Returns the kept count.  */
+int64_t orc_ngff_finish(uint8_t* keep, int64_t T, int32_t M_min, int32_t* added) {
+  const int32_t cap = (M_min > 0 ? M_min : 0) + 1;
+  for (int32_t i = 0; i < cap; ++i) added[i] = -1;
+  if (T <= 0) return 0;
+  uint8_t* before = (uint8_t*)malloc((size_t)T);
+  if (!before) return -1;
+  memcpy(before, keep, (size_t)T);
+  int64_t kept = 0;
+  keep[T - 1] = 1;
+  for (int64_t t = 0; t < T; ++t) kept += keep[t];
+  if (M_min >= 2 && kept < M_min) {
+    for (int64_t i = 0; i < M_min; ++i) {
+      const int64_t u = (i * (T - 1)) / (M_min - 1);
+      if (!keep[u]) {
+        keep[u] = 1;
+        ++kept;
+      }
+    }
+  }
+  int32_t a = 0;
+  for (int64_t t = 0; t < T; ++t)
+    if (keep[t] && !before[t]) added[a++] = (int32_t)t;
+  free(before);
+  return kept;
+}
