@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--report", default="", help="with --configs: also write a markdown table here")
     ap.add_argument("--ms-streams", type=int, default=8,
                     help="with --configs 5: streams whose queries are ranked (of 32)")
+    ap.add_argument("--push-batch", type=int, default=64,
+                    help="with --configs: frames per stream and push of the online NGFF pass")
     return ap.parse_args()
 
 
@@ -409,6 +411,7 @@ def config_report(args, cfgs):
         reps = 30 if n * frame_bytes < (1 << 30) else 10
         ngff_us = median_call_us(torch, ngff_call, reps)
         nk = profiled_kernels(torch, B, ngff_call, reps)
+        online = online_ngff(torch, B, wl, frames, tau, args.push_batch, mask)
         kept = int(count.sum().item())
         hist_gbs = n * frame_bytes / (nk["ngff_hist"] * 1e-6) / 1e9
         row = {"workload": wl.name, "config": cfg,
@@ -419,7 +422,7 @@ def config_report(args, cfgs):
                         "hist_frac_read_probe": round(hist_gbs / probe, 4),
                         "kept": kept, "retention": round(kept / n, 4), "target_retention": wl.retain,
                         "kernels_us": nk, "oracle_s": round(cpu_hist_s + cpu_sel_s, 3),
-                        "oracle_cores": oracle.num_threads()}}
+                        "oracle_cores": oracle.num_threads(), "online": online}}
         mask_np = mask.cpu().numpy()
         seg_len = wl.T if wl.n_streams > 1 else 0
         cidx, cseg = B.cofie_mask_compact(mask, seg_len)
@@ -439,6 +442,36 @@ def config_report(args, cfgs):
         rows.append(row)
     if args.report:
         write_report(args, rows, probe)
+
+
+def online_ngff(torch, B, wl, frames, tau, batch, mask_one_shot):
+    """The same streams pushed `batch` frames at a time through the online
+    state and finished: GPU time of all pushes and the finish (state creation
+    outside), median of three passes; the final mask must equal the one-shot
+    filter's."""
+    S, T = wl.n_streams, wl.T
+    fr = frames.view(S, T, wl.H, wl.W, 3)
+    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, tau_per_segment=tau)
+    scores = torch.empty((S, T), dtype=torch.float32, device="cuda")
+    mask = torch.empty((S, T), dtype=torch.uint8, device="cuda")
+    runs = []
+    for _ in range(3):
+        st = B.cofie_ngff_stream_create(S, wl.H, wl.W, 3, wl.bins, rule)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t0 in range(0, T, batch):
+            B.cofie_ngff_stream_push(st, fr, scores, mask, col=t0, b=min(batch, T - t0))
+        B.cofie_ngff_stream_finish(st, mask, T)
+        e1.record()
+        torch.cuda.synchronize()
+        B.cofie_ngff_stream_destroy(st)
+        runs.append(e0.elapsed_time(e1) * 1e3)
+    us = float(np.median(runs))
+    same = bool(torch.equal(mask.view(-1), mask_one_shot))
+    pushes = -(-T // batch)
+    return {"batch": batch, "pushes": pushes, "us_total": round(us, 1), "us_per_push": round(us / pushes, 2),
+            "frames_per_s": round(S * T / (us * 1e-6), 1), "equals_one_shot": same}
 
 
 def qer_figures(calls, n_cand, total_us, kbytes, score_us, flops, flops_head, kernels, cpu_s, probe):
@@ -574,6 +607,14 @@ def write_report(args, rows, probe):
                      f"{g['hist_GBps']:.0f} | {100 * g['hist_frac_hbm']:.1f} | "
                      f"{100 * g['hist_frac_read_probe']:.1f} | {g['kept']} ({g['retention']:.3f}; "
                      f"{g['target_retention']}) | {g['oracle_s']:.2f} ({g['oracle_cores']}) |")
+    lines += ["", "Online NGFF (`cofie_ngff_stream_push` of every stream, then `cofie_ngff_stream_finish`; "
+              "GPU time of the whole stream, state creation outside):", "",
+              "| workload | frames per push and stream | pushes | µs per push | frames/s | final mask equals one-shot |",
+              "|---|---|---|---|---|---|"]
+    for r in rows:
+        o = r["ngff"]["online"]
+        lines.append(f"| {r['workload']} | {o['batch']} | {o['pushes']} | {o['us_per_push']:.1f} | "
+                     f"{o['frames_per_s']:,.0f} | {o['equals_one_shot']} |")
     lines += ["", "## QER", "",
               "| workload | calls | candidates | µs total | candidates/s | score GB/s | % of 8 TB/s | "
               "% of read probe | MFMA util | per-head TFLOP/s | oracle s |",

@@ -150,6 +150,57 @@ int cofie_ngff_calibrate(const uint8_t* frames, int64_t n, int32_t H, int32_t W,
                          int32_t bins, const cofie_keep_rule* keep_rule,
                          int64_t target_per_segment, float* out_tau, void* stream);
 
+/* ---- NGFF as frames arrive ---------------------------------------------- */
+/* The keep rule applied online (Sec. 3.1: the model sees the current video
+ * prefix; Sec. 3.2): each frame is decided when it is pushed, by the rule
+ * above without its two end-of-stream safeguards (frame T-1 kept, the M_min
+ * top-up), which cofie_ngff_stream_finish applies once the streams end.
+ * Pushing a stream's frames in any batches and finishing gives exactly the
+ * scores and mask of one cofie_ngff_filter call over the whole stream.  The
+ * state holds, per stream, the histograms of the last L_max frames, the last
+ * kept frame and the kept count; it lives on the device current at creation
+ * and is used from one stream at a time. */
+typedef struct cofie_ngff_stream cofie_ngff_stream;
+
+/* New state for n_streams streams of H x W x C frames (as cofie_ngff_histogram).
+ * From `rule` (host, read during the call): hist_mode, tau_h or
+ * tau_per_segment (device [n_streams], copied), L_max (>= 1 required, else
+ * EUNSUPPORTED: the rule then compares against a kept frame that can be
+ * arbitrarily old) and M_min; segment_len, out_hist, out_count and the
+ * workspace are ignored.  Allocates device memory (synchronous).  Errors as
+ * cofie_ngff_filter, plus ENOMEM. */
+int cofie_ngff_stream_create(int32_t n_streams, int32_t H, int32_t W, int32_t C, int32_t bins,
+                             const cofie_keep_rule* rule, cofie_ngff_stream** out_state);
+
+/* Push b >= 0 new frames of every stream.
+ *   frames      device uint8: frame j of stream s at frames + (s*frames_ld + j)
+ *               * H*W*C, frames_ld >= b (b for a packed [n_streams][b] batch;
+ *               T with frames pointing at column t0 of a [n_streams][T] array)
+ *   out_scores  device float: s_t of stream s's new frame j at out_scores[s*ld + j]
+ *   out_mask    device uint8, same layout: 1 = kept by the rule so far
+ *   ld          row stride of the outputs (>= b); pointing the outputs at
+ *               column t0 of [n_streams][T] arrays collects whole streams
+ * Scratch is allocated stream-ordered.  Errors: EINVAL for NULL pointers,
+ * b < 0, ld or frames_ld < b, a finished state or another current device. */
+int cofie_ngff_stream_push(cofie_ngff_stream* state, const uint8_t* frames, int64_t frames_ld, int32_t b,
+                           float* out_scores, uint8_t* out_mask, int64_t ld, void* stream);
+
+/* End of the streams: in mask_all (device uint8 [n_streams][ld], frames
+ * 0..T-1 of every stream as pushed) frame T-1 is kept and, where fewer than
+ * M_min frames are kept, the top-up frames are added.  out_added (optional,
+ * device int32 [n_streams][M_min+1]) receives the frames this adds,
+ * increasing and -1 padded; out_count (optional, device int32 [n_streams])
+ * the kept counts.  The state accepts no push afterwards. */
+int cofie_ngff_stream_finish(cofie_ngff_stream* state, uint8_t* mask_all, int64_t ld, int32_t* out_added,
+                             int32_t* out_count, void* stream);
+
+/* Frames pushed per stream so far (-1 for NULL). */
+int64_t cofie_ngff_stream_frames(const cofie_ngff_stream* state);
+
+/* Release the state (NULL is accepted).  Frees device memory: call it after
+ * the work enqueued with the state has completed. */
+int cofie_ngff_stream_destroy(cofie_ngff_stream* state);
+
 /* ---- QER ---------------------------------------------------------------- */
 
 typedef struct cofie_qer_desc {

@@ -95,6 +95,12 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_calibrate": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), i64, P, P]),
         "cofie_qer_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32]),
         "cofie_qer_rank": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
+        "cofie_ngff_stream_create": (ctypes.c_int, [i32, i32, i32, i32, i32, ctypes.POINTER(KeepRule),
+                                                    ctypes.POINTER(P)]),
+        "cofie_ngff_stream_push": (ctypes.c_int, [P, P, i64, i32, P, P, i64, P]),
+        "cofie_ngff_stream_finish": (ctypes.c_int, [P, P, i64, P, P, P]),
+        "cofie_ngff_stream_frames": (i64, [P]),
+        "cofie_ngff_stream_destroy": (ctypes.c_int, [P]),
         "cofie_mask_compact": (ctypes.c_int, [P, i64, i64, P, P, P]),
         "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
@@ -341,3 +347,42 @@ def cofie_gather_frames(src, frame_offsets, sel, dst=None, capacity: Optional[in
         _dev(dst, "dst") if capacity else None, capacity, _dev(out_offsets, "out_offsets"),
         _dev(out_rows, "out_rows") if out_rows is not None else None, _stream(stream)))
     return dst, out_offsets, out_rows
+
+
+def cofie_ngff_stream_create(n_streams: int, H: int, W: int, C: int, bins: int, rule: KeepRule):
+    """Online NGFF state (an opaque handle, release with cofie_ngff_stream_destroy)."""
+    h = ctypes.c_void_p()
+    _check(lib().cofie_ngff_stream_create(n_streams, H, W, C, bins, ctypes.byref(rule), ctypes.byref(h)))
+    return h
+
+
+def cofie_ngff_stream_push(state, frames, out_scores, out_mask, col: int = 0, b: Optional[int] = None,
+                           stream=None):
+    """Push frames: either a packed batch [n_streams][b][H][W][C], or (with b
+    given) columns col .. col+b-1 of a resident [n_streams][T][H][W][C] array.
+    out_scores (float32) and out_mask (uint8) are [n_streams][ld] arrays; the
+    results go to columns col .. col+b-1."""
+    packed = b is None
+    b = frames.shape[1] if packed else b
+    ld = out_scores.shape[1]
+    if out_mask.shape[1] != ld or col + b > ld:
+        raise ValueError("outputs must be [n_streams][ld] with col + b <= ld")
+    fb = frames.numel() // (frames.shape[0] * frames.shape[1]) if frames.numel() else 0
+    fp = _dev(frames, "frames") + (0 if packed else col * fb)
+    frames_ld = frames.shape[1]
+    sp = _dev(out_scores, "out_scores") + 4 * col
+    mp = _dev(out_mask, "out_mask") + col
+    _check(lib().cofie_ngff_stream_push(state, fp if b else None, frames_ld, b, sp, mp, ld, _stream(stream)))
+
+
+def cofie_ngff_stream_finish(state, mask_all, ld: int, out_added=None, out_count=None, stream=None):
+    _check(lib().cofie_ngff_stream_finish(state, _dev(mask_all, "mask_all"), ld, _dev(out_added, "out_added"),
+                                          _dev(out_count, "out_count"), _stream(stream)))
+
+
+def cofie_ngff_stream_frames(state) -> int:
+    return int(lib().cofie_ngff_stream_frames(state))
+
+
+def cofie_ngff_stream_destroy(state) -> None:
+    _check(lib().cofie_ngff_stream_destroy(state))

@@ -41,6 +41,10 @@ struct HistArgs {
   int32_t splits; // workgroups per frame
   int32_t units;  // whole 768-byte units covered by the vector path
   int32_t atomic; // 1: several workgroups per frame add into a zeroed histogram
+  // frame t of the launch reads frame (t / group) * in_stride + in_off + t % group
+  // and writes histogram row (t / group) * out_stride + out_off + t % group;
+  // group = 0: frame t, row t
+  int64_t group, in_stride, in_off, out_stride, out_off;
 };
 
 struct __attribute__((packed, aligned(4))) U3 {
@@ -135,7 +139,9 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
   const int wave = tid >> 6, nw = nthr >> 6;
   const int64_t t = blockIdx.x / a.splits;
   const int s = (int)(blockIdx.x - t * a.splits);
-  const uint8_t* f = a.frames + t * a.frame_bytes;
+  const int64_t src_frame = a.group ? (t / a.group) * a.in_stride + a.in_off + t % a.group : t;
+  const int64_t dst_row = a.group ? (t / a.group) * a.out_stride + a.out_off + t % a.group : t;
+  const uint8_t* f = a.frames + src_frame * a.frame_bytes;
   const int G = a.splits * nw;  // waves sharing this frame
   const int g = s * nw + wave;
   // batches of kUnroll units per wave (unit u0 + j G), software pipelined: the
@@ -186,7 +192,7 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
   // the bin so that the lanes of a wave hit distinct banks), then combine
   constexpr int J = P >= 8 ? 8 : P;
   constexpr int PER = P / J;
-  uint32_t* out = a.hist + t * a.nbins;
+  uint32_t* out = a.hist + dst_row * a.nbins;
   const int bins_per_pass = nthr / J;
   const int j = tid % J;
   for (int b0 = 0; b0 < a.nbins; b0 += bins_per_pass) {
@@ -818,10 +824,21 @@ int launch_hist_kind(const HistArgs& args, const HistPlan& p, int64_t n, hipStre
   }
 }
 
-int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hipStream_t s) {
+struct HistMap {  // see HistArgs: group = 0 is the identity
+  int64_t group = 0, in_stride = 0, in_off = 0, out_stride = 0, out_off = 0;
+  int64_t out_rows = 0;  // rows of the output buffer (for the zero fill), 0 = n
+};
+
+int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hipStream_t s,
+                  const HistMap& map = HistMap()) {
   if (sh.n == 0) return COFIE_OK;
   const HistPlan p = plan_hist(sh, frames);
   HistArgs a;
+  a.group = map.group;
+  a.in_stride = map.in_stride;
+  a.in_off = map.in_off;
+  a.out_stride = map.out_stride;
+  a.out_off = map.out_off;
   a.frames = frames;
   a.frame_bytes = sh.frame_bytes;
   a.npix = sh.npix;
@@ -834,7 +851,7 @@ int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hi
   a.units = p.units;
   a.atomic = p.splits > 1;
   if (a.atomic) {
-    const int64_t cnt = sh.n * sh.nbins;
+    const int64_t cnt = (map.out_rows ? map.out_rows : sh.n) * sh.nbins;
     int rc = launch("ngff_fill", fill_u32_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(cnt, 256), 4096)),
                     dim3(256), 0, s, hist, 0u, cnt);
     if (rc) return rc;
@@ -940,10 +957,194 @@ int validate_rule(const cofie_keep_rule* r) {
   return COFIE_OK;
 }
 
+// ---- NGFF as frames arrive ----------------------------------------------------------
+// The keep rule decided frame by frame as a stream grows (Sec. 3.1: the model
+// sees the current video prefix).  A push histograms the new frames of every
+// stream into a per-stream buffer [L window rows | nb new rows] (the window =
+// the L = L_max frames before the push, carried in the state), computes the
+// band of that buffer, and one workgroup per stream decides the new frames:
+// next[r] for the carried last kept frame and every new frame (open at the
+// batch end: no keep found within the frames seen -> "beyond"), the chain
+// walked from the carried frame, r(t) by a block prefix maximum, the scores.
+// The end-of-stream safeguards (last frame, M_min top-up) wait for finish.
+struct PushArgs {
+  const int32_t* band;   // [S][L + nb][L]
+  int32_t L;             // L_max (>= 1): band width and gap rule
+  int32_t nb;            // new frames per stream in this push (<= 1024)
+  int64_t t0;            // frames of each stream before this push
+  int64_t twoM;
+  float tau;
+  const float* tau_seg;  // [S] or null
+  int32_t* r_state;      // [S] last kept frame
+  int32_t* kept_state;   // [S] kept frames so far
+  float* out_scores;     // row s at out_scores + s * ld
+  uint8_t* out_mask;
+  int64_t ld;
+};
+
+__global__ __launch_bounds__(1024) void ngff_push_kernel(PushArgs a) {
+  extern __shared__ int32_t psm[];
+  int32_t* bandL = psm;                          // [nb][L]
+  int32_t* next_sh = bandL + a.nb * a.L;         // [nb + 1]: slot 0 = carried frame, 1 + j = new frame j
+  int32_t* keep_sh = next_sh + a.nb + 1;         // [nb]
+  int32_t* incl_sh = keep_sh + a.nb;             // [nb]
+  __shared__ int64_t theta_sh;
+  __shared__ int wtmp[16];
+  const int s = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
+  const int L = a.L, nb = a.nb;
+  const int64_t t0 = a.t0, tend = t0 + nb;
+  const int32_t* src = a.band + ((int64_t)s * (L + nb) + L) * L;
+  for (int i = tid; i < nb * L; i += nthr) bandL[i] = src[i];
+  for (int j = tid; j < nb; j += nthr) keep_sh[j] = 0;
+  if (tid == 0) theta_sh = theta_of(a.tau_seg ? a.tau_seg[s] : a.tau, a.twoM);
+  const int64_t rc = t0 > 0 ? a.r_state[s] : -1;  // carried last kept frame
+  __syncthreads();
+  const int64_t theta = theta_sh;
+  // next[r]: the first u in (r, r + L] (u >= t0) whose max(D(u, u-1), D(u, r))
+  // reaches theta, else r + L (gap rule) if that frame has arrived, else beyond
+  for (int q = tid; q <= nb; q += nthr) {
+    const int64_t r = q == 0 ? rc : t0 + q - 1;
+    int64_t found = tend;
+    if (r >= 0) {
+      const int64_t ulo = r + 1 > t0 ? r + 1 : t0;
+      const int64_t uhi = r + L < tend - 1 ? r + L : tend - 1;
+      for (int64_t u = ulo; u <= uhi; ++u) {
+        const int32_t* row = bandL + (u - t0) * L;
+        const int32_t Dadj = row[0], Dref = row[u - r - 1];
+        if ((Dadj > Dref ? Dadj : Dref) >= theta) {
+          found = u;
+          break;
+        }
+      }
+      if (found == tend && r + L <= tend - 1) found = r + L;
+    }
+    // relative to t0, nb = beyond; a carried frame is never L or more before
+    // t0 (the gap rule), the clamp only keeps a corrupted state in bounds
+    next_sh[q] = (int32_t)(found < t0 ? 0 : found - t0);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t r = rc;
+    int slot = 0, count = 0;
+    if (t0 == 0) {  // the stream's first frame is kept
+      keep_sh[0] = 1;
+      r = 0;
+      slot = 1;
+      count = 1;
+    }
+    for (;;) {
+      const int nx = next_sh[slot];
+      if (nx >= nb) break;
+      keep_sh[nx] = 1;
+      ++count;
+      r = t0 + nx;
+      slot = nx + 1;
+    }
+    a.r_state[s] = (int32_t)r;
+    a.kept_state[s] = (t0 > 0 ? a.kept_state[s] : 0) + count;
+  }
+  __syncthreads();
+  // r(t) = the last kept frame before t: prefix maximum over this push, then the carried frame
+  for (int j0 = 0; j0 < nb; j0 += nthr) {
+    const int j = j0 + tid;
+    const int v = (j < nb && keep_sh[j]) ? j : -1;
+    const int x = block_inclusive_max(v, wtmp);
+    if (j < nb) incl_sh[j] = x;
+  }
+  __syncthreads();
+  const float den = (float)a.twoM;
+  for (int j = tid; j < nb; j += nthr) {
+    const int64_t t = t0 + j;
+    float score = 1.0f;
+    if (t > 0) {
+      const int prev = j > 0 ? incl_sh[j - 1] : -1;
+      const int64_t rt = prev >= 0 ? t0 + prev : rc;
+      const int32_t* row = bandL + j * L;
+      const int64_t k = t - rt;  // 1 <= k <= L by the gap rule
+      const int32_t Dadj = row[0], Dref = row[k < 1 ? 0 : (k > L ? L - 1 : k - 1)];
+      score = (float)(Dadj > Dref ? Dadj : Dref) / den;
+    }
+    a.out_scores[s * a.ld + j] = score;
+    a.out_mask[s * a.ld + j] = (uint8_t)keep_sh[j];
+  }
+}
+
+// comb[s][0..L) <- window[s] (dir 0) or window[s] <- comb[s][nb..nb+L) (dir 1)
+__global__ void ngff_window_kernel(uint32_t* comb, uint32_t* window, int32_t S, int32_t L, int32_t nb,
+                                   int64_t nbins, int32_t dir) {
+  const int64_t per = (int64_t)L * nbins, total = per * S;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t s = i / per, w = i - s * per;
+    uint32_t* c = comb + s * (L + nb) * nbins;
+    if (dir == 0)
+      c[w] = window[i];
+    else
+      window[i] = c[(int64_t)nb * nbins + w];
+  }
+}
+
+// End of the streams: frame T-1 kept, then the M_min top-up (one thread per
+// stream); out_added row s receives the frames this adds, increasing and -1
+// padded to M_min + 1 entries.
+__global__ void ngff_finish_kernel(uint8_t* mask_all, int64_t ld, int32_t S, int64_t T, int32_t M_min,
+                                   int32_t* kept_state, int32_t* out_added, int32_t* out_count) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  uint8_t* m = mask_all + s * ld;
+  const int cap = (M_min > 0 ? M_min : 0) + 1;
+  int32_t* add = out_added ? out_added + (int64_t)s * cap : nullptr;
+  int na = 0;
+  auto record = [&](int64_t u) {
+    if (!add) return;
+    int i = na++;
+    while (i > 0 && add[i - 1] > u) {  // insertion keeps the list increasing
+      add[i] = add[i - 1];
+      --i;
+    }
+    add[i] = (int32_t)u;
+  };
+  int64_t kept = T > 0 ? kept_state[s] : 0;
+  if (T > 0) {
+    if (!m[T - 1]) {
+      m[T - 1] = 1;
+      ++kept;
+      record(T - 1);
+    }
+    if (M_min >= 2 && kept < M_min) {
+      for (int64_t i = 0; i < M_min; ++i) {
+        const int64_t u = (i * (T - 1)) / (M_min - 1);
+        if (!m[u]) {
+          m[u] = 1;
+          ++kept;
+          record(u);
+        }
+      }
+    }
+  }
+  if (add)
+    for (int i = na; i < cap; ++i) add[i] = -1;
+  kept_state[s] = (int32_t)kept;
+  if (out_count) out_count[s] = (int32_t)kept;
+}
+
 }  // namespace
 }  // namespace cofie
 
 using namespace cofie;
+
+// ---- online NGFF state --------------------------------------------------------------
+struct cofie_ngff_stream {
+  int device = 0;
+  NgffShape sh{};          // n unused
+  int32_t S = 0, L = 0, M_min = 0;
+  float tau = 0.f;
+  float* tau_dev = nullptr;    // [S] copy of tau_per_segment, or null
+  uint32_t* window = nullptr;  // [S][L][nbins]: histograms of the L frames before t0
+  int32_t* r = nullptr;        // [S] last kept frame
+  int32_t* kept = nullptr;     // [S] kept frames so far
+  int64_t t0 = 0;              // frames pushed per stream
+  bool finished = false;
+};
 
 extern "C" {
 
@@ -1108,6 +1309,165 @@ int cofie_ngff_calibrate(const uint8_t* frames, int64_t n, int32_t H, int32_t W,
   if (rc) return rc;
   return launch("ngff_calib_final", calib_final_kernel, dim3((unsigned)ceil_div(rp.nseg, 256)),
                 dim3(256), 0, s, (const int32_t*)w.best, rp.nseg, twoM, out_tau);
+}
+
+
+int cofie_ngff_stream_create(int32_t n_streams, int32_t H, int32_t W, int32_t C, int32_t bins,
+                             const cofie_keep_rule* rule, cofie_ngff_stream** out_state) {
+  clear_error();
+  if (!out_state) return set_error(COFIE_EINVAL, "out_state is NULL");
+  *out_state = nullptr;
+  if (!rule) return set_error(COFIE_EINVAL, "keep_rule is NULL");
+  if (n_streams < 1) return set_error(COFIE_EINVAL, "n_streams = %d must be >= 1", n_streams);
+  NgffShape sh;
+  int rc = validate_frames(nullptr, 0, H, W, C, bins, rule->hist_mode, &sh);
+  if (rc) return rc;
+  if (rule->L_max < 1) return set_error(COFIE_EUNSUPPORTED, "the streaming keep rule needs L_max >= 1");
+  if (rule->M_min < 0) return set_error(COFIE_EINVAL, "M_min is negative");
+  if (!rule->tau_per_segment && !(rule->tau_h == rule->tau_h)) return set_error(COFIE_EINVAL, "tau_h is NaN");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return set_error(COFIE_EHIP, "hipGetDevice failed");
+  auto* st = new cofie_ngff_stream();
+  st->device = dev;
+  st->sh = sh;
+  st->S = n_streams;
+  st->L = rule->L_max;
+  st->M_min = rule->M_min;
+  st->tau = rule->tau_h;
+  const size_t wbytes = (size_t)n_streams * st->L * sh.nbins * sizeof(uint32_t);
+  bool ok = hipMalloc(&st->window, wbytes) == hipSuccess &&
+            hipMalloc(&st->r, n_streams * sizeof(int32_t)) == hipSuccess &&
+            hipMalloc(&st->kept, n_streams * sizeof(int32_t)) == hipSuccess &&
+            hipMemset(st->window, 0, wbytes) == hipSuccess &&
+            hipMemset(st->r, 0, n_streams * sizeof(int32_t)) == hipSuccess &&
+            hipMemset(st->kept, 0, n_streams * sizeof(int32_t)) == hipSuccess;
+  if (ok && rule->tau_per_segment) {
+    ok = hipMalloc(&st->tau_dev, n_streams * sizeof(float)) == hipSuccess &&
+         hipMemcpy(st->tau_dev, rule->tau_per_segment, n_streams * sizeof(float), hipMemcpyDeviceToDevice) ==
+             hipSuccess;
+  }
+  if (!ok) {
+    cofie_ngff_stream_destroy(st);
+    return set_error(COFIE_ENOMEM, "allocating the stream state failed");
+  }
+  *out_state = st;
+  return COFIE_OK;
+}
+
+int cofie_ngff_stream_destroy(cofie_ngff_stream* st) {
+  clear_error();
+  if (!st) return COFIE_OK;
+  int dev = 0;
+  hipGetDevice(&dev);
+  if (dev != st->device) hipSetDevice(st->device);
+  if (st->window) hipFree(st->window);
+  if (st->r) hipFree(st->r);
+  if (st->kept) hipFree(st->kept);
+  if (st->tau_dev) hipFree(st->tau_dev);
+  if (dev != st->device) hipSetDevice(dev);
+  delete st;
+  return COFIE_OK;
+}
+
+int64_t cofie_ngff_stream_frames(const cofie_ngff_stream* st) { return st ? st->t0 : -1; }
+
+int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t frames_ld, int32_t b,
+                           float* out_scores, uint8_t* out_mask, int64_t ld, void* stream) {
+  clear_error();
+  if (!st) return set_error(COFIE_EINVAL, "state is NULL");
+  if (st->finished) return set_error(COFIE_EINVAL, "the streams were finished");
+  if (b < 0) return set_error(COFIE_EINVAL, "b is negative");
+  if (b == 0) return COFIE_OK;
+  if (!frames || !out_scores || !out_mask) return set_error(COFIE_EINVAL, "frames or an output is NULL");
+  if (ld < b) return set_error(COFIE_EINVAL, "ld = %lld is smaller than b = %d", (long long)ld, b);
+  if (frames_ld < b) return set_error(COFIE_EINVAL, "frames_ld = %lld is smaller than b = %d", (long long)frames_ld, b);
+  if (st->t0 + b >= (int64_t(1) << 31)) return set_error(COFIE_EUNSUPPORTED, "stream longer than 2^31 frames");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev != st->device)
+    return set_error(COFIE_EINVAL, "the current device is not the state's device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int32_t S = st->S, L = st->L;
+  // pushes of at most nbmax frames per stream: the new frames' band rows sit in LDS
+  const int32_t nbmax = (int32_t)std::max<int64_t>(1, std::min<int64_t>(1024, 12288 / L));
+  for (int32_t j0 = 0; j0 < b; j0 += nbmax) {
+    const int32_t nb = std::min(nbmax, b - j0);
+    const int64_t rows = (int64_t)S * (L + nb);
+    Arena plan;
+    plan.take<uint32_t>((size_t)rows * st->sh.nbins);
+    plan.take<int32_t>((size_t)rows * L);
+    Scratch scratch;
+    int rc = scratch.acquire(nullptr, 0, plan.bytes(), s);
+    if (rc) return rc;
+    Arena ar;
+    ar.base = scratch.ptr();
+    uint32_t* comb = ar.take<uint32_t>((size_t)rows * st->sh.nbins);
+    int32_t* band = ar.take<int32_t>((size_t)rows * L);
+    NgffShape sh = st->sh;
+    sh.n = (int64_t)S * nb;
+    HistMap map;
+    map.group = nb;
+    map.in_stride = frames_ld;
+    map.in_off = j0;
+    map.out_stride = L + nb;
+    map.out_off = L;
+    map.out_rows = rows;
+    rc = run_histogram(frames, sh, comb, s, map);
+    if (rc) return rc;
+    const int64_t wwords = (int64_t)S * L * st->sh.nbins;
+    const unsigned wgrid = (unsigned)std::min<int64_t>(ceil_div(wwords, 256), 4096);
+    rc = launch("ngff_window", ngff_window_kernel, dim3(wgrid), dim3(256), 0, s, comb, st->window, S, L, nb,
+                st->sh.nbins, 0);
+    if (rc) return rc;
+    NgffShape bsh = st->sh;
+    bsh.n = rows;
+    RulePlan rp;
+    rp.seg_len = L + nb;
+    rp.nseg = S;
+    rp.gap_rule = true;
+    rp.L = L;
+    rc = run_band(comb, bsh, rp, band, s);
+    if (rc) return rc;
+    PushArgs pa;
+    pa.band = band;
+    pa.L = L;
+    pa.nb = nb;
+    pa.t0 = st->t0;
+    pa.twoM = 2 * st->sh.mass;
+    pa.tau = st->tau;
+    pa.tau_seg = st->tau_dev;
+    pa.r_state = st->r;
+    pa.kept_state = st->kept;
+    pa.out_scores = out_scores + j0;
+    pa.out_mask = out_mask + j0;
+    pa.ld = ld;
+    const size_t lds = ((size_t)nb * L + 3 * (size_t)nb + 1) * sizeof(int32_t);
+    rc = allow_lds(ngff_push_kernel, lds);
+    if (rc) return rc;
+    rc = launch("ngff_push", ngff_push_kernel, dim3(S), dim3(1024), lds, s, pa);
+    if (rc) return rc;
+    rc = launch("ngff_window", ngff_window_kernel, dim3(wgrid), dim3(256), 0, s, comb, st->window, S, L, nb,
+                st->sh.nbins, 1);
+    if (rc) return rc;
+    st->t0 += nb;
+  }
+  return COFIE_OK;
+}
+
+int cofie_ngff_stream_finish(cofie_ngff_stream* st, uint8_t* mask_all, int64_t ld, int32_t* out_added,
+                             int32_t* out_count, void* stream) {
+  clear_error();
+  if (!st) return set_error(COFIE_EINVAL, "state is NULL");
+  if (st->finished) return set_error(COFIE_EINVAL, "the streams were already finished");
+  if (st->t0 > 0 && !mask_all) return set_error(COFIE_EINVAL, "mask_all is NULL");
+  if (ld < st->t0) return set_error(COFIE_EINVAL, "ld is smaller than the frames pushed");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev != st->device)
+    return set_error(COFIE_EINVAL, "the current device is not the state's device");
+  const int rc = launch("ngff_finish", ngff_finish_kernel, dim3((unsigned)ceil_div(st->S, 64)), dim3(64), 0,
+                        static_cast<hipStream_t>(stream), mask_all, ld, st->S, st->t0, st->M_min, st->kept,
+                        out_added, out_count);
+  if (rc == COFIE_OK) st->finished = true;
+  return rc;
 }
 
 }  // extern "C"

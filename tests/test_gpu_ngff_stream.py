@@ -1,0 +1,106 @@
+"""GPU parity of online NGFF (frames pushed in batches, the keep rule decided
+as they arrive, the end-of-stream safeguards on finish) against the oracle's
+online reading of Sec. 3.2, bit for bit: after every push the decided scores
+and masks equal the oracle's open scan of each stream's prefix; after finish
+they equal the one-shot rule (and the GPU's one-shot cofie_ngff_filter)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_03675_amd import binding as B
+from paper_2609_03675_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import require_gpu, to_dev  # noqa: E402
+
+MODES = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    B.lib()
+
+
+def run_stream(frames, bins, mode, tau, L_max, M_min, batches, tau_per_stream=None):
+    """frames [S][T][H][W][C] pushed in the given batch sizes; checks every push."""
+    S, T, H, W, C = frames.shape
+    M = oracle.mass(MODES[mode], H, W)
+    hists = [oracle.histogram(frames[s], bins, MODES[mode]) for s in range(S)]
+    taus = tau_per_stream if tau_per_stream is not None else np.full(S, tau, np.float32)
+    rule = B.keep_rule(mode, tau, L_max, M_min,
+                       tau_per_segment=to_dev(taus) if tau_per_stream is not None else None)
+    st = B.cofie_ngff_stream_create(S, H, W, C, bins, rule)
+    scores = torch.zeros((S, T), dtype=torch.float32, device="cuda")
+    mask = torch.zeros((S, T), dtype=torch.uint8, device="cuda")
+    fd = to_dev(frames)
+    t0 = 0
+    try:
+        for i, b in enumerate(batches):
+            print(f"push t0={t0} b={b}", flush=True)
+            if i % 2:  # a packed batch, or columns of the resident streams
+                B.cofie_ngff_stream_push(st, fd[:, t0:t0 + b].contiguous(), scores, mask, col=t0)
+            else:
+                B.cofie_ngff_stream_push(st, fd, scores, mask, col=t0, b=b)
+            t0 += b
+            assert B.cofie_ngff_stream_frames(st) == t0
+            torch.cuda.synchronize()
+            sc, mk = scores.cpu().numpy(), mask.cpu().numpy()
+            for s in range(S):
+                so, mo, _ = oracle.ngff_scan_open(hists[s][:t0], M, float(taus[s]), L_max)
+                assert np.array_equal(sc[s, :t0].view(np.uint32), so.view(np.uint32)), f"scores s={s} t0={t0}"
+                assert np.array_equal(mk[s, :t0], mo), f"mask s={s} t0={t0}"
+        added = torch.zeros((S, M_min + 1), dtype=torch.int32, device="cuda")
+        count = torch.zeros(S, dtype=torch.int32, device="cuda")
+        B.cofie_ngff_stream_finish(st, mask, T, out_added=added, out_count=count)
+        torch.cuda.synchronize()
+    finally:
+        B.cofie_ngff_stream_destroy(st)
+    mk, ad, ct = mask.cpu().numpy(), added.cpu().numpy(), count.cpu().numpy()
+    for s in range(S):
+        s1, m1, k1 = oracle.ngff_select(hists[s], M, float(taus[s]), L_max, M_min)
+        _, mo, _ = oracle.ngff_scan_open(hists[s], M, float(taus[s]), L_max)
+        _, ao = oracle.ngff_finish(mo, M_min)
+        assert np.array_equal(mk[s], m1) and ct[s] == k1[0]
+        assert np.array_equal(ad[s], ao)
+    return mk, scores.cpu().numpy()
+
+
+@pytest.mark.parametrize("batches", [[64], [1] * 40 + [24], [7, 30, 1, 26], [3, 61]])
+def test_push_batches_single_stream(batches):
+    frames = synth.random_frames(21, 64, 24, 32, scenes=6)[None]
+    run_stream(frames, 16, "per_channel", 0.05, 8, 4, batches)
+
+
+@pytest.mark.parametrize("mode,bins", [("gray", 32), ("joint3d", 8)])
+def test_push_modes_and_streams(mode, bins):
+    frames = np.stack([synth.random_frames(30 + s, 50, 20, 28, scenes=4 + s) for s in range(3)])
+    run_stream(frames, bins, mode, 0.08, 5, 3, [7, 1, 12, 3, 9, 18],
+               tau_per_stream=np.array([0.02, 0.08, 0.3], np.float32))
+
+
+def test_push_matches_one_shot_filter_on_workload():
+    """Eight streams of the multi-stream workload pushed 64 frames at a time:
+    after finish, the masks and scores equal one cofie_ngff_filter call over
+    the same batch with segment_len = 512 and the same per-stream tau."""
+    cfg, S = 5, 8
+    wl = synth.WORKLOADS[cfg]
+    frames = np.stack([synth.StreamPlan(cfg, s).frames() for s in range(S)])
+    fd = to_dev(frames.reshape(S * wl.T, wl.H, wl.W, 3))
+    rule0 = B.keep_rule(wl.hist_mode, 0.3, 30, 4, wl.T)
+    tau = B.cofie_ngff_calibrate(fd, wl.bins, rule0, wl.target)
+    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, wl.T, tau_per_segment=tau)
+    sc1, m1 = B.cofie_ngff_filter(fd, wl.bins, rule)
+    mk, sc = run_stream(frames, wl.bins, wl.hist_mode, 0.3, 30, 4, [64] * (wl.T // 64),
+                        tau_per_stream=tau.cpu().numpy())
+    assert np.array_equal(mk.reshape(-1), m1.cpu().numpy())
+    assert np.array_equal(sc.reshape(-1).view(np.uint32), sc1.cpu().numpy().view(np.uint32))
+
+
+def test_push_large_batch_is_split():
+    """A push larger than one internal sub-push (the band rows of at most
+    12288 / L_max frames per stream fit the push kernel's LDS)."""
+    frames = synth.random_frames(44, 900, 8, 8, scenes=30)[None]
+    run_stream(frames, 8, "per_channel", 0.1, 30, 4, [900])
