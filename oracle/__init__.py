@@ -20,7 +20,9 @@ pinned by hand-built cases, numpy's flatnonzero and a row-by-row brute force
 (``ngff_scan_open`` / ``ngff_finish``: decisions as frames arrive, the two
 end-of-stream safeguards when the stream ends) is pinned by a hand-computed
 stream, causality, and equality with the one-shot rule
-(``tests/test_oracle_ngff_stream.py``).
+(``tests/test_oracle_ngff_stream.py``).  The evidence-preservation metrics of
+the appendix are pinned by hand-computed cases and a numpy brute force
+(``tests/test_oracle_evidence.py``).
 """
 from __future__ import annotations
 
@@ -81,6 +83,8 @@ def _load():
     lib.orc_ngff_scan_open.restype = i64
     lib.orc_ngff_finish.argtypes = [P, i64, i32, P]
     lib.orc_ngff_finish.restype = i64
+    lib.orc_evidence_preservation.argtypes = [P, P, i32, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)]
+    lib.orc_evidence_preservation.restype = ctypes.c_int
     lib.orc_mask_compact.argtypes = [P, i64, i64, P, P]
     lib.orc_mask_compact.restype = i64
     lib.orc_gather_frames.argtypes = [P, i64, i64, P, i32, P, i32, P, i64, P, P]
@@ -256,3 +260,15 @@ def ngff_finish(mask: np.ndarray, M_min: int = 4):
     added = np.full(max(M_min, 0) + 1, -1, dtype=np.int32)
     _load().orc_ngff_finish(_ptr(m), m.size, M_min, _ptr(added))
     return m, added
+
+
+def evidence_preservation(w: np.ndarray, mask: np.ndarray, p: float = 0.2):
+    """(Attention Preservation Ratio, Top-Evidence Recall@p) of an NGFF mask
+    against full-video QER scores w (appendix, evidence preservation)."""
+    a = np.ascontiguousarray(w, dtype=np.float64)
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    apr, rec = ctypes.c_double(0), ctypes.c_double(0)
+    rc = _load().orc_evidence_preservation(_ptr(a), _ptr(m), a.size, float(p), ctypes.byref(apr),
+                                           ctypes.byref(rec))
+    assert rc == 0
+    return apr.value, rec.value

@@ -537,3 +537,37 @@ int64_t orc_ngff_finish(uint8_t* keep, int64_t T, int32_t M_min, int32_t* added)
   free(before);
   return kept;
 }
+
+/* ---- evidence preservation (App., "Preservation of Answer-Relevant
+ * Evidence") ------------------------------------------------------------- */
+
+/* With w the QER scores of the full, unfiltered video (as an attention mass:
+ * non-negative, e.g. the SOFTMAX mode) and mask the frames NGFF retains:
+ *   APR      = sum of w over the retained frames / sum of w over all frames
+ *              (0 when the total is 0)
+ *   Recall@p = |TopK(w, k) intersected with the retained frames| / k, with
+ *              k = max(1, round(p n)) (half to even), TopK as Eq. 8.
+ * Sums in fp64 in frame order.                                              */
+int orc_evidence_preservation(const double* w, const uint8_t* mask, int32_t n, double p, double* apr,
+                              double* recall) {
+  double tot = 0, kept = 0;
+  for (int32_t f = 0; f < n; ++f) {
+    tot += w[f];
+    if (mask[f]) kept += w[f];
+  }
+  *apr = tot != 0 ? kept / tot : 0;
+  *recall = 0;
+  if (n <= 0) return 0;
+  const double x = p * (double)n;
+  int64_t k = (int64_t)nearbyint(x);
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  int32_t* idx = (int32_t*)malloc((size_t)k * sizeof(int32_t));
+  if (!idx) return -2;
+  orc_topk(w, n, (int32_t)k, idx);
+  int64_t hit = 0;
+  for (int64_t i = 0; i < k; ++i) hit += mask[idx[i]] ? 1 : 0;
+  *recall = (double)hit / (double)k;
+  free(idx);
+  return 0;
+}
