@@ -288,6 +288,25 @@ int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, cons
                         int64_t dst_capacity_rows, int32_t* out_offsets, int32_t* out_rows,
                         void* stream);
 
+/* Eq. 8's selection on given scores: the k_top frames of largest w (device
+ * float [n]), ties to the lower index, NaN ranked as -inf, in chronological
+ * order and -1 padded, to out_idx (device int32 [k_top]).  Errors: EINVAL for
+ * NULL pointers or negative sizes. */
+int cofie_topk(const float* w, int32_t n, int32_t k_top, int32_t* out_idx, void* stream);
+
+/* Evidence preservation of a coarse filter (appendix, "Preservation of
+ * Answer-Relevant Evidence"), with w the QER scores of the full, unfiltered
+ * video used as attention mass (device float [n], e.g. the SOFTMAX mode) and
+ * mask the frames the filter retains (device uint8 [n]):
+ *   out[0]  Attention Preservation Ratio = sum of w over retained frames /
+ *           sum of w (0 when that sum is 0)
+ *   out[1]  Top-Evidence Recall = share of the top k = max(1, round(top_frac n))
+ *           frames (as cofie_topk) that are retained; the paper uses 20 %
+ * out: device double [2]; sums in fp64.  Errors: EINVAL for NULL pointers,
+ * n < 0 or a negative or NaN top_frac. */
+int cofie_evidence_preservation(const float* w, const uint8_t* mask, int32_t n, double top_frac, double* out,
+                                void* stream);
+
 /* ---- host helpers ------------------------------------------------------- */
 
 /* k = max(1, round(rho * n_candidates)) (Eq. 8), rounding half to even;

@@ -101,6 +101,8 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_stream_finish": (ctypes.c_int, [P, P, i64, P, P, P]),
         "cofie_ngff_stream_frames": (i64, [P]),
         "cofie_ngff_stream_destroy": (ctypes.c_int, [P]),
+        "cofie_topk": (ctypes.c_int, [P, i32, i32, P, P]),
+        "cofie_evidence_preservation": (ctypes.c_int, [P, P, i32, f64, P, P]),
         "cofie_mask_compact": (ctypes.c_int, [P, i64, i64, P, P, P]),
         "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
@@ -386,3 +388,24 @@ def cofie_ngff_stream_frames(state) -> int:
 
 def cofie_ngff_stream_destroy(state) -> None:
     _check(lib().cofie_ngff_stream_destroy(state))
+
+
+def cofie_topk(w, k_top: int, out_idx=None, stream=None):
+    """Top-k frames of scores w (float32 [n] on the GPU), chronological, -1 padded."""
+    import torch
+    if out_idx is None:
+        out_idx = torch.empty(max(k_top, 1), dtype=torch.int32, device=w.device)
+    n = w.numel()
+    _check(lib().cofie_topk(_dev(w, "w") if n else None, n, k_top, _dev(out_idx, "out_idx"), _stream(stream)))
+    return out_idx[:k_top]
+
+
+def cofie_evidence_preservation(w, mask, top_frac: float = 0.2, out=None, stream=None):
+    """(APR, Recall) as a float64 [2] GPU tensor."""
+    import torch
+    if out is None:
+        out = torch.empty(2, dtype=torch.float64, device=w.device)
+    n = w.numel()
+    _check(lib().cofie_evidence_preservation(_dev(w, "w") if n else None, _dev(mask, "mask") if n else None, n,
+                                             float(top_frac), _dev(out, "out"), _stream(stream)))
+    return out

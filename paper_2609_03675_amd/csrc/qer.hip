@@ -609,6 +609,48 @@ __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, 
   for (int i = k + tid; i < k_top; i += nthr) out_idx[i] = -1;
 }
 
+// ---- top-k of given scores; evidence preservation ----------------------------------
+__global__ void order_keys_kernel(const float* w, int32_t n, uint32_t* keys) {
+  for (int64_t f = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; f < n; f += (int64_t)gridDim.x * blockDim.x)
+    keys[f] = order_key(w[f]);
+}
+
+// out[0] = sum of w over the masked frames / sum over all (0 if the total is
+// 0); out[1] = share of the top-k frames that are masked.  fp64 sums, one
+// workgroup: each thread a contiguous chunk of frames, then a fixed tree.
+__global__ __launch_bounds__(1024) void evidence_kernel(const float* w, const uint8_t* mask, int32_t n,
+                                                        const int32_t* top, int32_t k, double* out) {
+  __shared__ double tot_sh[1024], kept_sh[1024];
+  __shared__ int hit_sh[1024];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int chunk = (n + nthr - 1) / nthr;
+  const int lo = tid * chunk < n ? tid * chunk : n, hi = lo + chunk < n ? lo + chunk : n;
+  double tot = 0, kept = 0;
+  for (int f = lo; f < hi; ++f) {
+    const double v = (double)w[f];
+    tot += v;
+    if (mask[f]) kept += v;
+  }
+  int hit = 0;
+  for (int i = tid; i < k; i += nthr) hit += mask[top[i]] ? 1 : 0;
+  tot_sh[tid] = tot;
+  kept_sh[tid] = kept;
+  hit_sh[tid] = hit;
+  __syncthreads();
+  for (int o = nthr / 2; o > 0; o >>= 1) {
+    if (tid < o) {
+      tot_sh[tid] += tot_sh[tid + o];
+      kept_sh[tid] += kept_sh[tid + o];
+      hit_sh[tid] += hit_sh[tid + o];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    out[0] = tot_sh[0] != 0 ? kept_sh[0] / tot_sh[0] : 0.0;
+    out[1] = k > 0 ? (double)hit_sh[0] / (double)k : 0.0;
+  }
+}
+
 // ---- SOFTMAX mode -------------------------------------------------------------------
 // Per-head scores s^h_ij = scale * <q_i^h, k_j^g(h)> are recomputed in both
 // passes (K is read twice).  Pass 1 writes, per workgroup of 32 tokens, the
@@ -1040,5 +1082,47 @@ int64_t cofie_qer_k_from_ratio(double rho, int64_t n) {
 }
 
 double cofie_drop_total(double d_ngff, double d_qer) { return 1.0 - (1.0 - d_ngff) * (1.0 - d_qer); }
+
+
+int cofie_topk(const float* w, int32_t n, int32_t k_top, int32_t* out_idx, void* stream) {
+  clear_error();
+  if (n < 0 || k_top < 0) return set_error(COFIE_EINVAL, "negative n or k_top");
+  if (k_top > 0 && !out_idx) return set_error(COFIE_EINVAL, "out_idx is NULL");
+  if (n > 0 && !w) return set_error(COFIE_EINVAL, "w is NULL");
+  if (k_top == 0) return COFIE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Scratch scratch;
+  int rc = scratch.acquire(nullptr, 0, (size_t)(n > 0 ? n : 1) * sizeof(uint32_t), s);
+  if (rc) return rc;
+  uint32_t* keys = reinterpret_cast<uint32_t*>(scratch.ptr());
+  if (n > 0) {
+    rc = launch("qer_order_keys", order_keys_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)),
+                dim3(256), 0, s, w, n, keys);
+    if (rc) return rc;
+  }
+  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)keys, n, k_top, out_idx);
+}
+
+int cofie_evidence_preservation(const float* w, const uint8_t* mask, int32_t n, double top_frac, double* out,
+                                void* stream) {
+  clear_error();
+  if (n < 0) return set_error(COFIE_EINVAL, "n is negative");
+  if (!out) return set_error(COFIE_EINVAL, "out is NULL");
+  if (n > 0 && (!w || !mask)) return set_error(COFIE_EINVAL, "w or mask is NULL");
+  if (!(top_frac >= 0)) return set_error(COFIE_EINVAL, "top_frac must be a non-negative number");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int64_t k = n > 0 ? cofie_qer_k_from_ratio(top_frac, n) : 0;
+  if (k > n) k = n;
+  Scratch scratch;
+  int rc = scratch.acquire(nullptr, 0, (size_t)(k > 0 ? k : 1) * sizeof(int32_t), s);
+  if (rc) return rc;
+  int32_t* top = reinterpret_cast<int32_t*>(scratch.ptr());
+  if (k > 0) {
+    rc = cofie_topk(w, n, (int32_t)k, top, stream);
+    if (rc) return rc;
+  }
+  return launch("qer_evidence", evidence_kernel, dim3(1), dim3(1024), 0, s, w, mask, n, (const int32_t*)top,
+                (int32_t)k, out);
+}
 
 }  // extern "C"
