@@ -245,6 +245,21 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
                    const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
                    int32_t* out_idx, void* stream);
 
+/* Several queries sharing one key sequence, K read once for all of them
+ * (the multi-stream workload: a stream's queries rank prefixes of its
+ * candidates).  Query g has heads->n_q rows of Q (device
+ * [n_queries][n_q][H_q][d]) and ranks the first n_frames_per_query[g] frames
+ * of frame_offsets (host int32 [n_queries], each in [0, n_frames]) exactly as
+ * cofie_qer_rank would: out_scores row g (device float [n_queries][n_frames])
+ * holds its w_f (-inf past its prefix), out_idx row g (device int32
+ * [n_queries][k_top]) its top-k.  With n_queries > 1: LOGIT mode and n_q a
+ * multiple of 16, else EUNSUPPORTED.  Workspace: the descriptor's, of
+ * cofie_qer_batched_workspace_bytes() bytes. */
+size_t cofie_qer_batched_workspace_bytes(const cofie_qer_desc* heads, int32_t n_queries, int32_t k_top);
+int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_offsets,
+                           const cofie_qer_desc* heads, int32_t n_queries, const int32_t* n_frames_per_query,
+                           int32_t k_top, float* out_scores, int32_t* out_idx, void* stream);
+
 /* ---- coarse-to-fine glue ------------------------------------------------ */
 
 /* The NGFF candidate set S_c as frame indices (Sec. 3.1-3.2: the candidates
@@ -324,9 +339,9 @@ const char* cofie_version(void);
 
 /* ---- measurement -------------------------------------------------------- */
 
-/* Kernel timing: when enabled, every kernel the library enqueues is bracketed
- * by a pair of HIP events on its stream, so per-kernel durations are measured
- * on the GPU's own clock.  cofie_profiler_read synchronises those events and
+/* Kernel timing: when enabled, every kernel the library enqueues carries a
+ * start/stop HIP event pair in its own dispatch (hipExtLaunchKernel), so
+ * per-kernel durations are the kernels' own, on the GPU's clock.  cofie_profiler_read synchronises those events and
  * returns, for kernels whose name contains `name_substr`, the summed duration
  * (ms) and the number of launches.  Process-wide state; not for concurrent
  * use from several host threads. */

@@ -105,6 +105,8 @@ def lib() -> ctypes.CDLL:
         "cofie_evidence_preservation": (ctypes.c_int, [P, P, i32, f64, P, P]),
         "cofie_mask_compact": (ctypes.c_int, [P, i64, i64, P, P, P]),
         "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
+        "cofie_qer_batched_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32, i32]),
+        "cofie_qer_rank_batched": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, i32, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
         "cofie_drop_total": (f64, [f64, f64]),
         "cofie_last_error": (ctypes.c_char_p, []),
@@ -409,3 +411,27 @@ def cofie_evidence_preservation(w, mask, top_frac: float = 0.2, out=None, stream
     _check(lib().cofie_evidence_preservation(_dev(w, "w") if n else None, _dev(mask, "mask") if n else None, n,
                                              float(top_frac), _dev(out, "out"), _stream(stream)))
     return out
+
+
+def cofie_qer_rank_batched(Q, K, frame_offsets, n_frames_per_query, k_top: int, score_mode=LOGIT,
+                           scale: float = 0.0, out_scores=None, out_idx=None, workspace=None, stream=None):
+    """Q [n_queries][n_q][H_q][d] sharing K [n_vis][H_kv][d]; query g ranks the
+    first n_frames_per_query[g] frames.  Returns (w [n_queries][n_frames],
+    idx [n_queries][k_top])."""
+    import numpy as np
+    import torch
+    n_queries, n_q, H_q, d = Q.shape
+    n_vis, H_kv, _ = K.shape
+    n_frames = frame_offsets.numel() - 1
+    dtype = BF16 if Q.dtype == torch.bfloat16 else F32
+    desc = qer_desc(n_q, n_vis, n_frames, H_q, H_kv, d, dtype, score_mode, scale, workspace)
+    if out_scores is None:
+        out_scores = torch.empty((n_queries, max(n_frames, 1)), dtype=torch.float32, device=Q.device)
+    if out_idx is None:
+        out_idx = torch.empty((n_queries, max(k_top, 1)), dtype=torch.int32, device=Q.device)
+    nf = np.ascontiguousarray(n_frames_per_query, dtype=np.int32)
+    _check(lib().cofie_qer_rank_batched(_dev(Q, "Q"), _dev(K, "K"), _dev(frame_offsets, "frame_offsets"),
+                                        ctypes.byref(desc), n_queries, nf.ctypes.data_as(ctypes.c_void_p), k_top,
+                                        _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
+                                        _stream(stream)))
+    return out_scores[:, :n_frames], out_idx[:, :k_top]

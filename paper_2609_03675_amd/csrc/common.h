@@ -2,6 +2,7 @@
 // launch with optional event timing, and a stream-ordered scratch arena.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -25,22 +26,25 @@ void clear_error();
   } while (0)
 
 // ---- kernel timing ------------------------------------------------------------
-// When the profiler is enabled, prof_begin records a start event on the stream
-// and returns a slot; prof_end records the matching stop event.
-int prof_begin(const char* name, hipStream_t s);
-void prof_end(int slot, hipStream_t s);
+// When the profiler is enabled, prof_slot hands out a start/stop event pair for
+// one launch (and returns false otherwise).  The launch carries the pair in its
+// own dispatch (hipExtLaunchKernel), so the elapsed time is the kernel's alone,
+// without the latency of separate event packets on the stream.
+bool prof_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 
-// Launch `kernel` on `s` (bracketed by timing events when profiling is on) and
-// turn a launch failure into COFIE_EHIP.
+// Launch `kernel` on `s` (timed when profiling is on) and turn a launch failure
+// into COFIE_EHIP.
 template <typename... KArgs, typename... Args>
 int launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds,
            hipStream_t s, Args... args) {
   if (grid.x == 0 || grid.y == 0 || grid.z == 0) return COFIE_OK;
   (void)hipGetLastError();
-  int slot = prof_begin(name, s);
-  hipLaunchKernelGGL(kernel, grid, block, lds, s, static_cast<KArgs>(args)...);
+  hipEvent_t start = nullptr, stop = nullptr;
+  if (prof_slot(name, &start, &stop))
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, start, stop, 0u, static_cast<KArgs>(args)...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, static_cast<KArgs>(args)...);
   hipError_t e = hipGetLastError();
-  prof_end(slot, s);
   if (e != hipSuccess)
     return set_error(COFIE_EHIP, "launch of %s failed: %s", name, hipGetErrorString(e));
   return COFIE_OK;

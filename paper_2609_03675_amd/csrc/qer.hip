@@ -106,6 +106,9 @@ struct ScoreLdsArgs {
   float scale;
   float* m;
   int32_t accumulate;
+  int32_t group_rows;  // > 0: query rows form queries of this many rows (a multiple of
+                       // 16), each with its own row of m: m[g * m_stride + j]
+  int64_t m_stride;
 };
 
 constexpr int kLdsWaves = 8;
@@ -361,23 +364,51 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     }
 
     // m_j = scale * max over the query rows: registers over nb, then the 16
-    // lanes of a row group
+    // lanes of a row group; with several queries, one max per query (whole
+    // 16-row blocks), max-accumulated when a query began in an earlier chunk
 #pragma unroll
     for (int j = 0; j < MB; ++j) {
       if (j < nmb) {
         const int64_t tile = rb + wave + kLdsWaves * j;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float v = -INFINITY;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            if (qok[nb]) v = fmaxf(v, acc[j][nb][r]);
-#pragma unroll
-          for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
           const int64_t tok = tile * 16 + g4 * 4 + r;
-          if (r16 == 0 && tok < a.n_vis) {
-            const float x = v * a.scale;
-            a.m[tok] = a.accumulate ? fmaxf(a.m[tok], x) : x;
+          if (a.group_rows == 0) {
+            float v = -INFINITY;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              if (qok[nb]) v = fmaxf(v, acc[j][nb][r]);
+#pragma unroll
+            for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
+            if (r16 == 0 && tok < a.n_vis) {
+              const float x = v * a.scale;
+              a.m[tok] = a.accumulate ? fmaxf(a.m[tok], x) : x;
+            }
+          } else {
+            auto store = [&](int g, float v) {
+              if (r16 == 0 && tok < a.n_vis) {
+                float* dst = a.m + (int64_t)g * a.m_stride + tok;
+                const float x = v * a.scale;
+                *dst = (int64_t)g * a.group_rows < a.q0 ? fmaxf(*dst, x) : x;
+              }
+            };
+            float vg = -INFINITY;
+            int gcur = -1;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              float v = qok[nb] ? acc[j][nb][r] : -INFINITY;
+#pragma unroll
+              for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
+              const int g = (a.q0 + nb * 16) / a.group_rows;
+              if (g != gcur) {
+                if (gcur >= 0) store(gcur, vg);
+                gcur = g;
+                vg = v;
+              } else {
+                vg = fmaxf(vg, v);
+              }
+            }
+            store(gcur, vg);
           }
         }
       }
@@ -461,12 +492,27 @@ __device__ int block_exscan(int v, int* total, int* wsum) {
 
 // Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
 // fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
+// Several queries (blockIdx.y): query g reads row g of m, covers its first
+// nf_q[g] frames (all when nf_q is null) and writes row g of the scores and
+// keys; frames past its prefix score -inf.
 __global__ __launch_bounds__(256) void qer_frame_mean_kernel(const float* m, int32_t n_vis,
                                                              const int32_t* offs, int32_t n_frames,
-                                                             float* out_scores, uint32_t* keys) {
+                                                             float* out_scores, uint32_t* keys,
+                                                             const int32_t* nf_q) {
   const int lane = threadIdx.x & 63;
   const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (f >= n_frames) return;
+  const int64_t g = blockIdx.y;
+  m += g * n_vis;
+  out_scores += g * n_frames;
+  keys += g * n_frames;
+  if (nf_q && f >= nf_q[g]) {
+    if (lane == 0) {
+      out_scores[f] = -INFINITY;
+      keys[f] = order_key(-INFINITY);
+    }
+    return;
+  }
   int lo = offs[f], hi = offs[f + 1];
   lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
   hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
@@ -502,8 +548,14 @@ constexpr int kTopkStage = 8192;  // up to this many frames: keys staged in LDS
 // and how many keys equal to it are taken; a scan over the frames in index
 // order then writes the selected indices, each thread owning a contiguous
 // chunk of frames.
-__global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_frames,
-                                                        int32_t k_top, int32_t* out_idx) {
+// Several queries: workgroup g ranks the first nf_q[g] keys of row g (stride
+// n_stride) and writes row g of out_idx; nf_q null = one query of n_stride keys.
+__global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_stride,
+                                                        int32_t k_top, int32_t* out_idx, const int32_t* nf_q) {
+  const int64_t gq = blockIdx.x;
+  keys_g += gq * n_stride;
+  out_idx += gq * k_top;
+  const int32_t n_frames = nf_q ? nf_q[gq] : n_stride;
   __shared__ __align__(16) uint32_t keys_sh[kTopkStage];
   __shared__ int hist[256];
   __shared__ int wsum[16];
@@ -822,18 +874,20 @@ struct QerPlan {
 };
 
 struct QerScratch {
-  float* m;
-  uint32_t* keys;
+  float* m;        // [n_queries][n_vis]
+  uint32_t* keys;  // [n_queries][n_frames]
   uint8_t* qp;
   float2* partial;
   float2* stats;
+  int32_t* nf;     // [n_queries] frames per query (several queries only)
 };
 
-QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p) {
+QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32_t n_queries = 1) {
   QerScratch w;
-  w.m = ar.take<float>((size_t)(h.n_vis > 0 ? h.n_vis : 1));
-  w.keys = ar.take<uint32_t>((size_t)(h.n_frames > 0 ? h.n_frames : 1));
-  w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * h.n_q * p.Lc * p.esize) : nullptr;
+  w.m = ar.take<float>((size_t)n_queries * (h.n_vis > 0 ? h.n_vis : 1));
+  w.keys = ar.take<uint32_t>((size_t)n_queries * (h.n_frames > 0 ? h.n_frames : 1));
+  w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * n_queries * h.n_q * p.Lc * p.esize) : nullptr;
+  w.nf = n_queries > 1 ? ar.take<int32_t>((size_t)n_queries) : nullptr;
   if (h.score_mode == COFIE_SCORE_SOFTMAX) {
     w.partial = ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
     w.stats = ar.take<float2>((size_t)h.H_q * h.n_q);
@@ -948,41 +1002,25 @@ int launch_soft(const SoftArgs& sa, int NB, int64_t nblk, int pass, hipStream_t 
   }
 }
 
-}  // namespace
-}  // namespace cofie
-
-using namespace cofie;
-
-extern "C" {
-
-size_t cofie_qer_workspace_bytes(const cofie_qer_desc* heads, int32_t k_top) {
-  static const uint64_t dummy[4] = {0, 0, 0, 0};
-  static const int32_t doffs = 0;
-  float dscore;
-  int32_t didx;
-  if (validate_qer(dummy, dummy, &doffs, heads, k_top, &dscore, &didx)) return 0;
-  Arena ar;
-  carve_qer(ar, *heads, plan_qer(*heads));
-  return ar.bytes();
-}
-
-int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
-                   const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
-                   int32_t* out_idx, void* stream) {
-  clear_error();
-  int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
-  if (rc) return rc;
-  const cofie_qer_desc& h = *heads;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+// QER for n_queries queries of h.n_q rows each sharing K (one query: the
+// single-query path); query g covers its first nf_host[g] frames.
+int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const cofie_qer_desc& h,
+              int32_t n_queries, const int32_t* nf_host, int32_t k_top, float* out_scores, int32_t* out_idx,
+              hipStream_t s) {
+  int rc;
+  const bool multi = n_queries > 1;
+  const int32_t R = n_queries * h.n_q;  // query rows
   const QerPlan p = plan_qer(h);
   Arena plan;
-  carve_qer(plan, h, p);
+  carve_qer(plan, h, p, n_queries);
   Scratch scratch;
   rc = scratch.acquire(h.workspace, h.workspace_bytes, plan.bytes(), s);
   if (rc) return rc;
   Arena ar;
   ar.base = scratch.ptr();
-  QerScratch w = carve_qer(ar, h, p);
+  QerScratch w = carve_qer(ar, h, p, n_queries);
+  if (multi && hipMemcpyAsync(w.nf, nf_host, n_queries * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess)
+    return set_error(COFIE_EHIP, "copying the per-query frame counts failed");
   const bool bf16 = h.dtype == COFIE_BF16;
   const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
 
@@ -990,12 +1028,12 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
     if (h.score_mode == COFIE_SCORE_LOGIT) {
       const uint8_t* qp = static_cast<const uint8_t*>(Q);
       if (p.fold) {
-        const int64_t total = (int64_t)h.n_q * p.Lc;
+        const int64_t total = (int64_t)R * p.Lc;
         const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 8192);
         rc = bf16 ? launch("qer_fold", qer_fold_kernel<bf16_t>, dim3(grid), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(Q), h.n_q, h.H_q, h.H_kv, h.d, (void*)w.qp)
+                           static_cast<const bf16_t*>(Q), R, h.H_q, h.H_kv, h.d, (void*)w.qp)
                   : launch("qer_fold", qer_fold_kernel<float>, dim3(grid), dim3(256), 0, s,
-                           static_cast<const float*>(Q), h.n_q, h.H_q, h.H_kv, h.d, (void*)w.qp);
+                           static_cast<const float*>(Q), R, h.H_q, h.H_kv, h.d, (void*)w.qp);
         if (rc) return rc;
         qp = w.qp;
       }
@@ -1003,16 +1041,18 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
       sa.K = static_cast<const uint8_t*>(K);
       sa.Qp = qp;
       sa.n_vis = h.n_vis;
-      sa.nq_total = h.n_q;
+      sa.nq_total = R;
+      sa.group_rows = multi ? h.n_q : 0;
+      sa.m_stride = h.n_vis;
       sa.Lc = (int32_t)p.Lc;
       const int kps = bf16 ? Mma<bf16_t>::KPS : Mma<float>::KPS;
       sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
       const int cus = device_cu_count();
-      for (int q0 = 0; q0 < h.n_q; q0 += 64) {
+      for (int q0 = 0; q0 < R; q0 += 64) {
         sa.q0 = q0;
-        sa.n_q = std::min(64, h.n_q - q0);
+        sa.n_q = std::min(64, R - q0);
         sa.accumulate = q0 > 0;
         const int NB = (sa.n_q + 15) / 16;
         const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P * NB, cus);
@@ -1062,14 +1102,76 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
     }
   }
   if (h.n_frames > 0) {
-    rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4)),
+    rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4), n_queries),
                 dim3(256), 0, s, (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores,
-                w.keys);
+                w.keys, (const int32_t*)w.nf);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
-  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)w.keys,
-                h.n_frames, k_top, out_idx);
+  return launch("qer_topk", qer_topk_kernel, dim3(n_queries), dim3(1024), 0, s, (const uint32_t*)w.keys,
+                h.n_frames, k_top, out_idx, (const int32_t*)w.nf);
+}
+
+}  // namespace
+}  // namespace cofie
+
+using namespace cofie;
+
+extern "C" {
+
+size_t cofie_qer_workspace_bytes(const cofie_qer_desc* heads, int32_t k_top) {
+  static const uint64_t dummy[4] = {0, 0, 0, 0};
+  static const int32_t doffs = 0;
+  float dscore;
+  int32_t didx;
+  if (validate_qer(dummy, dummy, &doffs, heads, k_top, &dscore, &didx)) return 0;
+  Arena ar;
+  carve_qer(ar, *heads, plan_qer(*heads));
+  return ar.bytes();
+}
+
+int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
+                   const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
+                   int32_t* out_idx, void* stream) {
+  clear_error();
+  int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
+  if (rc) return rc;
+  return rank_impl(Q, K, frame_offsets, *heads, 1, nullptr, k_top, out_scores, out_idx,
+                   static_cast<hipStream_t>(stream));
+}
+
+size_t cofie_qer_batched_workspace_bytes(const cofie_qer_desc* heads, int32_t n_queries, int32_t k_top) {
+  static const uint64_t dummy[4] = {0, 0, 0, 0};
+  static const int32_t doffs = 0;
+  float dscore;
+  int32_t didx;
+  if (n_queries < 1 || validate_qer(dummy, dummy, &doffs, heads, k_top, &dscore, &didx)) return 0;
+  Arena ar;
+  carve_qer(ar, *heads, plan_qer(*heads), n_queries);
+  return ar.bytes();
+}
+
+int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_offsets,
+                           const cofie_qer_desc* heads, int32_t n_queries, const int32_t* n_frames_per_query,
+                           int32_t k_top, float* out_scores, int32_t* out_idx, void* stream) {
+  clear_error();
+  int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
+  if (rc) return rc;
+  const cofie_qer_desc& h = *heads;
+  if (n_queries < 1) return set_error(COFIE_EINVAL, "n_queries = %d must be >= 1", n_queries);
+  if (!n_frames_per_query) return set_error(COFIE_EINVAL, "n_frames_per_query is NULL");
+  for (int32_t g = 0; g < n_queries; ++g)
+    if (n_frames_per_query[g] < 0 || n_frames_per_query[g] > h.n_frames)
+      return set_error(COFIE_EINVAL, "query %d: %d frames outside [0, n_frames = %d]", g, n_frames_per_query[g],
+                       h.n_frames);
+  if (n_queries > 1 && h.n_q % 16 != 0)
+    return set_error(COFIE_EUNSUPPORTED, "several queries need n_q (%d) a multiple of 16", h.n_q);
+  if (n_queries > 1 && h.score_mode != COFIE_SCORE_LOGIT)
+    return set_error(COFIE_EUNSUPPORTED, "several queries are ranked in LOGIT mode only");
+  if ((int64_t)n_queries * h.n_q * h.H_q * h.d >= (int64_t(1) << 31))
+    return set_error(COFIE_EUNSUPPORTED, "queries too large");
+  return rank_impl(Q, K, frame_offsets, h, n_queries, n_frames_per_query, k_top, out_scores, out_idx,
+                   static_cast<hipStream_t>(stream));
 }
 
 int64_t cofie_qer_k_from_ratio(double rho, int64_t n) {
@@ -1100,7 +1202,8 @@ int cofie_topk(const float* w, int32_t n, int32_t k_top, int32_t* out_idx, void*
                 dim3(256), 0, s, w, n, keys);
     if (rc) return rc;
   }
-  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)keys, n, k_top, out_idx);
+  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)keys, n, k_top, out_idx,
+                (const int32_t*)nullptr);
 }
 
 int cofie_evidence_preservation(const float* w, const uint8_t* mask, int32_t n, double top_frac, double* out,

@@ -1,4 +1,4 @@
-// Host runtime of libcofie: thread-local error strings, the event-based kernel
+// Host runtime of libcofie: thread-local error strings, the per-dispatch kernel
 // timer, the scratch arena and device queries.
 #include <cstdarg>
 #include <cstring>
@@ -52,26 +52,20 @@ Profiler& prof() {
 }
 }  // namespace
 
-int prof_begin(const char* name, hipStream_t s) {
+bool prof_slot(const char* name, hipEvent_t* start, hipEvent_t* stop) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> lk(p.mu);
-  if (!p.on) return -1;
+  if (!p.on) return false;
   hipEvent_t a = p.get(), b = p.get();
-  if (!a || !b) return -1;
-  if (hipEventRecord(a, s) != hipSuccess) {
-    p.spare.push_back(a);
-    p.spare.push_back(b);
-    return -1;
+  if (!a || !b) {
+    if (a) p.spare.push_back(a);
+    if (b) p.spare.push_back(b);
+    return false;
   }
   p.recs.push_back({name, a, b});
-  return (int)p.recs.size() - 1;
-}
-
-void prof_end(int slot, hipStream_t s) {
-  if (slot < 0) return;
-  Profiler& p = prof();
-  std::lock_guard<std::mutex> lk(p.mu);
-  if (slot < (int)p.recs.size()) (void)hipEventRecord(p.recs[slot].stop, s);
+  *start = a;
+  *stop = b;
+  return true;
 }
 
 // ---- LDS attribute cache ----------------------------------------------------------
