@@ -197,6 +197,22 @@ int cofie_ngff_stream_finish(cofie_ngff_stream* state, uint8_t* mask_all, int64_
 /* Frames pushed per stream so far (-1 for NULL). */
 int64_t cofie_ngff_stream_frames(const cofie_ngff_stream* state);
 
+/* Checkpoint and resume of the streams (the keep rule of Sec. 3.2 needs only
+ * the last L_max histograms, r and the kept count of every stream).
+ * cofie_ngff_stream_state_bytes: size of a saved state (0 for NULL).
+ * cofie_ngff_stream_save writes it to host memory `buf` (bytes >= that size)
+ * once the work enqueued before it on `stream` has run; it returns after the
+ * copy (synchronises `stream`).  cofie_ngff_stream_restore loads such a blob
+ * into a state created with the same n_streams, frame shape, bins and keep
+ * rule (thresholds compared bit for bit), on the state's device; the next
+ * push continues where the saved streams stopped, with the same results as
+ * an uninterrupted run.  The caller keeps the masks of the frames already
+ * pushed (cofie_ngff_stream_finish needs them).  Errors: EINVAL for NULL,
+ * a short buffer, another device, a blob of another format, shape or rule. */
+size_t cofie_ngff_stream_state_bytes(const cofie_ngff_stream* state);
+int cofie_ngff_stream_save(const cofie_ngff_stream* state, void* buf, size_t bytes, void* stream);
+int cofie_ngff_stream_restore(cofie_ngff_stream* state, const void* buf, size_t bytes, void* stream);
+
 /* Release the state (NULL is accepted).  Frees device memory: call it after
  * the work enqueued with the state has completed. */
 int cofie_ngff_stream_destroy(cofie_ngff_stream* state);

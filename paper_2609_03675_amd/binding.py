@@ -100,6 +100,9 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_stream_push": (ctypes.c_int, [P, P, i64, i32, P, P, i64, P]),
         "cofie_ngff_stream_finish": (ctypes.c_int, [P, P, i64, P, P, P]),
         "cofie_ngff_stream_frames": (i64, [P]),
+        "cofie_ngff_stream_state_bytes": (sz, [P]),
+        "cofie_ngff_stream_save": (ctypes.c_int, [P, P, sz, P]),
+        "cofie_ngff_stream_restore": (ctypes.c_int, [P, P, sz, P]),
         "cofie_ngff_stream_destroy": (ctypes.c_int, [P]),
         "cofie_topk": (ctypes.c_int, [P, i32, i32, P, P]),
         "cofie_evidence_preservation": (ctypes.c_int, [P, P, i32, f64, P, P]),
@@ -181,6 +184,8 @@ def keep_rule(hist_mode="gray", tau_h: float = 0.30, L_max: int = 30, M_min: int
     if workspace is not None:
         r.workspace = _dev(workspace, "workspace")
         r.workspace_bytes = workspace.numel() * workspace.element_size()
+    # the rule holds raw device pointers: keep their tensors alive with it
+    r._tensors = (tau_per_segment, out_hist, out_count, workspace)
     return r
 
 
@@ -247,6 +252,7 @@ def qer_desc(n_q: int, n_vis: int, n_frames: int, H_q: int, H_kv: int, d: int, d
     if workspace is not None:
         h.workspace = _dev(workspace, "workspace")
         h.workspace_bytes = workspace.numel() * workspace.element_size()
+        h._tensors = (workspace,)
     return h
 
 
@@ -386,6 +392,23 @@ def cofie_ngff_stream_finish(state, mask_all, ld: int, out_added=None, out_count
 
 def cofie_ngff_stream_frames(state) -> int:
     return int(lib().cofie_ngff_stream_frames(state))
+
+
+def cofie_ngff_stream_state_bytes(state) -> int:
+    return int(lib().cofie_ngff_stream_state_bytes(state))
+
+
+def cofie_ngff_stream_save(state, stream=None) -> bytes:
+    """The streams' state as bytes (a checkpoint)."""
+    n = cofie_ngff_stream_state_bytes(state)
+    buf = ctypes.create_string_buffer(n)
+    _check(lib().cofie_ngff_stream_save(state, buf, n, _stream(stream)))
+    return buf.raw
+
+
+def cofie_ngff_stream_restore(state, blob: bytes, stream=None) -> None:
+    buf = ctypes.create_string_buffer(bytes(blob), len(blob))
+    _check(lib().cofie_ngff_stream_restore(state, buf, len(blob), _stream(stream)))
 
 
 def cofie_ngff_stream_destroy(state) -> None:

@@ -19,6 +19,8 @@
 // theta = min{D : fl32(D)/fl32(2M) >= tau}, exact because fl32(D)/fl32(2M) is
 // strictly increasing in D for 2M < 2^24.  Scores are fl32(D)/fl32(2M), one
 // IEEE division, so they are bit-identical to any correct implementation.
+#include <cstring>
+#include <vector>
 #include "common.h"
 
 namespace cofie {
@@ -1146,6 +1148,43 @@ struct cofie_ngff_stream {
   bool finished = false;
 };
 
+namespace cofie {
+namespace {
+// Host header of a saved stream state; the device arrays follow it.
+struct StreamBlobHeader {
+  char magic[8];
+  int32_t S, L, M_min, mode, H, W, C, B;
+  int64_t nbins;
+  uint32_t tau_bits;
+  int32_t per_segment_tau;
+  int64_t t0;
+  int32_t finished, pad;
+};
+
+StreamBlobHeader blob_header(const cofie_ngff_stream& st) {
+  StreamBlobHeader h;
+  std::memset(&h, 0, sizeof h);
+  std::memcpy(h.magic, "CFNGST01", 8);
+  h.S = st.S;
+  h.L = st.L;
+  h.M_min = st.M_min;
+  h.mode = st.sh.mode;
+  h.H = st.sh.H;
+  h.W = st.sh.W;
+  h.C = st.sh.C;
+  h.B = st.sh.B;
+  h.nbins = st.sh.nbins;
+  // the scalar threshold matters only without per-stream thresholds
+  const float tau = st.tau_dev ? 0.f : st.tau;
+  std::memcpy(&h.tau_bits, &tau, sizeof tau);
+  h.per_segment_tau = st.tau_dev ? 1 : 0;
+  h.t0 = st.t0;
+  h.finished = st.finished ? 1 : 0;
+  return h;
+}
+}  // namespace
+}  // namespace cofie
+
 extern "C" {
 
 void cofie_keep_rule_default(cofie_keep_rule* r) {
@@ -1370,6 +1409,80 @@ int cofie_ngff_stream_destroy(cofie_ngff_stream* st) {
 }
 
 int64_t cofie_ngff_stream_frames(const cofie_ngff_stream* st) { return st ? st->t0 : -1; }
+
+size_t cofie_ngff_stream_state_bytes(const cofie_ngff_stream* st) {
+  if (!st) return 0;
+  return sizeof(StreamBlobHeader) + (st->tau_dev ? (size_t)st->S * sizeof(float) : 0) +
+         (size_t)st->S * st->L * st->sh.nbins * sizeof(uint32_t) + 2 * (size_t)st->S * sizeof(int32_t);
+}
+
+int cofie_ngff_stream_save(const cofie_ngff_stream* st, void* buf, size_t bytes, void* stream) {
+  clear_error();
+  if (!st || !buf) return set_error(COFIE_EINVAL, "state or buffer is NULL");
+  const size_t need = cofie_ngff_stream_state_bytes(st);
+  if (bytes < need) return set_error(COFIE_EINVAL, "buffer of %zu bytes is smaller than the %zu required", bytes, need);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev != st->device)
+    return set_error(COFIE_EINVAL, "the current device is not the state's device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  StreamBlobHeader h = blob_header(*st);
+  char* p = static_cast<char*>(buf);
+  std::memcpy(p, &h, sizeof h);
+  p += sizeof h;
+  if (st->tau_dev) {
+    COFIE_CHECK_HIP(hipMemcpyAsync(p, st->tau_dev, (size_t)st->S * sizeof(float), hipMemcpyDeviceToHost, s));
+    p += (size_t)st->S * sizeof(float);
+  }
+  const size_t wbytes = (size_t)st->S * st->L * st->sh.nbins * sizeof(uint32_t);
+  COFIE_CHECK_HIP(hipMemcpyAsync(p, st->window, wbytes, hipMemcpyDeviceToHost, s));
+  p += wbytes;
+  COFIE_CHECK_HIP(hipMemcpyAsync(p, st->r, (size_t)st->S * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  p += (size_t)st->S * sizeof(int32_t);
+  COFIE_CHECK_HIP(hipMemcpyAsync(p, st->kept, (size_t)st->S * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  COFIE_CHECK_HIP(hipStreamSynchronize(s));
+  return COFIE_OK;
+}
+
+int cofie_ngff_stream_restore(cofie_ngff_stream* st, const void* buf, size_t bytes, void* stream) {
+  clear_error();
+  if (!st || !buf) return set_error(COFIE_EINVAL, "state or buffer is NULL");
+  const size_t need = cofie_ngff_stream_state_bytes(st);
+  if (bytes < need) return set_error(COFIE_EINVAL, "buffer of %zu bytes is smaller than the %zu required", bytes, need);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev != st->device)
+    return set_error(COFIE_EINVAL, "the current device is not the state's device");
+  StreamBlobHeader h;
+  std::memcpy(&h, buf, sizeof h);
+  const StreamBlobHeader want = blob_header(*st);
+  if (std::memcmp(h.magic, want.magic, sizeof h.magic) != 0)
+    return set_error(COFIE_EINVAL, "not a saved NGFF stream state (or another format version)");
+  if (h.S != want.S || h.L != want.L || h.M_min != want.M_min || h.mode != want.mode || h.H != want.H ||
+      h.W != want.W || h.C != want.C || h.B != want.B || h.nbins != want.nbins || h.tau_bits != want.tau_bits ||
+      h.per_segment_tau != want.per_segment_tau)
+    return set_error(COFIE_EINVAL, "the saved state was made with another frame shape or keep rule");
+  if (h.t0 < 0 || h.t0 >= (int64_t(1) << 31) || (h.finished != 0 && h.finished != 1))
+    return set_error(COFIE_EINVAL, "corrupt saved state");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const char* p = static_cast<const char*>(buf) + sizeof h;
+  if (st->tau_dev) {
+    std::vector<float> mine(st->S);
+    COFIE_CHECK_HIP(hipMemcpyAsync(mine.data(), st->tau_dev, (size_t)st->S * sizeof(float), hipMemcpyDeviceToHost, s));
+    COFIE_CHECK_HIP(hipStreamSynchronize(s));
+    if (std::memcmp(mine.data(), p, (size_t)st->S * sizeof(float)) != 0)
+      return set_error(COFIE_EINVAL, "the saved state was made with other per-stream thresholds");
+    p += (size_t)st->S * sizeof(float);
+  }
+  const size_t wbytes = (size_t)st->S * st->L * st->sh.nbins * sizeof(uint32_t);
+  COFIE_CHECK_HIP(hipMemcpyAsync(st->window, p, wbytes, hipMemcpyHostToDevice, s));
+  p += wbytes;
+  COFIE_CHECK_HIP(hipMemcpyAsync(st->r, p, (size_t)st->S * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  p += (size_t)st->S * sizeof(int32_t);
+  COFIE_CHECK_HIP(hipMemcpyAsync(st->kept, p, (size_t)st->S * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  COFIE_CHECK_HIP(hipStreamSynchronize(s));
+  st->t0 = h.t0;
+  st->finished = h.finished != 0;
+  return COFIE_OK;
+}
 
 int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t frames_ld, int32_t b,
                            float* out_scores, uint8_t* out_mask, int64_t ld, void* stream) {

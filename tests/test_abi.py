@@ -166,3 +166,24 @@ def test_diag_copy_validation(L):
     assert L.cofie_diag_stream_copy(FAKE, FAKE, 0, None) == B.COFIE_OK
     if _no_gpu():
         assert L.cofie_diag_stream_copy(FAKE, FAKE + 8, 32, None) == B.COFIE_EINVAL
+
+
+def test_stream_checkpoint_validation(L):
+    assert L.cofie_ngff_stream_state_bytes(None) == 0
+    buf = ctypes.create_string_buffer(64)
+    assert L.cofie_ngff_stream_save(None, buf, 64, None) == B.COFIE_EINVAL
+    assert L.cofie_ngff_stream_restore(None, buf, 64, None) == B.COFIE_EINVAL
+
+
+def test_batched_qer_validation(L):
+    d = B.qer_desc(16, 64, 4, 2, 2, 32)
+    nf = (ctypes.c_int32 * 2)(4, 5)   # 5 > n_frames
+    assert L.cofie_qer_rank_batched(FAKE, FAKE, FAKE, ctypes.byref(d), 2, nf, 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    nf[1] = 3
+    assert L.cofie_qer_rank_batched(FAKE, FAKE, FAKE, ctypes.byref(d), 0, nf, 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_qer_rank_batched(FAKE, FAKE, FAKE, ctypes.byref(d), 2, None, 2, FAKE, FAKE, None) == B.COFIE_EINVAL
+    d20 = B.qer_desc(20, 64, 4, 2, 2, 32)
+    assert L.cofie_qer_rank_batched(FAKE, FAKE, FAKE, ctypes.byref(d20), 2, nf, 2, FAKE, FAKE,
+                                    None) == B.COFIE_EUNSUPPORTED
+    assert B.lib().cofie_qer_batched_workspace_bytes(ctypes.byref(d), 3, 2) > \
+        B.lib().cofie_qer_workspace_bytes(ctypes.byref(d), 2)

@@ -24,8 +24,10 @@ def _gpu():
     B.lib()
 
 
-def run_stream(frames, bins, mode, tau, L_max, M_min, batches, tau_per_stream=None):
-    """frames [S][T][H][W][C] pushed in the given batch sizes; checks every push."""
+def run_stream(frames, bins, mode, tau, L_max, M_min, batches, tau_per_stream=None, checkpoints=()):
+    """frames [S][T][H][W][C] pushed in the given batch sizes; checks every push.
+    After the pushes numbered in `checkpoints` the state is saved, destroyed
+    and restored into a fresh one, which takes the remaining pushes."""
     S, T, H, W, C = frames.shape
     M = oracle.mass(MODES[mode], H, W)
     hists = [oracle.histogram(frames[s], bins, MODES[mode]) for s in range(S)]
@@ -46,6 +48,14 @@ def run_stream(frames, bins, mode, tau, L_max, M_min, batches, tau_per_stream=No
                 B.cofie_ngff_stream_push(st, fd, scores, mask, col=t0, b=b)
             t0 += b
             assert B.cofie_ngff_stream_frames(st) == t0
+            if i in checkpoints:
+                blob = B.cofie_ngff_stream_save(st)
+                assert len(blob) == B.cofie_ngff_stream_state_bytes(st)
+                B.cofie_ngff_stream_destroy(st)
+                st = None
+                st = B.cofie_ngff_stream_create(S, H, W, C, bins, rule)
+                B.cofie_ngff_stream_restore(st, blob)
+                assert B.cofie_ngff_stream_frames(st) == t0
             torch.cuda.synchronize()
             sc, mk = scores.cpu().numpy(), mask.cpu().numpy()
             for s in range(S):
@@ -57,7 +67,8 @@ def run_stream(frames, bins, mode, tau, L_max, M_min, batches, tau_per_stream=No
         B.cofie_ngff_stream_finish(st, mask, T, out_added=added, out_count=count)
         torch.cuda.synchronize()
     finally:
-        B.cofie_ngff_stream_destroy(st)
+        if st is not None:
+            B.cofie_ngff_stream_destroy(st)
     mk, ad, ct = mask.cpu().numpy(), added.cpu().numpy(), count.cpu().numpy()
     for s in range(S):
         s1, m1, k1 = oracle.ngff_select(hists[s], M, float(taus[s]), L_max, M_min)
@@ -104,3 +115,47 @@ def test_push_large_batch_is_split():
     12288 / L_max frames per stream fit the push kernel's LDS)."""
     frames = synth.random_frames(44, 900, 8, 8, scenes=30)[None]
     run_stream(frames, 8, "per_channel", 0.1, 30, 4, [900])
+
+
+@pytest.mark.parametrize("checkpoints", [(0,), (1, 2), (0, 1, 2, 3, 4)])
+def test_checkpoint_and_resume(checkpoints):
+    """Saved after some pushes, restored into a new state: every later push
+    and the finish equal the oracle's uninterrupted stream."""
+    frames = np.stack([synth.random_frames(50 + s, 60, 16, 24, scenes=5) for s in range(2)])
+    run_stream(frames, 16, "per_channel", 0.06, 6, 4, [5, 12, 1, 20, 22], checkpoints=checkpoints,
+               tau_per_stream=np.array([0.04, 0.1], np.float32))
+    run_stream(frames[:1], 16, "gray", 0.05, 30, 3, [9, 40, 11], checkpoints=checkpoints[:1])
+
+
+def test_restore_rejects_other_states():
+    frames = synth.random_frames(60, 20, 16, 24, scenes=3)
+    rule = B.keep_rule("per_channel", 0.06, 6, 4)
+    st = B.cofie_ngff_stream_create(1, 16, 24, 3, 16, rule)
+    scores = torch.zeros((1, 20), dtype=torch.float32, device="cuda")
+    mask = torch.zeros((1, 20), dtype=torch.uint8, device="cuda")
+    others = []
+    try:
+        B.cofie_ngff_stream_push(st, to_dev(frames)[None], scores, mask)
+        blob = B.cofie_ngff_stream_save(st)
+        for r, shape in [(B.keep_rule("per_channel", 0.06, 7, 4), (16, 24, 3, 16)),   # other L_max
+                         (B.keep_rule("per_channel", 0.07, 6, 4), (16, 24, 3, 16)),   # other tau
+                         (B.keep_rule("per_channel", 0.06, 6, 4), (16, 24, 3, 8)),    # other bins
+                         (B.keep_rule("per_channel", 0.06, 6, 4), (24, 16, 3, 16))]:  # other shape
+            o = B.cofie_ngff_stream_create(1, *shape[:3], shape[3], r)
+            others.append(o)
+            with pytest.raises(B.CofieError) as e:
+                B.cofie_ngff_stream_restore(o, blob)
+            assert e.value.code == B.COFIE_EINVAL
+        o = B.cofie_ngff_stream_create(1, 16, 24, 3, 16, rule)
+        others.append(o)
+        for bad in (blob[:-1], b"X" + blob[1:]):                     # short, wrong format
+            with pytest.raises(B.CofieError) as e:
+                B.cofie_ngff_stream_restore(o, bad)
+            assert e.value.code == B.COFIE_EINVAL
+        assert B.cofie_ngff_stream_frames(o) == 0                   # untouched by the failures
+        B.cofie_ngff_stream_restore(o, blob)
+        assert B.cofie_ngff_stream_frames(o) == 20
+    finally:
+        B.cofie_ngff_stream_destroy(st)
+        for o in others:
+            B.cofie_ngff_stream_destroy(o)
