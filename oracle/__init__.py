@@ -22,7 +22,11 @@ end-of-stream safeguards when the stream ends) is pinned by a hand-computed
 stream, causality, and equality with the one-shot rule
 (``tests/test_oracle_ngff_stream.py``).  The evidence-preservation metrics of
 the appendix are pinned by hand-computed cases and a numpy brute force
-(``tests/test_oracle_evidence.py``).
+(``tests/test_oracle_evidence.py``).  The causal attention whose QK^T tiles
+QER reads (``attention``) is pinned by closed forms (the first row, uniform
+logits giving prefix means, a two-key sigmoid, the hard-attention limit) and
+invariants (causality, key shifts, grouped heads as repeated heads, weights
+that sum to one) in ``tests/test_oracle_attention.py``.
 """
 from __future__ import annotations
 
@@ -85,6 +89,8 @@ def _load():
     lib.orc_ngff_finish.restype = i64
     lib.orc_evidence_preservation.argtypes = [P, P, i32, f64, ctypes.POINTER(f64), ctypes.POINTER(f64)]
     lib.orc_evidence_preservation.restype = ctypes.c_int
+    lib.orc_attention_rows.argtypes = [P, P, P, i32, i32, i32, i32, i32, f64, P, i32, P]
+    lib.orc_attention_rows.restype = ctypes.c_int
     lib.orc_mask_compact.argtypes = [P, i64, i64, P, P]
     lib.orc_mask_compact.restype = i64
     lib.orc_gather_frames.argtypes = [P, i64, i64, P, i32, P, i32, P, i64, P, P]
@@ -272,3 +278,25 @@ def evidence_preservation(w: np.ndarray, mask: np.ndarray, p: float = 0.2):
                                            ctypes.byref(rec))
     assert rc == 0
     return apr.value, rec.value
+
+
+def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float = 0.0, rows=None) -> np.ndarray:
+    """Causal softmax attention in fp64 of the given query rows (default: all),
+    every head: Q [L][H_q][d], K and V [L][H_kv][d] (float32, or bf16 bit
+    patterns as uint16).  Returns [len(rows)][H_q][d] float64."""
+    Q = np.ascontiguousarray(Q)
+    K = np.ascontiguousarray(K)
+    V = np.ascontiguousarray(V)
+    L, H_q, d = Q.shape
+    H_kv = K.shape[1]
+    if not (Q.dtype == K.dtype == V.dtype) or Q.dtype not in (np.float32, np.uint16):
+        raise TypeError("Q, K, V must all be float32 or all bf16 bits (uint16)")
+    assert K.shape == (L, H_kv, d) and V.shape == (L, H_kv, d)
+    dtype = F32 if Q.dtype == np.float32 else BF16
+    r = np.arange(L, dtype=np.int32) if rows is None else np.ascontiguousarray(rows, dtype=np.int32)
+    out = np.zeros((max(r.size, 1), H_q, d), dtype=np.float64)
+    rc = _load().orc_attention_rows(_ptr(Q), _ptr(K), _ptr(V), dtype, L, H_q, H_kv, d, float(scale),
+                                    _ptr(r), r.size, _ptr(out))
+    if rc != 0:
+        raise ValueError(f"orc_attention_rows failed ({rc})")
+    return out[:r.size]

@@ -23,6 +23,8 @@
  *   a_ij           head-mean scaled dot product                (Sec. 3.3, Eq. 6)
  *   w_f            max-over-text, mean-over-frame score        (Sec. 3.3, Eq. 7)
  *   S_e            TopK of w_f                                 (Sec. 3.3, Eq. 8)
+ *   o_i^h          causal softmax attention of the last layer, whose QK^T
+ *                  tiles QER reads                            (Sec. 3.3)
  */
 #include <math.h>
 #include <stdint.h>
@@ -570,4 +572,59 @@ int orc_evidence_preservation(const double* w, const uint8_t* mask, int32_t n, d
   *recall = (double)hit / (double)k;
   free(idx);
   return 0;
+}
+
+/* ---- last-layer prefill attention (the attention whose QK^T tiles QER
+ * reads, Sec. 3.3) ------------------------------------------------------- */
+
+/* Causal softmax attention of the listed query rows, every head, in fp64:
+ *   s_ij = scale * <q_i^h, k_j^g(h)>            for j <= i (positions)
+ *   o_i^h = sum_{j<=i} exp(s_ij - max_j s_ij) v_j^g(h) / sum_{j<=i} exp(...)
+ * Q [L][H_q][d], K and V [L][H_kv][d] (dtype as orc_qer_scores); query head
+ * h reads key/value head g(h) = floor(h * H_kv / H_q).  O receives
+ * [n_rows][H_q][d] for the rows given (each in [0, L)).  scale <= 0 selects
+ * 1/sqrt(d).                                                                */
+int orc_attention_rows(const void* Q, const void* K, const void* V, int32_t dtype, int32_t L, int32_t H_q,
+                       int32_t H_kv, int32_t d, double scale, const int32_t* rows, int32_t n_rows, double* O) {
+  if (scale <= 0) scale = 1.0 / sqrt((double)d);
+  const int64_t qstride = (int64_t)H_q * d, kstride = (int64_t)H_kv * d;
+  for (int32_t r = 0; r < n_rows; ++r)
+    if (rows[r] < 0 || rows[r] >= L) return -1;
+  int rc = 0;
+#pragma omp parallel
+  {
+    double* s = (double*)malloc((size_t)(L > 0 ? L : 1) * sizeof(double));
+    if (!s) {
+#pragma omp atomic write
+      rc = -2;
+    }
+#pragma omp for collapse(2) schedule(dynamic, 1)
+    for (int32_t r = 0; r < n_rows; ++r)
+      for (int h = 0; h < H_q; ++h) {
+        if (!s) continue;
+        const int64_t i = rows[r];
+        const int g = (int)(((int64_t)h * H_kv) / H_q);
+        double mx = -INFINITY;
+        for (int64_t j = 0; j <= i; ++j) {
+          double dot = 0;
+          for (int x = 0; x < d; ++x)
+            dot += val_of(Q, dtype, i * qstride + (int64_t)h * d + x) * val_of(K, dtype, j * kstride + (int64_t)g * d + x);
+          s[j] = dot * scale;
+          if (s[j] > mx) mx = s[j];
+        }
+        double z = 0;
+        for (int64_t j = 0; j <= i; ++j) {
+          s[j] = exp(s[j] - mx);
+          z += s[j];
+        }
+        double* o = O + ((int64_t)r * H_q + h) * d;
+        for (int x = 0; x < d; ++x) {
+          double acc = 0;
+          for (int64_t j = 0; j <= i; ++j) acc += s[j] * val_of(V, dtype, j * kstride + (int64_t)g * d + x);
+          o[x] = acc / z;
+        }
+      }
+    free(s);
+  }
+  return rc;
 }
