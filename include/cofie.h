@@ -276,6 +276,40 @@ int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_of
                            const cofie_qer_desc* heads, int32_t n_queries, const int32_t* n_frames_per_query,
                            int32_t k_top, float* out_scores, int32_t* out_idx, void* stream);
 
+/* ---- last-layer prefill attention with QER from its QK^T tiles ------------ */
+
+typedef struct cofie_attn_desc {
+  int32_t L;          /* prefill tokens (rows of Q, K, V), >= 1                      */
+  int32_t H_q, H_kv;  /* heads; H_q % H_kv == 0, query head h reads key/value head   */
+                      /*   h / (H_q / H_kv)                                         */
+  int32_t d;          /* head dimension: 128 (others EUNSUPPORTED)                   */
+  int32_t vis_begin;  /* visual tokens are [vis_begin, vis_end); every other token   */
+  int32_t vis_end;    /*   is text (the scoring set of Sec. 3.3), 1 to 64 of them    */
+  int32_t n_frames;   /* frames of the visual tokens, >= 0                           */
+  float scale;        /* softmax and QER scale; <= 0 selects 1/sqrt(d)               */
+  void* workspace;    /* optional device scratch of                                  */
+  size_t workspace_bytes; /* cofie_attn_qer_workspace_bytes(); else allocated        */
+} cofie_attn_desc;
+
+/* Bytes of device scratch cofie_attn_qer needs (0 for an invalid descriptor). */
+size_t cofie_attn_qer_workspace_bytes(const cofie_attn_desc* desc);
+
+/* The causal softmax attention of the last prefill layer, with QER (Sec. 3.3,
+ * Eqs. 6-8) taken from the same QK^T tiles instead of a pass of its own:
+ *   out[i][h]  = sum_{j<=i} softmax_j(scale <q_i^h, k_j^g>) v_j^g  (bf16)
+ *   out_scores = w_f and out_idx = S_e exactly as cofie_qer_rank in LOGIT
+ *                mode for Q = the text rows (in sequence order) and K = the
+ *                visual rows, frame_offsets relative to vis_begin
+ *   Q            device bf16 [L][H_q][128]; K, V device bf16 [L][H_kv][128]
+ *   out          device bf16 [L][H_q][128]
+ *   frame_offsets device int32 [n_frames+1] (clamped as in cofie_qer_rank)
+ * 16-byte aligned tensors.  Errors: EINVAL for NULL pointers or an invalid
+ * descriptor, EUNSUPPORTED for d != 128 or a text count outside 1..64,
+ * ENOMEM for a short workspace. */
+int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* frame_offsets,
+                   const cofie_attn_desc* desc, int32_t k_top, void* out, float* out_scores, int32_t* out_idx,
+                   void* stream);
+
 /* ---- coarse-to-fine glue ------------------------------------------------ */
 
 /* The NGFF candidate set S_c as frame indices (Sec. 3.1-3.2: the candidates

@@ -61,6 +61,21 @@ class QerDesc(ctypes.Structure):
     ]
 
 
+class AttnDesc(ctypes.Structure):
+    _fields_ = [
+        ("L", ctypes.c_int32),
+        ("H_q", ctypes.c_int32),
+        ("H_kv", ctypes.c_int32),
+        ("d", ctypes.c_int32),
+        ("vis_begin", ctypes.c_int32),
+        ("vis_end", ctypes.c_int32),
+        ("n_frames", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
 _lib = None
 
 
@@ -110,6 +125,8 @@ def lib() -> ctypes.CDLL:
         "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
         "cofie_qer_batched_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32, i32]),
         "cofie_qer_rank_batched": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, i32, P, P, P]),
+        "cofie_attn_qer_workspace_bytes": (sz, [ctypes.POINTER(AttnDesc)]),
+        "cofie_attn_qer": (ctypes.c_int, [P, P, P, P, ctypes.POINTER(AttnDesc), i32, P, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
         "cofie_drop_total": (f64, [f64, f64]),
         "cofie_last_error": (ctypes.c_char_p, []),
@@ -458,3 +475,40 @@ def cofie_qer_rank_batched(Q, K, frame_offsets, n_frames_per_query, k_top: int, 
                                         _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
                                         _stream(stream)))
     return out_scores[:, :n_frames], out_idx[:, :k_top]
+
+
+def attn_desc(L: int, H_q: int, H_kv: int, d: int, vis_begin: int, vis_end: int, n_frames: int,
+              scale: float = 0.0, workspace=None) -> AttnDesc:
+    h = AttnDesc(L, H_q, H_kv, d, vis_begin, vis_end, n_frames, scale, None, 0)
+    if workspace is not None:
+        h.workspace = _dev(workspace, "workspace")
+        h.workspace_bytes = workspace.numel() * workspace.element_size()
+        h._tensors = (workspace,)
+    return h
+
+
+def attn_qer_workspace_bytes(desc: AttnDesc) -> int:
+    return int(lib().cofie_attn_qer_workspace_bytes(ctypes.byref(desc)))
+
+
+def cofie_attn_qer(Q, K, V, frame_offsets, vis_begin: int, vis_end: int, k_top: int, scale: float = 0.0,
+                   out=None, out_scores=None, out_idx=None, workspace=None, stream=None):
+    """Last-layer causal attention of Q [L][H_q][128] over K, V [L][H_kv][128]
+    (bf16) with QER from the same QK^T tiles: the visual tokens are
+    [vis_begin, vis_end), every other token is text.  Returns (out [L][H_q][128]
+    bf16, w [n_frames], idx [k_top])."""
+    import torch
+    L, H_q, d = Q.shape
+    H_kv = K.shape[1]
+    n_frames = frame_offsets.numel() - 1
+    desc = attn_desc(L, H_q, H_kv, d, vis_begin, vis_end, n_frames, scale, workspace)
+    if out is None:
+        out = torch.empty_like(Q)
+    if out_scores is None:
+        out_scores = torch.empty(max(n_frames, 1), dtype=torch.float32, device=Q.device)
+    if out_idx is None:
+        out_idx = torch.empty(max(k_top, 1), dtype=torch.int32, device=Q.device)
+    _check(lib().cofie_attn_qer(_dev(Q, "Q"), _dev(K, "K"), _dev(V, "V"), _dev(frame_offsets, "frame_offsets"),
+                                ctypes.byref(desc), k_top, _dev(out, "out"), _dev(out_scores, "out_scores"),
+                                _dev(out_idx, "out_idx"), _stream(stream)))
+    return out, out_scores[:n_frames], out_idx[:k_top]

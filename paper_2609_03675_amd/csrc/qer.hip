@@ -1113,6 +1113,21 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
 }
 
 }  // namespace
+
+// Eqs. 7-8 from a finished m (one query): w_f and its top-k.  keys: scratch
+// of n_frames words.  Shared with the fused attention path.
+int qer_rank_from_m(const float* m, int32_t n_vis, const int32_t* offs, int32_t n_frames, int32_t k_top,
+                    float* out_scores, uint32_t* keys, int32_t* out_idx, hipStream_t s) {
+  if (n_frames > 0) {
+    int rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(n_frames, 4), 1), dim3(256),
+                    0, s, m, n_vis, offs, n_frames, out_scores, keys, (const int32_t*)nullptr);
+    if (rc) return rc;
+  }
+  if (k_top == 0) return COFIE_OK;
+  return launch("qer_topk", qer_topk_kernel, dim3(1), dim3(1024), 0, s, (const uint32_t*)keys, n_frames, k_top,
+                out_idx, (const int32_t*)nullptr);
+}
+
 }  // namespace cofie
 
 using namespace cofie;

@@ -40,7 +40,7 @@ from typing import Optional
 import numpy as np
 
 SEED0 = (2609, 3675)
-PURPOSE_FRAMES, PURPOSE_QK, PURPOSE_TIMESTAMPS, PURPOSE_NOISE, PURPOSE_QUERY = 0, 1, 2, 3, 4
+PURPOSE_FRAMES, PURPOSE_QK, PURPOSE_TIMESTAMPS, PURPOSE_NOISE, PURPOSE_QUERY, PURPOSE_ATTN = 0, 1, 2, 3, 4, 5
 _POOL_WINDOWS = 65536
 
 
@@ -235,6 +235,28 @@ def qer_inputs(cfg: int, stream: int = 0):
     K = _normal(r, (wl.n_frames * wl.tokens, wl.H_kv, wl.d), wl.qk_dtype)
     offs = frame_offsets(np.full(wl.n_frames, wl.tokens))
     return Q, K, offs
+
+
+def attn_layout(cfg: int):
+    """(L, vis_begin, vis_end) of the last-layer prefill sequence of workloads
+    1-4: a quarter of the text tokens (a system prompt) before the candidate
+    frames' visual tokens, the rest (the question) after them."""
+    wl = WORKLOADS[cfg]
+    n_vis = wl.n_frames * wl.tokens
+    n_pre = wl.n_q // 4
+    return wl.n_q + n_vis, n_pre, n_pre + n_vis
+
+
+def attn_inputs(cfg: int):
+    """bf16 Q [L][H_q][d], K and V [L][H_kv][d] of the whole prefill sequence
+    (standard normal, rounded to bf16) and the visual frames' offsets."""
+    wl = WORKLOADS[cfg]
+    L, _, _ = attn_layout(cfg)
+    r = rng(cfg, 0, PURPOSE_ATTN)
+    Q = _normal(r, (L, wl.H_q, wl.d), "bf16")
+    K = _normal(r, (L, wl.H_kv, wl.d), "bf16")
+    V = _normal(r, (L, wl.H_kv, wl.d), "bf16")
+    return Q, K, V, frame_offsets(np.full(wl.n_frames, wl.tokens))
 
 
 def multistream_queries(cfg: int, stream: int):
