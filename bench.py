@@ -53,6 +53,9 @@ def parse():
                     help="with --configs 5: streams whose queries are ranked (of 32)")
     ap.add_argument("--push-batch", type=int, default=64,
                     help="with --configs: frames per stream and push of the online NGFF pass")
+    ap.add_argument("--attn-qer", default="",
+                    help="comma-separated workload ids (2-4): time the last-layer prefill attention "
+                         "with QER from its QK^T tiles (one JSON line each) instead of the headline step")
     return ap.parse_args()
 
 
@@ -74,6 +77,9 @@ def main():
     B.lib()
     if args.configs:
         config_report(args, [int(c) for c in args.configs.split(",")])
+        return
+    if args.attn_qer:
+        attn_qer_report(args, [int(c) for c in args.attn_qer.split(",")])
         return
     cfg = 2
     wl = synth.WORKLOADS[cfg]
@@ -340,7 +346,7 @@ def profiled_kernels(torch, B, fn, reps: int) -> dict:
     out = {}
     # names are matched as substrings: these are the kernels of the paths used
     for name in ("ngff_fill", "ngff_hist", "ngff_band_next", "ngff_select", "qer_fold", "qer_score",
-                 "qer_frame_mean", "qer_topk"):
+                 "qer_frame_mean", "qer_topk", "attn_qer", "attn_merge"):
         ms, cnt = B.cofie_profiler_read(name)
         if cnt:
             out[name] = round(1e3 * ms / cnt, 2)
@@ -616,6 +622,60 @@ def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams)
                           "speedup_vs_one_call_per_query": round(total_us / bat_us, 3),
                           "scores_equal_one_call_per_query": bat_equal}
     return out
+
+
+def attn_qer_report(args, cfgs):
+    """The last layer's prefill attention with QER read from its QK^T tiles
+    (cofie_attn_qer) on the candidate frames of workloads 2-4: whole-call time,
+    per-kernel times, and the attention kernel's rate against the bf16 MFMA
+    peak.  Algorithmic flops: 4 d H_q per (query, visible key) pair of the
+    causal attention, L (L + 1) / 2 pairs per head; QER adds no pass of its
+    own.  For reference, the separate ranking pass (cofie_qer_rank over the
+    same text rows and visual keys) is timed too."""
+    import torch
+
+    from paper_2609_03675_amd import binding as B
+    from paper_2609_03675_amd import synth
+
+    for cfg in cfgs:
+        wl = synth.WORKLOADS[cfg]
+        L, vb, ve = synth.attn_layout(cfg)
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(2609_3675_000 + cfg)
+        Q = torch.randn((L, wl.H_q, wl.d), generator=gen, device="cuda").to(torch.bfloat16)
+        K = torch.randn((L, wl.H_kv, wl.d), generator=gen, device="cuda").to(torch.bfloat16)
+        V = torch.randn((L, wl.H_kv, wl.d), generator=gen, device="cuda").to(torch.bfloat16)
+        offs = torch.from_numpy(synth.frame_offsets(np.full(wl.n_frames, wl.tokens))).cuda()
+        out = torch.empty_like(Q)
+        w = torch.empty(wl.n_frames, dtype=torch.float32, device="cuda")
+        idx = torch.empty(wl.k_top, dtype=torch.int32, device="cuda")
+        ws = torch.empty(B.attn_qer_workspace_bytes(B.attn_desc(L, wl.H_q, wl.H_kv, wl.d, vb, ve, wl.n_frames)),
+                         dtype=torch.uint8, device="cuda")
+
+        def call(i):
+            B.cofie_attn_qer(Q, K, V, offs, vb, ve, wl.k_top, out=out, out_scores=w, out_idx=idx, workspace=ws)
+
+        us = median_call_us(torch, call, 5, warmup=2)
+        kern = profiled_kernels(torch, B, call, 5)
+        Qt = torch.cat([Q[:vb], Q[ve:]]).contiguous()
+        Kv = K[vb:ve].contiguous()
+
+        def sep(i):
+            B.cofie_qer_rank(Qt, Kv, offs, wl.k_top)
+
+        sep_us = median_call_us(torch, sep, 10)
+        flops = 4.0 * wl.d * wl.H_q * L * (L + 1) / 2
+        tf = flops / (kern["attn_qer"] * 1e-6) / 1e12
+        print(json.dumps({
+            "workload": wl.name, "L": L, "visual_tokens": ve - vb, "text_tokens": L - (ve - vb),
+            "H_q": wl.H_q, "H_kv": wl.H_kv, "d": wl.d, "frames": wl.n_frames, "k_top": wl.k_top,
+            "us_per_call": round(us, 1), "kernels_us": kern,
+            "roofline": {"kernel": "attn_qer", "bound": "mfma", "achieved": round(tf, 1),
+                         "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                         "algorithmic_flops": flops},
+            "separate_qer_rank_us": round(sep_us, 1)}), flush=True)
+        del Q, K, V, out, ws, Qt, Kv
+        torch.cuda.empty_cache()
 
 
 def write_report(args, rows, probe):

@@ -2,12 +2,13 @@
 // (Sec. 3.3: the scores QER needs are the ones the prefill attention already
 // forms, so ranking adds no pass over the keys) on gfx950.
 //
-// One launch, two kinds of workgroup (4 waves each, d = 128, bf16 in, fp32
+// One launch, two kinds of workgroup (8 waves each, d = 128, bf16 in, fp32
 // accumulation):
 //
-//  * visual-row workgroups: causal flash attention of 256 visual query rows
-//    (64 per wave) for one head.  Keys and values stream through LDS in
-//    stages of 64 tokens (double buffered, one barrier per stage); each wave
+//  * visual-row workgroups: causal flash attention of 384 visual query rows
+//    (48 per wave, two waves per SIMD) for one head.  Keys and values stream
+//    through LDS in stages of 64 tokens (double buffered, one barrier per
+//    stage); each wave
 //    forms S^T = K Q^T with bf16 MFMA 16x16x32 (the queries sit in registers
 //    as the B operand), keeps the running row max and sum in the base-2
 //    domain, and accumulates O^T = V^T P^T with P taken straight from the
@@ -15,7 +16,7 @@
 //    the accumulator layout is the B operand layout; V is stored transposed
 //    in LDS in the same order).  Heaviest query blocks first; the blocks of
 //    one head are kept on one XCD so that its L2 serves their key reads.
-//  * text-row workgroups (first in the grid): one per 512-token chunk of the
+//  * text-row workgroups (first in the grid): one per 256-token chunk of the
 //    key sequence, all text rows (<= 64, one 16-row tile per wave), looping
 //    over every head.  The per-head S^T tiles serve both the text rows'
 //    attention (a partial softmax over the chunk, merged afterwards) and QER:
@@ -23,8 +24,10 @@
 //    head-mean logit of Eq. 6 up to the factor scale / H; its max over the
 //    text rows is m_j (Eq. 7) for the chunk's visual keys.
 //
-// attn_merge combines the text rows' chunk partials; qer_rank_from_m then
-// takes the frame means and the top-k (Eqs. 7-8).
+// attn_vt first writes V transposed (d-major rows of tokens, in the operand
+// order of the value product) into the workspace; attn_merge combines the
+// text rows' chunk partials; qer_rank_from_m then takes the frame means and
+// the top-k (Eqs. 7-8).
 #include <cmath>
 
 #include "common.h"
@@ -41,20 +44,22 @@ typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kD = 128;          // head dimension
-constexpr int kThreads = 256;    // 4 waves
-constexpr int kRowsA = 64;       // visual rows per wave
-constexpr int kBM = 4 * kRowsA;  // visual rows per workgroup
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kNT = 3;           // 16-row query tiles per wave (visual rows)
+constexpr int kRowsA = 16 * kNT; // visual rows per wave
+constexpr int kBM = kWaves * kRowsA;  // visual rows per workgroup
 constexpr int kBN = 64;          // tokens per LDS stage
-constexpr int kChunk = 512;      // tokens per text-row workgroup
+constexpr int kChunk = 256;      // tokens per text-row workgroup
 constexpr int kStages = kChunk / kBN;
 constexpr int kMaxText = 64;
 
 struct AttnArgs {
   const uint16_t* Q;  // [L][H_q][128]
   const uint16_t* K;  // [L][H_kv][128]
-  const uint16_t* V;
+  const uint16_t* Vt; // [H_kv][128][Lp]: V transposed, tokens permuted (vpos32) in 32-token groups
   uint16_t* O;        // [L][H_q][128]
-  int32_t L, H_q, H_kv, vb, ve, n_text, ntp;  // ntp: text rows rounded up to 16
+  int32_t L, Lp, H_q, H_kv, vb, ve, n_text, ntp;  // Lp: L rounded up to 64; ntp: text rows to 16
   int32_t n_chunks, nb_pad, qb;               // text workgroups (padded to 8), query blocks per head
   float c2;          // scale * log2(e)
   float qer_scale;   // scale / H_q
@@ -74,78 +79,73 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 }
 
 // ---- LDS stage: 64 tokens of one key/value head ---------------------------------------
-// K: [64 tokens][16 chunks of 16 B], chunk c of token t at (c ^ (t & 15)).
-// V^T: [128 d][64 tokens] (128 B rows, 8 chunks of 16 B).  Inside each
-// 32-token step, token k sits at vpos(k) so that the 8 tokens lane group g of
-// an S^T accumulator holds (4g..4g+3 and 16+4g..16+4g+3) are contiguous;
-// chunk q of row d is stored at (q ^ vswz(d)).
-constexpr int kKWords = kBN * kD / 8;          // uint4 per K stage
-constexpr int kVWords = kD * kBN / 2;          // uint32 per V^T stage
-constexpr int kStageU4 = kKWords + kVWords / 4;  // 16 KiB + 16 KiB
+// K: [64 tokens] rows of 256 B padded to 272 B.  V^T: [128 d] rows of 64
+// tokens (128 B) padded to 144 B; inside each 32-token step, token k sits at
+// vpos(k), so that the 8 tokens lane group g of an S^T accumulator holds
+// (4g..4g+3 and 16+4g..16+4g+3) are contiguous.  The paddings make the 16
+// rows one fragment read touches start on 16 different 16-byte bank groups,
+// and every fragment of a stage is one base address plus an immediate.
+// V^T comes from the pre-pass below, already transposed and permuted.
+constexpr int kKRow = kD * 2 + 16;             // 272 B
+constexpr int kVRow = kBN * 2 + 16;            // 144 B
+constexpr int kKBytes = kBN * kKRow;           // 17408 B
+constexpr int kStageBytes = kKBytes + kD * kVRow;  // + 18432 B
 
-__device__ __forceinline__ int vpos(int k) {
-  const int kk = k & 31;
-  return (k & 32) + 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3);
-}
-__device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 3)) & 7; }
+__host__ __device__ constexpr int vpos32(int kk) { return 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3); }
+
+constexpr int kLoads = 1024 / kThreads;  // 16-byte chunks per thread per stage (K and V^T each)
 
 struct StageRegs {
-  uint4 k[4];
-  uint4 v[4];
+  uint4 k[kLoads];
+  uint4 v[kLoads];
 };
 
-// Global loads of tokens k0..k0+63 of head g (rows clamped to the sequence).
-// Every load instruction covers 4 tokens x 256 contiguous bytes.
+// Global loads of stage k0 of head g: keys (4 tokens x 256 B per load
+// instruction, rows clamped to the sequence) and transposed values (8 rows x
+// 128 B per instruction; k0 clamped to the last stage of V^T).
 __device__ __forceinline__ void stage_load(StageRegs& r, const AttnArgs& a, int g, int k0) {
   const int t = threadIdx.x, c = t & 15, kr = t >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int tok = min(k0 + kr + 16 * i, a.L - 1);
+  for (int i = 0; i < kLoads; ++i) {
+    const int tok = min(k0 + kr + (kThreads / 16) * i, a.L - 1);
     r.k[i] = *reinterpret_cast<const uint4*>(a.K + ((int64_t)tok * a.H_kv + g) * kD + 8 * c);
   }
+  const int kv = min(k0, a.Lp - kBN);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int tok = min(k0 + 2 * kr + p + 32 * i, a.L - 1);
-      r.v[2 * i + p] = *reinterpret_cast<const uint4*>(a.V + ((int64_t)tok * a.H_kv + g) * kD + 8 * c);
-    }
+  for (int i = 0; i < kLoads; ++i) {
+    const int id = t + kThreads * i, d = id >> 3, q = id & 7;
+    r.v[i] = *reinterpret_cast<const uint4*>(a.Vt + ((int64_t)g * kD + d) * a.Lp + kv + 8 * q);
+  }
 }
 
-__device__ __forceinline__ void stage_store(const StageRegs& r, uint4* st) {
+__device__ __forceinline__ void stage_store(const StageRegs& r, char* st) {
   const int t = threadIdx.x, c = t & 15, kr = t >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int tok = kr + 16 * i;
-    st[tok * 16 + (c ^ (tok & 15))] = r.k[i];
-  }
-  uint32_t* vt = reinterpret_cast<uint32_t*>(st + kKWords);
+  for (int i = 0; i < kLoads; ++i)
+    *reinterpret_cast<uint4*>(st + (kr + (kThreads / 16) * i) * kKRow + 16 * c) = r.k[i];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int tok = 2 * kr + 32 * i;  // even: tok and tok + 1 are neighbours in V^T
-    const int p = vpos(tok);
-    const uint32_t w0[4] = {r.v[2 * i].x, r.v[2 * i].y, r.v[2 * i].z, r.v[2 * i].w};
-    const uint32_t w1[4] = {r.v[2 * i + 1].x, r.v[2 * i + 1].y, r.v[2 * i + 1].z, r.v[2 * i + 1].w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int d = 8 * c + e;
-      const uint32_t lo = (w0[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-      const uint32_t hi = (w1[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-      vt[d * 32 + (((p >> 3) ^ vswz(d)) << 2) + ((p & 7) >> 1)] = lo | (hi << 16);
-    }
+  for (int i = 0; i < kLoads; ++i) {
+    const int id = t + kThreads * i, d = id >> 3, q = id & 7;
+    *reinterpret_cast<uint4*>(st + kKBytes + d * kVRow + 16 * q) = r.v[i];
   }
 }
 
+// lane bases of the fragment reads
+__device__ __forceinline__ int k_base() {
+  const int l = threadIdx.x & 63;
+  return (l & 15) * kKRow + 16 * (l >> 4);
+}
+__device__ __forceinline__ int v_base() {
+  const int l = threadIdx.x & 63;
+  return kKBytes + (l & 15) * kVRow + 16 * (l >> 4);
+}
 // A operand of S^T for key tile kt (16 tokens) and contraction step s (32 d)
-__device__ __forceinline__ uint4 k_frag(const uint4* st, int kt, int s) {
-  const int l = threadIdx.x & 63, tok = 16 * kt + (l & 15);
-  return st[tok * 16 + ((4 * s + (l >> 4)) ^ (tok & 15))];
+__device__ __forceinline__ uint4 k_frag(const char* st, int kb, int kt, int s) {
+  return *reinterpret_cast<const uint4*>(st + kb + kt * 16 * kKRow + 64 * s);
 }
-
 // A operand of O^T for d tile dt (16 d) and token step sub (32 tokens)
-__device__ __forceinline__ uint4 v_frag(const uint4* st, int dt, int sub) {
-  const int l = threadIdx.x & 63, d = 16 * dt + (l & 15);
-  return st[kKWords + d * 8 + ((4 * sub + (l >> 4)) ^ vswz(d))];
+__device__ __forceinline__ uint4 v_frag(const char* st, int vb, int dt, int sub) {
+  return *reinterpret_cast<const uint4*>(st + vb + dt * 16 * kVRow + 64 * sub);
 }
 
 // LDS-only barrier: the stage buffers are the only shared state.
@@ -209,26 +209,28 @@ __device__ __forceinline__ void softmax_stage(f32x4 (&s)[4][NT], float (&m)[NT],
 }
 
 template <int NT>
-__device__ __forceinline__ void pv_stage(const uint4* st, f32x4 (&o)[8][NT], const uint4 (&p)[2][NT]) {
+__device__ __forceinline__ void pv_stage(const char* st, f32x4 (&o)[8][NT], const uint4 (&p)[2][NT]) {
+  const int vb = v_base();
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const uint4 vf = v_frag(st, dt, sub);
+      const uint4 vf = v_frag(st, vb, dt, sub);
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) mfma(o[dt][rt], vf, p[sub][rt]);
     }
 }
 
 template <int NT>
-__device__ __forceinline__ void qk_stage(const uint4* st, f32x4 (&s)[4][NT], const uint4 (&q)[4][NT]) {
+__device__ __forceinline__ void qk_stage(const char* st, f32x4 (&s)[4][NT], const uint4 (&q)[4][NT]) {
+  const int kb = k_base();
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) s[kt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const uint4 kf = k_frag(st, kt, ks);
+      const uint4 kf = k_frag(st, kb, kt, ks);
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) mfma(s[kt][rt], kf, q[ks][rt]);
     }
@@ -242,7 +244,98 @@ __device__ __forceinline__ uint4 q_frag(const AttnArgs& a, int pos, int h, int s
 }
 
 // ---- visual rows: causal flash attention -----------------------------------------------------
-__device__ void visual_block(const AttnArgs& a, int b, uint4* lds) {
+// Eight waves of 48 rows, two per SIMD: while one wave of a SIMD runs its
+// softmax on the VALU the other keeps the matrix core busy.  Stages are
+// double buffered.  The running max is raised lazily: the accumulators are
+// rescaled only when a row's max grows by more than kLazy (base 2), so
+// probabilities stay below 2^kLazy and most steps skip the rescale.
+constexpr float kLazy = 8.f;
+
+__device__ __forceinline__ float max_xor16_32(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                                  false, false);
+  x = fmaxf(__builtin_bit_cast(float, a[0]), __builtin_bit_cast(float, a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                                  false, false);
+  return fmaxf(__builtin_bit_cast(float, b[0]), __builtin_bit_cast(float, b[1]));
+}
+
+// S^T of one 32-token step (key tiles 2 half, 2 half + 1 of the stage)
+__device__ __forceinline__ void qk_half(const char* st, int kb, int half, f32x4 (&s)[2][kNT],
+                                        const uint4 (&q)[4][kNT]) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) s[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint4 kf = k_frag(st, kb, 2 * half + j, ks);
+#pragma unroll
+      for (int rt = 0; rt < kNT; ++rt) mfma(s[j][rt], kf, q[ks][rt]);
+    }
+}
+
+// softmax of one 32-token step -> P (B operand of O^T), lazy max
+__device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT], float (&lsum)[kNT], f32x4 (&o)[8][kNT],
+                                             uint4 (&p)[kNT], const int (&row)[kNT], int k0, bool masked, float c2) {
+  const int l = threadIdx.x & 63;
+  float mx[kNT];
+#pragma unroll
+  for (int rt = 0; rt < kNT; ++rt) {
+    float v = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (masked && k0 + 16 * j + 4 * (l >> 4) + e > row[rt]) s[j][rt][e] = -INFINITY;
+        v = fmaxf(v, s[j][rt][e]);
+      }
+    mx[rt] = max_xor16_32(v) * c2;
+  }
+  bool grow = false;
+#pragma unroll
+  for (int rt = 0; rt < kNT; ++rt) grow |= mx[rt] > m[rt] + kLazy;
+  if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) {
+      if (mx[rt] > m[rt] + kLazy) {
+        const float alpha = __builtin_amdgcn_exp2f(m[rt] - mx[rt]);  // m = -inf: 0
+        m[rt] = mx[rt];
+        lsum[rt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) o[dt][rt] *= alpha;
+      }
+    }
+  }
+#pragma unroll
+  for (int rt = 0; rt < kNT; ++rt) {
+    float pv[2][4];
+    const float nm = -m[rt];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pv[j][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][rt][e], c2, nm));
+        lsum[rt] += pv[j][e];
+      }
+    p[rt] = make_uint4(pack2(pv[0][0], pv[0][1]), pack2(pv[0][2], pv[0][3]), pack2(pv[1][0], pv[1][1]),
+                       pack2(pv[1][2], pv[1][3]));
+  }
+}
+
+__device__ __forceinline__ void pv_half(const char* st, int vb, int half, f32x4 (&o)[8][kNT],
+                                        const uint4 (&p)[kNT]) {
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    const uint4 vf = v_frag(st, vb, dt, half);
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) mfma(o[dt][rt], vf, p[rt]);
+  }
+}
+
+__device__ void visual_block(const AttnArgs& a, int b, char* lds) {
   const int total = a.qb * a.H_q, t8 = total / 8;
   const int w = b < 8 * t8 ? (b % 8) * t8 + b / 8 : b;  // the blocks of one XCD: consecutive work
   const int h = w / a.qb, qb = a.qb - 1 - w % a.qb;        // heaviest first within a head
@@ -251,26 +344,28 @@ __device__ void visual_block(const AttnArgs& a, int b, uint4* lds) {
   const int r0 = a.vb + kBM * qb, rw = r0 + kRowsA * wave;
   const int last = min(r0 + kBM, a.ve) - 1;  // last query row of the block
   const int nst = last / kBN + 1;
-  const bool active = rw < a.ve;              // wave has rows
+  // stages this wave sees (0 if it has no rows): tokens up to its last row
+  const int nsw = rw < a.ve ? min(nst, (min(rw + kRowsA, a.ve) - 1) / kBN + 1) : 0;
 
-  uint4 q[4][4];
-  int row[4];
+  uint4 q[4][kNT];
+  int row[kNT];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
+  for (int rt = 0; rt < kNT; ++rt) {
     row[rt] = rw + 16 * rt + (l & 15);
     const int pos = min(row[rt], a.L - 1);
 #pragma unroll
     for (int s = 0; s < 4; ++s) q[s][rt] = q_frag(a, pos, h, s);
   }
-  f32x4 o[8][4];
-  float m[4], lsum[4];
+  f32x4 o[8][kNT];
+  float m[kNT], lsum[kNT];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
+  for (int rt = 0; rt < kNT; ++rt) {
     m[rt] = -INFINITY;
     lsum[rt] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  const int kb = k_base(), vb = v_base();
 
   StageRegs r;
   stage_load(r, a, g, 0);
@@ -278,22 +373,32 @@ __device__ void visual_block(const AttnArgs& a, int b, uint4* lds) {
   lds_barrier();
   for (int st = 0; st < nst; ++st) {
     const int k0 = st * kBN;
-    if (st + 1 < nst) stage_load(r, a, g, k0 + kBN);
-    const uint4* cur = lds + (st & 1) * kStageU4;
-    if (active && k0 <= rw + kRowsA - 1) {  // some token of the stage is visible to the wave
-      f32x4 s[4][4];
-      uint4 p[2][4];
-      qk_stage<4>(cur, s, q);
-      softmax_stage<4>(s, m, lsum, o, p, row, k0, k0 + kBN - 1 > rw, a.c2);
-      pv_stage<4>(cur, o, p);
+    const char* cur = lds + (st & 1) * kStageBytes;
+    // unconditional: past the end the rows are clamped and the buffer
+    // written is one that no later step reads (a guarded load makes the
+    // compiler merge old and new registers and serialise the loads)
+    stage_load(r, a, g, k0 + kBN);
+    if (st < nsw) {
+      const bool masked = k0 + kBN - 1 > rw;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        f32x4 s[2][kNT];
+        uint4 p[kNT];
+        qk_half(cur, kb, half, s, q);
+        softmax_half(s, m, lsum, o, p, row, k0 + 32 * half, masked, a.c2);
+        pv_half(cur, vb, half, o, p);
+      }
     }
-    if (st + 1 < nst) stage_store(r, lds + ((st + 1) & 1) * kStageU4);
+    stage_store(r, lds + ((st + 1) & 1) * kStageBytes);
     lds_barrier();
   }
-  if (!active) return;
+  if (nsw == 0) return;
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const float inv = 1.f / wave_sum4(lsum[rt]);
+  for (int rt = 0; rt < kNT; ++rt) {
+    float ls = lsum[rt];
+    ls += __shfl_xor(ls, 16);
+    ls += __shfl_xor(ls, 32);
+    const float inv = 1.f / ls;
     if (row[rt] >= a.ve) continue;
     uint16_t* out = a.O + ((int64_t)row[rt] * a.H_q + h) * kD + 4 * (l >> 4);
 #pragma unroll
@@ -305,7 +410,7 @@ __device__ void visual_block(const AttnArgs& a, int b, uint4* lds) {
 }
 
 // ---- text rows: chunk partials of their attention, and QER's m_j --------------------------
-__device__ void text_block(const AttnArgs& a, int c, uint4* lds, float* red) {
+__device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int c0 = c * kChunk;
   const int nst = min(kStages, (a.L - c0 + kBN - 1) / kBN);
@@ -348,7 +453,7 @@ __device__ void text_block(const AttnArgs& a, int c, uint4* lds, float* red) {
           const int nh = st + 1 < nst ? h : h + 1;
           stage_load(r, a, nh / per, st + 1 < nst ? k0 + kBN : c0);
         }
-        const uint4* cur = lds + buf * kStageU4;
+        const char* cur = lds + buf * kStageBytes;
         if (active) {
           f32x4 s[4][1];
           uint4 p[2][1];
@@ -358,7 +463,7 @@ __device__ void text_block(const AttnArgs& a, int c, uint4* lds, float* red) {
           softmax_stage<1>(s, m, lsum, o, p, row, k0, true, a.c2);
           pv_stage<1>(cur, o, p);
         }
-        if (more) stage_store(r, lds + (buf ^ 1) * kStageU4);
+        if (more) stage_store(r, lds + (buf ^ 1) * kStageBytes);
         lds_barrier();
         buf ^= 1;
       }
@@ -407,13 +512,48 @@ __device__ void text_block(const AttnArgs& a, int c, uint4* lds, float* red) {
 }
 
 __global__ __launch_bounds__(kThreads, 1) void attn_qer_kernel(AttnArgs a) {
-  extern __shared__ uint4 lds[];
+  extern __shared__ __align__(16) char lds[];
   const int b = blockIdx.x;
   if (b < a.nb_pad) {
-    if (b < a.n_chunks) text_block(a, b, lds, reinterpret_cast<float*>(lds + 2 * kStageU4));
+    if (b < a.n_chunks) text_block(a, b, lds, reinterpret_cast<float*>(lds + 2 * kStageBytes));
     return;
   }
   visual_block(a, b - a.nb_pad, lds);
+}
+
+// V^T for the value stages: Vt[g][d][p] = V[k][g][d] with p = 32 (k / 32) +
+// vpos32(k % 32), zero past L.  One workgroup per 64 tokens and head, the
+// tile transposed through LDS; 16-byte loads and stores.
+__global__ __launch_bounds__(kThreads) void attn_vt_kernel(const uint16_t* V, int32_t L, int32_t H_kv, int32_t Lp,
+                                                           uint16_t* Vt) {
+  __shared__ __align__(16) uint16_t tile[kBN][kD + 8];
+  const int k0 = blockIdx.x * kBN, g = blockIdx.y, t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) {
+    const int id = t + kThreads * i, tok = id >> 4, c = id & 15;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (k0 + tok < L) v = *reinterpret_cast<const uint4*>(V + ((int64_t)(k0 + tok) * H_kv + g) * kD + 8 * c);
+    *reinterpret_cast<uint4*>(&tile[tok][8 * c]) = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) {
+    const int id = t + kThreads * i, d = id >> 3, q = id & 7;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      uint32_t pair = 0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int p = 8 * q + 2 * e + h;  // position in the stage
+        const int half = p >> 5, pp = p & 31, grp = pp >> 3, j = pp & 7;
+        const int tok = 32 * half + 4 * grp + (j & 3) + 16 * (j >> 2);  // the token at position p
+        pair |= (uint32_t)tile[tok][d] << (16 * h);
+      }
+      w[e] = pair;
+    }
+    *reinterpret_cast<uint4*>(Vt + ((int64_t)g * kD + d) * Lp + k0 + 8 * q) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
 }
 
 // Text rows: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c over the chunks.
@@ -436,7 +576,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(AttnArgs a) {
 }
 
 struct AttnPlan {
-  int32_t n_vis, n_text, ntp, n_chunks, nb_pad, qb;
+  int32_t n_vis, n_text, ntp, n_chunks, nb_pad, qb, Lp;
 };
 
 AttnPlan plan_attn(const cofie_attn_desc& h) {
@@ -447,11 +587,13 @@ AttnPlan plan_attn(const cofie_attn_desc& h) {
   p.n_chunks = ceil_div(h.L, kChunk);
   p.nb_pad = (p.n_chunks + 7) / 8 * 8;
   p.qb = ceil_div(p.n_vis, kBM);
+  p.Lp = ceil_div(h.L, kBN) * kBN;
   return p;
 }
 
 void carve_attn(Arena& ar, const cofie_attn_desc& h, const AttnPlan& p, float** m, uint32_t** keys, float** po,
-                float2** pml) {
+                float2** pml, uint16_t** vt) {
+  *vt = ar.take<uint16_t>((size_t)h.H_kv * kD * p.Lp);
   *m = ar.take<float>((size_t)(p.n_vis > 0 ? p.n_vis : 1));
   *keys = ar.take<uint32_t>((size_t)(h.n_frames > 0 ? h.n_frames : 1));
   *po = ar.take<float>((size_t)p.n_chunks * h.H_q * p.ntp * kD);
@@ -483,7 +625,7 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
   return COFIE_OK;
 }
 
-constexpr size_t kLdsBytes = 2 * kStageU4 * sizeof(uint4) + 4 * kChunk * sizeof(float);  // 64 KiB + 8 KiB
+constexpr size_t kLdsBytes = 2 * kStageBytes + 4 * kChunk * sizeof(float);  // 70 KiB + 4 KiB
 
 }  // namespace
 }  // namespace cofie
@@ -502,7 +644,8 @@ size_t cofie_attn_qer_workspace_bytes(const cofie_attn_desc* desc) {
   float *m, *po;
   uint32_t* keys;
   float2* pml;
-  carve_attn(ar, *desc, plan_attn(*desc), &m, &keys, &po, &pml);
+  uint16_t* vt;
+  carve_attn(ar, *desc, plan_attn(*desc), &m, &keys, &po, &pml, &vt);
   return ar.bytes();
 }
 
@@ -519,20 +662,22 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   float *m, *po;
   uint32_t* keys;
   float2* pml;
-  carve_attn(plan, h, p, &m, &keys, &po, &pml);
+  uint16_t* vt;
+  carve_attn(plan, h, p, &m, &keys, &po, &pml, &vt);
   Scratch scratch;
   rc = scratch.acquire(h.workspace, h.workspace_bytes, plan.bytes(), s);
   if (rc) return rc;
   Arena ar;
   ar.base = scratch.ptr();
-  carve_attn(ar, h, p, &m, &keys, &po, &pml);
+  carve_attn(ar, h, p, &m, &keys, &po, &pml, &vt);
 
   AttnArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
   a.K = static_cast<const uint16_t*>(K);
-  a.V = static_cast<const uint16_t*>(V);
+  a.Vt = vt;
   a.O = static_cast<uint16_t*>(out);
   a.L = h.L;
+  a.Lp = p.Lp;
   a.H_q = h.H_q;
   a.H_kv = h.H_kv;
   a.vb = h.vis_begin;
@@ -548,6 +693,9 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   a.m = m;
   a.part_o = po;
   a.part_ml = pml;
+  rc = launch("attn_vt", attn_vt_kernel, dim3((unsigned)(p.Lp / kBN), (unsigned)h.H_kv), dim3(kThreads), 0, s,
+              static_cast<const uint16_t*>(V), h.L, h.H_kv, p.Lp, vt);
+  if (rc) return rc;
   rc = allow_lds(attn_qer_kernel, kLdsBytes);
   if (rc) return rc;
   const int64_t blocks = (int64_t)p.nb_pad + (int64_t)p.qb * h.H_q;
