@@ -6,9 +6,9 @@
 // accumulation):
 //
 //  * visual-row workgroups: causal flash attention of 384 visual query rows
-//    (48 per wave, two waves per SIMD) for one head.  Keys and values stream
-//    through LDS in stages of 64 tokens (double buffered, one barrier per
-//    stage); each wave
+//    (48 per wave, two waves per SIMD in a ping-pong) for one head.  Keys and
+//    values stream through LDS in stages of 64 tokens (three buffers); each
+//    wave
 //    forms S^T = K Q^T with bf16 MFMA 16x16x32 (the queries sit in registers
 //    as the B operand), keeps the running row max and sum in the base-2
 //    domain, and accumulates O^T = V^T P^T with P taken straight from the
@@ -79,73 +79,73 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 }
 
 // ---- LDS stage: 64 tokens of one key/value head ---------------------------------------
-// K: [64 tokens] rows of 256 B padded to 272 B.  V^T: [128 d] rows of 64
-// tokens (128 B) padded to 144 B; inside each 32-token step, token k sits at
-// vpos(k), so that the 8 tokens lane group g of an S^T accumulator holds
-// (4g..4g+3 and 16+4g..16+4g+3) are contiguous.  The paddings make the 16
-// rows one fragment read touches start on 16 different 16-byte bank groups,
-// and every fragment of a stage is one base address plus an immediate.
-// V^T comes from the pre-pass below, already transposed and permuted.
-constexpr int kKRow = kD * 2 + 16;             // 272 B
-constexpr int kVRow = kBN * 2 + 16;            // 144 B
-constexpr int kKBytes = kBN * kKRow;           // 17408 B
-constexpr int kStageBytes = kKBytes + kD * kVRow;  // + 18432 B
+// K: [64 tokens][256 B]; V^T: [128 d][64 tokens = 128 B] (from the pre-pass
+// below, already transposed, and inside each 32-token step with token k at
+// vpos32(k), so that the 8 tokens lane group g of an S^T accumulator holds
+// (4g..4g+3 and 16+4g..16+4g+3) are contiguous).  Both are filled by
+// global-to-LDS DMA: a load instruction writes 64 lanes x 16 B to 1 KiB of
+// consecutive LDS, so the bank swizzle is applied on the global side -- the
+// 16-byte chunk c of key token t sits at slot c ^ (t & 15), chunk c of V^T row
+// d at slot c ^ ((d >> 1) & 7).  A fragment read then touches 16 different
+// bank groups, and every fragment of a stage is a per-lane base plus an
+// immediate.
+constexpr int kKBytes = kBN * kD * 2;              // 16 KiB
+constexpr int kStageBytes = kKBytes + kD * kBN * 2;  // + 16 KiB
 
 __host__ __device__ constexpr int vpos32(int kk) { return 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3); }
 
-constexpr int kLoads = 1024 / kThreads;  // 16-byte chunks per thread per stage (K and V^T each)
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
 
-struct StageRegs {
-  uint4 k[kLoads];
-  uint4 v[kLoads];
-};
+// DMA of stage k0 of head g into st: 32 load instructions of 1 KiB, each wave
+// issuing kDma of them (keys: 4 tokens each, rows clamped to the sequence;
+// values: 8 rows of V^T each, k0 clamped to its last stage).
+constexpr int kDma = 32 / kWaves;
 
-// Global loads of stage k0 of head g: keys (4 tokens x 256 B per load
-// instruction, rows clamped to the sequence) and transposed values (8 rows x
-// 128 B per instruction; k0 clamped to the last stage of V^T).
-__device__ __forceinline__ void stage_load(StageRegs& r, const AttnArgs& a, int g, int k0) {
-  const int t = threadIdx.x, c = t & 15, kr = t >> 4;
-#pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int tok = min(k0 + kr + (kThreads / 16) * i, a.L - 1);
-    r.k[i] = *reinterpret_cast<const uint4*>(a.K + ((int64_t)tok * a.H_kv + g) * kD + 8 * c);
-  }
+__device__ __forceinline__ void stage_dma(const AttnArgs& a, int g, int k0, char* st) {
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int kv = min(k0, a.Lp - kBN);
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int id = t + kThreads * i, d = id >> 3, q = id & 7;
-    r.v[i] = *reinterpret_cast<const uint4*>(a.Vt + ((int64_t)g * kD + d) * a.Lp + kv + 8 * q);
+  for (int j = 0; j < kDma; ++j) {
+    const int i = wave + kWaves * j;  // instruction 0..31
+    if (i < 16) {
+      const int tok = 4 * i + (l >> 4), c = (l & 15) ^ (tok & 15);
+      const int row = min(k0 + tok, a.L - 1);
+      __builtin_amdgcn_global_load_lds((global_void*)(a.K + ((int64_t)row * a.H_kv + g) * kD + 8 * c),
+                                       (lds_void*)(st + 1024 * i), 16, 0, 0);
+    } else {
+      const int d = 8 * (i - 16) + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
+      __builtin_amdgcn_global_load_lds((global_void*)(a.Vt + ((int64_t)g * kD + d) * a.Lp + kv + 8 * c),
+                                       (lds_void*)(st + kKBytes + 1024 * (i - 16)), 16, 0, 0);
+    }
   }
 }
 
-__device__ __forceinline__ void stage_store(const StageRegs& r, char* st) {
-  const int t = threadIdx.x, c = t & 15, kr = t >> 4;
-#pragma unroll
-  for (int i = 0; i < kLoads; ++i)
-    *reinterpret_cast<uint4*>(st + (kr + (kThreads / 16) * i) * kKRow + 16 * c) = r.k[i];
-#pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int id = t + kThreads * i, d = id >> 3, q = id & 7;
-    *reinterpret_cast<uint4*>(st + kKBytes + d * kVRow + 16 * q) = r.v[i];
-  }
-}
+// this wave's DMA has landed in LDS (vmcnt(0); expcnt and lgkmcnt untouched)
+__device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// lane bases of the fragment reads
-__device__ __forceinline__ int k_base() {
-  const int l = threadIdx.x & 63;
-  return (l & 15) * kKRow + 16 * (l >> 4);
-}
-__device__ __forceinline__ int v_base() {
-  const int l = threadIdx.x & 63;
-  return kKBytes + (l & 15) * kVRow + 16 * (l >> 4);
+// lane bases of the fragment reads: ka[s] for contraction step s (key tile
+// kt adds kt * 4 KiB), va[sub] for token step sub (d tile dt adds dt * 2 KiB)
+struct FragBase {
+  int ka[4];
+  int va[2];
+};
+__device__ __forceinline__ FragBase frag_base() {
+  const int l = threadIdx.x & 63, g = l >> 4, r = l & 15;
+  FragBase f;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) f.ka[s] = r * 256 + 16 * ((4 * s + g) ^ r);
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) f.va[sub] = kKBytes + r * 128 + 16 * ((4 * sub + g) ^ ((r >> 1) & 7));
+  return f;
 }
 // A operand of S^T for key tile kt (16 tokens) and contraction step s (32 d)
-__device__ __forceinline__ uint4 k_frag(const char* st, int kb, int kt, int s) {
-  return *reinterpret_cast<const uint4*>(st + kb + kt * 16 * kKRow + 64 * s);
+__device__ __forceinline__ uint4 k_frag(const char* st, const FragBase& f, int kt, int s) {
+  return *reinterpret_cast<const uint4*>(st + f.ka[s] + kt * 4096);
 }
 // A operand of O^T for d tile dt (16 d) and token step sub (32 tokens)
-__device__ __forceinline__ uint4 v_frag(const char* st, int vb, int dt, int sub) {
-  return *reinterpret_cast<const uint4*>(st + vb + dt * 16 * kVRow + 64 * sub);
+__device__ __forceinline__ uint4 v_frag(const char* st, const FragBase& f, int dt, int sub) {
+  return *reinterpret_cast<const uint4*>(st + f.va[sub] + dt * 2048);
 }
 
 // LDS-only barrier: the stage buffers are the only shared state.
@@ -209,28 +209,28 @@ __device__ __forceinline__ void softmax_stage(f32x4 (&s)[4][NT], float (&m)[NT],
 }
 
 template <int NT>
-__device__ __forceinline__ void pv_stage(const char* st, f32x4 (&o)[8][NT], const uint4 (&p)[2][NT]) {
-  const int vb = v_base();
+__device__ __forceinline__ void pv_stage(const char* st, const FragBase& f, f32x4 (&o)[8][NT],
+                                         const uint4 (&p)[2][NT]) {
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const uint4 vf = v_frag(st, vb, dt, sub);
+      const uint4 vf = v_frag(st, f, dt, sub);
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) mfma(o[dt][rt], vf, p[sub][rt]);
     }
 }
 
 template <int NT>
-__device__ __forceinline__ void qk_stage(const char* st, f32x4 (&s)[4][NT], const uint4 (&q)[4][NT]) {
-  const int kb = k_base();
+__device__ __forceinline__ void qk_stage(const char* st, const FragBase& f, f32x4 (&s)[4][NT],
+                                         const uint4 (&q)[4][NT]) {
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) s[kt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const uint4 kf = k_frag(st, kb, kt, ks);
+      const uint4 kf = k_frag(st, f, kt, ks);
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) mfma(s[kt][rt], kf, q[ks][rt]);
     }
@@ -244,11 +244,16 @@ __device__ __forceinline__ uint4 q_frag(const AttnArgs& a, int pos, int h, int s
 }
 
 // ---- visual rows: causal flash attention -----------------------------------------------------
-// Eight waves of 48 rows, two per SIMD: while one wave of a SIMD runs its
-// softmax on the VALU the other keeps the matrix core busy.  Stages are
-// double buffered.  The running max is raised lazily: the accumulators are
-// rescaled only when a row's max grows by more than kLazy (base 2), so
-// probabilities stay below 2^kLazy and most steps skip the rescale.
+// Eight waves of 48 rows, two per SIMD, in a ping-pong: waves 4-7 run one
+// barrier interval behind waves 0-3, and each wave alternates an interval of
+// matrix work (the value product of one 32-token step and the key product of
+// the next) with an interval of softmax, so in every interval one wave of a
+// SIMD feeds the matrix core while the other uses the VALU.  Three stage
+// buffers: the lagging waves still multiply the values of stage st - 1 while
+// the leading ones start stage st + 1's keys.  The running max is raised
+// lazily: the accumulators are rescaled only when a row's max grows by more
+// than kLazy (base 2), so probabilities stay below 2^kLazy and most steps
+// skip the rescale.
 constexpr float kLazy = 8.f;
 
 __device__ __forceinline__ float max_xor16_32(float x) {
@@ -261,7 +266,7 @@ __device__ __forceinline__ float max_xor16_32(float x) {
 }
 
 // S^T of one 32-token step (key tiles 2 half, 2 half + 1 of the stage)
-__device__ __forceinline__ void qk_half(const char* st, int kb, int half, f32x4 (&s)[2][kNT],
+__device__ __forceinline__ void qk_half(const char* st, const FragBase& f, int half, f32x4 (&s)[2][kNT],
                                         const uint4 (&q)[4][kNT]) {
 #pragma unroll
   for (int j = 0; j < 2; ++j)
@@ -271,7 +276,7 @@ __device__ __forceinline__ void qk_half(const char* st, int kb, int half, f32x4 
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const uint4 kf = k_frag(st, kb, 2 * half + j, ks);
+      const uint4 kf = k_frag(st, f, 2 * half + j, ks);
 #pragma unroll
       for (int rt = 0; rt < kNT; ++rt) mfma(s[j][rt], kf, q[ks][rt]);
     }
@@ -281,6 +286,15 @@ __device__ __forceinline__ void qk_half(const char* st, int kb, int half, f32x4 
 __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT], float (&lsum)[kNT], f32x4 (&o)[8][kNT],
                                              uint4 (&p)[kNT], const int (&row)[kNT], int k0, bool masked, float c2) {
   const int l = threadIdx.x & 63;
+  if (masked) {
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (k0 + 16 * j + 4 * (l >> 4) + e > row[rt]) s[j][rt][e] = -INFINITY;
+  }
   float mx[kNT];
 #pragma unroll
   for (int rt = 0; rt < kNT; ++rt) {
@@ -288,10 +302,7 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (masked && k0 + 16 * j + 4 * (l >> 4) + e > row[rt]) s[j][rt][e] = -INFINITY;
-        v = fmaxf(v, s[j][rt][e]);
-      }
+      for (int e = 0; e < 4; ++e) v = fmaxf(v, s[j][rt][e]);
     mx[rt] = max_xor16_32(v) * c2;
   }
   bool grow = false;
@@ -325,11 +336,11 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
   }
 }
 
-__device__ __forceinline__ void pv_half(const char* st, int vb, int half, f32x4 (&o)[8][kNT],
+__device__ __forceinline__ void pv_half(const char* st, const FragBase& f, int half, f32x4 (&o)[8][kNT],
                                         const uint4 (&p)[kNT]) {
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
-    const uint4 vf = v_frag(st, vb, dt, half);
+    const uint4 vf = v_frag(st, f, dt, half);
 #pragma unroll
     for (int rt = 0; rt < kNT; ++rt) mfma(o[dt][rt], vf, p[rt]);
   }
@@ -341,6 +352,7 @@ __device__ void visual_block(const AttnArgs& a, int b, char* lds) {
   const int h = w / a.qb, qb = a.qb - 1 - w % a.qb;        // heaviest first within a head
   const int g = h / (a.H_q / a.H_kv);
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const bool lag = wave >= kWaves / 2;  // one interval behind
   const int r0 = a.vb + kBM * qb, rw = r0 + kRowsA * wave;
   const int last = min(r0 + kBM, a.ve) - 1;  // last query row of the block
   const int nst = last / kBN + 1;
@@ -365,33 +377,57 @@ __device__ void visual_block(const AttnArgs& a, int b, char* lds) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int kb = k_base(), vb = v_base();
+  const FragBase fb = frag_base();
 
-  StageRegs r;
-  stage_load(r, a, g, 0);
-  stage_store(r, lds);
+  stage_dma(a, g, 0, lds);
+  stage_dma(a, g, kBN, lds + kStageBytes);
+  dma_wait();
   lds_barrier();
-  for (int st = 0; st < nst; ++st) {
+  if (lag) lds_barrier();
+
+  f32x4 s[2][kNT];
+  uint4 p[kNT];
+  for (int st = 0; st <= nst; ++st) {
+    const char* cur = lds + (st % 3) * kStageBytes;
+    const char* prev = lds + ((st + 2) % 3) * kStageBytes;
     const int k0 = st * kBN;
-    const char* cur = lds + (st & 1) * kStageBytes;
-    // unconditional: past the end the rows are clamped and the buffer
-    // written is one that no later step reads (a guarded load makes the
-    // compiler merge old and new registers and serialise the loads)
-    stage_load(r, a, g, k0 + kBN);
-    if (st < nsw) {
-      const bool masked = k0 + kBN - 1 > rw;
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        f32x4 s[2][kNT];
-        uint4 p[kNT];
-        qk_half(cur, kb, half, s, q);
-        softmax_half(s, m, lsum, o, p, row, k0 + 32 * half, masked, a.c2);
-        pv_half(cur, vb, half, o, p);
-      }
+    const bool on = st < nsw, was = st > 0 && st - 1 < nsw;
+    const bool masked = k0 + kBN - 1 > rw;
+    // Stage st + 2 goes into the buffer of stage st - 1 in the interval after
+    // that buffer's last read (a lagging wave's interval 0): the leading waves
+    // in their interval 2, the lagging ones in their interval 1 -- the same
+    // interval of the workgroup.  Each wave first waits for its share of stage
+    // st + 1, which the following barrier then publishes.
+    char* next = lds + ((st + 2) % 3) * kStageBytes;
+    // interval 0: values of the previous stage's second step, keys of this
+    // stage's first step
+    if (was) pv_half(prev, fb, 1, o, p);
+    if (on) qk_half(cur, fb, 0, s, q);
+    lds_barrier();
+    if (st == nst) break;
+    // interval 1: softmax of the first step
+    if (lag) {
+      dma_wait();
+      stage_dma(a, g, k0 + 2 * kBN, next);
     }
-    stage_store(r, lds + ((st + 1) & 1) * kStageBytes);
+    if (on) softmax_half(s, m, lsum, o, p, row, k0, masked, a.c2);
+    lds_barrier();
+    // interval 2: values of the first step, keys of the second
+    if (!lag) {
+      dma_wait();
+      stage_dma(a, g, k0 + 2 * kBN, next);
+    }
+    if (on) {
+      pv_half(cur, fb, 0, o, p);
+      qk_half(cur, fb, 1, s, q);
+    }
+    lds_barrier();
+    // interval 3: softmax of the second step
+    if (on) softmax_half(s, m, lsum, o, p, row, k0 + 32, masked, a.c2);
     lds_barrier();
   }
+  if (!lag) lds_barrier();
+  dma_wait();  // no DMA may land in LDS after the workgroup is gone
   if (nsw == 0) return;
 #pragma unroll
   for (int rt = 0; rt < kNT; ++rt) {
@@ -427,9 +463,9 @@ __device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
     for (int kt = 0; kt < 4; ++kt) acc[i][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int per = a.H_q / a.H_kv;
-  StageRegs r;
-  stage_load(r, a, 0, c0);
-  stage_store(r, lds);
+  const FragBase fb = frag_base();
+  stage_dma(a, 0, c0, lds);
+  dma_wait();
   lds_barrier();
   int buf = 0;
   for (int h = 0; h < a.H_q; ++h) {
@@ -449,21 +485,21 @@ __device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
       if (st < nst) {
         const int k0 = c0 + st * kBN;
         const bool more = st + 1 < nst || h + 1 < a.H_q;
-        if (more) {
+        if (more) {  // into the other buffer, whose readers passed the last barrier
           const int nh = st + 1 < nst ? h : h + 1;
-          stage_load(r, a, nh / per, st + 1 < nst ? k0 + kBN : c0);
+          stage_dma(a, nh / per, st + 1 < nst ? k0 + kBN : c0, lds + (buf ^ 1) * kStageBytes);
         }
         const char* cur = lds + buf * kStageBytes;
         if (active) {
           f32x4 s[4][1];
           uint4 p[2][1];
-          qk_stage<1>(cur, s, q);
+          qk_stage<1>(cur, fb, s, q);
 #pragma unroll
           for (int kt = 0; kt < 4; ++kt) acc[st][kt] += s[kt][0];
           softmax_stage<1>(s, m, lsum, o, p, row, k0, true, a.c2);
-          pv_stage<1>(cur, o, p);
+          pv_stage<1>(cur, fb, o, p);
         }
-        if (more) stage_store(r, lds + (buf ^ 1) * kStageBytes);
+        dma_wait();
         lds_barrier();
         buf ^= 1;
       }
@@ -478,6 +514,7 @@ __device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
     }
   }
 
+  dma_wait();
   // m_j: max over the text rows of the head sum, the chunk's visual tokens
   for (int i = threadIdx.x; i < 4 * kChunk; i += kThreads) red[i] = -INFINITY;
   __syncthreads();
@@ -524,6 +561,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_qer_kernel(AttnArgs a) {
 // V^T for the value stages: Vt[g][d][p] = V[k][g][d] with p = 32 (k / 32) +
 // vpos32(k % 32), zero past L.  One workgroup per 64 tokens and head, the
 // tile transposed through LDS; 16-byte loads and stores.
+constexpr int kLoads = 1024 / kThreads;  // 16-byte chunks per thread of a 64-token tile
+
 __global__ __launch_bounds__(kThreads) void attn_vt_kernel(const uint16_t* V, int32_t L, int32_t H_kv, int32_t Lp,
                                                            uint16_t* Vt) {
   __shared__ __align__(16) uint16_t tile[kBN][kD + 8];
@@ -625,7 +664,7 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
   return COFIE_OK;
 }
 
-constexpr size_t kLdsBytes = 2 * kStageBytes + 4 * kChunk * sizeof(float);  // 70 KiB + 4 KiB
+constexpr size_t kLdsBytes = 3 * kStageBytes;  // 96 KiB (the text rows use 2 stages + 4 KiB)
 
 }  // namespace
 }  // namespace cofie
