@@ -181,7 +181,7 @@ def main():
     torch.cuda.synchronize()
     B.cofie_profiler_enable(False)
     kern = {}
-    for name in ("ngff_fill", "ngff_hist", "ngff_band_next", "ngff_select", "qer_fold",
+    for name in ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select", "qer_fold",
                  "qer_score", "qer_frame_mean", "qer_topk"):
         ms, cnt = B.cofie_profiler_read(name)
         if cnt:
@@ -345,7 +345,7 @@ def profiled_kernels(torch, B, fn, reps: int) -> dict:
     B.cofie_profiler_enable(False)
     out = {}
     # names are matched as substrings: these are the kernels of the paths used
-    for name in ("ngff_fill", "ngff_hist", "ngff_band_next", "ngff_select", "qer_fold", "qer_score",
+    for name in ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select", "qer_fold", "qer_score",
                  "qer_frame_mean", "qer_topk", "attn_qer", "attn_merge"):
         ms, cnt = B.cofie_profiler_read(name)
         if cnt:

@@ -108,4 +108,75 @@ inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // Number of compute units of the current device (cached).
 int device_cu_count();
 
+// ---- last workgroup to arrive -------------------------------------------------
+// Lets the workgroups of one launch finish a reduction without a second
+// launch: the one workgroup that arrives last continues with everything the
+// others published.  Measured on gfx950, a device-scope fence costs a whole
+// L2 writeback and invalidate (tens of microseconds when every workgroup of a
+// grid does it), and atomics on one address serialise at ~20-30 ns each, so:
+//  * published data is written with device-coherent stores (st_agent: relaxed
+//    agent-scope atomic stores, which write through to the coherence point),
+//    so no contributor has to write its L2 back or invalidate it;
+//  * each wave waits for its own stores to complete (s_waitcnt vmcnt(0))
+//    before the workgroup barrier, and one thread then adds to the counter
+//    (an agent-scope release RMW);
+//  * only the last arriver acquires (one L2/L1 invalidate, completed before
+//    the workgroup barrier), after which plain loads of every wave see the
+//    published data;
+//  * up to kArriveFlat contributors count on one counter; more go through a
+//    two-level tree: workgroup b of nb counts at sub-counter b % G
+//    (G = kArriveFan), the last of each sub-counter at the root, so no
+//    counter sees more than max(ceil(nb / G), G) arrivals.  Counters sit
+//    `stride` ints apart.
+// A tree is (G + 1) * stride ints, zero on entry (an earlier kernel on the
+// stream clears it).  Nobody waits for anybody, so this cannot deadlock.
+constexpr int kArriveFan = 8;
+constexpr int kArriveFlat = 32;
+
+template <typename T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// This wave's vector-memory operations have completed (gfx9 s_waitcnt
+// encoding: vmcnt = 0, expcnt and lgkmcnt not waited for).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// One counter: true in every thread of the workgroup whose addition completes
+// `total` arrivals.
+__device__ inline bool arrive_counter(int32_t* counter, int32_t total, int32_t* flag_sh) {
+  wait_vmem();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int32_t old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = old + 1 == total;
+    if (last) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      wait_vmem();  // the invalidate has completed before the other waves load
+    }
+    *flag_sh = last;
+  }
+  __syncthreads();
+  return *flag_sh != 0;
+}
+
+// Sub-counters of a tree for nb contributors (0: one flat counter).
+inline __host__ __device__ int32_t arrive_fan(int32_t nb) { return nb <= kArriveFlat ? 0 : kArriveFan; }
+
+// Workgroup b (0 <= b < nb) of the contributors to `tree` arrives; true in the
+// last one.  Every thread of the workgroup calls it, after its st_agent stores.
+__device__ inline bool arrive_last(int32_t* tree, int32_t stride, int32_t b, int32_t nb, int32_t* flag_sh) {
+  if (nb <= 1) {  // the only contributor: its own waves' stores are complete
+    wait_vmem();
+    __syncthreads();
+    return true;
+  }
+  if (nb <= kArriveFlat) return arrive_counter(tree, nb, flag_sh);
+  const int32_t G = arrive_fan(nb);
+  const int32_t j = b % G;
+  const int32_t expect = (nb - 1 - j) / G + 1;  // contributors b' < nb with b' % G == j
+  if (!arrive_counter(tree + (1 + j) * stride, expect, flag_sh)) return false;
+  return arrive_counter(tree, G, flag_sh);
+}
+
 }  // namespace cofie

@@ -7,12 +7,17 @@
 //              registers, increments into 64 lane-private LDS copies laid out
 //              bin-major ([bin][lane]) so that the lanes of one instruction
 //              always hit 64 distinct banks; one merge per workgroup
-//   band_next  exact integer L1 distances D(t, t-k), 1 <= k <= L_max, from
-//              histogram rows staged in LDS, and for every frame r the frame
-//              the keep rule would keep next if r were the last kept frame
-//              (that depends only on the band and theta)
-//   select     one workgroup per stream follows the next[] chain from frame 0,
-//              applies the M_min top-up and writes scores, mask and counts
+//   band_keep  exact integer L1 distances D(t, t-k), 1 <= k <= L_max, from
+//              histogram rows staged in LDS (each row computed once), and per
+//              frame t one word whose bit k says whether t would be kept by
+//              novelty if t-k were the last kept frame (that depends only on
+//              the band and theta)
+//   select     one workgroup per stream: next[r] (the frame kept after r)
+//              from those words, the keep chain from frame 0 by pointer
+//              doubling inside 64-frame windows and a walk across windows,
+//              the M_min top-up, scores, mask and counts
+// With L_max > 31 or histogram rows too wide for LDS, the band, next[] and
+// the selection run as separate kernels (band from global memory).
 // Without the gap rule (L_max <= 0) a sequential kernel per stream measures
 // D(t, r(t)) directly.
 // Novelty comparisons run on integers: s >= tau  <=>  max(D) >= theta with
@@ -331,131 +336,6 @@ __global__ void ngff_next_kernel(RuleArgs a, int32_t* next) {
   next[r] = (int32_t)u;
 }
 
-// Band and next[] in one pass.  A workgroup owns frames [t0, t0+TB): it stages
-// histogram rows [t0-L, t0+TB+L) in LDS, computes the band rows
-// [t0, t0+TB+L) there (the extra L rows are the look-ahead next[] needs),
-// writes its own band rows and next[r] for r in [t0, t0+TB).
-struct BandNextArgs {
-  const uint32_t* hist;
-  int64_t n;
-  int32_t nbins;
-  int32_t stride;  // LDS row stride in words (multiple of 4, >= nbins)
-  int32_t TB;
-  RuleArgs rule;   // band pointer = output band
-  int32_t* band;
-  int32_t* next;
-};
-
-__global__ __launch_bounds__(1024) void ngff_band_next_kernel(BandNextArgs a) {
-  extern __shared__ uint32_t sm[];
-  __shared__ int64_t theta_sh;
-  const int L = a.rule.L;
-  const int n = (int)a.n;
-  const int seg_len = (int)a.rule.seg_len;
-  const int tid = threadIdx.x, nthr = blockDim.x;
-  const int lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
-  const int t0 = blockIdx.x * a.TB;
-  const int r0 = t0 - L > 0 ? t0 - L : 0;
-  const int r1 = t0 + a.TB + L < n ? t0 + a.TB + L : n;  // histogram rows [r0, r1)
-  // histogram rows transposed in LDS: rows[b * RS + (r - r0)], so lanes that
-  // read consecutive frames of one bin touch consecutive words
-  const int RS = a.stride;
-  uint32_t* rows = sm;
-  int32_t* bl = reinterpret_cast<int32_t*>(sm + (size_t)a.nbins * RS);
-  {
-    // rows [r0, r1) are contiguous in global memory; all loads are issued
-    // before any store (indices past the end are clamped to 0 and rewrite
-    // element 0 with its own value)
-    const int total = (r1 - r0) * a.nbins;
-    const uint32_t* src = a.hist + (int64_t)r0 * a.nbins;
-    constexpr int V = 8;
-    for (int i0 = tid; i0 < total; i0 += V * nthr) {
-      uint32_t v[V];
-      int idx[V];
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const int i = i0 + j * nthr;
-        idx[j] = i < total ? i : 0;
-        v[j] = src[idx[j]];
-      }
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const int r = idx[j] / a.nbins, b = idx[j] - r * a.nbins;
-        rows[b * RS + r] = v[j];
-      }
-    }
-  }
-  if (tid == 0) theta_sh = theta_of(tau_of_segment(a.rule, t0 / seg_len), a.rule.twoM);
-  __syncthreads();
-  // band rows [t0, r1): one wave per row; LPP lanes share one lag k, each
-  // adding a slice of the bins, combined with shuffles
-  int LPP = 1;
-  while (LPP < 16 && 2 * LPP * L <= 64) LPP <<= 1;
-  const int per_pass = 64 / LPP;  // lags per wave pass
-  const int sub = lane % LPP, kl = lane / LPP;
-  const int blo = (a.nbins * sub) / LPP, bhi = (a.nbins * (sub + 1)) / LPP;
-  for (int t = t0 + wave; t < r1; t += nw) {
-    const int seg0 = (t / seg_len) * seg_len;
-    const uint32_t* x = rows + (t - r0);
-    for (int kb = 0; kb < L; kb += per_pass) {
-      const int k = kb + kl + 1;
-      uint32_t D = 0;
-      if (k <= L && t - k >= seg0) {
-        const uint32_t* y = rows + (t - k - r0);
-#pragma unroll 8
-        for (int b = blo; b < bhi; ++b) {
-          const uint32_t u = x[b * RS], v = y[b * RS];
-          D += u > v ? u - v : v - u;
-        }
-      }
-      for (int o = 1; o < LPP; o <<= 1) D += __shfl_xor(D, o, LPP);
-      if (sub == 0 && k <= L) {
-        bl[(t - t0) * L + (k - 1)] = (int32_t)D;
-        if (t < t0 + a.TB) a.band[(int64_t)t * L + (k - 1)] = (int32_t)D;
-      }
-    }
-  }
-  __syncthreads();
-  // next[r]: one wave per r, lane k tests frame r+k, the first hit wins
-  const int tend = t0 + a.TB < n ? t0 + a.TB : n;
-  for (int r = t0 + wave; r < tend; r += nw) {
-    const int seg = r / seg_len, s0 = seg * seg_len;
-    const int T = n - s0 < seg_len ? n - s0 : seg_len;
-    const int rr = r - s0;
-    int nxt = T;
-    if (rr < T - 1) {
-      const int64_t theta = (seg == t0 / seg_len) ? theta_sh
-                                                   : theta_of(tau_of_segment(a.rule, seg), a.rule.twoM);
-      // the rule keeps frame rr + kmax at the latest (gap rule or last frame)
-      const int kmax = L < T - 1 - rr ? L : T - 1 - rr;
-      int found = kmax;
-      for (int kb = 1; kb <= kmax; kb += 64) {
-        const int k = kb + lane;
-        bool hit = false;
-        if (k < kmax) {
-          const int32_t* row = bl + (r + k - t0) * L;
-          const int32_t Dadj = row[0], Dref = row[k - 1];
-          hit = (Dadj > Dref ? Dadj : Dref) >= theta;
-        }
-        const uint64_t m = __ballot(hit);
-        if (m) {
-          found = kb + (int)__builtin_ctzll(m);
-          break;
-        }
-      }
-      nxt = rr + found;
-    }
-    if (lane == 0) a.next[r] = nxt;
-  }
-}
-
-// Is t one of the uniformly spaced top-up frames floor(i (T-1)/(m-1)), 0 <= i < m?
-__device__ __forceinline__ bool is_uniform(int64_t t, int64_t T, int64_t m) {
-  if (T <= 1) return t == 0;
-  const int64_t i = (t * (m - 1) + (T - 2)) / (T - 1);  // ceil(t (m-1) / (T-1))
-  return i < m && (i * (T - 1)) / (m - 1) == t;
-}
-
 // Block-wide sum of v (blockDim.x a multiple of 64, <= 1024).
 __device__ int64_t block_sum(int64_t v, int64_t* red) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -486,100 +366,297 @@ __device__ int block_inclusive_max(int v, int* wtmp) {
   return x > before ? x : before;
 }
 
-// One workgroup per stream.  The frames the rule keeps are the chain
-// 0 -> next[0] -> next[next[0]] -> ... -> T-1; it is marked by pointer
-// doubling: with J = next^(2^j), every marked frame also marks J of itself,
-// then J <- J o J, so after ceil(log2 T) + 1 rounds the whole chain is marked
-// (marks made early within a round are chain frames too).  r(t) is then a
-// prefix maximum of kept indices, and every frame's score is formed in
-// parallel.  next/J/flags/r live in LDS when USE_LDS, else in global scratch.
-template <bool USE_LDS>
-__global__ __launch_bounds__(1024) void ngff_select_kernel(RuleArgs a, const int32_t* next_g,
-                                                           uint8_t* flag_g, int32_t* jump_g,
-                                                           int32_t* rprev_g, float* scores,
-                                                           uint8_t* mask, int32_t* count) {
-  extern __shared__ int32_t lds_i[];
+// Selection of one stream by one workgroup (1024 threads), in chunks of C
+// frames (a multiple of 64; the whole stream when it fits):
+//  1. stage(c0, c1, nx) writes next[r] (stream-relative) for r in [c0, c1)
+//     into LDS;
+//  2. windows of 64 frames, one wave each: lane l starts at frame w + l, and
+//     six rounds of pointer doubling over the lanes (shuffles) give, for every
+//     lane, the mask of the chain frames inside the window reached from it and
+//     the first chain frame past the window (its exit);
+//  3. one thread follows the chain across windows: the entry of window i is
+//     the exit of window i-1's entry, so its kept frames are the entry's mask;
+//  4. every thread finishes the chunk's frames: r(t) = the highest kept frame
+//     below t in its window's mask, else the last kept frame before the
+//     window; score = max(D(t,t-1), D(t,r(t))) / 2M from the band; mask bit.
+// Then, if fewer than M_min frames were kept, the top-up frames are added
+// (they never become r, so scores stay as they are).  LDS: next [C] ints,
+// marks [C] u64, window masks [C/64] u64, last kept before window [C/64].
+template <typename StageFn>
+__device__ void select_walk(const RuleArgs& a, int64_t seg, int C, StageFn stage, int32_t* nx, uint64_t* mk,
+                            uint64_t* kmask, int32_t* lastb, const int32_t* adj_g, float* scores, uint8_t* mask,
+                            int32_t* count) {
   __shared__ int64_t red[16];
-  __shared__ int wtmp[16];
-  const int64_t seg = blockIdx.x, s0 = seg * a.seg_len;
+  __shared__ int32_t walk_sh[3];  // carried entry frame, last kept frame, kept count
+  constexpr int U = 4;            // frames per thread and batch of the finishing pass
+  const int64_t s0 = seg * a.seg_len;
   const int T = (int)(a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len);
-  const int tid = threadIdx.x, nthr = blockDim.x;
-  int32_t *J0, *J1, *rp;
-  uint8_t* fl;
-  if constexpr (USE_LDS) {
-    J0 = lds_i;
-    J1 = lds_i + T;
-    rp = lds_i + 2 * T;
-    fl = reinterpret_cast<uint8_t*>(lds_i + 3 * T);
-  } else {
-    J0 = rprev_g + s0;  // rp reuses J0's slice once the chain is marked
-    J1 = jump_g + s0;
-    rp = rprev_g + s0;
-    fl = flag_g + s0;
-  }
+  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
   const float den = (float)a.twoM;
-  for (int t = tid; t < T; t += nthr) {
-    J0[t] = next_g[s0 + t];
-    fl[t] = t == 0;
+  const int32_t* band = a.band + s0 * a.L;
+  const int32_t* adj = adj_g ? adj_g + s0 : nullptr;  // D(t, t-1), contiguous
+  if (tid == 0) {
+    walk_sh[0] = 0;
+    walk_sh[1] = -1;
+    walk_sh[2] = 0;
   }
-  __syncthreads();
-  for (int span = 1; span < 2 * T; span <<= 1) {
-    for (int t = tid; t < T; t += nthr)
-      if (fl[t]) {
-        const int j = J0[t];
-        if (j < T) fl[j] = 1;
-      }
+  for (int c0 = 0; c0 < T; c0 += C) {
+    const int c1 = c0 + C < T ? c0 + C : T;
+    const int nwin = (c1 - c0 + 63) >> 6;
+    stage(c0, c1, nx);
     __syncthreads();
-    for (int t = tid; t < T; t += nthr) {
-      const int j = J0[t];
-      J1[t] = j < T ? J0[j] : T;
+    for (int wi = wave; wi < nwin; wi += nw) {
+      const int w = c0 + (wi << 6), f = w + lane;
+      int J = f < c1 ? nx[f - c0] - w : 64;  // >= 64: past the window
+      uint64_t M = f < c1 ? 1ull << lane : 0ull;
+#pragma unroll
+      for (int rnd = 0; rnd < 6; ++rnd) {
+        const bool in = J < 64;
+        const int src = in ? J : lane;
+        const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)M, src), hi = (uint32_t)__shfl((int)(uint32_t)(M >> 32), src);
+        const int Jo = __shfl(J, src);
+        if (in) {
+          M |= ((uint64_t)hi << 32) | lo;
+          J = Jo;
+        }
+      }
+      if (f < c1) {
+        mk[f - c0] = M;
+        nx[f - c0] = w + J;  // exit frame
+      }
     }
     __syncthreads();
-    int32_t* tmp = J0;
-    J0 = J1;
-    J1 = tmp;
+    if (tid == 0) {
+      // the chain across windows: the entry of window i is the exit of window
+      // i-1's entry (one thread; a few windows per stream)
+      int e = walk_sh[0], last = walk_sh[1], kept = walk_sh[2];
+      for (int wi = 0; wi < nwin; ++wi) {
+        const int w = c0 + (wi << 6);
+        lastb[wi] = last;
+        uint64_t m = 0;
+        if (e < w + 64 && e < T) {
+          m = mk[e - c0];
+          last = w + 63 - __builtin_clzll(m);
+          kept += __builtin_popcountll(m);
+          e = nx[e - c0];
+        }
+        kmask[wi] = m;
+      }
+      walk_sh[0] = e;
+      walk_sh[1] = last;
+      walk_sh[2] = kept;
+    }
+    __syncthreads();
+    for (int base = c0; base < c1; base += U * nthr) {
+      int32_t Da[U], Dr[U];
+      bool kp[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        int t = base + u * nthr + tid;
+        t = t < c1 ? t : c1 - 1;
+        const int wi = (t - c0) >> 6, bit = (t - c0) & 63;
+        const uint64_t m = kmask[wi];
+        const uint64_t below = m & ((1ull << bit) - 1);
+        const int r = below ? c0 + (wi << 6) + 63 - __builtin_clzll(below) : lastb[wi];
+        kp[u] = (m >> bit) & 1;
+        const int32_t* row = band + (int64_t)t * a.L;
+        Da[u] = adj ? adj[t] : row[0];
+        Dr[u] = row[t > 0 ? t - r - 1 : 0];  // t - r <= L: the gap rule bounds every jump
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int t = base + u * nthr + tid;
+        if (t < c1) {
+          mask[s0 + t] = kp[u];
+          scores[s0 + t] = t > 0 ? (float)(Da[u] > Dr[u] ? Da[u] : Dr[u]) / den : 1.0f;
+        }
+      }
+    }
+    __syncthreads();  // the next chunk reuses the LDS arrays
   }
-  // r(t) = last kept frame before t: exclusive prefix max over chunks
-  const int chunk = (T + nthr - 1) / nthr;
-  const int c0 = tid * chunk, c1 = c0 + chunk < T ? c0 + chunk : T;
-  int last = -1;
-  for (int t = c0; t < c1; ++t)
-    if (fl[t]) last = t;
-  __shared__ int incl_sh[1024];
-  incl_sh[tid] = block_inclusive_max(last, wtmp);
-  __syncthreads();
-  int run = tid > 0 ? incl_sh[tid - 1] : -1;  // max over the chunks before this one
-  for (int t = c0; t < c1; ++t) {
-    rp[t] = run;
-    if (fl[t]) run = t;
-  }
-  // top-up when the rule kept fewer than M_min frames
-  int64_t local = 0;
-  for (int t = tid; t < T; t += nthr) local += fl[t] != 0;
-  const int64_t kept = block_sum(local, red);
-  if (a.M_min >= 2 && kept < a.M_min) {
+  const int K = walk_sh[2];
+  int64_t added = 0;
+  if (a.M_min >= 2 && K < a.M_min) {
+    // top-up: the frames floor(i (T-1) / (M_min-1)), i < M_min (non-decreasing
+    // in i; each distinct frame not kept yet is added once)
+    wait_vmem();  // this wave's mask stores have completed
+    __syncthreads();
     for (int64_t i = tid; i < a.M_min; i += nthr) {
       const int64_t u = (i * (T - 1)) / (a.M_min - 1);
-      if (fl[u] == 0) fl[u] = 2;
+      const bool first = i == 0 || ((i - 1) * (T - 1)) / (a.M_min - 1) != u;
+      added += first && mask[s0 + u] == 0;
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < a.M_min; i += nthr) mask[s0 + (i * (T - 1)) / (a.M_min - 1)] = 1;
+  }
+  const int64_t total = K + block_sum(added, red);
+  if (count && tid == 0) count[seg] = (int32_t)total;
+}
+
+// LDS bytes of select_walk's arrays for chunks of C frames (plus the
+// keep-test words of [c0, c1 + 32) when next[] is formed from them).
+__host__ __device__ constexpr size_t select_lds(int C, bool from_words) {
+  return (size_t)C * 12 + (size_t)(C / 64) * 12 + (from_words ? (size_t)(C + 32) * 4 : 0) + 64;
+}
+
+// One workgroup per stream.  FROM_WORDS: next[r] is the first k <
+// min(L, T-1-r) with bit k of the keep-test word G[r+k] set, else that bound
+// (the gap rule or the last frame); otherwise next[] is read from next_g.
+template <bool FROM_WORDS>
+__global__ __launch_bounds__(1024) void ngff_select_kernel(RuleArgs a, const uint32_t* G, const int32_t* next_g,
+                                                           const int32_t* adj, int32_t C, float* scores,
+                                                           uint8_t* mask, int32_t* count) {
+  extern __shared__ __align__(16) int32_t lds_i[];
+  const int64_t seg = blockIdx.x, s0 = seg * a.seg_len;
+  const int T = (int)(a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len);
+  uint64_t* mk = reinterpret_cast<uint64_t*>(lds_i);
+  uint64_t* kmask = mk + C;
+  int32_t* nx = reinterpret_cast<int32_t*>(kmask + C / 64);
+  int32_t* lastb = nx + C;
+  uint32_t* gs = reinterpret_cast<uint32_t*>(lastb + C / 64);  // FROM_WORDS: G of [c0, c1 + 32)
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int L = a.L;
+  auto stage = [&](int c0, int c1, int32_t* dst) __attribute__((always_inline)) {
+    if constexpr (FROM_WORDS) {
+      const int ce = c1 + 32 < T ? c1 + 32 : T;
+      constexpr int V = 4;  // loads in flight per thread
+      for (int t0 = c0 + tid; t0 < ce; t0 += V * nthr) {
+        uint32_t v[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int t = t0 + j * nthr;
+          v[j] = G[s0 + (t < ce ? t : c0)];
+        }
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int t = t0 + j * nthr;
+          if (t < ce) gs[t - c0] = v[j];
+        }
+      }
+      __syncthreads();
+      for (int r = c0 + tid; r < c1; r += nthr) {
+        const int kmax = L < T - 1 - r ? L : T - 1 - r;  // keep at r + kmax at the latest
+        int found = kmax;
+        // words read 8 at a time (entries past the staged ones are never
+        // used: k < kmax keeps r + k < T - 1)
+        for (int k0 = 1; k0 < kmax && found == kmax; k0 += 8) {
+          uint32_t hit = 0;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int k = k0 + j;
+            hit |= (uint32_t)(k < kmax && ((gs[r + k - c0] >> k) & 1u)) << j;
+          }
+          if (hit) found = k0 + __builtin_ctz(hit);
+        }
+        dst[r - c0] = r == T - 1 ? T : r + found;
+      }
+    } else {
+      for (int t = c0 + tid; t < c1; t += nthr) dst[t - c0] = next_g[s0 + t];
+    }
+  };
+  select_walk(a, seg, C, stage, nx, mk, kmask, lastb, adj, scores, mask, count);
+}
+
+// Band rows and keep-test words (L_max <= 31).  Workgroup b owns frames
+// [t0, t0+TB): it stages histogram rows [t0-L, t0+TB) transposed in LDS
+// ([bin][row]), computes the band rows D(t, t-k) of its frames (lanes split
+// the (row, lag) pairs and the bins), and packs the keep tests each row
+// decides into one word: bit k of G[t] is set when, with r = t-k the last
+// kept frame, the rule keeps t by novelty (max(D(t,t-1), D(t,r)) >= theta,
+// t-k in t's stream).
+struct BandKeepArgs {
+  const uint32_t* hist;
+  int64_t n;
+  int32_t nbins;
+  int32_t TB;       // frames per workgroup
+  int32_t RS;       // LDS row stride (words) of the staged rows, >= TB + L
+  RuleArgs rule;
+  int32_t* band;    // [n][L]
+  int32_t* adj;     // [n] D(t, t-1) (the band's first column, contiguous)
+  uint32_t* G;      // [n] keep-test words
+};
+
+__global__ __launch_bounds__(1024) void ngff_band_keep_kernel(BandKeepArgs a) {
+  extern __shared__ __align__(16) uint32_t sm[];
+  const RuleArgs& ru = a.rule;
+  const int L = ru.L;
+  const int64_t n = a.n, seg_len = ru.seg_len;
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int64_t t0 = (int64_t)blockIdx.x * a.TB;
+  const int64_t t1 = t0 + a.TB < n ? t0 + a.TB : n;
+  const int64_t r0 = t0 - L > 0 ? t0 - L : 0;  // histogram rows [r0, t1)
+  const int RS = a.RS;
+  uint32_t* rows = sm;                                                  // [nbins][RS]
+  int32_t* bl = reinterpret_cast<int32_t*>(sm + (size_t)a.nbins * RS);  // [TB][L]
+  {
+    // rows [r0, t1) are contiguous in global memory; all loads are issued
+    // before any store (indices past the end are clamped to 0 and rewrite
+    // element 0 with its own value)
+    const int total = (int)(t1 - r0) * a.nbins;
+    const uint32_t* src = a.hist + r0 * a.nbins;
+    constexpr int V = 8;
+    for (int i0 = tid; i0 < total; i0 += V * nthr) {
+      uint32_t v[V];
+      int idx[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int i = i0 + j * nthr;
+        idx[j] = i < total ? i : 0;
+        v[j] = src[idx[j]];
+      }
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int r = idx[j] / a.nbins, b = idx[j] - r * a.nbins;
+        rows[b * RS + r] = v[j];
+      }
     }
   }
   __syncthreads();
-  local = 0;
-  for (int t = tid; t < T; t += nthr) {
-    const uint8_t f = fl[t];
-    local += f != 0;
-    mask[s0 + t] = f != 0;
-    float sc = 1.0f;
-    if (t > 0) {
-      const int r = rp[t];  // t - r <= L: the gap rule bounds every jump
-      const int32_t* row = a.band + (s0 + t) * a.L;
-      const int32_t Dadj = row[0], Dref = row[t - r - 1];
-      sc = (float)(Dadj > Dref ? Dadj : Dref) / den;
+  // band: (row, lag) pairs, LPP lanes per pair (a power of two <= 64, so a
+  // group never straddles a wave), bins strided over the group
+  const int npairs = (int)(t1 - t0) * L;
+  int LPP = 1;
+  while (LPP < 64 && 2 * LPP * npairs <= nthr) LPP <<= 1;
+  const int sub = tid & (LPP - 1);
+  const int groups = nthr / LPP;
+  const int passes = (npairs + groups - 1) / groups;  // whole passes: every lane runs the shuffles
+  for (int ps = 0; ps < passes; ++ps) {
+    const int pi = ps * groups + tid / LPP;
+    const bool ok = pi < npairs;
+    const int64_t t = t0 + (ok ? pi / L : 0);
+    const int k = ok ? pi % L + 1 : 1;
+    const int64_t seg0 = (t / seg_len) * seg_len;
+    uint32_t D = 0;
+    if (ok && t - k >= seg0) {
+      const uint32_t* x = rows + (t - r0);
+      const uint32_t* y = rows + (t - k - r0);
+      for (int b = sub; b < a.nbins; b += LPP) {
+        const uint32_t u = x[b * RS], v = y[b * RS];
+        D += u > v ? u - v : v - u;
+      }
     }
-    scores[s0 + t] = sc;
+    for (int o = 1; o < LPP; o <<= 1) D += __shfl_xor(D, o, LPP);
+    if (ok && sub == 0) {
+      bl[pi] = (int32_t)D;
+      a.band[t * L + (k - 1)] = (int32_t)D;
+    }
   }
-  const int64_t total = block_sum(local, red);
-  if (count && tid == 0) count[seg] = (int32_t)total;
+  __syncthreads();
+  // keep-test words of these rows
+  for (int64_t t = t0 + tid; t < t1; t += nthr) {
+    const int64_t seg = t / seg_len;
+    const int kmax = (int)(t - seg * seg_len) < L ? (int)(t - seg * seg_len) : L;  // t - k stays in the stream
+    const int64_t theta = theta_of(tau_of_segment(ru, seg), ru.twoM);
+    const int32_t* row = bl + (t - t0) * L;
+    const int32_t Dadj = row[0];
+    a.adj[t] = Dadj;
+    uint32_t g = 0;
+    for (int k = 1; k <= kmax; ++k) {
+      const int32_t Dref = row[k - 1];
+      g |= (uint32_t)((Dadj > Dref ? Dadj : Dref) >= theta) << k;
+    }
+    a.G[t] = g;
+  }
 }
 
 // L_max <= 0: no gap rule, so r(t) can lie arbitrarily far back.  One
@@ -881,26 +958,65 @@ RulePlan plan_rule(const NgffShape& sh, const cofie_keep_rule* r) {
   return p;
 }
 
+// Launch plan of the band/keep-word kernel: TB frames per workgroup (about
+// one workgroup per CU, at most ~48 Ki |difference| terms of band work each),
+// the transposed histogram rows (nbins x RS words, RS = TB + L made odd so
+// that lanes reading consecutive bins hit distinct banks) and the tile's band
+// rows (TB x L words) in LDS.  ok = false when L_max > 31 (one keep-test word
+// per frame) or even one frame's rows exceed the LDS budget.
+constexpr size_t kLdsBudget = 150 * 1024;
+
+struct BandKeepPlan {
+  bool ok;
+  int TB, RS;
+  size_t lds;
+};
+
+BandKeepPlan plan_band_keep(const NgffShape& sh, const RulePlan& rp) {
+  BandKeepPlan p;
+  const int64_t cus = device_cu_count();
+  int64_t tb = (sh.n + cus - 1) / cus;
+  int64_t tb_max = 49152 / ((int64_t)rp.L * sh.nbins);
+  tb_max = tb_max < 1 ? 1 : (tb_max > 64 ? 64 : tb_max);
+  p.TB = (int)(tb < 1 ? 1 : (tb > tb_max ? tb_max : tb));
+  auto stage = [&](int TB) {
+    const int RS = (TB + rp.L) | 1;
+    return (size_t)sh.nbins * RS * 4 + (size_t)TB * rp.L * 4;
+  };
+  while (p.TB > 1 && stage(p.TB) > kLdsBudget) --p.TB;
+  p.RS = (p.TB + rp.L) | 1;
+  p.lds = stage(p.TB);
+  p.ok = rp.L <= 31 && p.lds <= kLdsBudget;
+  return p;
+}
+
+// Frames per selection chunk: the stream rounded up to 64, at most 4096.
+inline int select_chunk(int64_t seg_len) {
+  const int64_t c = (seg_len + 63) / 64 * 64;
+  return (int)(c < 4096 ? c : 4096);
+}
+
 // Scratch layout of filter/calibrate (same sequence sizes and carves).
 struct NgffScratch {
   uint32_t* hist;
   int32_t* band;
-  int32_t* next;
-  int32_t* rprev;
-  int32_t* jump;
-  uint8_t* flags;
-  int32_t* best;
+  int32_t* next;   // next-keep table of the separate kernels
+  uint8_t* flags;  // per-frame flags of the sequential selection (no gap rule)
+  int32_t* best;   // calibration: best threshold per stream
+  uint32_t* G;     // [n] keep-test words
+  int32_t* adj;    // [n] D(t, t-1)
 };
 
 NgffScratch carve(Arena& ar, const NgffShape& sh, const RulePlan& rp, bool need_hist) {
   NgffScratch w;
+  const size_t nseg = (size_t)(rp.nseg > 0 ? rp.nseg : 1);
   w.hist = need_hist ? ar.take<uint32_t>((size_t)(sh.n * sh.nbins)) : nullptr;
   w.band = ar.take<int32_t>((size_t)(sh.n * rp.L));
   w.next = ar.take<int32_t>((size_t)sh.n);
-  w.rprev = ar.take<int32_t>((size_t)sh.n);
-  w.jump = ar.take<int32_t>((size_t)sh.n);
   w.flags = ar.take<uint8_t>((size_t)sh.n);
-  w.best = ar.take<int32_t>((size_t)(rp.nseg > 0 ? rp.nseg : 1));
+  w.best = ar.take<int32_t>(nseg);
+  w.G = ar.take<uint32_t>((size_t)sh.n);
+  w.adj = ar.take<int32_t>((size_t)sh.n);
   return w;
 }
 
@@ -928,13 +1044,6 @@ int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int3
   int rc = allow_lds(ngff_band_kernel, lds);
   if (rc) return rc;
   return launch("ngff_band", ngff_band_kernel, dim3((unsigned)ceil_div(sh.n, TB)), dim3(256), lds, s, b);
-}
-
-// LDS bytes of the fused band/next kernel for a tile of TB frames: the
-// transposed histogram rows (nbins x RS words, RS >= TB + 2L) and the band
-// rows of the tile plus look-ahead ((TB + L) x L words).
-size_t band_next_lds(const NgffShape& sh, int L, int TB, int RS) {
-  return (size_t)sh.nbins * RS * 4 + (size_t)(TB + L) * L * 4;
 }
 
 RuleArgs rule_args(const NgffShape& sh, const RulePlan& rp, const cofie_keep_rule* r,
@@ -1256,48 +1365,49 @@ int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, in
   NgffScratch w = carve(ar, sh, rp, need_hist);
   uint32_t* hist = need_hist ? w.hist : keep_rule->out_hist;
 
+  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
   rc = run_histogram(frames, sh, hist, s);
   if (rc) return rc;
-  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
-  if (rp.gap_rule) {
-    int TB = 8;
-    auto rs_of = [&](int tb) { return tb + 2 * rp.L; };
-    while (TB > 1 && band_next_lds(sh, rp.L, TB, rs_of(TB)) > 150 * 1024) TB >>= 1;
-    const int stride = rs_of(TB);
-    const size_t lds_bn = band_next_lds(sh, rp.L, TB, stride);
-    if (lds_bn <= 150 * 1024) {
-      BandNextArgs bn;
-      bn.hist = hist;
-      bn.n = sh.n;
-      bn.nbins = (int32_t)sh.nbins;
-      bn.stride = stride;
-      bn.TB = TB;
-      bn.rule = ra;
-      bn.band = w.band;
-      bn.next = w.next;
-      rc = allow_lds(ngff_band_next_kernel, lds_bn);
-      if (rc) return rc;
-      rc = launch("ngff_band_next", ngff_band_next_kernel, dim3((unsigned)ceil_div(sh.n, TB)),
-                  dim3(1024), lds_bn, s, bn);
-    } else {
-      rc = run_band(hist, sh, rp, w.band, s);
-      if (rc) return rc;
-      rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0,
-                  s, ra, w.next);
-    }
+  const BandKeepPlan bp = plan_band_keep(sh, rp);
+  const int chunk = select_chunk(rp.seg_len);
+  if (rp.gap_rule && bp.ok) {
+    BandKeepArgs bk;
+    bk.hist = hist;
+    bk.n = sh.n;
+    bk.nbins = (int32_t)sh.nbins;
+    bk.TB = bp.TB;
+    bk.RS = bp.RS;
+    bk.rule = ra;
+    bk.band = w.band;
+    bk.adj = w.adj;
+    bk.G = w.G;
+    rc = allow_lds(ngff_band_keep_kernel, bp.lds);
     if (rc) return rc;
-    const size_t lds = (size_t)rp.seg_len * 13 + 16;
-    if (lds <= 96 * 1024) {
-      rc = allow_lds(ngff_select_kernel<true>, lds);
-      if (rc) return rc;
-      rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(1024), lds,
-                  s, ra, (const int32_t*)w.next, w.flags, w.jump, w.rprev, out_scores, out_mask,
-                  keep_rule->out_count);
-    } else {
-      rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(1024), 0, s,
-                  ra, (const int32_t*)w.next, w.flags, w.jump, w.rprev, out_scores, out_mask,
-                  keep_rule->out_count);
-    }
+    rc = launch("ngff_keep", ngff_band_keep_kernel, dim3((unsigned)ceil_div(sh.n, bp.TB)), dim3(1024),
+                bp.lds, s, bk);
+    if (rc) return rc;
+    const size_t lds = select_lds(chunk, true);
+    rc = allow_lds(ngff_select_kernel<true>, lds);
+    if (rc) return rc;
+    rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(1024), lds, s, ra,
+                (const uint32_t*)w.G, (const int32_t*)nullptr, (const int32_t*)w.adj, (int32_t)chunk, out_scores,
+                out_mask,
+                keep_rule->out_count);
+  } else if (rp.gap_rule) {
+    // L_max > 31 or histogram rows too wide for LDS: band and next[] as
+    // kernels of their own
+    rc = run_band(hist, sh, rp, w.band, s);
+    if (rc) return rc;
+    rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0, s, ra,
+                w.next);
+    if (rc) return rc;
+    const size_t lds = select_lds(chunk, false);
+    rc = allow_lds(ngff_select_kernel<false>, lds);
+    if (rc) return rc;
+    rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(1024), lds, s, ra,
+                (const uint32_t*)nullptr, (const int32_t*)w.next, (const int32_t*)nullptr, (int32_t)chunk,
+                out_scores, out_mask,
+                keep_rule->out_count);
   } else {
     rc = run_band(hist, sh, rp, w.band, s);
     if (rc) return rc;

@@ -15,10 +15,13 @@
 //   staged in LDS phase by phase.  The epilogue takes the max over query rows
 //   (registers, then 16-lane shuffles) and writes m_j = scale * max_i S_ij:
 //   the text-by-vision matrix is never stored.
-// qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7).
-// qer_topk: one workgroup ranks the frames by (score desc, frame asc) on
-//   order-preserving 32-bit keys (a 4-pass radix select) and writes the top k
-//   in chronological order (Eq. 8).
+// qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7); the
+//   last workgroup to finish (an arrival counter the score kernel clears)
+//   ranks the frames by (score desc, frame asc) on order-preserving 32-bit
+//   keys (counting ranks, or a 4-pass radix select) and writes the top k in
+//   chronological order (Eq. 8).
+// qer_topk: the same selection as a kernel of its own (SOFTMAX mode, the
+//   fused attention path, cofie_topk).
 // SOFTMAX mode: per-(head, query) row statistics over all visual keys, merged
 //   across workgroups, then a second pass forming the head mean of the
 //   normalised probabilities and its max over query rows.
@@ -109,6 +112,8 @@ struct ScoreLdsArgs {
   int32_t group_rows;  // > 0: query rows form queries of this many rows (a multiple of
                        // 16), each with its own row of m: m[g * m_stride + j]
   int64_t m_stride;
+  int32_t* clear;      // workgroup 0 zeroes clear[0, nclear) (the frame-mean kernel's
+  int32_t nclear;      // arrival counters), may be null
 };
 
 constexpr int kLdsWaves = 8;
@@ -163,6 +168,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   const uint4* Qq = reinterpret_cast<const uint4*>(a.Qp);
   const int t_begin = (int)((int64_t)a.tiles * blockIdx.x / a.nwg);
   const int t_end = (int)((int64_t)a.tiles * (blockIdx.x + 1) / a.nwg);
+  if (blockIdx.x == 0 && a.clear)
+    for (int i = tid; i < a.nclear; i += kLdsThreads) a.clear[i] = 0;
 
   bool qok[NB];
 #pragma unroll
@@ -490,72 +497,19 @@ __device__ int block_exscan(int v, int* total, int* wsum) {
   return before + x - v;
 }
 
-// Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
-// fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
-// Several queries (blockIdx.y): query g reads row g of m, covers its first
-// nf_q[g] frames (all when nf_q is null) and writes row g of the scores and
-// keys; frames past its prefix score -inf.
-__global__ __launch_bounds__(256) void qer_frame_mean_kernel(const float* m, int32_t n_vis,
-                                                             const int32_t* offs, int32_t n_frames,
-                                                             float* out_scores, uint32_t* keys,
-                                                             const int32_t* nf_q) {
-  const int lane = threadIdx.x & 63;
-  const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (f >= n_frames) return;
-  const int64_t g = blockIdx.y;
-  m += g * n_vis;
-  out_scores += g * n_frames;
-  keys += g * n_frames;
-  if (nf_q && f >= nf_q[g]) {
-    if (lane == 0) {
-      out_scores[f] = -INFINITY;
-      keys[f] = order_key(-INFINITY);
-    }
-    return;
-  }
-  int lo = offs[f], hi = offs[f + 1];
-  lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
-  hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
-  // four loads in flight per lane (clamped indices, masked adds)
-  double s = 0.0;
-  for (int j0 = lo + lane; j0 < hi; j0 += 256) {
-    float v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int j = j0 + 64 * u;
-      v[u] = m[j < hi ? j : lo];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) s += (j0 + 64 * u < hi) ? (double)v[u] : 0.0;
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-  if (lane == 0) {
-    const float w = hi > lo ? (float)(s / (double)(hi - lo)) : -INFINITY;
-    out_scores[f] = w;
-    keys[f] = order_key(w);
-  }
-}
-
+// Eq. 8: the k frames of largest score (ties to the lower index), written in
+// chronological order and padded with -1, by the whole workgroup (blockDim a
+// multiple of 64, at least 256).  Up to kTopkCount frames each frame's rank
+// is counted against every key.  Beyond, a radix select on the
+// order-preserving 32-bit keys finds the k-th largest key (8 bits per pass,
+// the digit located by a suffix scan of the 256 digit counts) and how many
+// keys equal to it are taken; a scan over the frames in index order then
+// writes the selected indices, each thread owning a contiguous chunk of
+// frames.
 constexpr int kTopkCount = 128;   // up to this many frames: ranks by counting
 constexpr int kTopkStage = 8192;  // up to this many frames: keys staged in LDS
 
-// Eq. 8: the k frames of largest score (ties to the lower index), written in
-// chronological order and padded with -1.  One workgroup.  Up to kTopkCount
-// frames each frame's rank is counted against every key.  Beyond, a radix
-// select on the order-preserving 32-bit keys finds the k-th largest key (8
-// bits per pass, the digit located by a suffix scan of the 256 digit counts)
-// and how many keys equal to it are taken; a scan over the frames in index
-// order then writes the selected indices, each thread owning a contiguous
-// chunk of frames.
-// Several queries: workgroup g ranks the first nf_q[g] keys of row g (stride
-// n_stride) and writes row g of out_idx; nf_q null = one query of n_stride keys.
-__global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_stride,
-                                                        int32_t k_top, int32_t* out_idx, const int32_t* nf_q) {
-  const int64_t gq = blockIdx.x;
-  keys_g += gq * n_stride;
-  out_idx += gq * k_top;
-  const int32_t n_frames = nf_q ? nf_q[gq] : n_stride;
+__device__ void topk_block(const uint32_t* keys_g, int32_t n_frames, int32_t k_top, int32_t* out_idx) {
   __shared__ __align__(16) uint32_t keys_sh[kTopkStage];
   __shared__ int hist[256];
   __shared__ int wsum[16];
@@ -659,6 +613,71 @@ __global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, 
     }
   }
   for (int i = k + tid; i < k_top; i += nthr) out_idx[i] = -1;
+}
+
+// Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
+// fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
+// Several queries (blockIdx.y): query g reads row g of m, covers its first
+// nf_q[g] frames (all when nf_q is null) and writes row g of the scores and
+// keys; frames past its prefix score -inf.
+// trees != null (1024 threads; one zeroed arrival tree of tree_ints ints per
+// query): the last workgroup of query g to finish also selects its top k
+// (Eq. 8) into row g of out_idx, so the selection needs no launch of its own.
+__global__ __launch_bounds__(1024) void qer_frame_mean_kernel(const float* m, int32_t n_vis,
+                                                              const int32_t* offs, int32_t n_frames,
+                                                              float* out_scores, uint32_t* keys,
+                                                              const int32_t* nf_q, int32_t* trees,
+                                                              int32_t tree_ints, int32_t tree_stride,
+                                                              int32_t k_top, int32_t* out_idx) {
+  const int lane = threadIdx.x & 63;
+  const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t g = blockIdx.y;
+  const int32_t nf = nf_q ? nf_q[g] : n_frames;
+  m += g * n_vis;
+  out_scores += g * n_frames;
+  keys += g * n_frames;
+  if (f < n_frames && f >= nf) {
+    if (lane == 0) {
+      out_scores[f] = -INFINITY;
+      st_agent(keys + f, order_key(-INFINITY));
+    }
+  } else if (f < n_frames) {
+    int lo = offs[f], hi = offs[f + 1];
+    lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
+    hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
+    // four loads in flight per lane (clamped indices, masked adds)
+    double s = 0.0;
+    for (int j0 = lo + lane; j0 < hi; j0 += 256) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + 64 * u;
+        v[u] = m[j < hi ? j : lo];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s += (j0 + 64 * u < hi) ? (double)v[u] : 0.0;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) {
+      const float w = hi > lo ? (float)(s / (double)(hi - lo)) : -INFINITY;
+      out_scores[f] = w;
+      st_agent(keys + f, order_key(w));
+    }
+  }
+  if (trees) {
+    __shared__ int32_t last_sh;
+    if (arrive_last(trees + g * tree_ints, tree_stride, (int32_t)blockIdx.x, (int32_t)gridDim.x, &last_sh))
+      topk_block(keys, nf, k_top, out_idx + g * k_top);
+  }
+}
+
+// Several queries: workgroup g ranks the first nf_q[g] keys of row g (stride
+// n_stride) and writes row g of out_idx; nf_q null = one query of n_stride keys.
+__global__ __launch_bounds__(1024) void qer_topk_kernel(const uint32_t* keys_g, int32_t n_stride,
+                                                        int32_t k_top, int32_t* out_idx, const int32_t* nf_q) {
+  const int64_t gq = blockIdx.x;
+  topk_block(keys_g + gq * n_stride, nf_q ? nf_q[gq] : n_stride, k_top, out_idx + gq * k_top);
 }
 
 // ---- top-k of given scores; evidence preservation ----------------------------------
@@ -880,7 +899,20 @@ struct QerScratch {
   float2* partial;
   float2* stats;
   int32_t* nf;     // [n_queries] frames per query (several queries only)
+  int32_t* done;   // [n_queries][tree_ints] arrival trees of the frame-mean kernel
 };
+
+// Arrival trees of the frame-mean kernel (16 frames per workgroup).
+struct QerTrees {
+  int32_t nwg, ints, stride;
+};
+inline QerTrees qer_trees(int32_t n_frames) {
+  QerTrees t;
+  t.nwg = (n_frames + 15) / 16;
+  t.stride = arrive_fan(t.nwg) > 0 ? 16 : 1;
+  t.ints = (arrive_fan(t.nwg) + 1) * t.stride;
+  return t;
+}
 
 QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32_t n_queries = 1) {
   QerScratch w;
@@ -888,6 +920,7 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   w.keys = ar.take<uint32_t>((size_t)n_queries * (h.n_frames > 0 ? h.n_frames : 1));
   w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * n_queries * h.n_q * p.Lc * p.esize) : nullptr;
   w.nf = n_queries > 1 ? ar.take<int32_t>((size_t)n_queries) : nullptr;
+  w.done = ar.take<int32_t>((size_t)n_queries * qer_trees(h.n_frames).ints);
   if (h.score_mode == COFIE_SCORE_SOFTMAX) {
     w.partial = ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
     w.stats = ar.take<float2>((size_t)h.H_q * h.n_q);
@@ -1023,6 +1056,9 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
     return set_error(COFIE_EHIP, "copying the per-query frame counts failed");
   const bool bf16 = h.dtype == COFIE_BF16;
   const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
+  // the top-k runs in the frame-mean kernel's last workgroup when the score
+  // kernel (launched first) clears its arrival counters
+  const bool fused_tail = h.score_mode == COFIE_SCORE_LOGIT && h.n_vis > 0 && h.n_frames > 0 && k_top > 0;
 
   if (h.n_vis > 0) {
     if (h.score_mode == COFIE_SCORE_LOGIT) {
@@ -1049,8 +1085,10 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
+      sa.nclear = n_queries * qer_trees(h.n_frames).ints;
       const int cus = device_cu_count();
       for (int q0 = 0; q0 < R; q0 += 64) {
+        sa.clear = (q0 == 0 && fused_tail) ? w.done : nullptr;
         sa.q0 = q0;
         sa.n_q = std::min(64, R - q0);
         sa.accumulate = q0 > 0;
@@ -1101,10 +1139,16 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       }
     }
   }
+  if (fused_tail) {
+    const QerTrees tr = qer_trees(h.n_frames);
+    return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, n_queries), dim3(1024), 0, s,
+                  (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores, w.keys, (const int32_t*)w.nf,
+                  w.done, tr.ints, tr.stride, k_top, out_idx);
+  }
   if (h.n_frames > 0) {
     rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4), n_queries),
                 dim3(256), 0, s, (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores,
-                w.keys, (const int32_t*)w.nf);
+                w.keys, (const int32_t*)w.nf, (int32_t*)nullptr, 0, 0, k_top, out_idx);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
@@ -1120,7 +1164,8 @@ int qer_rank_from_m(const float* m, int32_t n_vis, const int32_t* offs, int32_t 
                     float* out_scores, uint32_t* keys, int32_t* out_idx, hipStream_t s) {
   if (n_frames > 0) {
     int rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(n_frames, 4), 1), dim3(256),
-                    0, s, m, n_vis, offs, n_frames, out_scores, keys, (const int32_t*)nullptr);
+                    0, s, m, n_vis, offs, n_frames, out_scores, keys, (const int32_t*)nullptr, (int32_t*)nullptr,
+                    0, 0, k_top, out_idx);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;

@@ -184,6 +184,49 @@ def test_filter_long_segment_global_scratch_path():
                         oracle_filter(f, 8, "per_channel", np.float32(0.4), L_max=5))
 
 
+@pytest.mark.parametrize("n,seg_len,L_max,mode,bins", [
+    (2100, 1, 30, "per_channel", 16),   # several one-frame streams per workgroup
+    (2100, 3, 9, "per_channel", 16),    # streams straddling workgroups
+    (2100, 7, 30, "gray", 32),
+    (9000, 0, 31, "per_channel", 8),    # three selection chunks, the widest keep word
+    (3000, 0, 45, "per_channel", 8),    # L_max > 31: separate kernels
+    (600, 0, 33, "per_channel", 16),
+    (300, 0, 16, "joint3d", 4),
+    (300, 0, 30, "joint3d", 16),        # 4096 bins: rows too wide to stage, separate kernels
+])
+def test_filter_band_keep_geometry(n, seg_len, L_max, mode, bins):
+    """The band/keep-word kernel and the selection across their launch shapes:
+    several frames and several streams per workgroup, selection chunks, and
+    the separate-kernel path for L_max > 31 or histograms too wide for LDS."""
+    f = synth.random_frames(26, n, 6, 10, scenes=n // 9)
+    print(f"filter n={n} seg_len={seg_len} L_max={L_max} {mode} {bins}", flush=True)
+    assert_filter_equal(run_filter(f, bins, mode, 0.25, L_max=L_max, M_min=4, seg_len=seg_len),
+                        oracle_filter(f, bins, mode, np.float32(0.25), L_max=L_max, M_min=4,
+                                      seg_len=seg_len))
+
+
+def test_filter_poisoned_workspace():
+    """Tables in a reused workspace start from whatever the previous call (or
+    nothing) left there: fill it with 0xFF, then call twice."""
+    f = synth.random_frames(27, 700, 6, 10, scenes=60)
+    fd = to_dev(f)
+    nb = B.cofie_ngff_nbins("per_channel", 16)
+    for seg_len in (0, 100):
+        rule = B.keep_rule("per_channel", 0.3, 30, 4, seg_len)
+        ws = torch.full((B.ngff_workspace_bytes(700, 6, 10, 3, 16, rule),), 255, dtype=torch.uint8,
+                        device="cuda")
+        nseg = 1 if seg_len == 0 else 7
+        o = oracle_filter(f, 16, "per_channel", np.float32(0.3), seg_len=seg_len)
+        for _ in range(2):
+            hist = torch.empty((700, nb), dtype=torch.int32, device="cuda")
+            count = torch.empty(nseg, dtype=torch.int32, device="cuda")
+            r = B.keep_rule("per_channel", 0.3, 30, 4, seg_len, out_hist=hist, out_count=count,
+                            workspace=ws)
+            s, m = B.cofie_ngff_filter(fd, 16, r)
+            torch.cuda.synchronize()
+            assert_filter_equal((s.cpu().numpy(), m.cpu().numpy(), hist_np(hist), count.cpu().numpy()), o)
+
+
 def test_filter_deterministic_and_workspace():
     f = synth.frames(2, 0, 0, 64)
     fd = to_dev(f)

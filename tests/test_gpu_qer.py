@@ -131,6 +131,21 @@ def test_deterministic_and_workspace():
     assert torch.equal(w1, w2) and torch.equal(i1, i2)
 
 
+def test_poisoned_workspace():
+    """The frame-mean kernel's arrival counters live in the workspace: fill it
+    with 0xFF, then rank twice with it (single query and several queries)."""
+    Q, K, offs = synth.qer_inputs(1)
+    wl = synth.WORKLOADS[1]
+    Qd, Kd, od = qk_dev(Q), qk_dev(K), to_dev(offs)
+    w1, i1 = B.cofie_qer_rank(Qd, Kd, od, wl.k_top)
+    desc = B.qer_desc(wl.n_q, K.shape[0], len(offs) - 1, wl.H_q, wl.H_kv, wl.d, dtype=B.F32)
+    ws = torch.full((B.qer_workspace_bytes(desc, wl.k_top),), 255, dtype=torch.uint8, device="cuda")
+    for _ in range(2):
+        w2, i2 = B.cofie_qer_rank(Qd, Kd, od, wl.k_top, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(w1, w2) and torch.equal(i1, i2)
+
+
 def test_many_tokens_per_workgroup():
     """More 16-token tiles than one pass of a workgroup's waves covers (the
     score kernel loops over rounds of tiles, refilling the query phases), with
