@@ -114,6 +114,7 @@ struct ScoreLdsArgs {
   int64_t m_stride;
   int32_t* clear;      // workgroup 0 zeroes clear[0, nclear) (the frame-mean kernel's
   int32_t nclear;      // arrival counters), may be null
+  int32_t lgS;         // log2 S
 };
 
 constexpr int kLdsWaves = 8;
@@ -162,6 +163,24 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int qs_lane = r16 / R;  // load index holding this lane's own row
+  // Query fragments in LDS: [step][term][block][lane] (16 bytes per lane, a
+  // phase of S steps), lane = 16 g + (r ^ swz(step, g)) for the row r and
+  // lane group g of the fragment.  The swizzle (step mod the batch length U,
+  // a power of two <= 8, and g give 16 values) spreads the 64 stores of a
+  // contiguous query-row load over the banks; readers undo it.  Phase column
+  // c (a 16-byte chunk of a query row) belongs to virtual step
+  // VPS (c / SEGC) + c % VPS and lane group (c % SEGC) / VPS, the order in
+  // which the key segments are read (phases hold whole segments); the tail
+  // steps past the whole segments use the same order.
+  constexpr int LOGU = U >= 8 ? 3 : (U >= 4 ? 2 : 1);
+  auto swz = [](int ls, int g) __attribute__((always_inline)) { return ((ls & (U - 1)) | (g << LOGU)) & 15; };
+  auto q_slot = [&](int c, int f, int r) __attribute__((always_inline)) {
+    const int ls = VPS * (c / SEGC) + c % VPS, g = (c % SEGC) / VPS;
+    return ((ls * FPS + f) << 6) + (g << 4) + (r ^ swz(ls, g));
+  };
+  int lsw[U];  // this lane's swizzled slot for steps congruent to u mod U
+#pragma unroll
+  for (int u = 0; u < U; ++u) lsw[u] = lane ^ swz(u, g4);
   const int pfull = VPS * a.nseg;
   const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
   const uint4* Kq = reinterpret_cast<const uint4*>(a.K);
@@ -175,35 +194,41 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) qok[nb] = nb * 16 + r16 < a.n_q;
 
-  // fragments of phase ph: element e = tid + kLdsThreads * i of the buffer;
-  // rows past n_q, columns past Lc and steps past the phase are zero.  Loads
-  // are unconditional (clamped addresses); the zeroing is a select made when
-  // the registers are stored, so that issuing the loads never waits for them.
+  // fragments of phase ph.  The phase covers the 16-byte columns
+  // [4 S ph, 4 S ph + 4 S) of every query row (its S virtual steps, 4 lane
+  // groups each), so element e = tid + kLdsThreads * i is taken in row-major
+  // order: row e / 4S, column 4 S ph + e % 4S, and a wave's load is one
+  // contiguous run of a row (1 KiB for 4S = 64) instead of 16 rows x 64 bytes
+  // in operand shape.  The store puts it at its operand slot (q_slot).  Rows
+  // past n_q and columns past Lc are zero.  Loads are unconditional (clamped
+  // addresses); the zeroing is a select made when the registers are stored,
+  // so that issuing the loads never waits for them.
   uint32_t qmask = 0;
+  const int lgC = a.lgS + 2;  // log2 of the 16-byte columns per row and phase (4 S, S a power of two)
   auto q_load = [&](int ph, uint4 (&qr)[kQRegs]) __attribute__((always_inline)) {
-    const int nstep = min(a.S, a.ksteps - ph * a.S);
     qmask = 0;
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
       const int e = tid + kLdsThreads * i;
-      const int frag = e >> 6, ln = e & 63;
-      const int ls = frag / FPS, rem = frag - ls * FPS;
-      const int p = rem / NB, nb = rem - p * NB;
-      const int q = nb * 16 + (ln & 15);
-      const int v = ph * a.S + ls, g = ln >> 4;
-      const int col = v < pfull ? SEGC * (v / VPS) + VPS * g + v % VPS : 4 * v + g;
-      const bool ok = ls < nstep && q < a.n_q && col * M::EPL < a.Lc;
-      const int64_t row = (int64_t)p * a.nq_total + a.q0 + (ok ? q : 0);
-      qr[i] = Qq[row * row_u4 + (ok ? col : 0)];
+      const int row = e >> lgC, f = row >> 4;
+      const int p = f / NB, nb = f - p * NB;
+      const int q = nb * 16 + (row & 15);
+      const int col = (ph << lgC) + (e & ((1 << lgC) - 1));
+      const bool ok = f < FPS && q < a.n_q && col * M::EPL < a.Lc;
+      const int64_t grow = (int64_t)p * a.nq_total + a.q0 + (ok ? q : 0);
+      qr[i] = Qq[grow * row_u4 + (ok ? col : 0)];
       qmask |= ok ? 1u << i : 0u;
     }
   };
   auto q_store = [&](int ph, const uint4 (&qr)[kQRegs]) __attribute__((always_inline)) {
-    uint4* dst = qs + (ph & 1) * kPhaseU4 + tid;
+    uint4* dst = qs + (ph & 1) * kPhaseU4;
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
+      const int e = tid + kLdsThreads * i;
+      const int row = e >> lgC, f = row >> 4;
       const bool ok = (qmask >> i) & 1u;
-      dst[kLdsThreads * i] = uint4{ok ? qr[i].x : 0u, ok ? qr[i].y : 0u, ok ? qr[i].z : 0u, ok ? qr[i].w : 0u};
+      dst[f < FPS ? q_slot(e & ((1 << lgC) - 1), f, row & 15) : e] =
+          uint4{ok ? qr[i].x : 0u, ok ? qr[i].y : 0u, ok ? qr[i].z : 0u, ok ? qr[i].w : 0u};
     }
   };
   auto barrier_lds = []() __attribute__((always_inline)) {
@@ -270,7 +295,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
         q_store(ph + 1, qr);
         pending = false;
       }
-      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (ms - ph * a.S) * FPS * 64 + lane;
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (ms - ph * a.S) * FPS * 64;  // ms - ph S is a multiple of U
 #pragma unroll
       for (int h = 0; h < U / VPS; ++h) {
         if (!guard || ms + VPS * h < pfull) {
@@ -308,7 +333,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             }
             uint4 qf[FPS];
 #pragma unroll
-            for (int f = 0; f < FPS; ++f) qf[f] = qb[((VPS * h + k) * FPS + f) * 64];
+            for (int f = 0; f < FPS; ++f) qf[f] = qb[((VPS * h + k) * FPS + f) * 64 + lsw[VPS * h + k]];
 #pragma unroll
             for (int p = 0; p < P; ++p)
 #pragma unroll
@@ -353,7 +378,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     for (int v = pfull; v < a.ksteps; ++v) {
       const int col = SEGC * a.nseg + 4 * (v - pfull);  // 16-byte column of lane group 0
       const bool in = (col + g4) * M::EPL < a.Lc;
-      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (v - ph * a.S) * FPS * 64 + lane;
+      const int cph = (col + g4) - (ph << lgC);  // this lane's column within the phase
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + q_slot(cph, 0, r16);
       uint4 kf[MB];
 #pragma unroll
       for (int j = 0; j < MB; ++j) {
@@ -972,7 +998,7 @@ int validate_qer(const void* Q, const void* K, const int32_t* offs, const cofie_
 // tiles per wave per round, 4-row key segments unless the batch is too short
 // to hold one, phases as long as a 64 KiB buffer allows.
 struct LdsPlan {
-  int MB, R, nwg, S, nphase, nseg, ksteps;
+  int MB, R, nwg, S, lgS, nphase, nseg, ksteps;
   size_t lds;
 };
 
@@ -989,7 +1015,13 @@ LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int PNB, int cus
   L.nseg = (int)(Lc / seg_el);
   L.ksteps = (int)((16 / L.R) * L.nseg + ceil_div(Lc % seg_el, kps));
   const int phase_u4 = lds_q_regs(PNB) * kLdsThreads;
-  L.S = (int)std::min<int64_t>((phase_u4 / 64) / PNB / U * U, ceil_div(L.ksteps, U) * U);
+  // S: a power of two (>= U), as large as the phase buffer holds, no larger
+  // than the contraction needs
+  const int64_t cap = (phase_u4 / 64) / PNB;
+  L.S = U;
+  while (2 * L.S <= cap && L.S < L.ksteps) L.S *= 2;
+  L.lgS = 0;
+  while ((1 << L.lgS) < L.S) ++L.lgS;
   L.nphase = (int)ceil_div(L.ksteps, L.S);
   L.lds = (size_t)(L.nphase > 1 ? 2 : 1) * phase_u4 * sizeof(uint4);
   return L;
@@ -1097,6 +1129,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         sa.nseg = L.nseg;
         sa.ksteps = L.ksteps;
         sa.S = L.S;
+        sa.lgS = L.lgS;
         sa.nphase = L.nphase;
         sa.nwg = L.nwg;
         if (bf16)
