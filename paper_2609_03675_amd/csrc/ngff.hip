@@ -161,7 +161,12 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
     for (int j = 0; j < kUnroll; ++j) {
       int u = g + (b * kUnroll + j) * G;
       u = u < a.units ? u : a.units - 1;
-      v[j] = *reinterpret_cast<const U3*>(f + (int64_t)u * kUnitBytes + lane * 12);
+      // frames are read once: non-temporal loads (1 fps stream 28.0 -> 26.4 us,
+      // high-res 1031 -> 938 us)
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(f + (int64_t)u * kUnitBytes + lane * 12);
+      v[j].x = __builtin_nontemporal_load(src);
+      v[j].y = __builtin_nontemporal_load(src + 1);
+      v[j].z = __builtin_nontemporal_load(src + 2);
     }
   };
   auto count_batch = [&](const U3 (&v)[kUnroll], int b) __attribute__((always_inline)) {

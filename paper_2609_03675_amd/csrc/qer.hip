@@ -33,6 +33,7 @@ namespace cofie {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 struct bf16_t {
   uint16_t bits;
@@ -272,7 +273,11 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
         for (int q = 0; q < VPS; ++q)
 #pragma unroll
-          for (int j = 0; j < MB; ++j) f[VPS * h + q][j] = kq[j][q][SEGC * seg];
+          for (int j = 0; j < MB; ++j) {
+            // keys are read once: non-temporal loads (1 fps stream 46.0 -> 43.4 us)
+            const u32x4v t = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(kq[j][q] + SEGC * seg));
+            f[VPS * h + q][j] = uint4{t.x, t.y, t.z, t.w};
+          }
       }
     };
 
