@@ -242,45 +242,79 @@ struct BandArgs {
   int32_t TB;      // frames per workgroup
   int32_t stride;  // LDS row stride in words (nbins + 1), 0 = read global memory
   int32_t* band;   // [n][L]: band[t*L + k-1] = D(t, t-k), 0 if t-k precedes the stream
+  // when window != null, the first wrows rows of every stream are read from
+  // window[stream][row] ([n / seg_len][wrows][nbins]) instead of hist
+  const uint32_t* window;
+  int32_t wrows;
 };
+
+__device__ __forceinline__ const uint32_t* band_row(const BandArgs& a, int64_t r) {
+  if (a.window) {
+    const int64_t sg = r / a.seg_len, q = r - sg * a.seg_len;
+    if (q < a.wrows) return a.window + (sg * a.wrows + q) * a.nbins;
+  }
+  return a.hist + r * a.nbins;
+}
 
 __global__ __launch_bounds__(256) void ngff_band_kernel(BandArgs a) {
   extern __shared__ uint32_t rows[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
   const int64_t t0 = (int64_t)blockIdx.x * a.TB;
   const int64_t r0 = t0 - a.L > 0 ? t0 - a.L : 0;
   const int64_t r1 = t0 + a.TB < a.n ? t0 + a.TB : a.n;
   if (a.stride) {
-    const int64_t nrows = r1 - r0;
-    for (int64_t i = threadIdx.x; i < nrows * a.nbins; i += blockDim.x) {
-      const int64_t r = i / a.nbins, b = i - r * a.nbins;
-      rows[r * a.stride + b] = a.hist[(r0 + r) * a.nbins + b];
+    // all loads of a batch are issued before their stores (clamped indices)
+    const int64_t total = (r1 - r0) * a.nbins;
+    constexpr int V = 8;
+    for (int64_t i0 = tid; i0 < total; i0 += (int64_t)V * nthr) {
+      uint32_t v[V];
+      int64_t idx[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int64_t i = i0 + (int64_t)j * nthr;
+        idx[j] = i < total ? i : 0;
+        const int64_t r = idx[j] / a.nbins;
+        v[j] = band_row(a, r0 + r)[idx[j] - r * a.nbins];
+      }
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int64_t r = idx[j] / a.nbins;
+        rows[r * a.stride + (idx[j] - r * a.nbins)] = v[j];
+      }
     }
     __syncthreads();
   }
-  for (int p = threadIdx.x; p < a.TB * a.L; p += blockDim.x) {
-    const int64_t t = t0 + p / a.L;
-    const int k = p % a.L + 1;
-    if (t >= a.n) continue;
+  // (row, lag) pairs, LPP lanes per pair (a power of two <= 64: a group never
+  // straddles a wave), bins strided over the group, combined with shuffles
+  const int npairs = (int)(r1 - t0) * a.L;
+  int LPP = 1;
+  while (LPP < 64 && 2 * LPP * npairs <= nthr) LPP <<= 1;
+  const int sub = tid & (LPP - 1), groups = nthr / LPP;
+  const int passes = (npairs + groups - 1) / groups;  // whole passes: every lane runs the shuffles
+  for (int ps = 0; ps < passes; ++ps) {
+    const int pi = ps * groups + tid / LPP;
+    const bool ok = pi < npairs;
+    const int64_t t = t0 + (ok ? pi / a.L : 0);
+    const int k = ok ? pi % a.L + 1 : 1;
     const int64_t seg0 = (t / a.seg_len) * a.seg_len;
-    int32_t D = 0;
-    if (t - k >= seg0) {
+    uint32_t D = 0;
+    if (ok && t - k >= seg0) {
       const uint32_t* x;
       const uint32_t* y;
       if (a.stride) {
         x = rows + (t - r0) * a.stride;
         y = rows + (t - k - r0) * a.stride;
       } else {
-        x = a.hist + t * a.nbins;
-        y = a.hist + (t - k) * a.nbins;
+        x = band_row(a, t);
+        y = band_row(a, t - k);
       }
-      uint32_t acc = 0;
-      for (int b = 0; b < a.nbins; ++b) {
+      for (int b = sub; b < a.nbins; b += LPP) {
         const uint32_t u = x[b], v = y[b];
-        acc += u > v ? u - v : v - u;
+        D += u > v ? u - v : v - u;
       }
-      D = (int32_t)acc;
     }
-    a.band[t * a.L + (k - 1)] = D;
+    for (int o = 1; o < LPP; o <<= 1) D += __shfl_xor(D, o, LPP);
+    if (ok && sub == 0) a.band[t * a.L + (k - 1)] = (int32_t)D;
   }
 }
 
@@ -911,6 +945,7 @@ int launch_hist_kind(const HistArgs& args, const HistPlan& p, int64_t n, hipStre
 struct HistMap {  // see HistArgs: group = 0 is the identity
   int64_t group = 0, in_stride = 0, in_off = 0, out_stride = 0, out_off = 0;
   int64_t out_rows = 0;  // rows of the output buffer (for the zero fill), 0 = n
+  bool zeroed = false;   // the output rows are known zero: no fill before accumulating
 };
 
 int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hipStream_t s,
@@ -934,7 +969,7 @@ int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hi
   a.splits = p.splits;
   a.units = p.units;
   a.atomic = p.splits > 1;
-  if (a.atomic) {
+  if (a.atomic && !map.zeroed) {
     const int64_t cnt = (map.out_rows ? map.out_rows : sh.n) * sh.nbins;
     int rc = launch("ngff_fill", fill_u32_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(cnt, 256), 4096)),
                     dim3(256), 0, s, hist, 0u, cnt);
@@ -1027,8 +1062,10 @@ NgffScratch carve(Arena& ar, const NgffShape& sh, const RulePlan& rp, bool need_
 
 // Separate band kernel (rows read from global memory when they do not fit LDS).
 int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int32_t* band,
-             hipStream_t s) {
+             hipStream_t s, const uint32_t* window = nullptr, int32_t wrows = 0) {
   BandArgs b;
+  b.window = window;
+  b.wrows = wrows;
   b.hist = hist;
   b.n = sh.n;
   b.nbins = (int32_t)sh.nbins;
@@ -1036,7 +1073,10 @@ int run_band(const uint32_t* hist, const NgffShape& sh, const RulePlan& rp, int3
   b.seg_len = rp.seg_len;
   const size_t budget = 64 * 1024;
   const size_t row = (size_t)(sh.nbins + 1) * 4;
-  int TB = 64;
+  // about one workgroup per CU (a 94-row push band took 45 us with 64 frames
+  // per workgroup, i.e. two workgroups), at most 64 frames each
+  const int64_t cus = device_cu_count();
+  int TB = (int)std::min<int64_t>(64, std::max<int64_t>(1, (sh.n + cus - 1) / cus));
   while (TB > 1 && (size_t)(TB + rp.L) * row > budget) TB >>= 1;
   size_t lds = (size_t)(TB + rp.L) * row;
   b.TB = TB;
@@ -1096,6 +1136,10 @@ struct PushArgs {
   float* out_scores;     // row s at out_scores + s * ld
   uint8_t* out_mask;
   int64_t ld;
+  uint32_t* comb;        // [S][L + nb][nbins]: rows L.. hold the new frames' histograms
+                         // (zeroed here once read, for the next push's accumulation)
+  uint32_t* window;      // [S][L][nbins]: histograms of the L frames before t0, updated here
+  int64_t nbins;
 };
 
 __global__ __launch_bounds__(1024) void ngff_push_kernel(PushArgs a) {
@@ -1183,21 +1227,36 @@ __global__ __launch_bounds__(1024) void ngff_push_kernel(PushArgs a) {
     a.out_scores[s * a.ld + j] = score;
     a.out_mask[s * a.ld + j] = (uint8_t)keep_sh[j];
   }
+  // the window becomes the last L frames: row q <- row nb + q of (old window,
+  // new frames).  When nb < L this shifts the window down in place, so it is
+  // copied in chunks, each read completely before any of it is written (later
+  // chunks only read above what earlier chunks wrote).
+  uint32_t* win = a.window + (int64_t)s * L * a.nbins;
+  uint32_t* cs = a.comb + (int64_t)s * (L + nb) * a.nbins;
+  const int64_t total = (int64_t)L * a.nbins;
+  constexpr int V = 4;
+  for (int64_t c0 = 0; c0 < total; c0 += (int64_t)V * nthr) {
+    uint32_t v[V];
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+      const int64_t i = c0 + u * nthr + tid;
+      const int64_t q = i / a.nbins;  // window row
+      v[u] = i >= total ? 0u : (nb + q < L ? win[i + (int64_t)nb * a.nbins] : cs[i + (int64_t)nb * a.nbins]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+      const int64_t i = c0 + u * nthr + tid;
+      if (i < total) win[i] = v[u];
+    }
+    __syncthreads();
+  }
+  // the new frames' rows start the next push at zero (its histogram adds into
+  // them when several workgroups share a frame), so that push needs no fill
+  for (int64_t i = tid; i < (int64_t)nb * a.nbins; i += nthr) cs[(int64_t)L * a.nbins + i] = 0u;
 }
 
 // comb[s][0..L) <- window[s] (dir 0) or window[s] <- comb[s][nb..nb+L) (dir 1)
-__global__ void ngff_window_kernel(uint32_t* comb, uint32_t* window, int32_t S, int32_t L, int32_t nb,
-                                   int64_t nbins, int32_t dir) {
-  const int64_t per = (int64_t)L * nbins, total = per * S;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t s = i / per, w = i - s * per;
-    uint32_t* c = comb + s * (L + nb) * nbins;
-    if (dir == 0)
-      c[w] = window[i];
-    else
-      window[i] = c[(int64_t)nb * nbins + w];
-  }
-}
 
 // End of the streams: frame T-1 kept, then the M_min top-up (one thread per
 // stream); out_added row s receives the frames this adds, increasing and -1
@@ -1260,6 +1319,9 @@ struct cofie_ngff_stream {
   int32_t* kept = nullptr;     // [S] kept frames so far
   int64_t t0 = 0;              // frames pushed per stream
   bool finished = false;
+  void* scratch = nullptr;     // push scratch (new frames' histograms, band), kept between pushes
+  size_t scratch_bytes = 0;
+  int32_t zero_nb = -1;        // the push size whose new-frame rows in scratch are known zero
 };
 
 namespace cofie {
@@ -1518,6 +1580,7 @@ int cofie_ngff_stream_destroy(cofie_ngff_stream* st) {
   if (st->r) hipFree(st->r);
   if (st->kept) hipFree(st->kept);
   if (st->tau_dev) hipFree(st->tau_dev);
+  if (st->scratch) hipFree(st->scratch);
   if (dev != st->device) hipSetDevice(dev);
   delete st;
   return COFIE_OK;
@@ -1623,11 +1686,18 @@ int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t
     Arena plan;
     plan.take<uint32_t>((size_t)rows * st->sh.nbins);
     plan.take<int32_t>((size_t)rows * L);
-    Scratch scratch;
-    int rc = scratch.acquire(nullptr, 0, plan.bytes(), s);
-    if (rc) return rc;
+    if (plan.bytes() > st->scratch_bytes) {
+      // grown once for the largest push; hipFree waits for the pushes that used it
+      if (st->scratch) hipFree(st->scratch);
+      st->scratch = nullptr;
+      st->scratch_bytes = 0;
+      if (hipMalloc(&st->scratch, plan.bytes()) != hipSuccess)
+        return set_error(COFIE_ENOMEM, "allocating %zu bytes of push scratch failed", plan.bytes());
+      st->scratch_bytes = plan.bytes();
+      st->zero_nb = -1;
+    }
     Arena ar;
-    ar.base = scratch.ptr();
+    ar.base = static_cast<char*>(st->scratch);
     uint32_t* comb = ar.take<uint32_t>((size_t)rows * st->sh.nbins);
     int32_t* band = ar.take<int32_t>((size_t)rows * L);
     NgffShape sh = st->sh;
@@ -1639,13 +1709,11 @@ int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t
     map.out_stride = L + nb;
     map.out_off = L;
     map.out_rows = rows;
-    rc = run_histogram(frames, sh, comb, s, map);
+    map.zeroed = st->zero_nb == nb;  // the previous push of this size left the rows at zero
+    st->zero_nb = -1;                // until this push's kernel has zeroed them again
+    int rc = run_histogram(frames, sh, comb, s, map);
     if (rc) return rc;
-    const int64_t wwords = (int64_t)S * L * st->sh.nbins;
-    const unsigned wgrid = (unsigned)std::min<int64_t>(ceil_div(wwords, 256), 4096);
-    rc = launch("ngff_window", ngff_window_kernel, dim3(wgrid), dim3(256), 0, s, comb, st->window, S, L, nb,
-                st->sh.nbins, 0);
-    if (rc) return rc;
+    // the band reads each stream's first L rows (the frames before t0) from the window
     NgffShape bsh = st->sh;
     bsh.n = rows;
     RulePlan rp;
@@ -1653,7 +1721,7 @@ int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t
     rp.nseg = S;
     rp.gap_rule = true;
     rp.L = L;
-    rc = run_band(comb, bsh, rp, band, s);
+    rc = run_band(comb, bsh, rp, band, s, st->window, L);
     if (rc) return rc;
     PushArgs pa;
     pa.band = band;
@@ -1668,14 +1736,15 @@ int cofie_ngff_stream_push(cofie_ngff_stream* st, const uint8_t* frames, int64_t
     pa.out_scores = out_scores + j0;
     pa.out_mask = out_mask + j0;
     pa.ld = ld;
+    pa.comb = comb;
+    pa.window = st->window;
+    pa.nbins = st->sh.nbins;
     const size_t lds = ((size_t)nb * L + 3 * (size_t)nb + 1) * sizeof(int32_t);
     rc = allow_lds(ngff_push_kernel, lds);
     if (rc) return rc;
     rc = launch("ngff_push", ngff_push_kernel, dim3(S), dim3(1024), lds, s, pa);
     if (rc) return rc;
-    rc = launch("ngff_window", ngff_window_kernel, dim3(wgrid), dim3(256), 0, s, comb, st->window, S, L, nb,
-                st->sh.nbins, 1);
-    if (rc) return rc;
+    st->zero_nb = nb;
     st->t0 += nb;
   }
   return COFIE_OK;

@@ -110,6 +110,15 @@ def test_push_matches_one_shot_filter_on_workload():
     assert np.array_equal(sc.reshape(-1).view(np.uint32), sc1.cpu().numpy().view(np.uint32))
 
 
+def test_push_shared_frames_repeated_and_changed_sizes():
+    """Large frames pushed a few at a time, so several workgroups share each
+    frame's histogram (accumulated into rows that must start at zero): pushes
+    of a repeated size reuse the rows the previous push zeroed, a new size
+    clears them first."""
+    frames = synth.frames(2, 0, 0, 96)[None]
+    run_stream(frames, 32, "per_channel", 0.2, 30, 4, [8, 8, 8, 16, 16, 8, 32])
+
+
 def test_push_large_batch_is_split():
     """A push larger than one internal sub-push (the band rows of at most
     12288 / L_max frames per stream fit the push kernel's LDS)."""
