@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--rotate", type=int, default=3, help="input copies cycled through")
     ap.add_argument("--mode", choices=["graph", "eager"], default="eager",
                     help="call the library eagerly, or replay the step as a captured HIP graph")
+    ap.add_argument("--overlap", choices=["on", "off"], default="off",
+                    help="on: NGFF's keep rule (after its histograms) runs on the main stream while QER runs "
+                         "on a second stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="target wall time of the CPU oracle sample")
@@ -113,11 +116,27 @@ def main():
     w_out = torch.empty(n_frames, dtype=torch.float32, device="cuda")
     idx_out = torch.empty(wl.k_top, dtype=torch.int32, device="cuda")
 
+    hist_buf = torch.empty((n, B.cofie_ngff_nbins(wl.hist_mode, wl.bins)), dtype=torch.int32, device="cuda")
+    qer_stream = torch.cuda.Stream()
+    hist_done = torch.cuda.Event()
+
     def step(i):
         r = i % args.rotate
-        B.cofie_ngff_filter(frames[r], wl.bins, rule, out_scores=scores, out_mask=mask)
-        B.cofie_qer_rank(Qd, Kd[r], offs, wl.k_top, out_scores=w_out, out_idx=idx_out,
-                         workspace=qer_ws)
+        if args.overlap == "off":
+            B.cofie_ngff_filter(frames[r], wl.bins, rule, out_scores=scores, out_mask=mask)
+            B.cofie_qer_rank(Qd, Kd[r], offs, wl.k_top, out_scores=w_out, out_idx=idx_out,
+                             workspace=qer_ws)
+            return
+        # the histograms, then QER on its own stream beside NGFF's keep rule
+        main = torch.cuda.current_stream()
+        B.cofie_ngff_histogram(frames[r], wl.bins, wl.hist_mode, out=hist_buf)
+        hist_done.record(main)
+        qer_stream.wait_event(hist_done)
+        with torch.cuda.stream(qer_stream):
+            B.cofie_qer_rank(Qd, Kd[r], offs, wl.k_top, out_scores=w_out, out_idx=idx_out,
+                             workspace=qer_ws)
+        B.cofie_ngff_filter_hist(hist_buf, H, W, C, wl.bins, rule, out_scores=scores, out_mask=mask)
+        main.wait_stream(qer_stream)
 
     for i in range(max(args.warmup, args.rotate)):
         step(i)
@@ -256,7 +275,7 @@ def main():
                    "qer": {"n_q": wl.n_q, "H_q": wl.H_q, "H_kv": wl.H_kv, "d": wl.d,
                            "candidates": n_frames, "tokens_per_frame": wl.tokens,
                            "k_top": wl.k_top, "dtype": "bf16", "score_mode": "logit"},
-                   "step": args.mode, "rotated_copies": args.rotate},
+                   "step": args.mode, "overlap": args.overlap, "rotated_copies": args.rotate},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages": {

@@ -136,6 +136,19 @@ int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, in
                       int32_t bins, const cofie_keep_rule* keep_rule, float* out_scores,
                       uint8_t* out_mask, void* stream);
 
+/* NGFF's keep rule on histograms computed earlier (for example by
+ * cofie_ngff_histogram on another stream, so that independent work can run
+ * beside the rule): everything cofie_ngff_filter does after its histogram
+ * (Sec. 3.2, Eqs. 2-5 and safeguards), with the same scores and mask.
+ *   hist      device uint32 [n][nbins] counts as cofie_ngff_histogram writes
+ *             them for frames of shape H x W x C and `bins` (they fix M and
+ *             nbins); read only
+ * Other arguments, outputs and errors as cofie_ngff_filter;
+ * keep_rule->out_hist is ignored. */
+int cofie_ngff_filter_hist(const uint32_t* hist, int64_t n, int32_t H, int32_t W, int32_t C, int32_t bins,
+                           const cofie_keep_rule* keep_rule, float* out_scores, uint8_t* out_mask,
+                           void* stream);
+
 /* Threshold calibration for a retention target (the paper fixes tau_h; a
  * target kept count per stream is an extension).  Per stream, among the
  * candidate integer thresholds theta in {0, 2M+1} and every distance

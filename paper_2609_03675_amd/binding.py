@@ -107,6 +107,7 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_workspace_bytes": (sz, [i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule)]),
         "cofie_ngff_histogram": (ctypes.c_int, [P, i64, i32, i32, i32, i32, i32, P, P]),
         "cofie_ngff_filter": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), P, P, P]),
+        "cofie_ngff_filter_hist": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), P, P, P]),
         "cofie_ngff_calibrate": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), i64, P, P]),
         "cofie_qer_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32]),
         "cofie_qer_rank": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
@@ -240,6 +241,22 @@ def cofie_ngff_filter(frames, bins: int, rule: KeepRule, out_scores=None, out_ma
     _check(lib().cofie_ngff_filter(_dev(frames, "frames"), n, H, W, C, bins, ctypes.byref(rule),
                                    _dev(out_scores, "out_scores"), _dev(out_mask, "out_mask"),
                                    _stream(stream)))
+    return out_scores, out_mask
+
+
+def cofie_ngff_filter_hist(hist, H: int, W: int, C: int, bins: int, rule: KeepRule, out_scores=None,
+                           out_mask=None, stream=None):
+    """The keep rule of cofie_ngff_filter on histograms computed earlier
+    (int32/uint32 [n][nbins] counts of H x W x C frames): scores and mask."""
+    import torch
+    n = hist.shape[0]
+    if out_scores is None:
+        out_scores = torch.empty(n, dtype=torch.float32, device=hist.device)
+    if out_mask is None:
+        out_mask = torch.empty(n, dtype=torch.uint8, device=hist.device)
+    _check(lib().cofie_ngff_filter_hist(_dev(hist, "hist"), n, H, W, C, bins, ctypes.byref(rule),
+                                        _dev(out_scores, "out_scores"), _dev(out_mask, "out_mask"),
+                                        _stream(stream)))
     return out_scores, out_mask
 
 

@@ -1302,6 +1302,85 @@ __global__ void ngff_finish_kernel(uint8_t* mask_all, int64_t ld, int32_t S, int
   if (out_count) out_count[s] = (int32_t)kept;
 }
 
+// Workgroup sizes of the keep-rule kernels: small enough (4 waves, one per
+// SIMD) to run beside the QER score kernel's workgroups on the same CUs when
+// a caller overlaps the two on separate streams; the selection takes 1024
+// threads only for long streams.
+constexpr int kKeepThreads = 256;
+inline int select_threads(const RulePlan& rp) { return rp.seg_len <= 2048 ? 256 : 1024; }
+
+// cofie_ngff_filter after validation: the histograms of `frames`, or the
+// given ones (hist_in), then the keep rule.
+int filter_impl(const uint8_t* frames, const uint32_t* hist_in, const NgffShape& sh,
+                const cofie_keep_rule* keep_rule, float* out_scores, uint8_t* out_mask, hipStream_t s) {
+  int rc;
+  const RulePlan rp = plan_rule(sh, keep_rule);
+  const bool need_hist = hist_in == nullptr && keep_rule->out_hist == nullptr;
+  Arena plan;
+  carve(plan, sh, rp, need_hist);
+  Scratch scratch;
+  rc = scratch.acquire(keep_rule->workspace, keep_rule->workspace_bytes, plan.bytes(), s);
+  if (rc) return rc;
+  Arena ar;
+  ar.base = scratch.ptr();
+  NgffScratch w = carve(ar, sh, rp, need_hist);
+  const uint32_t* hist = hist_in ? hist_in : (need_hist ? w.hist : keep_rule->out_hist);
+
+  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
+  if (!hist_in) {
+    rc = run_histogram(frames, sh, const_cast<uint32_t*>(hist), s);
+    if (rc) return rc;
+  }
+  const BandKeepPlan bp = plan_band_keep(sh, rp);
+  const int chunk = select_chunk(rp.seg_len);
+  if (rp.gap_rule && bp.ok) {
+    BandKeepArgs bk;
+    bk.hist = hist;
+    bk.n = sh.n;
+    bk.nbins = (int32_t)sh.nbins;
+    bk.TB = bp.TB;
+    bk.RS = bp.RS;
+    bk.rule = ra;
+    bk.band = w.band;
+    bk.adj = w.adj;
+    bk.G = w.G;
+    rc = allow_lds(ngff_band_keep_kernel, bp.lds);
+    if (rc) return rc;
+    rc = launch("ngff_keep", ngff_band_keep_kernel, dim3((unsigned)ceil_div(sh.n, bp.TB)), dim3(kKeepThreads),
+                bp.lds, s, bk);
+    if (rc) return rc;
+    const size_t lds = select_lds(chunk, true);
+    rc = allow_lds(ngff_select_kernel<true>, lds);
+    if (rc) return rc;
+    rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(select_threads(rp)), lds, s, ra,
+                (const uint32_t*)w.G, (const int32_t*)nullptr, (const int32_t*)w.adj, (int32_t)chunk, out_scores,
+                out_mask,
+                keep_rule->out_count);
+  } else if (rp.gap_rule) {
+    // L_max > 31 or histogram rows too wide for LDS: band and next[] as
+    // kernels of their own
+    rc = run_band(hist, sh, rp, w.band, s);
+    if (rc) return rc;
+    rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0, s, ra,
+                w.next);
+    if (rc) return rc;
+    const size_t lds = select_lds(chunk, false);
+    rc = allow_lds(ngff_select_kernel<false>, lds);
+    if (rc) return rc;
+    rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(select_threads(rp)), lds, s, ra,
+                (const uint32_t*)nullptr, (const int32_t*)w.next, (const int32_t*)nullptr, (int32_t)chunk,
+                out_scores, out_mask,
+                keep_rule->out_count);
+  } else {
+    rc = run_band(hist, sh, rp, w.band, s);
+    if (rc) return rc;
+    rc = launch("ngff_select_seq", ngff_select_seq_kernel, dim3((unsigned)rp.nseg), dim3(256), 0, s,
+                ra, (const uint32_t*)hist, (int32_t)sh.nbins, w.flags, out_scores, out_mask,
+                keep_rule->out_count);
+  }
+  return rc;
+}
+
 }  // namespace
 }  // namespace cofie
 
@@ -1419,70 +1498,22 @@ int cofie_ngff_filter(const uint8_t* frames, int64_t n, int32_t H, int32_t W, in
   if (n > 0 && (!out_scores || !out_mask))
     return set_error(COFIE_EINVAL, "out_scores / out_mask is NULL");
   if (n == 0) return COFIE_OK;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const RulePlan rp = plan_rule(sh, keep_rule);
-  const bool need_hist = keep_rule->out_hist == nullptr;
-  Arena plan;
-  carve(plan, sh, rp, need_hist);
-  Scratch scratch;
-  rc = scratch.acquire(keep_rule->workspace, keep_rule->workspace_bytes, plan.bytes(), s);
-  if (rc) return rc;
-  Arena ar;
-  ar.base = scratch.ptr();
-  NgffScratch w = carve(ar, sh, rp, need_hist);
-  uint32_t* hist = need_hist ? w.hist : keep_rule->out_hist;
+  return filter_impl(frames, nullptr, sh, keep_rule, out_scores, out_mask, static_cast<hipStream_t>(stream));
+}
 
-  RuleArgs ra = rule_args(sh, rp, keep_rule, w.band);
-  rc = run_histogram(frames, sh, hist, s);
+int cofie_ngff_filter_hist(const uint32_t* hist, int64_t n, int32_t H, int32_t W, int32_t C, int32_t bins,
+                           const cofie_keep_rule* keep_rule, float* out_scores, uint8_t* out_mask,
+                           void* stream) {
+  clear_error();
+  int rc = validate_rule(keep_rule);
   if (rc) return rc;
-  const BandKeepPlan bp = plan_band_keep(sh, rp);
-  const int chunk = select_chunk(rp.seg_len);
-  if (rp.gap_rule && bp.ok) {
-    BandKeepArgs bk;
-    bk.hist = hist;
-    bk.n = sh.n;
-    bk.nbins = (int32_t)sh.nbins;
-    bk.TB = bp.TB;
-    bk.RS = bp.RS;
-    bk.rule = ra;
-    bk.band = w.band;
-    bk.adj = w.adj;
-    bk.G = w.G;
-    rc = allow_lds(ngff_band_keep_kernel, bp.lds);
-    if (rc) return rc;
-    rc = launch("ngff_keep", ngff_band_keep_kernel, dim3((unsigned)ceil_div(sh.n, bp.TB)), dim3(1024),
-                bp.lds, s, bk);
-    if (rc) return rc;
-    const size_t lds = select_lds(chunk, true);
-    rc = allow_lds(ngff_select_kernel<true>, lds);
-    if (rc) return rc;
-    rc = launch("ngff_select", ngff_select_kernel<true>, dim3((unsigned)rp.nseg), dim3(1024), lds, s, ra,
-                (const uint32_t*)w.G, (const int32_t*)nullptr, (const int32_t*)w.adj, (int32_t)chunk, out_scores,
-                out_mask,
-                keep_rule->out_count);
-  } else if (rp.gap_rule) {
-    // L_max > 31 or histogram rows too wide for LDS: band and next[] as
-    // kernels of their own
-    rc = run_band(hist, sh, rp, w.band, s);
-    if (rc) return rc;
-    rc = launch("ngff_next", ngff_next_kernel, dim3((unsigned)ceil_div(sh.n, 256)), dim3(256), 0, s, ra,
-                w.next);
-    if (rc) return rc;
-    const size_t lds = select_lds(chunk, false);
-    rc = allow_lds(ngff_select_kernel<false>, lds);
-    if (rc) return rc;
-    rc = launch("ngff_select", ngff_select_kernel<false>, dim3((unsigned)rp.nseg), dim3(1024), lds, s, ra,
-                (const uint32_t*)nullptr, (const int32_t*)w.next, (const int32_t*)nullptr, (int32_t)chunk,
-                out_scores, out_mask,
-                keep_rule->out_count);
-  } else {
-    rc = run_band(hist, sh, rp, w.band, s);
-    if (rc) return rc;
-    rc = launch("ngff_select_seq", ngff_select_seq_kernel, dim3((unsigned)rp.nseg), dim3(256), 0, s,
-                ra, (const uint32_t*)hist, (int32_t)sh.nbins, w.flags, out_scores, out_mask,
-                keep_rule->out_count);
-  }
-  return rc;
+  NgffShape sh;
+  rc = validate_frames(reinterpret_cast<const uint8_t*>(hist), n, H, W, C, bins, keep_rule->hist_mode, &sh);
+  if (rc) return rc;
+  if (n > 0 && (!out_scores || !out_mask))
+    return set_error(COFIE_EINVAL, "out_scores / out_mask is NULL");
+  if (n == 0) return COFIE_OK;
+  return filter_impl(nullptr, hist, sh, keep_rule, out_scores, out_mask, static_cast<hipStream_t>(stream));
 }
 
 int cofie_ngff_calibrate(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,

@@ -133,6 +133,13 @@ def test_filter_validation(L):
     assert L.cofie_ngff_filter(None, 0, 8, 8, 3, 32, ctypes.byref(r), None, None, None) == B.COFIE_OK
     r.L_max = 0
     assert L.cofie_ngff_calibrate(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), 2, FAKE, None) == B.COFIE_EUNSUPPORTED
+    # the keep rule on given histograms validates the same way
+    r.L_max = 30
+    assert L.cofie_ngff_filter_hist(FAKE, 4, 8, 8, 3, 32, None, FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_ngff_filter_hist(None, 4, 8, 8, 3, 32, ctypes.byref(r), FAKE, FAKE, None) == B.COFIE_EINVAL
+    assert L.cofie_ngff_filter_hist(FAKE, 4, 8, 8, 3, 32, ctypes.byref(r), FAKE, None, None) == B.COFIE_EINVAL
+    assert L.cofie_ngff_filter_hist(FAKE, 4, 8, 8, 3, 24, ctypes.byref(r), FAKE, FAKE, None) == B.COFIE_EUNSUPPORTED
+    assert L.cofie_ngff_filter_hist(None, 0, 8, 8, 3, 32, ctypes.byref(r), None, None, None) == B.COFIE_OK
 
 
 @pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")

@@ -205,6 +205,29 @@ def test_filter_band_keep_geometry(n, seg_len, L_max, mode, bins):
                                       seg_len=seg_len))
 
 
+@pytest.mark.parametrize("seg_len,L_max", [(0, 30), (100, 9), (0, 45), (0, 0)])
+def test_filter_from_histograms(seg_len, L_max):
+    """cofie_ngff_filter_hist on cofie_ngff_histogram's counts, run on another
+    stream, equals cofie_ngff_filter bit for bit (and the oracle)."""
+    f = synth.random_frames(28, 700, 12, 16, scenes=60)
+    fd = to_dev(f)
+    nseg = 1 if seg_len == 0 else (700 + seg_len - 1) // seg_len
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        h = B.cofie_ngff_histogram(fd, 16, "per_channel")
+        count = torch.empty(nseg, dtype=torch.int32, device="cuda")
+        s2, m2 = B.cofie_ngff_filter_hist(h, 12, 16, 3, 16, B.keep_rule("per_channel", 0.25, L_max, 4, seg_len,
+                                                                       out_count=count))
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = (s2.cpu().numpy(), m2.cpu().numpy(), hist_np(h), count.cpu().numpy())
+    assert_filter_equal(g, oracle_filter(f, 16, "per_channel", np.float32(0.25), L_max, 4, seg_len))
+    s1, m1 = B.cofie_ngff_filter(fd, 16, B.keep_rule("per_channel", 0.25, L_max, 4, seg_len))
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(m1, m2)
+
+
 def test_filter_poisoned_workspace():
     """Tables in a reused workspace start from whatever the previous call (or
     nothing) left there: fill it with 0xFF, then call twice."""
