@@ -600,9 +600,11 @@ def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams)
             bat_score_us += profiled_kernels(torch, B, bcall, 10)["qer_score"]
             bat_calls += 1
             wb, _ = bcall(0)
+            # bit-equal to single-query calls over the same keys (the score
+            # kernel's work split depends on the key count)
             for qi in range(len(stamps)):
                 if nfq[qi]:
-                    w1, _ = B.cofie_qer_rank(Qsd[qi], Kd[:nfq[qi] * wl.tokens], offs_all[:nfq[qi] + 1].contiguous(), kb)
+                    w1, _ = B.cofie_qer_rank(Qsd[qi], Kd, offs_all[:nfq[qi] + 1].contiguous(), kb)
                     bat_equal &= bool(torch.equal(w1.view(torch.int32), wb[qi, :nfq[qi]].contiguous().view(torch.int32)))
             torch.cuda.synchronize()
         for qi, ts in enumerate(stamps):

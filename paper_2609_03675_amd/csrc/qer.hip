@@ -116,6 +116,7 @@ struct ScoreLdsArgs {
   int32_t* clear;      // workgroup 0 zeroes clear[0, nclear) (the frame-mean kernel's
   int32_t nclear;      // arrival counters), may be null
   int32_t lgS;         // log2 S
+  int32_t split_u4;    // contraction split NS ways: 16-byte columns from one slice to the next
 };
 
 constexpr int kLdsWaves = 8;
@@ -124,13 +125,17 @@ constexpr int kLdsThreads = kLdsWaves * 64;
 // 32 KiB phases when the query side is narrow (fewer registers held, a shorter
 // first fill: 1 fps stream 47.2 vs 48.8 us), 64 KiB otherwise (fewer phases:
 // high-res 20.4 vs 23.1 us)
-__host__ __device__ constexpr int lds_q_regs(int PNB) { return PNB <= 2 ? 4 : 8; }
+// With the contraction split NS ways inside the workgroup (NS > 1) a phase
+// holds NS slices and takes the 64 KiB buffer.
+__host__ __device__ constexpr int lds_q_regs(int PNB, int NS = 1) { return NS == 1 && PNB <= 2 ? 4 : 8; }
 
 // virtual steps per batch: 8 key loads per batch and wave (two batches in
 // flight), fewer where the query fragments and accumulators of wide query
-// blocks take the registers; at least one segment (16/R steps)
-__host__ __device__ constexpr int lds_batch(int MB, int PNB, int R) {
-  const int u = MB == 1 ? (PNB <= 4 ? 8 : 4) : (PNB <= 2 ? 4 : 2);
+// blocks take the registers, or where NS slices of a phase of U steps would
+// not fit its buffer; at least one segment (16/R steps)
+__host__ __device__ constexpr int lds_batch(int MB, int PNB, int R, int NS = 1) {
+  int u = MB == 1 ? (PNB <= 4 ? 8 : 4) : (PNB <= 2 ? 4 : 2);
+  while (u > 1 && NS * u * PNB * 64 > lds_q_regs(PNB, NS) * kLdsThreads) u >>= 1;
   return u > 16 / R ? u : 16 / R;
 }
 
@@ -148,20 +153,32 @@ __device__ __forceinline__ uint4 row_ror4(const uint4& v) {
 // segments) in this kernel on the 1 fps stream workload (48.9 vs 51.1 us).
 __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 
-template <typename T, int MB, int NB, int P>
+// NS > 1 splits the contraction inside the workgroup: wave w multiplies slice
+// w % NS (a.split_u4 columns from the previous one) of the tiles of wave group
+// w / NS, and the slices' accumulators are added in slice order through LDS
+// before the maximum over the query rows, so that few tiles still occupy every
+// wave of every CU.
+template <typename T, int MB, int NB, int P, int NS>
 __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) {
   using M = Mma<T>;
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
-  constexpr int U = lds_batch(MB, P * NB, R);
+  constexpr int U = lds_batch(MB, P * NB, R, NS);
   constexpr int FPS = P * NB;   // fragments per virtual step
-  constexpr int kQRegs = lds_q_regs(FPS);
+  constexpr int kQRegs = lds_q_regs(FPS, NS);
   constexpr int kPhaseU4 = kQRegs * kLdsThreads;
+  constexpr int TW = kLdsWaves / NS;  // waves per slice (tiles per round when MB = 1)
+  constexpr int LGNS = NS == 4 ? 2 : (NS == 2 ? 1 : 0);
   static_assert(U % VPS == 0, "batches hold whole segments");
-  extern __shared__ uint4 qs[];  // [2][kPhaseU4]: [S][P][NB][64] each
+  static_assert(NS == 1 || NS == 2 || NS == 4, "1, 2 or 4 slices");
+  static_assert(NS == 1 || MB == 1, "split contractions take one tile per wave");
+  // [2][kPhaseU4]: [NS][S][P][NB][64] each; with NS > 1 followed by the
+  // slice accumulators [NS - 1][TW][MB][NB][4][64] floats
+  extern __shared__ uint4 qs[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int slice = wave & (NS - 1), tw = wave >> LGNS;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int qs_lane = r16 / R;  // load index holding this lane's own row
   // Query fragments in LDS: [step][term][block][lane] (16 bytes per lane, a
@@ -184,7 +201,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   for (int u = 0; u < U; ++u) lsw[u] = lane ^ swz(u, g4);
   const int pfull = VPS * a.nseg;
   const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
-  const uint4* Kq = reinterpret_cast<const uint4*>(a.K);
+  const uint4* Kq = reinterpret_cast<const uint4*>(a.K) + (NS > 1 ? slice * a.split_u4 : 0);
   const uint4* Qq = reinterpret_cast<const uint4*>(a.Qp);
   const int t_begin = (int)((int64_t)a.tiles * blockIdx.x / a.nwg);
   const int t_end = (int)((int64_t)a.tiles * (blockIdx.x + 1) / a.nwg);
@@ -206,15 +223,18 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   // so that issuing the loads never waits for them.
   uint32_t qmask = 0;
   const int lgC = a.lgS + 2;  // log2 of the 16-byte columns per row and phase (4 S, S a power of two)
+  // With NS slices, consecutive runs of a row alternate between the slices:
+  // element e is slice (e >> lgC) % NS, row (e >> lgC) / NS.
   auto q_load = [&](int ph, uint4 (&qr)[kQRegs]) __attribute__((always_inline)) {
     qmask = 0;
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
       const int e = tid + kLdsThreads * i;
-      const int row = e >> lgC, f = row >> 4;
+      const int row = e >> (lgC + LGNS), f = row >> 4;
       const int p = f / NB, nb = f - p * NB;
       const int q = nb * 16 + (row & 15);
-      const int col = (ph << lgC) + (e & ((1 << lgC) - 1));
+      const int sl = (e >> lgC) & (NS - 1);
+      const int col = sl * a.split_u4 + (ph << lgC) + (e & ((1 << lgC) - 1));
       const bool ok = f < FPS && q < a.n_q && col * M::EPL < a.Lc;
       const int64_t grow = (int64_t)p * a.nq_total + a.q0 + (ok ? q : 0);
       qr[i] = Qq[grow * row_u4 + (ok ? col : 0)];
@@ -226,9 +246,10 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
       const int e = tid + kLdsThreads * i;
-      const int row = e >> lgC, f = row >> 4;
+      const int row = e >> (lgC + LGNS), f = row >> 4;
+      const int sl = (e >> lgC) & (NS - 1);
       const bool ok = (qmask >> i) & 1u;
-      dst[f < FPS ? q_slot(e & ((1 << lgC) - 1), f, row & 15) : e] =
+      dst[f < FPS ? (((sl * FPS) << (a.lgS + 6)) + q_slot(e & ((1 << lgC) - 1), f, row & 15)) : e] =
           uint4{ok ? qr[i].x : 0u, ok ? qr[i].y : 0u, ok ? qr[i].z : 0u, ok ? qr[i].w : 0u};
     }
   };
@@ -238,18 +259,18 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   };
 
-  for (int rb = t_begin; rb < t_end; rb += kLdsWaves * MB) {
-    // this wave's tiles: rb + wave + 8 j.  Missing ones repeat tile rb (the
+  for (int rb = t_begin; rb < t_end; rb += TW * MB) {
+    // this wave's tiles: rb + tw + TW j.  Missing ones repeat tile rb (the
     // first tile of wave 0 in this round): their loads hit the cache and their
     // results are never stored.
     int nmb = 0;
 #pragma unroll
-    for (int j = 0; j < MB; ++j) nmb += (rb + wave + kLdsWaves * j < t_end) ? 1 : 0;
+    for (int j = 0; j < MB; ++j) nmb += (rb + tw + TW * j < t_end) ? 1 : 0;
     const uint4* kq[MB][VPS];
     const uint4* k16[MB];
 #pragma unroll
     for (int j = 0; j < MB; ++j) {
-      const int64_t t0 = (int64_t)(j < nmb ? rb + wave + kLdsWaves * j : rb) * 16;
+      const int64_t t0 = (int64_t)(j < nmb ? rb + tw + TW * j : rb) * 16;
       const int64_t last = a.n_vis - 1;
 #pragma unroll
       for (int q = 0; q < VPS; ++q) {
@@ -300,7 +321,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
         q_store(ph + 1, qr);
         pending = false;
       }
-      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (ms - ph * a.S) * FPS * 64;  // ms - ph S is a multiple of U
+      // ms - ph S is a multiple of U; this wave's slice starts S FPS 64 slots further per slice
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + ((slice * a.S + ms - ph * a.S) * FPS) * 64;
 #pragma unroll
       for (int h = 0; h < U / VPS; ++h) {
         if (!guard || ms + VPS * h < pfull) {
@@ -384,7 +406,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       const int col = SEGC * a.nseg + 4 * (v - pfull);  // 16-byte column of lane group 0
       const bool in = (col + g4) * M::EPL < a.Lc;
       const int cph = (col + g4) - (ph << lgC);  // this lane's column within the phase
-      const uint4* qb = qs + (ph & 1) * kPhaseU4 + q_slot(cph, 0, r16);
+      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (((slice * FPS) << (a.lgS + 6)) + q_slot(cph, 0, r16));
       uint4 kf[MB];
 #pragma unroll
       for (int j = 0; j < MB; ++j) {
@@ -401,13 +423,40 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
         }
     }
 
+    // the slices' sums: slices 1.. NS-1 publish their accumulators, slice 0
+    // adds them in slice order (the buffer lies past the phase buffers in use)
+    if constexpr (NS > 1) {
+      float* red = reinterpret_cast<float*>(qs + (a.nphase > 1 ? 2 : 1) * kPhaseU4);
+      auto red_at = [&](int sl, int j, int nb, int r) __attribute__((always_inline)) {
+        return ((((((sl - 1) * TW + tw) * MB + j) * NB + nb) * 4 + r) << 6) + lane;
+      };
+      if (slice > 0) {
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[red_at(slice, j, nb, r)] = acc[j][nb][r];
+      }
+      barrier_lds();
+      if (slice > 0) continue;  // the next round begins with a barrier of all waves
+#pragma unroll
+      for (int sl = 1; sl < NS; ++sl)
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[j][nb][r] += red[red_at(sl, j, nb, r)];
+    }
+
     // m_j = scale * max over the query rows: registers over nb, then the 16
     // lanes of a row group; with several queries, one max per query (whole
     // 16-row blocks), max-accumulated when a query began in an earlier chunk
 #pragma unroll
     for (int j = 0; j < MB; ++j) {
       if (j < nmb) {
-        const int64_t tile = rb + wave + kLdsWaves * j;
+        const int64_t tile = rb + tw + TW * j;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t tok = tile * 16 + g4 * 4 + r;
@@ -1001,58 +1050,86 @@ int validate_qer(const void* Q, const void* K, const int32_t* offs, const cofie_
 // Work split of the LDS-staged score kernel: one workgroup per CU (fewer for
 // small inputs), tiles of 16 tokens spread evenly over the workgroups, 1 or 2
 // tiles per wave per round, 4-row key segments unless the batch is too short
-// to hold one, phases as long as a 64 KiB buffer allows.
+// to hold one, phases as long as a 64 KiB buffer allows.  Inputs of too few
+// tiles to give every wave of the chip a tile split the contraction NS ways
+// (NS depends on the tile count, the contraction and the query terms only, not
+// on the query rows, so that queries ranked together or alone add in the same
+// order).
 struct LdsPlan {
-  int MB, R, nwg, S, lgS, nphase, nseg, ksteps;
+  int MB, R, NS, nwg, S, lgS, nphase, nseg, ksteps, split_u4;
   size_t lds;
 };
 
-LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int PNB, int cus) {
+// Slices of the contraction for `tiles` tiles: the largest NS in {4, 2} whose
+// tiles still take one round (one tile per wave group on at most every CU:
+// each further round restages the whole query side and restarts the key
+// pipeline, measured at ~11 us per round for the multi-stream heads, more than
+// the split saves), else 1.  Whole segments per slice, no tail steps, one
+// query term.
+inline int plan_slices(int64_t tiles, int64_t Lc, size_t esize, int P, int cus) {
+  const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)esize;
+  if (P != 1 || Lc % seg_el != 0) return 1;
+  const int64_t nseg = Lc / seg_el;
+  for (int ns = 4; ns > 1; ns /= 2)
+    if (nseg % ns == 0 && tiles <= (int64_t)cus * (kLdsWaves / ns)) return ns;
+  return 1;
+}
+
+LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int P, int PNB, int cus) {
   LdsPlan L;
   const int64_t tiles = ceil_div(n_vis, 16);
-  L.nwg = (int)std::min<int64_t>(cus, ceil_div(tiles, kLdsWaves));
+  L.NS = plan_slices(tiles, Lc, esize, P, cus);
+  const int tw = kLdsWaves / L.NS;
+  L.nwg = (int)std::min<int64_t>(cus, ceil_div(tiles, tw));
   const int64_t tpw = ceil_div(tiles, L.nwg);
-  L.MB = tpw > kLdsWaves ? 2 : 1;
+  L.MB = (L.NS == 1 && tpw > kLdsWaves) ? 2 : 1;
   L.R = lds_rows(L.MB, PNB);
-  const int U = lds_batch(L.MB, PNB, L.R);
+  const int U = lds_batch(L.MB, PNB, L.R, L.NS);
   const int64_t kps = 64 / (int64_t)esize;             // elements per plain MFMA step
   const int64_t seg_el = (1024 / L.R) / (int64_t)esize;  // elements per segment
-  L.nseg = (int)(Lc / seg_el);
-  L.ksteps = (int)((16 / L.R) * L.nseg + ceil_div(Lc % seg_el, kps));
-  const int phase_u4 = lds_q_regs(PNB) * kLdsThreads;
-  // S: a power of two (>= U), as large as the phase buffer holds, no larger
-  // than the contraction needs
-  const int64_t cap = (phase_u4 / 64) / PNB;
+  const int64_t Ls = Lc / L.NS;                        // one slice (whole segments when NS > 1)
+  L.nseg = (int)(Ls / seg_el);
+  L.ksteps = (int)((16 / L.R) * L.nseg + ceil_div(Ls % seg_el, kps));
+  L.split_u4 = (int)(Ls * (int64_t)esize / 16);
+  const int phase_u4 = lds_q_regs(PNB, L.NS) * kLdsThreads;
+  // S: a power of two (>= U), as large as the phase buffer holds (NS slices
+  // of S steps), no larger than the contraction needs
+  const int64_t cap = (phase_u4 / 64) / PNB / L.NS;
   L.S = U;
   while (2 * L.S <= cap && L.S < L.ksteps) L.S *= 2;
   L.lgS = 0;
   while ((1 << L.lgS) < L.S) ++L.lgS;
   L.nphase = (int)ceil_div(L.ksteps, L.S);
   L.lds = (size_t)(L.nphase > 1 ? 2 : 1) * phase_u4 * sizeof(uint4);
+  if (L.NS > 1) L.lds += (size_t)(L.NS - 1) * tw * PNB * 4 * 64 * sizeof(float);
   return L;
 }
 
-template <typename T, int MB, int NB, int P>
+template <typename T, int MB, int NB, int P, int NS>
 int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, hipStream_t s) {
-  auto k = qer_score_kernel<T, MB, NB, P>;
+  auto k = qer_score_kernel<T, MB, NB, P, NS>;
   int rc = allow_lds(k, L.lds);
   if (rc) return rc;
   return launch("qer_score", k, dim3((unsigned)L.nwg), dim3(kLdsThreads), L.lds, s, sa);
 }
 
-template <typename T, int MB, int P>
+template <typename T, int MB, int P, int NS>
 int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
   switch (NB) {
-    case 1: return launch_lds_t<T, MB, 1, P>(sa, L, s);
-    case 2: return launch_lds_t<T, MB, 2, P>(sa, L, s);
-    case 3: return launch_lds_t<T, MB, 3, P>(sa, L, s);
-    default: return launch_lds_t<T, MB, 4, P>(sa, L, s);
+    case 1: return launch_lds_t<T, MB, 1, P, NS>(sa, L, s);
+    case 2: return launch_lds_t<T, MB, 2, P, NS>(sa, L, s);
+    case 3: return launch_lds_t<T, MB, 3, P, NS>(sa, L, s);
+    default: return launch_lds_t<T, MB, 4, P, NS>(sa, L, s);
   }
 }
 
 template <typename T, int P>
 int launch_lds(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
-  return L.MB == 1 ? launch_lds_nb<T, 1, P>(sa, L, NB, s) : launch_lds_nb<T, 2, P>(sa, L, NB, s);
+  if constexpr (P == 1) {
+    if (L.NS == 4) return launch_lds_nb<T, 1, P, 4>(sa, L, NB, s);
+    if (L.NS == 2) return launch_lds_nb<T, 1, P, 2>(sa, L, NB, s);
+  }
+  return L.MB == 1 ? launch_lds_nb<T, 1, P, 1>(sa, L, NB, s) : launch_lds_nb<T, 2, P, 1>(sa, L, NB, s);
 }
 
 template <typename T, int NB>
@@ -1130,13 +1207,14 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         sa.n_q = std::min(64, R - q0);
         sa.accumulate = q0 > 0;
         const int NB = (sa.n_q + 15) / 16;
-        const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P * NB, cus);
+        const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P, p.P * NB, cus);
         sa.nseg = L.nseg;
         sa.ksteps = L.ksteps;
         sa.S = L.S;
         sa.lgS = L.lgS;
         sa.nphase = L.nphase;
         sa.nwg = L.nwg;
+        sa.split_u4 = L.split_u4;
         if (bf16)
           rc = p.P == 3 ? launch_lds<bf16_t, 3>(sa, L, NB, s) : launch_lds<bf16_t, 1>(sa, L, NB, s);
         else

@@ -146,6 +146,21 @@ def test_poisoned_workspace():
         assert torch.equal(w1, w2) and torch.equal(i1, i2)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_q,H,d,tokens", [
+    (20, 8, 64, [97] * 99),        # ~600 tiles: contraction split 2 ways
+    (20, 8, 64, [100] * 81 + [3]),   # 507 tiles: split 4 ways, two tiles per workgroup, ragged last tile
+    (32, 28, 128, [144] * 49 + [7]),  # multi-stream heads, a short candidate prefix: split 4 ways
+])
+def test_split_contraction(dtype, n_q, H, d, tokens):
+    """Inputs with fewer 16-token tiles than waves on the chip: the score
+    kernel splits each tile's contraction over several waves and adds their
+    partial sums before the maximum over the query rows."""
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(777 + len(tokens), n_q, int(offs[-1]), H, H, d, dtype)
+    run_case(Q, K, offs, H, H, d, 16, dtype=dtype)
+
+
 def test_many_tokens_per_workgroup():
     """More 16-token tiles than one pass of a workgroup's waves covers (the
     score kernel loops over rounds of tiles, refilling the query phases), with

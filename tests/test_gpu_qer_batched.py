@@ -80,9 +80,18 @@ def test_batched_against_oracle(dtype, n_queries, n_q, H_q, H_kv, d, n_frames):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_batched_equals_single_query_calls(dtype):
-    n_queries, n_q, H_q, H_kv, d, n_frames = 5, 48, 28, 4, 128, 64
-    Q, K, offs, nf = make_case(7, n_queries, n_q, H_q, H_kv, d, n_frames, dtype)
+@pytest.mark.parametrize("n_q,H_q,H_kv,max_tokens", [
+    (48, 28, 4, 24),     # GQA fold (three query terms)
+    (32, 28, 28, 24),    # multi-stream heads: few tiles, contraction split 4 ways
+    (32, 8, 8, 300),     # 512-long contraction split 2 ways (~590 tiles)
+])
+def test_batched_equals_single_query_calls(dtype, n_q, H_q, H_kv, max_tokens):
+    """Per-query calls over the same keys add in the same order as the
+    batched call (also when the score kernel splits the contraction, whose
+    split depends on the keys and heads only), so the scores are equal bit for
+    bit."""
+    n_queries, d, n_frames = 5, 128 if H_q == 28 else 64, 64
+    Q, K, offs, nf = make_case(7, n_queries, n_q, H_q, H_kv, d, n_frames, dtype, max_tokens)
     w, idx = run_batched(Q, K, offs, nf, H_q, H_kv, d, 12, dtype)
     Kd, od = qk_dev(K), to_dev(offs)
     for g in range(n_queries):
