@@ -117,7 +117,25 @@ struct ScoreLdsArgs {
   int32_t nclear;      // arrival counters), may be null
   int32_t lgS;         // log2 S
   int32_t split_u4;    // contraction split NS ways: 16-byte columns from one slice to the next
+  int32_t k_row_u4;    // 16-byte chunks per key row (shorter than a query row in SOFTMAX GQA)
+  // SOFTMAX passes (the contraction runs over the query heads in order, one
+  // head every sph segments; query head h reads key head h / G)
+  int32_t sph;         // segments per head
+  int32_t H;           // query heads
+  int32_t G;           // query heads per key head
+  float soft_scale;    // scale inside the exponent
+  // pass 1: (max, sum of exp) of row r = h * nq_total + q per wave and round,
+  // part b = (workgroup * 8 + wave) * rounds + round at
+  // stats_part[((r / 16) * nparts + b) * 16 + r % 16]
+  float2* stats_part;
+  int32_t rounds;      // rounds per workgroup
+  int32_t nparts;      // nwg * 8 * rounds
+  const float2* stats; // pass 2: [H][nq_total] (max, sum of exp) over all keys
 };
+
+constexpr int kModeLogit = 0;     // Eq. 6-7: m_j = max_i a_ij
+constexpr int kModeSoftStats = 1; // SOFTMAX pass 1: per-head row statistics
+constexpr int kModeSoftProb = 2;  // SOFTMAX pass 2: m_j = max_i mean_h P^h_ij
 
 constexpr int kLdsWaves = 8;
 constexpr int kLdsThreads = kLdsWaves * 64;
@@ -149,6 +167,27 @@ __device__ __forceinline__ uint4 row_ror4(const uint4& v) {
   else return uint4{row_ror<N>(v.x), row_ror<N>(v.y), row_ror<N>(v.z), row_ror<N>(v.w)};
 }
 
+// Reductions over lanes l and l ^ 16 (l ^ 32) in the VALU: gfx950's
+// v_permlane16_swap / v_permlane32_swap hand each lane the pair (value of the
+// lower lane, value of the upper lane), in that order in both lanes (checked
+// on the device), so both lanes compute the same result.
+__device__ __forceinline__ float max_x16(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float max_x32(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float sum_x16(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float sum_x32(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
 // rows per key load.  8 (128-byte segments) measured faster than 4 (256-byte
 // segments) in this kernel on the 1 fps stream workload (48.9 vs 51.1 us).
 __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
@@ -158,13 +197,21 @@ __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 // w / NS, and the slices' accumulators are added in slice order through LDS
 // before the maximum over the query rows, so that few tiles still occupy every
 // wave of every CU.
-template <typename T, int MB, int NB, int P, int NS>
+//
+// MODE selects the epilogue: kModeLogit as above; the SOFTMAX passes close
+// every head (sph segments of the contraction) in registers: pass 1 writes the
+// head's (max, sum of exp) over the wave's tokens for every query row, pass 2
+// adds exp(s - max) / sum over the heads and ends like LOGIT with the head
+// mean's maximum over the query rows.
+template <typename T, int MB, int NB, int P, int NS, int MODE>
 __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) {
   using M = Mma<T>;
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
-  constexpr int U = lds_batch(MB, P * NB, R, NS);
+  // (SOFTMAX pass 1 with three or four query blocks and one tile per wave
+  // halves the host's batch, which would spill: S stays a multiple of it)
+  constexpr int U = lds_batch(MB, P * NB, R, NS) / (MODE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
   constexpr int FPS = P * NB;   // fragments per virtual step
   constexpr int kQRegs = lds_q_regs(FPS, NS);
   constexpr int kPhaseU4 = kQRegs * kLdsThreads;
@@ -173,6 +220,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   static_assert(U % VPS == 0, "batches hold whole segments");
   static_assert(NS == 1 || NS == 2 || NS == 4, "1, 2 or 4 slices");
   static_assert(NS == 1 || MB == 1, "split contractions take one tile per wave");
+  static_assert(MODE == kModeLogit || (NS == 1 && P == 1), "SOFTMAX passes: one query term, no split");
   // [2][kPhaseU4]: [NS][S][P][NB][64] each; with NS > 1 followed by the
   // slice accumulators [NS - 1][TW][MB][NB][4][64] floats
   extern __shared__ uint4 qs[];
@@ -201,12 +249,30 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   for (int u = 0; u < U; ++u) lsw[u] = lane ^ swz(u, g4);
   const int pfull = VPS * a.nseg;
   const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
+  const int64_t krow_u4 = a.k_row_u4;
   const uint4* Kq = reinterpret_cast<const uint4*>(a.K) + (NS > 1 ? slice * a.split_u4 : 0);
   const uint4* Qq = reinterpret_cast<const uint4*>(a.Qp);
   const int t_begin = (int)((int64_t)a.tiles * blockIdx.x / a.nwg);
   const int t_end = (int)((int64_t)a.tiles * (blockIdx.x + 1) / a.nwg);
   if (blockIdx.x == 0 && a.clear)
     for (int i = tid; i < a.nclear; i += kLdsThreads) a.clear[i] = 0;
+
+  // SOFTMAX passes: past the phase buffers, pass 2's row statistics of this
+  // query chunk ([H][n_q]: max, 1 / sum of exp) and, for grouped heads, the
+  // key segment of every contraction segment.  The first barrier of the round
+  // loop publishes them.
+  float2* st_sh = reinterpret_cast<float2*>(qs + (a.nphase > 1 ? 2 : 1) * kPhaseU4);
+  int32_t* seg_map = reinterpret_cast<int32_t*>(st_sh + (MODE == kModeSoftProb ? a.H * a.n_q : 0));
+  if constexpr (MODE != kModeLogit) {
+    if (a.G > 1)
+      for (int v = tid; v < a.nseg; v += kLdsThreads) seg_map[v] = (v / a.sph / a.G) * a.sph + v % a.sph;
+    if constexpr (MODE == kModeSoftProb)
+      for (int i = tid; i < a.H * a.n_q; i += kLdsThreads) {
+        const int hh = i / a.n_q, q = i - hh * a.n_q;
+        const float2 st = a.stats[(int64_t)hh * a.nq_total + a.q0 + q];
+        st_sh[i] = make_float2(st.x, 1.0f / st.y);
+      }
+  }
 
   bool qok[NB];
 #pragma unroll
@@ -276,9 +342,9 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       for (int q = 0; q < VPS; ++q) {
         const int64_t tok = min(t0 + R * q + (lane % R), last);
         const int chunk = VPS * g4 + ((((lane & 15) / R) - q) & (VPS - 1));
-        kq[j][q] = Kq + tok * row_u4 + chunk;
+        kq[j][q] = Kq + tok * krow_u4 + chunk;
       }
-      k16[j] = Kq + min(t0 + r16, last) * row_u4 + g4;
+      k16[j] = Kq + min(t0 + r16, last) * krow_u4 + g4;
     }
     f32x4 acc[MB][NB];
 #pragma unroll
@@ -286,11 +352,72 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // SOFTMAX passes: close query head hh, whose unscaled dot products are in
+    // acc, and start the next one from zero
+    f32x4 prob[MB][NB];  // pass 2: sum over the heads closed so far
+#pragma unroll
+    for (int j = 0; j < MB; ++j)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) prob[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int head = 0, head_seg = 0;
+    auto head_close = [&](int hh) __attribute__((always_inline)) {
+      if constexpr (MODE == kModeSoftStats) {
+        // (max, sum of exp(s - max)) over this wave's valid tokens, per query
+        // row; a wave without tokens writes (-inf, 0)
+        const int64_t slot = ((int64_t)blockIdx.x * kLdsWaves + wave) * a.rounds + (rb - t_begin) / (TW * MB);
+        const int64_t row0 = (int64_t)hh * a.nq_total + a.q0;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < MB; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
+              if (j < nmb && tok < a.n_vis) mx = fmaxf(mx, acc[j][nb][r]);
+            }
+          mx = max_x32(max_x16(mx));
+          float z = 0.f;
+#pragma unroll
+          for (int j = 0; j < MB; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
+              if (j < nmb && tok < a.n_vis) z += __expf((acc[j][nb][r] - mx) * a.soft_scale);
+            }
+          z = sum_x32(sum_x16(z));
+          const int q = nb * 16 + r16;
+          if (g4 == 0 && q < a.n_q) {
+            const int64_t row = row0 + q;  // 16 lanes: one or two 128-byte runs
+            a.stats_part[((row >> 4) * a.nparts + slot) * 16 + (row & 15)] = make_float2(mx * a.soft_scale, z);
+          }
+        }
+      } else if constexpr (MODE == kModeSoftProb) {
+        const float2* sth = st_sh + hh * a.n_q;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int q = nb * 16 + r16;
+          const float2 st = sth[q < a.n_q ? q : a.n_q - 1];
+#pragma unroll
+          for (int j = 0; j < MB; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) prob[j][nb][r] += __expf(acc[j][nb][r] * a.soft_scale - st.x) * st.y;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+
     // loads of the U virtual steps from ms (U/VPS segments, VPS loads each)
     auto k_load = [&](uint4 (&f)[U][MB], int ms) __attribute__((always_inline)) {
 #pragma unroll
       for (int h = 0; h < U / VPS; ++h) {
-        const int seg = min(ms / VPS + h, a.nseg - 1);
+        int seg = min(ms / VPS + h, a.nseg - 1);
+        if constexpr (MODE != kModeLogit) {
+          if (a.G > 1) seg = seg_map[seg];
+        }
 #pragma unroll
         for (int q = 0; q < VPS; ++q)
 #pragma unroll
@@ -367,6 +494,13 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
               for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int j = 0; j < MB; ++j) M::mac(acc[j][nb], fk[j], qf[p * NB + nb]);
+          }
+          if constexpr (MODE != kModeLogit) {
+            if (++head_seg == a.sph) {
+              head_close(head);
+              ++head;
+              head_seg = 0;
+            }
           }
         }
       }
@@ -450,6 +584,14 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             for (int r = 0; r < 4; ++r) acc[j][nb][r] += red[red_at(sl, j, nb, r)];
     }
 
+    if constexpr (MODE == kModeSoftStats) continue;  // the statistics are written
+    if constexpr (MODE == kModeSoftProb) {
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[j][nb] = prob[j][nb];
+    }
+
     // m_j = scale * max over the query rows: registers over nb, then the 16
     // lanes of a row group; with several queries, one max per query (whole
     // 16-row blocks), max-accumulated when a query began in an earlier chunk
@@ -498,6 +640,19 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             store(gcur, vg);
           }
         }
+      }
+    }
+  }
+  if constexpr (MODE == kModeSoftStats) {
+    // the rounds this workgroup does not run leave empty statistics (a zero
+    // sum), which the merge skips
+    const int nr = (t_end - t_begin + TW * MB - 1) / (TW * MB);
+    for (int rr = nr; rr < a.rounds; ++rr) {
+      const int64_t slot = ((int64_t)blockIdx.x * kLdsWaves + wave) * a.rounds + rr;
+      for (int i = lane; i < a.H * a.n_q; i += 64) {
+        const int hh = i / a.n_q, q = i - hh * a.n_q;
+        const int64_t row = (int64_t)hh * a.nq_total + a.q0 + q;
+        a.stats_part[((row >> 4) * a.nparts + slot) * 16 + (row & 15)] = make_float2(-INFINITY, 0.f);
       }
     }
   }
@@ -891,19 +1046,83 @@ __global__ __launch_bounds__(256) void qer_soft_stats_kernel(SoftArgs a) {
   }
 }
 
-// Merge per-workgroup (max, sumexp) pairs into row statistics, fixed order.
-__global__ void qer_soft_merge_kernel(const float2* partial, int64_t nblocks, int32_t rows,
-                                      float2* stats) {
-  const int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (r >= rows) return;
+// Row statistics from per-part (max, sum of exp) pairs, part b of row r at
+// partial[b * ps + r * rs]: one wave per row, parts strided over the lanes;
+// the max, then sum_b z_b exp(m_b - max) in fp64, each over the lanes and a
+// fixed xor tree.  Parts with a zero sum (no tokens) are skipped.
+// stats[r] = (max, sum of exp(s - max)).
+__global__ __launch_bounds__(256) void qer_soft_merge_kernel(const float2* partial, int64_t nparts, int64_t ps,
+                                                             int64_t rs, int32_t rows, float2* stats) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;  // whole waves; the kernel has no barrier
+  const float2* src = partial + r * rs;
   float mx = -INFINITY;
-  for (int64_t b = 0; b < nblocks; ++b) mx = fmaxf(mx, partial[b * rows + r].x);
-  double z = 0.0;
-  for (int64_t b = 0; b < nblocks; ++b) {
-    const float2 p = partial[b * rows + r];
-    if (p.y > 0.f) z += (double)p.y * exp((double)p.x - (double)mx);
+  for (int64_t b = lane; b < nparts; b += 64) {
+    const float2 v = src[b * ps];
+    if (v.y > 0.f) mx = fmaxf(mx, v.x);
   }
-  stats[r] = make_float2(mx, (float)z);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  double z = 0.0;
+  for (int64_t b = lane; b < nparts; b += 64) {
+    const float2 v = src[b * ps];
+    if (v.y > 0.f) z += (double)v.y * (double)__expf(v.x - mx);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
+  if (lane == 0) stats[r] = make_float2(mx, (float)z);
+}
+
+// The same for the score kernel's pass-1 layout (rows in blocks of 16, part b
+// of the block at [b][16]): workgroup per 16 rows, thread t takes row t % 16
+// and parts t / 16 + 64 u (each load of the workgroup is 64 consecutive
+// parts, 8 KiB), 32 of them in flight at a time: their max, then the sum of
+// z exp(m - max) in fp64 from registers, folded into the thread's running
+// pair.  The 64 pairs of a row are then combined pairwise in LDS (a fixed
+// tree of six levels).
+__global__ __launch_bounds__(1024) void qer_soft_merge_blocked_kernel(const float2* partial, int64_t nparts,
+                                                                      int32_t rows, float2* stats) {
+  __shared__ float mx_sh[64][16];
+  __shared__ double z_sh[64][16];
+  constexpr int C = 32;
+  const int tid = threadIdx.x, r16 = tid & 15, grp = tid >> 4;
+  const float2* src = partial + (int64_t)blockIdx.x * nparts * 16 + r16;
+  float M = -INFINITY;
+  double Z = 0.0;
+  for (int64_t b0 = grp; b0 < nparts; b0 += 64 * C) {
+    float2 v[C];
+#pragma unroll
+    for (int u = 0; u < C; ++u) {
+      const int64_t b = b0 + 64 * u;
+      v[u] = b < nparts ? src[b * 16] : make_float2(-INFINITY, 0.f);
+    }
+    float m = M;
+#pragma unroll
+    for (int u = 0; u < C; ++u) m = v[u].y > 0.f ? fmaxf(m, v[u].x) : m;
+    double z = Z > 0.0 ? Z * (double)__expf(M - m) : 0.0;
+#pragma unroll
+    for (int u = 0; u < C; ++u) z += v[u].y > 0.f ? (double)v[u].y * (double)__expf(v[u].x - m) : 0.0;
+    M = m;
+    Z = z;
+  }
+  mx_sh[grp][r16] = M;
+  z_sh[grp][r16] = Z;
+  for (int half = 32; half > 0; half >>= 1) {
+    __syncthreads();
+    if (grp < half) {
+      const float m1 = mx_sh[grp][r16], m2 = mx_sh[grp + half][r16];
+      const double z1 = z_sh[grp][r16], z2 = z_sh[grp + half][r16];
+      const float m = z1 > 0.0 ? (z2 > 0.0 ? fmaxf(m1, m2) : m1) : m2;
+      const double z = (z1 > 0.0 ? z1 * (double)__expf(m1 - m) : 0.0) + (z2 > 0.0 ? z2 * (double)__expf(m2 - m) : 0.0);
+      mx_sh[grp][r16] = m;
+      z_sh[grp][r16] = z;
+    }
+  }
+  if (tid < 16) {
+    const int64_t r = (int64_t)blockIdx.x * 16 + tid;
+    if (r < rows) stats[r] = make_float2(mx_sh[0][tid], (float)z_sh[0][tid]);
+  }
 }
 
 template <typename T, int NB>
@@ -970,6 +1189,11 @@ struct QerPlan {
   bool fold;
   size_t esize;
   int64_t nblk_soft;
+  // SOFTMAX through the LDS-staged score kernel: heads of whole 128-byte
+  // segments, the pass-2 statistics and the segment map within the LDS budget
+  bool soft_fast;
+  int64_t soft_nwg;     // workgroups of the score kernel
+  int64_t soft_rounds;  // their rounds
 };
 
 struct QerScratch {
@@ -999,10 +1223,15 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   w.m = ar.take<float>((size_t)n_queries * (h.n_vis > 0 ? h.n_vis : 1));
   w.keys = ar.take<uint32_t>((size_t)n_queries * (h.n_frames > 0 ? h.n_frames : 1));
   w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * n_queries * h.n_q * p.Lc * p.esize) : nullptr;
+  // (the SOFTMAX partial statistics are carved below)
   w.nf = n_queries > 1 ? ar.take<int32_t>((size_t)n_queries) : nullptr;
   w.done = ar.take<int32_t>((size_t)n_queries * qer_trees(h.n_frames).ints);
   if (h.score_mode == COFIE_SCORE_SOFTMAX) {
-    w.partial = ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
+    // the score kernel's statistics: rows (heads x query rows) in whole blocks
+    // of 16, per wave and round
+    const size_t rows16 = (size_t)ceil_div((int64_t)h.H_q * h.n_q, 16) * 16;
+    w.partial = p.soft_fast ? ar.take<float2>((size_t)p.soft_nwg * kLdsWaves * p.soft_rounds * rows16)
+                            : ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
     w.stats = ar.take<float2>((size_t)h.H_q * h.n_q);
   } else {
     w.partial = nullptr;
@@ -1011,6 +1240,8 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   return w;
 }
 
+void plan_soft(const cofie_qer_desc& h, QerPlan& p);
+
 QerPlan plan_qer(const cofie_qer_desc& h) {
   QerPlan p;
   p.esize = h.dtype == COFIE_BF16 ? 2 : 4;
@@ -1018,6 +1249,7 @@ QerPlan plan_qer(const cofie_qer_desc& h) {
   p.Lc = (int64_t)(p.fold ? h.H_kv : h.H_q) * h.d;  // MHA: H_q == H_kv
   p.P = (p.fold && h.dtype == COFIE_BF16) ? 3 : 1;
   p.nblk_soft = (h.n_vis + kMB * 16 - 1) / (kMB * 16);
+  plan_soft(h, p);
   return p;
 }
 
@@ -1075,10 +1307,10 @@ inline int plan_slices(int64_t tiles, int64_t Lc, size_t esize, int P, int cus) 
   return 1;
 }
 
-LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int P, int PNB, int cus) {
+LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int P, int PNB, int cus, bool split_ok) {
   LdsPlan L;
   const int64_t tiles = ceil_div(n_vis, 16);
-  L.NS = plan_slices(tiles, Lc, esize, P, cus);
+  L.NS = split_ok ? plan_slices(tiles, Lc, esize, P, cus) : 1;
   const int tw = kLdsWaves / L.NS;
   L.nwg = (int)std::min<int64_t>(cus, ceil_div(tiles, tw));
   const int64_t tpw = ceil_div(tiles, L.nwg);
@@ -1105,31 +1337,67 @@ LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int P, int PNB, 
   return L;
 }
 
-template <typename T, int MB, int NB, int P, int NS>
-int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, hipStream_t s) {
-  auto k = qer_score_kernel<T, MB, NB, P, NS>;
-  int rc = allow_lds(k, L.lds);
+template <typename T, int MB, int NB, int P, int NS, int MODE>
+int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, size_t lds, hipStream_t s) {
+  auto k = qer_score_kernel<T, MB, NB, P, NS, MODE>;
+  int rc = allow_lds(k, lds);
   if (rc) return rc;
-  return launch("qer_score", k, dim3((unsigned)L.nwg), dim3(kLdsThreads), L.lds, s, sa);
+  const char* name = MODE == kModeLogit ? "qer_score" : (MODE == kModeSoftStats ? "qer_soft_stats" : "qer_soft_score");
+  return launch(name, k, dim3((unsigned)L.nwg), dim3(kLdsThreads), lds, s, sa);
 }
 
-template <typename T, int MB, int P, int NS>
-int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
+template <typename T, int MB, int P, int NS, int MODE>
+int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, size_t lds, hipStream_t s) {
   switch (NB) {
-    case 1: return launch_lds_t<T, MB, 1, P, NS>(sa, L, s);
-    case 2: return launch_lds_t<T, MB, 2, P, NS>(sa, L, s);
-    case 3: return launch_lds_t<T, MB, 3, P, NS>(sa, L, s);
-    default: return launch_lds_t<T, MB, 4, P, NS>(sa, L, s);
+    case 1: return launch_lds_t<T, MB, 1, P, NS, MODE>(sa, L, lds, s);
+    case 2: return launch_lds_t<T, MB, 2, P, NS, MODE>(sa, L, lds, s);
+    case 3: return launch_lds_t<T, MB, 3, P, NS, MODE>(sa, L, lds, s);
+    default: return launch_lds_t<T, MB, 4, P, NS, MODE>(sa, L, lds, s);
   }
 }
 
-template <typename T, int P>
-int launch_lds(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s) {
-  if constexpr (P == 1) {
-    if (L.NS == 4) return launch_lds_nb<T, 1, P, 4>(sa, L, NB, s);
-    if (L.NS == 2) return launch_lds_nb<T, 1, P, 2>(sa, L, NB, s);
+// lds = 0: the plan's (the phase buffers and the slices' accumulators)
+template <typename T, int P, int MODE = kModeLogit>
+int launch_lds(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, hipStream_t s, size_t lds = 0) {
+  if (!lds) lds = L.lds;
+  if constexpr (P == 1 && MODE == kModeLogit) {
+    if (L.NS == 4) return launch_lds_nb<T, 1, P, 4, MODE>(sa, L, NB, lds, s);
+    if (L.NS == 2) return launch_lds_nb<T, 1, P, 2, MODE>(sa, L, NB, lds, s);
   }
-  return L.MB == 1 ? launch_lds_nb<T, 1, P, 1>(sa, L, NB, s) : launch_lds_nb<T, 2, P, 1>(sa, L, NB, s);
+  return L.MB == 1 ? launch_lds_nb<T, 1, P, 1, MODE>(sa, L, NB, lds, s)
+                   : launch_lds_nb<T, 2, P, 1, MODE>(sa, L, NB, lds, s);
+}
+
+// SOFTMAX through the score kernel: the LDS of a pass (phase buffers, pass 2's
+// statistics [H][nq] of its query chunk, the segment map for grouped heads)
+// and the pass-1 statistics per row (one per wave and round).
+size_t soft_lds(const LdsPlan& L, int mode, int H, int nq_chunk, int G, int64_t nseg) {
+  size_t b = L.lds;
+  if (mode == kModeSoftProb) b += (size_t)H * nq_chunk * sizeof(float2);
+  if (G > 1) b += (size_t)nseg * sizeof(int32_t);
+  return b;
+}
+int64_t soft_rounds(const LdsPlan& L, int64_t n_vis) {
+  const int64_t tiles = ceil_div(n_vis, 16);
+  return ceil_div(ceil_div(tiles, L.nwg), (int64_t)kLdsWaves * L.MB);
+}
+constexpr size_t kLdsMax = 160 * 1024;
+
+// Whether SOFTMAX takes the score kernel (each head whole 128-byte segments
+// of a key row, the widest query chunk's LDS within the CU's), and its
+// pass-1 statistics count.
+void plan_soft(const cofie_qer_desc& h, QerPlan& p) {
+  p.soft_fast = false;
+  p.soft_nwg = p.soft_rounds = 0;
+  if (h.score_mode != COFIE_SCORE_SOFTMAX || h.n_vis <= 0) return;
+  const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)p.esize;
+  if (h.d % seg_el != 0) return;
+  const int nq = std::min(64, h.n_q), NB = (nq + 15) / 16;
+  const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, device_cu_count(), false);
+  if (soft_lds(L, kModeSoftProb, h.H_q, nq, h.H_q / h.H_kv, p.Lc / seg_el) > kLdsMax) return;
+  p.soft_fast = true;
+  p.soft_nwg = L.nwg;
+  p.soft_rounds = soft_rounds(L, h.n_vis);
 }
 
 template <typename T, int NB>
@@ -1172,7 +1440,8 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
   const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
   // the top-k runs in the frame-mean kernel's last workgroup when the score
   // kernel (launched first) clears its arrival counters
-  const bool fused_tail = h.score_mode == COFIE_SCORE_LOGIT && h.n_vis > 0 && h.n_frames > 0 && k_top > 0;
+  const bool fused_tail =
+      (h.score_mode == COFIE_SCORE_LOGIT || p.soft_fast) && h.n_vis > 0 && h.n_frames > 0 && k_top > 0;
 
   if (h.n_vis > 0) {
     if (h.score_mode == COFIE_SCORE_LOGIT) {
@@ -1187,7 +1456,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         if (rc) return rc;
         qp = w.qp;
       }
-      ScoreLdsArgs sa;
+      ScoreLdsArgs sa{};
       sa.K = static_cast<const uint8_t*>(K);
       sa.Qp = qp;
       sa.n_vis = h.n_vis;
@@ -1195,7 +1464,6 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.group_rows = multi ? h.n_q : 0;
       sa.m_stride = h.n_vis;
       sa.Lc = (int32_t)p.Lc;
-      const int kps = bf16 ? Mma<bf16_t>::KPS : Mma<float>::KPS;
       sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
@@ -1207,7 +1475,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         sa.n_q = std::min(64, R - q0);
         sa.accumulate = q0 > 0;
         const int NB = (sa.n_q + 15) / 16;
-        const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P, p.P * NB, cus);
+        const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P, p.P * NB, cus, true);
         sa.nseg = L.nseg;
         sa.ksteps = L.ksteps;
         sa.S = L.S;
@@ -1215,11 +1483,71 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         sa.nphase = L.nphase;
         sa.nwg = L.nwg;
         sa.split_u4 = L.split_u4;
+        sa.k_row_u4 = (int32_t)(p.Lc * (int64_t)p.esize / 16);
         if (bf16)
           rc = p.P == 3 ? launch_lds<bf16_t, 3>(sa, L, NB, s) : launch_lds<bf16_t, 1>(sa, L, NB, s);
         else
           rc = launch_lds<float, 1>(sa, L, NB, s);
         if (rc) return rc;
+      }
+    } else if (p.soft_fast) {
+      // two passes of the score kernel over K (per-head statistics, then the
+      // probabilities), the statistics merged in between
+      ScoreLdsArgs sa{};
+      sa.K = static_cast<const uint8_t*>(K);
+      sa.Qp = static_cast<const uint8_t*>(Q);
+      sa.n_vis = h.n_vis;
+      sa.nq_total = h.n_q;
+      sa.group_rows = 0;
+      sa.m_stride = h.n_vis;
+      sa.Lc = (int32_t)p.Lc;
+      sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
+      sa.m = w.m;
+      sa.k_row_u4 = (int32_t)((int64_t)h.H_kv * h.d * (int64_t)p.esize / 16);
+      const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)p.esize;
+      sa.sph = (int32_t)(h.d / seg_el);
+      sa.H = h.H_q;
+      sa.G = h.H_q / h.H_kv;
+      sa.soft_scale = base_scale;
+      sa.stats_part = w.partial;
+      sa.stats = w.stats;
+      sa.nclear = qer_trees(h.n_frames).ints;
+      const int cus = device_cu_count();
+      for (int pass = 1; pass <= 2; ++pass) {
+        for (int q0 = 0; q0 < h.n_q; q0 += 64) {
+          sa.q0 = q0;
+          sa.n_q = std::min(64, h.n_q - q0);
+          sa.accumulate = pass == 2 && q0 > 0;
+          sa.clear = (pass == 2 && q0 == 0 && fused_tail) ? w.done : nullptr;
+          sa.scale = 1.0f / (float)h.H_q;  // pass 2: the head mean
+          const int NB = (sa.n_q + 15) / 16;
+          const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, cus, false);
+          sa.nseg = L.nseg;
+          sa.ksteps = L.ksteps;
+          sa.S = L.S;
+          sa.lgS = L.lgS;
+          sa.nphase = L.nphase;
+          sa.nwg = L.nwg;
+          sa.split_u4 = L.split_u4;
+          sa.rounds = (int32_t)soft_rounds(L, h.n_vis);
+          sa.nparts = (int32_t)(p.soft_nwg * kLdsWaves * p.soft_rounds);
+          const int mode = pass == 1 ? kModeSoftStats : kModeSoftProb;
+          const size_t lds = soft_lds(L, mode, h.H_q, sa.n_q, sa.G, L.nseg);
+          if (pass == 1)
+            rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftStats>(sa, L, NB, s, lds)
+                      : launch_lds<float, 1, kModeSoftStats>(sa, L, NB, s, lds);
+          else
+            rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftProb>(sa, L, NB, s, lds)
+                      : launch_lds<float, 1, kModeSoftProb>(sa, L, NB, s, lds);
+          if (rc) return rc;
+        }
+        if (pass == 1) {
+          const int32_t rows = h.H_q * h.n_q;
+          rc = launch("qer_soft_merge", qer_soft_merge_blocked_kernel, dim3((unsigned)ceil_div(rows, 16)),
+                      dim3(1024), 0, s, (const float2*)w.partial, p.soft_nwg * kLdsWaves * p.soft_rounds, rows,
+                      w.stats);
+          if (rc) return rc;
+        }
       }
     } else {
       SoftArgs sa;
@@ -1242,8 +1570,8 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
         rc = bf16 ? launch_soft<bf16_t>(sa, NB, p.nblk_soft, 1, s) : launch_soft<float>(sa, NB, p.nblk_soft, 1, s);
         if (rc) return rc;
       }
-      rc = launch("qer_soft_merge", qer_soft_merge_kernel, dim3((unsigned)ceil_div(rows, 256)), dim3(256),
-                  0, s, (const float2*)w.partial, p.nblk_soft, rows, w.stats);
+      rc = launch("qer_soft_merge", qer_soft_merge_kernel, dim3((unsigned)ceil_div(rows, 4)), dim3(256), 0, s,
+                  (const float2*)w.partial, p.nblk_soft, (int64_t)rows, (int64_t)1, rows, w.stats);
       if (rc) return rc;
       for (int q0 = 0; q0 < h.n_q; q0 += 64) {
         sa.q0 = q0;

@@ -74,6 +74,27 @@ def test_softmax_mode(dtype, n_q, H_q, H_kv, d):
     run_case(Q, K, offs, H_q, H_kv, d, 3, mode=B.SOFTMAX, dtype=dtype)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_q,H_q,H_kv,d,n_tok", [
+    (32, 28, 28, 128, 3001),   # the 1 fps stream's heads, ragged last tile
+    (48, 28, 4, 128, 2000),    # the high-res heads: seven query heads per key head
+    (70, 4, 4, 64, 1500),      # two query chunks (> 64 rows)
+    (16, 2, 1, 64, 65600),     # > 4096 tiles: two rounds in some workgroups, one in others
+])
+def test_softmax_through_score_kernel(dtype, n_q, H_q, H_kv, d, n_tok):
+    """SOFTMAX mode where every head is whole 128-byte segments of a key row:
+    both passes run in the LDS-staged score kernel (per-head statistics per
+    wave, merged, then the head mean of the probabilities)."""
+    per = max(1, n_tok // 9)
+    tokens = [per] * 8 + [n_tok - 8 * per]
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(n_q * 31 + H_q + n_tok, n_q, int(offs[-1]), H_q, H_kv, d, dtype)
+    w, idx, ref = run_case(Q, K, offs, H_q, H_kv, d, 4, mode=B.SOFTMAX, dtype=dtype)
+    w2, idx2 = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs.astype(np.int32)), 4, score_mode=B.SOFTMAX)
+    torch.cuda.synchronize()
+    assert np.array_equal(w, w2.cpu().numpy()), "SOFTMAX scores differ between two calls"
+
+
 def test_explicit_scale():
     offs = synth.frame_offsets([16] * 6)
     Q, K = synth.random_qk(5, 16, 96, 4, 4, 32, "bf16")
