@@ -365,7 +365,8 @@ def profiled_kernels(torch, B, fn, reps: int) -> dict:
     out = {}
     # names are matched as substrings: these are the kernels of the paths used
     for name in ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select", "qer_fold", "qer_score",
-                 "qer_frame_mean", "qer_topk", "attn_qer", "attn_merge"):
+                 "qer_soft_stats", "qer_soft_merge", "qer_soft_score", "qer_frame_mean", "qer_topk", "attn_qer",
+                 "attn_merge"):
         ms, cnt = B.cofie_profiler_read(name)
         if cnt:
             out[name] = round(1e3 * ms / cnt, 2)
@@ -553,6 +554,24 @@ def qer_single(torch, B, oracle, synth, wl, cfg, probe, copy_probe):
     fig = qer_figures(1, wl.n_frames, us, K.nbytes + Q.nbytes, kern["qer_score"], flops, flops_head, kern,
                       cpu_s, probe)
 
+    # SOFTMAX mode on the same inputs: two passes over K (statistics, then
+    # probabilities), their merge, the frame means and the top-k
+    sdesc = B.qer_desc(wl.n_q, K.shape[0], wl.n_frames, wl.H_q, wl.H_kv, wl.d, dtype=B.BF16 if bf16 else B.F32,
+                       score_mode=B.SOFTMAX)
+    sws = torch.empty(B.qer_workspace_bytes(sdesc, wl.k_top), dtype=torch.uint8, device="cuda")
+
+    def scall(i):
+        B.cofie_qer_rank(Qd, Kc[i % len(Kc)], offs_d, wl.k_top, out_scores=w_out, out_idx=idx, workspace=sws,
+                         score_mode=B.SOFTMAX)
+
+    sus = median_call_us(torch, scall, 20)
+    skern = profiled_kernels(torch, B, scall, 20)
+    passes_us = skern.get("qer_soft_stats", 0.0) + skern.get("qer_soft_score", 0.0)
+    fig["softmax"] = {"us_per_call": round(sus, 2), "kernels_us": skern,
+                      "passes_GBps": round(2 * K.nbytes / (passes_us * 1e-6) / 1e9, 1),
+                      "passes_frac_hbm": round(2 * K.nbytes / (passes_us * 1e-6) / 8e12, 4),
+                      "per_head_TFLOPs": round(2 * flops_head / (passes_us * 1e-6) / 1e12, 1)}
+
     cap = K.shape[0]
     dst = torch.empty_like(Kc[0])
     goffs = torch.empty(wl.k_top + 1, dtype=torch.int32, device="cuda")
@@ -736,6 +755,20 @@ def write_report(args, rows, probe):
                      f"{q['candidates_per_s']:,.0f} | {q['score_GBps']:.0f} | {100 * q['score_frac_hbm']:.1f} | "
                      f"{100 * q['score_frac_read_probe']:.1f} | {100 * q['mfma_util_computed']:.2f} % | "
                      f"{q['per_head_TFLOPs']:.1f} | {q['oracle_s']:.2f} |")
+    soft = [r for r in rows if r["qer"].get("softmax")]
+    if soft:
+        lines += ["", "SOFTMAX mode (same inputs; per-head row softmax over the visual keys, head mean, then "
+                  "Eq. 7): two passes over K.  GB/s counts 2·K over the two pass kernels' time; per-head TFLOP/s "
+                  "counts 2·2·n_q·n_vis·H_q·d over the same time.", "",
+                  "| workload | µs per call | pass 1 µs | merge µs | pass 2 µs | frame mean + top-k µs | "
+                  "passes GB/s | % of 8 TB/s | per-head TFLOP/s |", "|---|---|---|---|---|---|---|---|---|"]
+        for r in soft:
+            sm = r["qer"]["softmax"]
+            k = sm["kernels_us"]
+            lines.append(f"| {r['workload']} | {sm['us_per_call']:.1f} | {k.get('qer_soft_stats', 0):.1f} | "
+                         f"{k.get('qer_soft_merge', 0):.1f} | {k.get('qer_soft_score', 0):.1f} | "
+                         f"{k.get('qer_frame_mean', 0) + k.get('qer_topk', 0):.1f} | {sm['passes_GBps']:.0f} | "
+                         f"{100 * sm['passes_frac_hbm']:.1f} | {sm['per_head_TFLOPs']:.1f} |")
     for r in rows:
         b = r["qer"].get("batched")
         if b:
