@@ -136,6 +136,7 @@ struct ScoreLdsArgs {
 constexpr int kModeLogit = 0;     // Eq. 6-7: m_j = max_i a_ij
 constexpr int kModeSoftStats = 1; // SOFTMAX pass 1: per-head row statistics
 constexpr int kModeSoftProb = 2;  // SOFTMAX pass 2: m_j = max_i mean_h P^h_ij
+constexpr int kModeGqa = 4;       // flag: grouped query heads read their key head through a segment map
 
 constexpr int kLdsWaves = 8;
 constexpr int kLdsThreads = kLdsWaves * 64;
@@ -206,12 +207,14 @@ __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 template <typename T, int MB, int NB, int P, int NS, int MODE>
 __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) {
   using M = Mma<T>;
+  constexpr int BASE = MODE & 3;  // kModeLogit, kModeSoftStats or kModeSoftProb
+  constexpr bool GQA = (MODE & kModeGqa) != 0;
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
   // (SOFTMAX pass 1 with three or four query blocks and one tile per wave
   // halves the host's batch, which would spill: S stays a multiple of it)
-  constexpr int U = lds_batch(MB, P * NB, R, NS) / (MODE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
+  constexpr int U = lds_batch(MB, P * NB, R, NS) / (BASE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
   constexpr int FPS = P * NB;   // fragments per virtual step
   constexpr int kQRegs = lds_q_regs(FPS, NS);
   constexpr int kPhaseU4 = kQRegs * kLdsThreads;
@@ -220,7 +223,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   static_assert(U % VPS == 0, "batches hold whole segments");
   static_assert(NS == 1 || NS == 2 || NS == 4, "1, 2 or 4 slices");
   static_assert(NS == 1 || MB == 1, "split contractions take one tile per wave");
-  static_assert(MODE == kModeLogit || (NS == 1 && P == 1), "SOFTMAX passes: one query term, no split");
+  static_assert(BASE == kModeLogit || (NS == 1 && P == 1), "SOFTMAX passes: one query term, no split");
+  static_assert(!GQA || BASE != kModeLogit, "the segment map is for the SOFTMAX passes");
   // [2][kPhaseU4]: [NS][S][P][NB][64] each; with NS > 1 followed by the
   // slice accumulators [NS - 1][TW][MB][NB][4][64] floats
   extern __shared__ uint4 qs[];
@@ -262,11 +266,11 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   // key segment of every contraction segment.  The first barrier of the round
   // loop publishes them.
   float2* st_sh = reinterpret_cast<float2*>(qs + (a.nphase > 1 ? 2 : 1) * kPhaseU4);
-  int32_t* seg_map = reinterpret_cast<int32_t*>(st_sh + (MODE == kModeSoftProb ? a.H * a.n_q : 0));
-  if constexpr (MODE != kModeLogit) {
-    if (a.G > 1)
+  int32_t* seg_map = reinterpret_cast<int32_t*>(st_sh + (BASE == kModeSoftProb ? a.H * a.n_q : 0));
+  if constexpr (BASE != kModeLogit) {
+    if constexpr (GQA)
       for (int v = tid; v < a.nseg; v += kLdsThreads) seg_map[v] = (v / a.sph / a.G) * a.sph + v % a.sph;
-    if constexpr (MODE == kModeSoftProb)
+    if constexpr (BASE == kModeSoftProb)
       for (int i = tid; i < a.H * a.n_q; i += kLdsThreads) {
         const int hh = i / a.n_q, q = i - hh * a.n_q;
         const float2 st = a.stats[(int64_t)hh * a.nq_total + a.q0 + q];
@@ -361,7 +365,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       for (int nb = 0; nb < NB; ++nb) prob[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     int head = 0, head_seg = 0;
     auto head_close = [&](int hh) __attribute__((always_inline)) {
-      if constexpr (MODE == kModeSoftStats) {
+      if constexpr (BASE == kModeSoftStats) {
         // (max, sum of exp(s - max)) over this wave's valid tokens, per query
         // row; a wave without tokens writes (-inf, 0)
         const int64_t slot = ((int64_t)blockIdx.x * kLdsWaves + wave) * a.rounds + (rb - t_begin) / (TW * MB);
@@ -392,7 +396,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             a.stats_part[((row >> 4) * a.nparts + slot) * 16 + (row & 15)] = make_float2(mx * a.soft_scale, z);
           }
         }
-      } else if constexpr (MODE == kModeSoftProb) {
+      } else if constexpr (BASE == kModeSoftProb) {
         const float2* sth = st_sh + hh * a.n_q;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
@@ -415,9 +419,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
       for (int h = 0; h < U / VPS; ++h) {
         int seg = min(ms / VPS + h, a.nseg - 1);
-        if constexpr (MODE != kModeLogit) {
-          if (a.G > 1) seg = seg_map[seg];
-        }
+        if constexpr (GQA) seg = seg_map[seg];
 #pragma unroll
         for (int q = 0; q < VPS; ++q)
 #pragma unroll
@@ -442,8 +444,23 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     // one batch: prefetch the next batch into `nxt`, multiply `cur`, and at a
     // phase end publish the next phase's fragments
     int ph = 0;
+    // SOFTMAX with grouped heads: `nxt` holds the batch two before the one it
+    // is about to receive; when both read the same key segments (consecutive
+    // query heads of one key head), the keys are already in place
+    auto keys_in_place = [&](int X) __attribute__((always_inline)) {
+      if constexpr (!GQA) {
+        return false;
+      } else {
+        if (X < 2 * U) return false;
+        bool same = true;
+#pragma unroll
+        for (int h = 0; h < U / VPS; ++h)
+          same = same && seg_map[min(X / VPS + h, a.nseg - 1)] == seg_map[min((X - 2 * U) / VPS + h, a.nseg - 1)];
+        return same;
+      }
+    };
     auto batch = [&](int ms, const uint4 (&cur)[U][MB], uint4 (&nxt)[U][MB], bool guard) __attribute__((always_inline)) {
-      k_load(nxt, ms + U);
+      if (!keys_in_place(ms + U)) k_load(nxt, ms + U);
       if (pending && ms > ph * a.S) {
         q_store(ph + 1, qr);
         pending = false;
@@ -495,7 +512,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
                 for (int j = 0; j < MB; ++j) M::mac(acc[j][nb], fk[j], qf[p * NB + nb]);
           }
-          if constexpr (MODE != kModeLogit) {
+          if constexpr (BASE != kModeLogit) {
             if (++head_seg == a.sph) {
               head_close(head);
               ++head;
@@ -584,8 +601,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             for (int r = 0; r < 4; ++r) acc[j][nb][r] += red[red_at(sl, j, nb, r)];
     }
 
-    if constexpr (MODE == kModeSoftStats) continue;  // the statistics are written
-    if constexpr (MODE == kModeSoftProb) {
+    if constexpr (BASE == kModeSoftStats) continue;  // the statistics are written
+    if constexpr (BASE == kModeSoftProb) {
 #pragma unroll
       for (int j = 0; j < MB; ++j)
 #pragma unroll
@@ -643,7 +660,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       }
     }
   }
-  if constexpr (MODE == kModeSoftStats) {
+  if constexpr (BASE == kModeSoftStats) {
     // the rounds this workgroup does not run leave empty statistics (a zero
     // sum), which the merge skips
     const int nr = (t_end - t_begin + TW * MB - 1) / (TW * MB);
@@ -1342,7 +1359,8 @@ int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, size_t lds, hipStream
   auto k = qer_score_kernel<T, MB, NB, P, NS, MODE>;
   int rc = allow_lds(k, lds);
   if (rc) return rc;
-  const char* name = MODE == kModeLogit ? "qer_score" : (MODE == kModeSoftStats ? "qer_soft_stats" : "qer_soft_score");
+  const int base = MODE & 3;
+  const char* name = base == kModeLogit ? "qer_score" : (base == kModeSoftStats ? "qer_soft_stats" : "qer_soft_score");
   return launch(name, k, dim3((unsigned)L.nwg), dim3(kLdsThreads), lds, s, sa);
 }
 
@@ -1533,12 +1551,19 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
           sa.nparts = (int32_t)(p.soft_nwg * kLdsWaves * p.soft_rounds);
           const int mode = pass == 1 ? kModeSoftStats : kModeSoftProb;
           const size_t lds = soft_lds(L, mode, h.H_q, sa.n_q, sa.G, L.nseg);
-          if (pass == 1)
+          const bool gqa = sa.G > 1;
+          if (pass == 1 && !gqa)
             rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftStats>(sa, L, NB, s, lds)
                       : launch_lds<float, 1, kModeSoftStats>(sa, L, NB, s, lds);
-          else
+          else if (pass == 1)
+            rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftStats | kModeGqa>(sa, L, NB, s, lds)
+                      : launch_lds<float, 1, kModeSoftStats | kModeGqa>(sa, L, NB, s, lds);
+          else if (!gqa)
             rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftProb>(sa, L, NB, s, lds)
                       : launch_lds<float, 1, kModeSoftProb>(sa, L, NB, s, lds);
+          else
+            rc = bf16 ? launch_lds<bf16_t, 1, kModeSoftProb | kModeGqa>(sa, L, NB, s, lds)
+                      : launch_lds<float, 1, kModeSoftProb | kModeGqa>(sa, L, NB, s, lds);
           if (rc) return rc;
         }
         if (pass == 1) {
