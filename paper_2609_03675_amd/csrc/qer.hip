@@ -261,6 +261,10 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   if (blockIdx.x == 0 && a.clear)
     for (int i = tid; i < a.nclear; i += kLdsThreads) a.clear[i] = 0;
 
+  // pass 1: exp(scale acc - m) = exp2(acc c2 - m log2 e), one FMA and
+  // v_exp_f32 (pass 2 keeps __expf: the FMA form made the grouped-head,
+  // two-tile, 48-row variant spill)
+  const float c2 = a.soft_scale * 1.44269504088896341f;
   // SOFTMAX passes: past the phase buffers, pass 2's row statistics of this
   // query chunk ([H][n_q]: max, 1 / sum of exp) and, for grouped heads, the
   // key segment of every contraction segment.  The first barrier of the round
@@ -381,13 +385,14 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
               if (j < nmb && tok < a.n_vis) mx = fmaxf(mx, acc[j][nb][r]);
             }
           mx = max_x32(max_x16(mx));
+          const float mc = mx * c2;
           float z = 0.f;
 #pragma unroll
           for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
-              if (j < nmb && tok < a.n_vis) z += __expf((acc[j][nb][r] - mx) * a.soft_scale);
+              if (j < nmb && tok < a.n_vis) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
             }
           z = sum_x32(sum_x16(z));
           const int q = nb * 16 + r16;
