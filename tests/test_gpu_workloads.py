@@ -92,6 +92,23 @@ def test_qer_full_size(cfg):
     check_topk(idx.cpu().numpy(), ref, wl.k_top)
 
 
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_qer_softmax_full_size(cfg):
+    """SOFTMAX mode at the workloads' full sizes: both passes through the
+    score kernel (grouped heads at the high-res workload)."""
+    wl = synth.WORKLOADS[cfg]
+    Q, K, offs = synth.qer_inputs(cfg)
+    print(f"workload {cfg}: SOFTMAX n_q={wl.n_q} n_vis={K.shape[0]} heads {wl.H_q}/{wl.H_kv}", flush=True)
+    w, idx = B.cofie_qer_rank(bf16_dev(Q), bf16_dev(K), to_dev(offs), wl.k_top, score_mode=B.SOFTMAX)
+    torch.cuda.synchronize()
+    ref = oracle.qer_scores(Q, K, offs, wl.H_q, wl.H_kv, wl.d, B.SOFTMAX)
+    w = w.cpu().numpy()
+    err = rel_err(w, ref)
+    print(f"workload {cfg}: SOFTMAX max rel err {err:.3e}", flush=True)
+    assert err <= 2e-2
+    check_topk(idx.cpu().numpy(), ref, wl.k_top)
+
+
 @pytest.mark.parametrize("streams", [(0, 1, 2, 3), (17, 31)])
 def test_qer_multistream_queries(streams):
     """Each stream's queries rank that stream's NGFF candidates up to the query
