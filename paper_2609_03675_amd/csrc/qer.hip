@@ -368,6 +368,18 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) prob[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     int head = 0, head_seg = 0;
+    // pass 1: bit 4 j + r set when this lane's accumulator element (tile j,
+    // token 4 g4 + r) is a real token
+    uint32_t vmask = 0;
+    if constexpr (BASE == kModeSoftStats) {
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
+          vmask |= (j < nmb && tok < a.n_vis) ? 1u << (4 * j + r) : 0u;
+        }
+    }
     auto head_close = [&](int hh) __attribute__((always_inline)) {
       if constexpr (BASE == kModeSoftStats) {
         // (max, sum of exp(s - max)) over this wave's valid tokens, per query
@@ -380,20 +392,16 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
           for (int j = 0; j < MB; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
-              if (j < nmb && tok < a.n_vis) mx = fmaxf(mx, acc[j][nb][r]);
-            }
+            for (int r = 0; r < 4; ++r)
+              if ((vmask >> (4 * j + r)) & 1u) mx = fmaxf(mx, acc[j][nb][r]);
           mx = max_x32(max_x16(mx));
           const float mc = mx * c2;
           float z = 0.f;
 #pragma unroll
           for (int j = 0; j < MB; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
-              if (j < nmb && tok < a.n_vis) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
-            }
+            for (int r = 0; r < 4; ++r)
+              if ((vmask >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
           z = sum_x32(sum_x16(z));
           const int q = nb * 16 + r16;
           if (g4 == 0 && q < a.n_q) {
