@@ -1562,6 +1562,9 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
           sa.split_u4 = L.split_u4;
           sa.rounds = (int32_t)soft_rounds(L, h.n_vis);
           sa.nparts = (int32_t)(p.soft_nwg * kLdsWaves * p.soft_rounds);
+          if (L.nwg != p.soft_nwg || sa.rounds != p.soft_rounds)  // the scratch was sized for that plan
+            return set_error(COFIE_EHIP, "SOFTMAX plan mismatch (%d x %d against %lld x %lld)", L.nwg, sa.rounds,
+                             (long long)p.soft_nwg, (long long)p.soft_rounds);
           const int mode = pass == 1 ? kModeSoftStats : kModeSoftProb;
           const size_t lds = soft_lds(L, mode, h.H_q, sa.n_q, sa.G, L.nseg);
           const bool gqa = sa.G > 1;

@@ -182,6 +182,20 @@ def test_stream_checkpoint_validation(L):
     assert L.cofie_ngff_stream_restore(None, buf, 64, None) == B.COFIE_EINVAL
 
 
+def test_softmax_workspace_holds_per_wave_statistics(L):
+    """SOFTMAX with heads of whole 128-byte key segments runs both passes in
+    the score kernel; its workspace holds one (max, sum) pair per wave, round
+    and (head, query row), rows in blocks of 16.  Without a GPU the planner
+    takes 256 CUs: the 1 fps stream's 2048 tiles give 256 workgroups x 8 waves
+    in one round, 28 x 32 rows."""
+    soft = B.qer_workspace_bytes(B.qer_desc(32, 32768, 128, 28, 28, 128, score_mode=B.SOFTMAX), 16)
+    logit = B.qer_workspace_bytes(B.qer_desc(32, 32768, 128, 28, 28, 128), 16)
+    assert soft >= 256 * 8 * (28 * 32) * 8 > logit > 0
+    # heads of 32 bf16 elements take the per-head kernels: per 32-token block statistics
+    small = B.qer_workspace_bytes(B.qer_desc(32, 32768, 128, 28, 28, 32, score_mode=B.SOFTMAX), 16)
+    assert small >= (32768 // 32) * 28 * 32 * 8
+
+
 def test_batched_qer_validation(L):
     d = B.qer_desc(16, 64, 4, 2, 2, 32)
     nf = (ctypes.c_int32 * 2)(4, 5)   # 5 > n_frames
