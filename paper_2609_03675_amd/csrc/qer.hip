@@ -97,7 +97,7 @@ struct ScoreLdsArgs {
   const uint8_t* K;   // [n_vis][Lc] elements
   const uint8_t* Qp;  // [P][nq_total][Lc] elements
   int32_t n_vis;
-  int32_t n_q;        // query rows in this chunk (<= 64)
+  int32_t n_q;        // query rows in this chunk (<= 64; <= 128 with eight blocks)
   int32_t q0;
   int32_t nq_total;
   int32_t Lc;
@@ -1379,6 +1379,11 @@ int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, size_t lds, hipStream
 
 template <typename T, int MB, int P, int NS, int MODE>
 int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, size_t lds, hipStream_t s) {
+  // 128 query rows in one pass: LOGIT, one query term, one tile per wave
+  // (two spill)
+  if constexpr (MB == 1 && P == 1 && MODE == kModeLogit) {
+    if (NB == 8) return launch_lds_t<T, 1, 8, 1, NS, MODE>(sa, L, lds, s);
+  }
   switch (NB) {
     case 1: return launch_lds_t<T, MB, 1, P, NS, MODE>(sa, L, lds, s);
     case 2: return launch_lds_t<T, MB, 2, P, NS, MODE>(sa, L, lds, s);
@@ -1500,12 +1505,20 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.m = w.m;
       sa.nclear = n_queries * qer_trees(h.n_frames).ints;
       const int cus = device_cu_count();
-      for (int q0 = 0; q0 < R; q0 += 64) {
+      // query rows per pass over K: 64, or 128 (eight 16-row blocks) where the
+      // plan gives one tile per wave, no contraction split (its LDS would not
+      // fit; the split, which decides the summation order, stays a function of
+      // the keys alone) and one query term, so that K is read once for up to
+      // 128 rows (several queries of a stream)
+      const LdsPlan probe = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P, 4, cus, true);
+      const bool wide = p.P == 1 && R > 64 && probe.MB == 1 && probe.NS == 1;
+      const int chunk = wide ? 128 : 64;
+      for (int q0 = 0; q0 < R; q0 += chunk) {
         sa.clear = (q0 == 0 && fused_tail) ? w.done : nullptr;
         sa.q0 = q0;
-        sa.n_q = std::min(64, R - q0);
+        sa.n_q = std::min(chunk, R - q0);
         sa.accumulate = q0 > 0;
-        const int NB = (sa.n_q + 15) / 16;
+        const int NB = sa.n_q > 64 ? 8 : (sa.n_q + 15) / 16;
         const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, p.P, p.P * NB, cus, true);
         sa.nseg = L.nseg;
         sa.ksteps = L.ksteps;

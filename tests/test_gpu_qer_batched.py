@@ -80,10 +80,20 @@ def test_batched_against_oracle(dtype, n_queries, n_q, H_q, H_kv, d, n_frames):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_batched_wide_pass(dtype):
+    """128 query rows (four queries of 32) over more tiles than a split would
+    take: the score kernel multiplies all of them in one pass over K."""
+    Q, K, offs, nf = make_case(11, 4, 32, 8, 8, 64, 48, dtype, max_tokens=900)
+    assert K.shape[0] > 16 * 1024
+    run_batched(Q, K, offs, nf, 8, 8, 64, 10, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n_q,H_q,H_kv,max_tokens", [
     (48, 28, 4, 24),     # GQA fold (three query terms)
     (32, 28, 28, 24),    # multi-stream heads: few tiles, contraction split 4 ways
     (32, 8, 8, 300),     # 512-long contraction split 2 ways (~590 tiles)
+    (32, 8, 8, 700),     # ~1400 tiles, no split: 160 rows as one 128-row pass and one of 32
 ])
 def test_batched_equals_single_query_calls(dtype, n_q, H_q, H_kv, max_tokens):
     """Per-query calls over the same keys add in the same order as the
