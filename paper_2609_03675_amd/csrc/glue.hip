@@ -115,19 +115,37 @@ __global__ __launch_bounds__(kGlueThreads) void gather_offsets_kernel(const int3
 }
 
 // Copy of the selected frames' rows: blockIdx.y (strided) picks the frame,
-// blockIdx.x (strided) a slice of its bytes.  V = bytes per lane access.
+// blockIdx.x (strided) a slice of its bytes.  V = bytes per lane access (16:
+// non-temporal, both sides are touched once).  With out_offs null each
+// workgroup sums the row counts of the frames before its own, and workgroup
+// (0, 0) writes the output offsets to offs_out, so no offsets kernel runs
+// first.
+typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
+
 template <int V>
 __global__ __launch_bounds__(256) void gather_copy_kernel(const uint8_t* src, int64_t n_rows, int64_t row_bytes,
                                                           const int32_t* offs, int32_t n_frames,
                                                           const int32_t* sel, int32_t k, uint8_t* dst,
                                                           int64_t capacity, const int32_t* out_offs,
-                                                          int32_t* out_rows) {
-  using T = typename std::conditional<V == 16, uint4, typename std::conditional<V == 4, uint32_t, uint8_t>::type>::type;
+                                                          int32_t* offs_out, int32_t* out_rows) {
+  using T = typename std::conditional<V == 16, u32x4v, typename std::conditional<V == 4, uint32_t, uint8_t>::type>::type;
   constexpr int U = 4;  // accesses in flight per lane
+  __shared__ int64_t wsum[4];
   for (int32_t i = blockIdx.y; i < k; i += gridDim.y) {
     int64_t lo, hi;
     frame_rows(offs, n_frames, n_rows, sel[i], &lo, &hi);
-    const int64_t o = out_offs[i];
+    int64_t o;
+    if (out_offs) {
+      o = out_offs[i];
+    } else {
+      int64_t part = 0;
+      for (int32_t j = threadIdx.x; j < i; j += blockDim.x) {
+        int64_t a, b;
+        frame_rows(offs, n_frames, n_rows, sel[j], &a, &b);
+        part += b - a;
+      }
+      (void)block_exscan64(part, &o, wsum);
+    }
     int64_t rows = hi - lo;
     const int64_t room = capacity - o;
     rows = rows < room ? rows : (room > 0 ? room : 0);
@@ -141,12 +159,16 @@ __global__ __launch_bounds__(256) void gather_copy_kernel(const uint8_t* src, in
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t e = e0 + u * step;
-        v[u] = s[e < nv ? e : 0];
+        if constexpr (V == 16) v[u] = __builtin_nontemporal_load(s + (e < nv ? e : 0));
+        else v[u] = s[e < nv ? e : 0];
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t e = e0 + u * step;
-        if (e < nv) d[e] = v[u];
+        if (e < nv) {
+          if constexpr (V == 16) __builtin_nontemporal_store(v[u], d + e);
+          else d[e] = v[u];
+        }
       }
     }
     if (out_rows) {
@@ -154,7 +176,28 @@ __global__ __launch_bounds__(256) void gather_copy_kernel(const uint8_t* src, in
         out_rows[o + r] = (int32_t)(lo + r);
     }
   }
+  if (!out_offs && blockIdx.x == 0 && blockIdx.y == 0) {
+    int64_t base = 0;
+    for (int32_t i0 = 0; i0 < k; i0 += blockDim.x) {
+      const int32_t i = i0 + threadIdx.x;
+      int64_t len = 0;
+      if (i < k) {
+        int64_t lo, hi;
+        frame_rows(offs, n_frames, n_rows, sel[i], &lo, &hi);
+        len = hi - lo;
+      }
+      int64_t total;
+      const int64_t ex = block_exscan64(len, &total, wsum);
+      if (i < k) offs_out[i + 1] = (int32_t)(base + ex + len);
+      base += total;
+    }
+    if (threadIdx.x == 0) offs_out[0] = 0;
+  }
 }
+
+// at most this many frames take the one-kernel gather (each workgroup sums
+// the row counts before its frame)
+constexpr int32_t kGatherFused = 4096;
 
 }  // namespace
 }  // namespace cofie
@@ -188,9 +231,13 @@ int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, cons
   if (k > 0 && n_rows > 0 && (!src || (dst_capacity_rows > 0 && !dst)))
     return set_error(COFIE_EINVAL, "src or dst is NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int rc = launch("glue_gather_offsets", gather_offsets_kernel, dim3(1), dim3(kGlueThreads), 0, s,
-                  frame_offsets, n_frames, n_rows, sel, k, out_offsets);
-  if (rc || k == 0 || n_rows == 0 || dst_capacity_rows == 0) return rc;
+  const bool fused = k > 0 && k <= kGatherFused && n_rows > 0 && dst_capacity_rows > 0;
+  if (!fused) {
+    int rc = launch("glue_gather_offsets", gather_offsets_kernel, dim3(1), dim3(kGlueThreads), 0, s,
+                    frame_offsets, n_frames, n_rows, sel, k, out_offsets);
+    if (rc || k == 0 || n_rows == 0 || dst_capacity_rows == 0) return rc;
+  }
+  const int32_t* offs_in = fused ? nullptr : out_offsets;
   const int cus = device_cu_count();
   const unsigned gy = (unsigned)std::min<int64_t>(k, 65535);
   const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, ceil_div(4 * cus, k)));
@@ -199,12 +246,12 @@ int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, cons
   uint8_t* dp = static_cast<uint8_t*>(dst);
   if (al % 16 == 0)
     return launch("glue_gather_copy", gather_copy_kernel<16>, dim3(gx, gy), dim3(256), 0, s, sp, n_rows, row_bytes,
-                  frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, (const int32_t*)out_offsets, out_rows);
+                  frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, offs_in, out_offsets, out_rows);
   if (al % 4 == 0)
     return launch("glue_gather_copy", gather_copy_kernel<4>, dim3(gx, gy), dim3(256), 0, s, sp, n_rows, row_bytes,
-                  frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, (const int32_t*)out_offsets, out_rows);
+                  frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, offs_in, out_offsets, out_rows);
   return launch("glue_gather_copy", gather_copy_kernel<1>, dim3(gx, gy), dim3(256), 0, s, sp, n_rows, row_bytes,
-                frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, (const int32_t*)out_offsets, out_rows);
+                frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, offs_in, out_offsets, out_rows);
 }
 
 }  // extern "C"

@@ -83,6 +83,21 @@ def test_gather_frames(row_shape, dtype):
         check_gather(src, offs, sel, cap)
 
 
+@pytest.mark.parametrize("k", [4096, 5000])
+def test_gather_many_frames(k):
+    """Up to 4096 selected frames one kernel copies them (each workgroup sums
+    the row counts before its frame); more take the offsets kernel first."""
+    rng = np.random.default_rng([2609, 3675, 92, k])
+    n_frames = 6000
+    sizes = rng.integers(0, 4, n_frames)
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    src = rng.integers(0, 30000, (int(offs[-1]), 8)).astype(np.int16)
+    sel = np.sort(rng.choice(n_frames, k, replace=False)).astype(np.int32)
+    print(f"gather {k} of {n_frames} frames, {src.shape[0]} rows", flush=True)
+    for cap in (src.shape[0], src.shape[0] // 3):
+        check_gather(src, offs, sel, cap)
+
+
 def test_gather_malformed_offsets_and_misaligned_rows():
     src = np.arange(40 * 6, dtype=np.uint8).reshape(40, 6)
     offs = np.array([-5, 3, 2, 60, 7, 7, 40], np.int32)
