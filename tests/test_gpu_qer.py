@@ -95,6 +95,22 @@ def test_softmax_through_score_kernel(dtype, n_q, H_q, H_kv, d, n_tok):
     assert np.array_equal(w, w2.cpu().numpy()), "SOFTMAX scores differ between two calls"
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_q,H_q,H_kv,d,tokens", [
+    (1, 2, 2, 64, [1]),               # one query row, one token
+    (17, 4, 2, 64, [0, 5, 0, 3]),     # grouped heads, empty frames, a ragged tile
+    (3, 1, 1, 128, [16, 16]),         # one head, whole tiles
+    (2, 6, 3, 64, [300, 0, 41]),      # several tiles per wave group
+])
+def test_softmax_score_kernel_edges(dtype, n_q, H_q, H_kv, d, tokens):
+    """Edge shapes of SOFTMAX through the score kernel (heads of whole
+    128-byte segments)."""
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(n_q * 13 + d + len(tokens), n_q, int(offs[-1]), H_q, H_kv, d, dtype)
+    for k in (0, 1, 3):
+        run_case(Q, K, offs, H_q, H_kv, d, k, mode=B.SOFTMAX, dtype=dtype)
+
+
 def test_explicit_scale():
     offs = synth.frame_offsets([16] * 6)
     Q, K = synth.random_qk(5, 16, 96, 4, 4, 32, "bf16")
