@@ -65,7 +65,7 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the evidence-selection path runs on a single MI355X)", file=sys.stderr)
         sys.exit(2)
 

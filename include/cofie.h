@@ -42,7 +42,7 @@ extern "C" {
 /* ---- status codes ------------------------------------------------------- */
 #define COFIE_OK 0
 #define COFIE_EINVAL (-1)       /* invalid argument (null pointer, bad size or enum) */
-#define COFIE_EUNSUPPORTED (-2) /* valid but outside what this build implements */
+#define COFIE_EUNSUPPORTED (-2) /* valid but outside what the library implements */
 #define COFIE_EHIP (-3)         /* a HIP runtime call or kernel launch failed */
 #define COFIE_ENOMEM (-4)       /* scratch allocation failed or workspace too small */
 
