@@ -9,10 +9,12 @@
 // the bf16 MFMA still multiplies exact operands.
 //
 // qer_score: one 8-wave workgroup per CU; each wave owns MB x 16 visual tokens
-//   and all (<= 64) query rows of one chunk, over the whole contraction.  K
-//   rows stream from HBM exactly once, in 128-byte row segments that a lane
-//   select and a DPP swap turn into MFMA operands; the query fragments are
-//   staged in LDS phase by phase.  The epilogue takes the max over query rows
+//   and all (<= 64, or 128 in eight blocks) query rows of one chunk, over the
+//   whole contraction, or over one of NS slices of it where tiles are too few
+//   to give every wave of the chip one (the slices' sums meet in LDS).  K rows
+//   stream from HBM exactly once, in 128-byte row segments that a lane select
+//   and a DPP swap turn into MFMA operands; the query fragments are staged in
+//   LDS phase by phase.  The epilogue takes the max over query rows
 //   (registers, then 16-lane shuffles) and writes m_j = scale * max_i S_ij:
 //   the text-by-vision matrix is never stored.
 // qer_frame_mean: one wave per frame, fp64 mean of m over V_f (Eq. 7); the
@@ -20,11 +22,15 @@
 //   ranks the frames by (score desc, frame asc) on order-preserving 32-bit
 //   keys (counting ranks, or a 4-pass radix select) and writes the top k in
 //   chronological order (Eq. 8).
-// qer_topk: the same selection as a kernel of its own (SOFTMAX mode, the
-//   fused attention path, cofie_topk).
+// qer_topk: the same selection as a kernel of its own (the SOFTMAX fallback
+//   kernels, the fused attention path, cofie_topk).
 // SOFTMAX mode: per-(head, query) row statistics over all visual keys, merged
-//   across workgroups, then a second pass forming the head mean of the
-//   normalised probabilities and its max over query rows.
+//   across waves and workgroups, then a second pass forming the head mean of
+//   the normalised probabilities and its max over query rows.  Where every
+//   head is whole 128-byte segments of a key row, both passes are qer_score
+//   with a per-head epilogue (the contraction runs over the query heads in
+//   order, grouped heads reading their key head through a segment map);
+//   other head sizes take per-head kernels of their own.
 #include <cmath>
 
 #include "common.h"
@@ -88,8 +94,8 @@ struct Mma<float> {
 // contraction tail shorter than a segment is read in plain MFMA shape.
 //
 // Query fragments.  The contraction is cut into phases of S virtual steps; a
-// phase's query fragments sit in LDS in MFMA operand order ([step][term]
-// [16-query block][lane], 16 bytes per lane, read by every wave with
+// phase's query fragments sit in LDS in MFMA operand order ([slice][step]
+// [term][16-query block][lane], 16 bytes per lane, read by every wave with
 // conflict-free 16-byte LDS loads), double buffered: the fragments of phase
 // i+1 are fetched into registers at the start of phase i and written to LDS
 // one batch later.
