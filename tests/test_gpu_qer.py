@@ -111,6 +111,25 @@ def test_softmax_score_kernel_edges(dtype, n_q, H_q, H_kv, d, tokens):
         run_case(Q, K, offs, H_q, H_kv, d, k, mode=B.SOFTMAX, dtype=dtype)
 
 
+@pytest.mark.parametrize("H_q,H_kv", [(4, 4), (8, 2)])
+def test_softmax_identical_keys_tie(H_q, H_kv):
+    """Identical keys: every probability is 1/n_vis in both passes of the
+    score kernel, so every frame scores the same bits and the top-k is the
+    lowest frame indices (Eq. 8's tie rule)."""
+    n_q, d = 20, 64
+    tokens = [7, 30, 1, 64, 12, 5]
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(4711, n_q, int(offs[-1]), H_q, H_kv, d, "bf16")
+    K[:] = K[0]
+    w, idx = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs.astype(np.int32)), 3, score_mode=B.SOFTMAX)
+    torch.cuda.synchronize()
+    w = w.cpu().numpy()
+    assert np.all(w.view(np.uint32) == w[0].view(np.uint32)), w
+    assert idx.cpu().tolist() == [0, 1, 2]
+    ref = oracle.qer_scores(Q, K, offs, H_q, H_kv, d, B.SOFTMAX)
+    assert rel_err(w, ref) <= TOL["bf16"]
+
+
 def test_explicit_scale():
     offs = synth.frame_offsets([16] * 6)
     Q, K = synth.random_qk(5, 16, 96, 4, 4, 32, "bf16")
