@@ -281,8 +281,12 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
  * of frame_offsets (host int32 [n_queries], each in [0, n_frames]) exactly as
  * cofie_qer_rank would: out_scores row g (device float [n_queries][n_frames])
  * holds its w_f (-inf past its prefix), out_idx row g (device int32
- * [n_queries][k_top]) its top-k.  With n_queries > 1: LOGIT mode and n_q a
- * multiple of 16, else EUNSUPPORTED.  Workspace: the descriptor's, of
+ * [n_queries][k_top]) its top-k.  With n_queries > 1: n_q a multiple of 16,
+ * and in SOFTMAX mode head rows of whole 128-byte key segments (d a multiple
+ * of 64 bf16 or 32 fp32 elements), else EUNSUPPORTED; query g's softmax then
+ * normalises over the keys of its own prefix, as a call given only those keys
+ * would (equal to rounding: the work split, which orders the sums, follows the
+ * key count).  Workspace: the descriptor's, of
  * cofie_qer_batched_workspace_bytes() bytes. */
 size_t cofie_qer_batched_workspace_bytes(const cofie_qer_desc* heads, int32_t n_queries, int32_t k_top);
 int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_offsets,

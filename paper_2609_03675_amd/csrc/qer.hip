@@ -137,6 +137,10 @@ struct ScoreLdsArgs {
   int32_t rounds;      // rounds per workgroup
   int32_t nparts;      // nwg * 8 * rounds
   const float2* stats; // pass 2: [H][nq_total] (max, sum of exp) over all keys
+  // pass 1 with several queries (group_rows > 0): query g's rows see only the
+  // keys of its first soft_nf[g] frames, [0, soft_offs[soft_nf[g]]); null: all
+  const int32_t* soft_offs;
+  const int32_t* soft_nf;
 };
 
 constexpr int kModeLogit = 0;     // Eq. 6-7: m_j = max_i a_ij
@@ -277,6 +281,22 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   // loop publishes them.
   float2* st_sh = reinterpret_cast<float2*>(qs + (a.nphase > 1 ? 2 : 1) * kPhaseU4);
   int32_t* seg_map = reinterpret_cast<int32_t*>(st_sh + (BASE == kModeSoftProb ? a.H * a.n_q : 0));
+  // pass 1: the keys each 16-row block's query sees (padding blocks none)
+  int64_t key_lim[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    key_lim[nb] = a.n_vis;
+    if constexpr (BASE == kModeSoftStats) {
+      if (a.soft_nf) {
+        int64_t l = 0;
+        if (nb * 16 < a.n_q) {
+          l = a.soft_offs[a.soft_nf[(a.q0 + nb * 16) / a.group_rows]];
+          l = l < 0 ? 0 : (l > a.n_vis ? a.n_vis : l);
+        }
+        key_lim[nb] = l;
+      }
+    }
+  }
   if constexpr (BASE != kModeLogit) {
     if constexpr (GQA)
       for (int v = tid; v < a.nseg; v += kLdsThreads) seg_map[v] = (v / a.sph / a.G) * a.sph + v % a.sph;
@@ -316,7 +336,9 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       const int sl = (e >> lgC) & (NS - 1);
       const int col = sl * a.split_u4 + (ph << lgC) + (e & ((1 << lgC) - 1));
       const bool ok = f < FPS && q < a.n_q && col * M::EPL < a.Lc;
-      const int64_t grow = (int64_t)p * a.nq_total + a.q0 + (ok ? q : 0);
+      // slots past the P NB fragments (f >= FPS, so p >= P) and masked rows
+      // load row q0 of term 0, which every chunk has
+      const int64_t grow = ok ? (int64_t)p * a.nq_total + a.q0 + q : (int64_t)a.q0;
       qr[i] = Qq[grow * row_u4 + (ok ? col : 0)];
       qmask |= ok ? 1u << i : 0u;
     }
@@ -374,16 +396,20 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) prob[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     int head = 0, head_seg = 0;
-    // pass 1: bit 4 j + r set when this lane's accumulator element (tile j,
-    // token 4 g4 + r) is a real token
-    uint32_t vmask = 0;
+    // pass 1: bit 4 j + r of vmask[nb] set when this lane's accumulator
+    // element (tile j, token 4 g4 + r) is a key that block nb's query sees
+    uint32_t vmask[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) vmask[nb] = 0;
     if constexpr (BASE == kModeSoftStats) {
 #pragma unroll
       for (int j = 0; j < MB; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t tok = (int64_t)(rb + tw + TW * j) * 16 + g4 * 4 + r;
-          vmask |= (j < nmb && tok < a.n_vis) ? 1u << (4 * j + r) : 0u;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            vmask[nb] |= (j < nmb && tok < key_lim[nb]) ? 1u << (4 * j + r) : 0u;
         }
     }
     auto head_close = [&](int hh) __attribute__((always_inline)) {
@@ -399,7 +425,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
           for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if ((vmask >> (4 * j + r)) & 1u) mx = fmaxf(mx, acc[j][nb][r]);
+              if ((vmask[nb] >> (4 * j + r)) & 1u) mx = fmaxf(mx, acc[j][nb][r]);
           mx = max_x32(max_x16(mx));
           const float mc = mx * c2;
           float z = 0.f;
@@ -407,7 +433,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
           for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if ((vmask >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
+              if ((vmask[nb] >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
           z = sum_x32(sum_x16(z));
           const int q = nb * 16 + r16;
           if (g4 == 0 && q < a.n_q) {
@@ -1265,10 +1291,10 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   if (h.score_mode == COFIE_SCORE_SOFTMAX) {
     // the score kernel's statistics: rows (heads x query rows) in whole blocks
     // of 16, per wave and round
-    const size_t rows16 = (size_t)ceil_div((int64_t)h.H_q * h.n_q, 16) * 16;
+    const size_t rows16 = (size_t)ceil_div((int64_t)h.H_q * h.n_q * n_queries, 16) * 16;
     w.partial = p.soft_fast ? ar.take<float2>((size_t)p.soft_nwg * kLdsWaves * p.soft_rounds * rows16)
                             : ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
-    w.stats = ar.take<float2>((size_t)h.H_q * h.n_q);
+    w.stats = ar.take<float2>((size_t)h.H_q * h.n_q * n_queries);
   } else {
     w.partial = nullptr;
     w.stats = nullptr;
@@ -1276,16 +1302,17 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   return w;
 }
 
-void plan_soft(const cofie_qer_desc& h, QerPlan& p);
+void plan_soft(const cofie_qer_desc& h, int32_t n_queries, QerPlan& p);
 
-QerPlan plan_qer(const cofie_qer_desc& h) {
+// n_queries: queries of h.n_q rows each sharing K (cofie_qer_rank_batched)
+QerPlan plan_qer(const cofie_qer_desc& h, int32_t n_queries = 1) {
   QerPlan p;
   p.esize = h.dtype == COFIE_BF16 ? 2 : 4;
   p.fold = h.score_mode == COFIE_SCORE_LOGIT && h.H_q != h.H_kv;
   p.Lc = (int64_t)(p.fold ? h.H_kv : h.H_q) * h.d;  // MHA: H_q == H_kv
   p.P = (p.fold && h.dtype == COFIE_BF16) ? 3 : 1;
   p.nblk_soft = (h.n_vis + kMB * 16 - 1) / (kMB * 16);
-  plan_soft(h, p);
+  plan_soft(h, n_queries, p);
   return p;
 }
 
@@ -1428,13 +1455,13 @@ constexpr size_t kLdsMax = 160 * 1024;
 // Whether SOFTMAX takes the score kernel (each head whole 128-byte segments
 // of a key row, the widest query chunk's LDS within the CU's), and its
 // pass-1 statistics count.
-void plan_soft(const cofie_qer_desc& h, QerPlan& p) {
+void plan_soft(const cofie_qer_desc& h, int32_t n_queries, QerPlan& p) {
   p.soft_fast = false;
   p.soft_nwg = p.soft_rounds = 0;
   if (h.score_mode != COFIE_SCORE_SOFTMAX || h.n_vis <= 0) return;
   const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)p.esize;
   if (h.d % seg_el != 0) return;
-  const int nq = std::min(64, h.n_q), NB = (nq + 15) / 16;
+  const int nq = (int)std::min<int64_t>(64, (int64_t)h.n_q * n_queries), NB = (nq + 15) / 16;
   const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, device_cu_count(), false);
   if (soft_lds(L, kModeSoftProb, h.H_q, nq, h.H_q / h.H_kv, p.Lc / seg_el) > kLdsMax) return;
   p.soft_fast = true;
@@ -1467,7 +1494,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
   int rc;
   const bool multi = n_queries > 1;
   const int32_t R = n_queries * h.n_q;  // query rows
-  const QerPlan p = plan_qer(h);
+  const QerPlan p = plan_qer(h, n_queries);
   Arena plan;
   carve_qer(plan, h, p, n_queries);
   Scratch scratch;
@@ -1547,8 +1574,10 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.K = static_cast<const uint8_t*>(K);
       sa.Qp = static_cast<const uint8_t*>(Q);
       sa.n_vis = h.n_vis;
-      sa.nq_total = h.n_q;
-      sa.group_rows = 0;
+      sa.nq_total = R;  // several queries: their rows stacked, statistics per row
+      sa.group_rows = multi ? h.n_q : 0;
+      sa.soft_offs = multi ? frame_offsets : nullptr;
+      sa.soft_nf = multi ? w.nf : nullptr;
       sa.m_stride = h.n_vis;
       sa.Lc = (int32_t)p.Lc;
       sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
@@ -1561,12 +1590,12 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.soft_scale = base_scale;
       sa.stats_part = w.partial;
       sa.stats = w.stats;
-      sa.nclear = qer_trees(h.n_frames).ints;
+      sa.nclear = n_queries * qer_trees(h.n_frames).ints;
       const int cus = device_cu_count();
       for (int pass = 1; pass <= 2; ++pass) {
-        for (int q0 = 0; q0 < h.n_q; q0 += 64) {
+        for (int q0 = 0; q0 < R; q0 += 64) {
           sa.q0 = q0;
-          sa.n_q = std::min(64, h.n_q - q0);
+          sa.n_q = std::min(64, R - q0);
           sa.accumulate = pass == 2 && q0 > 0;
           sa.clear = (pass == 2 && q0 == 0 && fused_tail) ? w.done : nullptr;
           sa.scale = 1.0f / (float)h.H_q;  // pass 2: the head mean
@@ -1602,7 +1631,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
           if (rc) return rc;
         }
         if (pass == 1) {
-          const int32_t rows = h.H_q * h.n_q;
+          const int32_t rows = h.H_q * R;
           rc = launch("qer_soft_merge", qer_soft_merge_blocked_kernel, dim3((unsigned)ceil_div(rows, 16)),
                       dim3(1024), 0, s, (const float2*)w.partial, p.soft_nwg * kLdsWaves * p.soft_rounds, rows,
                       w.stats);
@@ -1711,7 +1740,7 @@ size_t cofie_qer_batched_workspace_bytes(const cofie_qer_desc* heads, int32_t n_
   int32_t didx;
   if (n_queries < 1 || validate_qer(dummy, dummy, &doffs, heads, k_top, &dscore, &didx)) return 0;
   Arena ar;
-  carve_qer(ar, *heads, plan_qer(*heads), n_queries);
+  carve_qer(ar, *heads, plan_qer(*heads, n_queries), n_queries);
   return ar.bytes();
 }
 
@@ -1730,8 +1759,10 @@ int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_of
                        h.n_frames);
   if (n_queries > 1 && h.n_q % 16 != 0)
     return set_error(COFIE_EUNSUPPORTED, "several queries need n_q (%d) a multiple of 16", h.n_q);
-  if (n_queries > 1 && h.score_mode != COFIE_SCORE_LOGIT)
-    return set_error(COFIE_EUNSUPPORTED, "several queries are ranked in LOGIT mode only");
+  if (n_queries > 1 && h.score_mode != COFIE_SCORE_LOGIT && !plan_qer(h, n_queries).soft_fast)
+    return set_error(COFIE_EUNSUPPORTED,
+                     "several queries in SOFTMAX mode need heads of whole 128-byte key segments "
+                     "(d a multiple of %d elements)", h.dtype == COFIE_BF16 ? 64 : 32);
   if ((int64_t)n_queries * h.n_q * h.H_q * h.d >= (int64_t(1) << 31))
     return set_error(COFIE_EUNSUPPORTED, "queries too large");
   return rank_impl(Q, K, frame_offsets, h, n_queries, n_frames_per_query, k_top, out_scores, out_idx,

@@ -42,12 +42,12 @@ def make_case(seed, n_queries, n_q, H_q, H_kv, d, n_frames, dtype, max_tokens=24
     return Q, K, offs, nf
 
 
-def run_batched(Q, K, offs, nf, H_q, H_kv, d, k_top, dtype):
+def run_batched(Q, K, offs, nf, H_q, H_kv, d, k_top, dtype, mode=B.LOGIT):
     n_queries, n_q = Q.shape[:2]
     n_frames = len(offs) - 1
     print(f"qer batched queries={n_queries} n_q={n_q} n_vis={K.shape[0]} frames={n_frames} "
-          f"H={H_q}/{H_kv} d={d} k={k_top} {dtype} nf={nf.tolist()}", flush=True)
-    w, idx = B.cofie_qer_rank_batched(qk_dev(Q), qk_dev(K), to_dev(offs), nf, k_top)
+          f"H={H_q}/{H_kv} d={d} k={k_top} {dtype} mode={mode} nf={nf.tolist()}", flush=True)
+    w, idx = B.cofie_qer_rank_batched(qk_dev(Q), qk_dev(K), to_dev(offs), nf, k_top, score_mode=mode)
     torch.cuda.synchronize()
     w = w.cpu().numpy()
     idx = idx.cpu().numpy()
@@ -55,7 +55,7 @@ def run_batched(Q, K, offs, nf, H_q, H_kv, d, k_top, dtype):
     for g in range(n_queries):
         f = int(nf[g])
         # the oracle on the prefix: the first f frames and their tokens only
-        ref = oracle.qer_scores(Q[g], K[:offs[f]], offs[:f + 1], H_q, H_kv, d)
+        ref = oracle.qer_scores(Q[g], K[:offs[f]], offs[:f + 1], H_q, H_kv, d, mode)
         worst = max(worst, rel_err(w[g, :f], ref))
         assert np.array_equal(np.isneginf(w[g, :f]), np.isneginf(ref)), f"query {g}: empty-frame scores differ"
         assert np.all(np.isneginf(w[g, f:])), f"query {g}: scores past its prefix are not -inf"
@@ -77,6 +77,30 @@ def run_batched(Q, K, offs, nf, H_q, H_kv, d, k_top, dtype):
 def test_batched_against_oracle(dtype, n_queries, n_q, H_q, H_kv, d, n_frames):
     Q, K, offs, nf = make_case(n_queries * 100 + n_q + d, n_queries, n_q, H_q, H_kv, d, n_frames, dtype)
     run_batched(Q, K, offs, nf, H_q, H_kv, d, 8, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n_queries,n_q,H_q,H_kv,d,n_frames,max_tokens", [
+    (3, 16, 4, 4, 64, 40, 24),        # one 64-row chunk holds all queries
+    (5, 32, 28, 4, 128, 30, 60),      # grouped heads, queries straddle 64-row chunks
+    (4, 32, 8, 8, 64, 48, 900),       # ~1500 tiles
+])
+def test_batched_softmax(dtype, n_queries, n_q, H_q, H_kv, d, n_frames, max_tokens):
+    """SOFTMAX for several queries: query g's softmax runs over the keys of
+    its own prefix (pass 1 counts no key past offs[nf[g]]), so every query
+    matches the oracle on its prefix, and a single-query call on the prefix to
+    rounding (the work split, which orders the sums, follows the key count)."""
+    Q, K, offs, nf = make_case(n_queries * 10 + d, n_queries, n_q, H_q, H_kv, d, n_frames, dtype, max_tokens)
+    w, idx = run_batched(Q, K, offs, nf, H_q, H_kv, d, 6, dtype, mode=B.SOFTMAX)
+    Kd, od = qk_dev(K), to_dev(offs)
+    for g in range(n_queries):
+        f = int(nf[g])
+        if f == 0:
+            continue
+        w1, _ = B.cofie_qer_rank(qk_dev(Q[g]), Kd[:int(offs[f])].contiguous(), od[:f + 1].contiguous(), 6,
+                                 score_mode=B.SOFTMAX)
+        torch.cuda.synchronize()
+        assert rel_err(w[g, :f], w1.cpu().numpy().astype(np.float64)) <= 1e-5, g
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -144,7 +168,7 @@ def test_batched_rejects_unsupported():
         B.cofie_qer_rank_batched(Qd, Kd, od, nf, 4)
     assert e.value.code == B.COFIE_EUNSUPPORTED
     Q16 = qk_dev(Q[:, :16].copy())
-    with pytest.raises(B.CofieError) as e:           # several queries in softmax mode
+    with pytest.raises(B.CofieError) as e:           # several queries in softmax mode, 32-element heads
         B.cofie_qer_rank_batched(Q16, Kd, od, nf, 4, score_mode=B.SOFTMAX)
     assert e.value.code == B.COFIE_EUNSUPPORTED
     with pytest.raises(B.CofieError) as e:           # a prefix longer than the sequence
