@@ -598,6 +598,7 @@ def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams)
     bat_us = bat_score_us = 0.0
     bat_calls = 0
     bat_equal = True
+    bat_soft_us = soft_single_us = soft_err = 0.0
     for st in range(min(n_streams, wl.n_streams)):
         kept = np.flatnonzero(mask_np[st * wl.T:(st + 1) * wl.T])
         stamps = synth.multistream_queries(cfg, st)
@@ -615,6 +616,25 @@ def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams)
             def bcall(i, Qsd=Qsd, offs_all=offs_all, nfq=nfq, kb=kb):
                 return B.cofie_qer_rank_batched(Qsd, Kd, offs_all, nfq, kb)
 
+            def bcall_soft(i, Qsd=Qsd, offs_all=offs_all, nfq=nfq, kb=kb):
+                return B.cofie_qer_rank_batched(Qsd, Kd, offs_all, nfq, kb, score_mode=B.SOFTMAX)
+
+            bat_soft_us += median_call_us(torch, bcall_soft, 10)
+            ws, _ = bcall_soft(0)
+            # SOFTMAX: each query normalises over its own prefix, like a call
+            # given only the prefix's keys (equal to rounding)
+            for qi in range(len(stamps)):
+                if nfq[qi]:
+                    n = int(nfq[qi])
+
+                    def call_soft(i, qi=qi, n=n, offs_all=offs_all, kb=kb):
+                        return B.cofie_qer_rank(Qsd[qi], Kd[:n * wl.tokens], offs_all[:n + 1].contiguous(), kb,
+                                                score_mode=B.SOFTMAX)
+
+                    soft_single_us += median_call_us(torch, call_soft, 10)
+                    w1, _ = call_soft(0)
+                    rd = (w1 - ws[qi, :n]).abs().max() / w1.abs().max()
+                    soft_err = max(soft_err, float(rd))
             bat_us += median_call_us(torch, bcall, 10)
             bat_score_us += profiled_kernels(torch, B, bcall, 10)["qer_score"]
             bat_calls += 1
@@ -660,7 +680,10 @@ def qer_multistream(torch, B, oracle, synth, wl, cfg, probe, mask_np, n_streams)
                           "candidates_per_s": round(n_cand / (bat_us * 1e-6), 1),
                           "score_us_total": round(bat_score_us, 2),
                           "speedup_vs_one_call_per_query": round(total_us / bat_us, 3),
-                          "scores_equal_one_call_per_query": bat_equal}
+                          "scores_equal_one_call_per_query": bat_equal,
+                          "softmax_us_total": round(bat_soft_us, 2),
+                          "softmax_one_call_per_query_us_total": round(soft_single_us, 2),
+                          "softmax_max_rel_diff_vs_prefix_calls": soft_err}
     return out
 
 
@@ -776,7 +799,11 @@ def write_report(args, rows, probe):
                       f"once per stream): {b['calls']} calls, {b['us_total']:.1f} µs total "
                       f"({b['candidates_per_s']:,.0f} candidates/s, {b['speedup_vs_one_call_per_query']:.2f}x one call "
                       f"per query; score kernels {b['score_us_total']:.1f} µs); scores equal to one call per query, "
-                      f"bit for bit: {b['scores_equal_one_call_per_query']}."]
+                      f"bit for bit: {b['scores_equal_one_call_per_query']}.  SOFTMAX mode (each query's softmax "
+                      f"over its own prefix): {b['softmax_us_total']:.1f} µs total in the same {b['calls']} calls, against "
+                      f"{b['softmax_one_call_per_query_us_total']:.1f} µs for one call per query given its prefix's keys "
+                      f"({b['softmax_one_call_per_query_us_total'] / b['softmax_us_total']:.2f}x); largest relative "
+                      f"difference between the two {b['softmax_max_rel_diff_vs_prefix_calls']:.1e}."]
     lines += ["", "## Glue", "",
               "| workload | compaction µs | gathered frames | rows | gather µs | gather GB/s (read + write) | "
               "% of copy probe |", "|---|---|---|---|---|---|---|"]
