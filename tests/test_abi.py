@@ -196,6 +196,24 @@ def test_softmax_workspace_holds_per_wave_statistics(L):
     assert small >= (32768 // 32) * 28 * 32 * 8
 
 
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+def test_batched_softmax_workspace_and_refusal(L):
+    """Several queries in SOFTMAX mode keep one (max, sum) pair per wave,
+    round and stacked (head, query row): four queries of 32 rows over the
+    1 fps stream's 2048 tiles take 256 workgroups x 8 waves x 28 x 128 rows.
+    Heads that are not whole 128-byte key segments are refused for several
+    queries (the per-head fallback has no per-query key range)."""
+    d = B.qer_desc(32, 32768, 128, 28, 28, 128, score_mode=B.SOFTMAX)
+    four = B.lib().cofie_qer_batched_workspace_bytes(ctypes.byref(d), 4, 16)
+    one = B.lib().cofie_qer_batched_workspace_bytes(ctypes.byref(d), 1, 16)
+    assert four >= 256 * 8 * (28 * 4 * 32) * 8 > one > 0
+    d32 = B.qer_desc(16, 64, 4, 2, 2, 32, score_mode=B.SOFTMAX)
+    nf = (ctypes.c_int32 * 2)(4, 3)
+    assert L.cofie_qer_rank_batched(FAKE, FAKE, FAKE, ctypes.byref(d32), 2, nf, 2, FAKE, FAKE,
+                                    None) == B.COFIE_EUNSUPPORTED
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
 def test_batched_qer_validation(L):
     d = B.qer_desc(16, 64, 4, 2, 2, 32)
     nf = (ctypes.c_int32 * 2)(4, 5)   # 5 > n_frames
