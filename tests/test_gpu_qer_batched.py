@@ -136,10 +136,12 @@ def test_batched_equals_single_query_calls(dtype, n_q, H_q, H_kv, max_tokens):
         assert np.array_equal(i1.cpu().numpy(), idx[g]), g
 
 
-def test_stream_queries_on_candidate_prefixes():
+@pytest.mark.parametrize("mode", [B.LOGIT, B.SOFTMAX])
+def test_stream_queries_on_candidate_prefixes(mode):
     """The multi-stream use: the queries of one stream of the multi-stream
     workload (T = 512, 144 tokens per frame), each ranking the candidates
-    that precede its timestamp."""
+    that precede its timestamp (in SOFTMAX mode, each query's softmax over the
+    keys of its own prefix)."""
     wl = synth.WORKLOADS[5]
     rng = np.random.default_rng([2609, 3675, 94])
     cands = np.sort(rng.choice(wl.T, 40, replace=False))
@@ -148,7 +150,7 @@ def test_stream_queries_on_candidate_prefixes():
     Q = np.stack([synth.multistream_q(5, 0, g) for g in range(len(ts))])
     K = synth.multistream_k(5, 0, cands)
     offs = np.arange(0, (len(cands) + 1) * wl.tokens, wl.tokens, dtype=np.int32)
-    run_batched(Q, K, offs, nf, wl.H_q, wl.H_kv, wl.d, wl.k_top, wl.qk_dtype)
+    run_batched(Q, K, offs, nf, wl.H_q, wl.H_kv, wl.d, wl.k_top, wl.qk_dtype, mode)
 
 
 def test_empty_prefixes_and_no_topk():
