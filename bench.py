@@ -1,13 +1,14 @@
 #!/usr/bin/env python3
 """Throughput of CoFiE's evidence-selection path (NGFF + QER) on one MI355X.
 
-One step is the whole path over one batch of the 1 fps workload: NGFF
-(histograms, novelty scores, keep rule) over a 256-frame 448x448 RGB stream,
-then QER (bf16 MFMA text-to-visual scores, per-frame aggregation, top-16)
-over 128 candidate frames of 256 visual tokens with 32 query tokens, 28
-heads, head dim 128.  Inputs are seeded synthetic data resident in HBM;
-several copies are rotated so that the 256 MiB last-level cache cannot serve
-a step from the previous one.
+One step is the whole path over one batch of the multi-stream workload, the
+largest one: NGFF (histograms, novelty scores, keep rule with a calibrated
+threshold per stream) over 32 streams x 512 RGB frames of 448x448 (9.87 GB),
+then QER for the 4 queries of every stream (128 queries of 32 text tokens,
+28 heads, head dim 128, bf16): each query ranks its stream's NGFF candidates
+up to its timestamp, 144 visual tokens per frame, top-16.  Inputs are seeded
+synthetic data resident in HBM (far larger than the 256 MiB last-level
+cache, so no step is served from the previous one).
 
 Prints one JSON line: whole-step frames/s, per-stage figures, the roofline
 fraction of the dominant kernel (its duration measured live with the HIP event
@@ -29,7 +30,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = ("NGFF frames/s (GB/s vs HBM peak); QER candidate frames ranked/s (MFMA util)")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_1fps_stream.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_multistream.md")
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
@@ -39,20 +40,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--rotate", type=int, default=3, help="input copies cycled through")
-    ap.add_argument("--mode", choices=["graph", "eager"], default="eager",
-                    help="call the library eagerly, or replay the step as a captured HIP graph")
-    ap.add_argument("--overlap", choices=["on", "off"], default="off",
-                    help="on: NGFF's keep rule (after its histograms) runs on the main stream while QER runs "
-                         "on a second stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=8.0,
-                    help="target wall time of the CPU oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target wall time of the CPU oracle sample (all host threads)")
     ap.add_argument("--configs", default="",
                     help="comma-separated workload ids (1-5): print a per-workload stage report "
                          "(one JSON line each) instead of the headline step")
     ap.add_argument("--report", default="", help="with --configs: also write a markdown table here")
-    ap.add_argument("--ms-streams", type=int, default=8,
+    ap.add_argument("--ms-streams", type=int, default=32,
                     help="with --configs 5: streams whose queries are ranked (of 32)")
     ap.add_argument("--push-batch", type=int, default=64,
                     help="with --configs: frames per stream and push of the online NGFF pass")
@@ -84,88 +79,102 @@ def main():
     if args.attn_qer:
         attn_qer_report(args, [int(c) for c in args.attn_qer.split(",")])
         return
-    cfg = 2
+    headline(args)
+
+
+NGFF_KERNELS = ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select")
+QER_KERNELS = ("qer_fold", "qer_score", "qer_frame_mean", "qer_topk")
+
+
+class MsQuery:
+    """The QER inputs of one stream of the multi-stream workload, resident on
+    the GPU: its candidates (the keep rule's frames up to the last query's
+    timestamp), their keys, the stacked queries and each query's prefix."""
+
+    def __init__(self, torch, B, synth, cfg, s, kept):
+        wl = synth.WORKLOADS[cfg]
+        stamps = synth.multistream_queries(cfg, s)
+        cand = kept[kept <= stamps.max()]
+        self.nf = np.array([int((kept <= ts).sum()) for ts in stamps], np.int32)
+        K = synth.multistream_k(cfg, s, cand)
+        Q = np.stack([synth.multistream_q(cfg, s, g) for g in range(len(stamps))])
+        self.n_cand = int(cand.size)
+        self.n_vis = int(K.shape[0])
+        self.K = torch.from_numpy(K.view(np.int16)).cuda().view(torch.bfloat16)
+        self.Q = torch.from_numpy(Q.view(np.int16)).cuda().view(torch.bfloat16)
+        self.offs = torch.from_numpy(synth.frame_offsets(np.full(self.n_cand, wl.tokens))).cuda()
+        self.k_top = wl.k_top
+        desc = B.qer_desc(wl.n_q, self.n_vis, self.n_cand, wl.H_q, wl.H_kv, wl.d)
+        self.ws = torch.empty(B.qer_batched_workspace_bytes(desc, len(stamps), wl.k_top), dtype=torch.uint8,
+                              device="cuda")
+        self.w = torch.empty((len(stamps), max(self.n_cand, 1)), dtype=torch.float32, device="cuda")
+        self.idx = torch.empty((len(stamps), wl.k_top), dtype=torch.int32, device="cuda")
+
+    def rank(self, B):
+        B.cofie_qer_rank_batched(self.Q, self.K, self.offs, self.nf, self.k_top, out_scores=self.w,
+                                 out_idx=self.idx, workspace=self.ws)
+
+
+def upload_frames(torch, synth, cfg, keep_host=0):
+    """Every frame of the workload in one device buffer, generated stream by
+    stream on the host; the host frames of the first `keep_host` streams are
+    returned for the CPU baseline."""
     wl = synth.WORKLOADS[cfg]
-    n, H, W, C = wl.T, wl.H, wl.W, 3
+    frames = torch.empty((wl.n, wl.H, wl.W, 3), dtype=torch.uint8, device="cuda")
+    kept_host = []
+    for s in range(wl.n_streams):
+        host = synth.StreamPlan(cfg, s).frames()
+        frames[s * wl.T:(s + 1) * wl.T].copy_(torch.from_numpy(host))
+        if s < keep_host:
+            kept_host.append(host)
+    return frames, kept_host
 
-    # ---- inputs (host generation, then resident copies in HBM) -------------------
-    frames_np = synth.frames(cfg)
-    Q_np, K_np, offs_np = synth.qer_inputs(cfg)
-    frames = [torch.from_numpy(frames_np).cuda() for _ in range(args.rotate)]
-    Kd = [torch.from_numpy(K_np.view(np.int16)).cuda().view(torch.bfloat16) for _ in range(args.rotate)]
-    Qd = torch.from_numpy(Q_np.view(np.int16)).cuda().view(torch.bfloat16)
-    offs = torch.from_numpy(offs_np).cuda()
-    n_vis = K_np.shape[0]
-    n_frames = offs_np.size - 1
 
-    # retention threshold for the target kept count, calibrated once on the GPU
-    rule0 = B.keep_rule(wl.hist_mode, 0.3, 30, 4)
-    tau = B.cofie_ngff_calibrate(frames[0], wl.bins, rule0, wl.target)
+def headline(args):
+    """The timed step on the multi-stream workload (module docstring)."""
+    import torch
 
-    # preallocated outputs and scratch: the step allocates nothing
+    from paper_2609_03675_amd import binding as B
+    from paper_2609_03675_amd import synth
+
+    cfg = 5
+    wl = synth.WORKLOADS[cfg]
+    S, T = wl.n_streams, wl.T
+    n, H, W, C = wl.n, wl.H, wl.W, 3
+
+    # ---- inputs: frames in HBM, per-stream thresholds calibrated once on the GPU ----------
+    frames, host_frames = upload_frames(torch, synth, cfg, keep_host=0 if args.no_cpu_baseline else 4)
+    rule0 = B.keep_rule(wl.hist_mode, 0.3, 30, 4, T)
+    tau = B.cofie_ngff_calibrate(frames, wl.bins, rule0, wl.target)
     scores = torch.empty(n, dtype=torch.float32, device="cuda")
     mask = torch.empty(n, dtype=torch.uint8, device="cuda")
-    count = torch.empty(1, dtype=torch.int32, device="cuda")
-    probe_rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4)
-    ngff_ws = torch.empty(B.ngff_workspace_bytes(n, H, W, C, wl.bins, probe_rule), dtype=torch.uint8,
-                          device="cuda")
-    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, tau_per_segment=tau, out_count=count,
-                       workspace=ngff_ws)
-    desc = B.qer_desc(wl.n_q, n_vis, n_frames, wl.H_q, wl.H_kv, wl.d)
-    qer_ws = torch.empty(B.qer_workspace_bytes(desc, wl.k_top), dtype=torch.uint8, device="cuda")
-    w_out = torch.empty(n_frames, dtype=torch.float32, device="cuda")
-    idx_out = torch.empty(wl.k_top, dtype=torch.int32, device="cuda")
-
-    hist_buf = torch.empty((n, B.cofie_ngff_nbins(wl.hist_mode, wl.bins)), dtype=torch.int32, device="cuda")
-    qer_stream = torch.cuda.Stream()
-    hist_done = torch.cuda.Event()
+    count = torch.empty(S, dtype=torch.int32, device="cuda")
+    ngff_ws = torch.empty(B.ngff_workspace_bytes(n, H, W, C, wl.bins, rule0), dtype=torch.uint8, device="cuda")
+    rule = B.keep_rule(wl.hist_mode, 0.3, 30, 4, T, tau_per_segment=tau, out_count=count, workspace=ngff_ws)
+    B.cofie_ngff_filter(frames, wl.bins, rule, out_scores=scores, out_mask=mask)
+    torch.cuda.synchronize()
+    # The keep rule's candidates are the same at every step (same frames, same
+    # thresholds), so each query's prefix length, which the host passes to the
+    # ranking call, is read once here from the GPU's mask; the keys of the
+    # candidates stand in for the encoder's output and are resident in HBM.
+    mask_np = mask.cpu().numpy()
+    qs = [MsQuery(torch, B, synth, cfg, s, np.flatnonzero(mask_np[s * T:(s + 1) * T])) for s in range(S)]
+    n_queries = sum(len(q.nf) for q in qs)
+    ranked = int(sum(int(q.nf.sum()) for q in qs))          # candidate frames ranked per step
+    k_bytes = sum(q.n_vis for q in qs) * wl.H_kv * wl.d * 2  # every stream's keys read once
+    q_bytes = sum(q.Q.numel() for q in qs) * 2
+    # flops of the contraction as issued: every query of a stream against all its keys
+    qer_flops = sum(2.0 * len(q.nf) * wl.n_q * q.n_vis * wl.H_q * wl.d for q in qs)
 
     def step(i):
-        r = i % args.rotate
-        if args.overlap == "off":
-            B.cofie_ngff_filter(frames[r], wl.bins, rule, out_scores=scores, out_mask=mask)
-            B.cofie_qer_rank(Qd, Kd[r], offs, wl.k_top, out_scores=w_out, out_idx=idx_out,
-                             workspace=qer_ws)
-            return
-        # the histograms, then QER on its own stream beside NGFF's keep rule
-        main = torch.cuda.current_stream()
-        B.cofie_ngff_histogram(frames[r], wl.bins, wl.hist_mode, out=hist_buf)
-        hist_done.record(main)
-        qer_stream.wait_event(hist_done)
-        with torch.cuda.stream(qer_stream):
-            B.cofie_qer_rank(Qd, Kd[r], offs, wl.k_top, out_scores=w_out, out_idx=idx_out,
-                             workspace=qer_ws)
-        B.cofie_ngff_filter_hist(hist_buf, H, W, C, wl.bins, rule, out_scores=scores, out_mask=mask)
-        main.wait_stream(qer_stream)
+        B.cofie_ngff_filter(frames, wl.bins, rule, out_scores=scores, out_mask=mask)
+        for q in qs:
+            q.rank(B)
 
-    for i in range(max(args.warmup, args.rotate)):
+    for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    kept = int(count.item())
-
-    graphs = None
-    if args.mode == "graph":
-        graphs = []
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            for r in range(args.rotate):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=side):
-                    step(r)
-                graphs.append(g)
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        for i in range(args.warmup):
-            graphs[i % args.rotate].replay()
-        torch.cuda.synchronize()
-
-    def run_steps(k):
-        for i in range(k):
-            if graphs is not None:
-                graphs[i % args.rotate].replay()
-            else:
-                step(i)
+    kept = int(count.sum().item())
 
     # ---- timed region ---------------------------------------------------------------
     torch.cuda.synchronize()
@@ -173,24 +182,12 @@ def main():
     t1 = torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
     t0.record()
-    run_steps(args.steps)
+    for i in range(args.steps):
+        step(i)
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / args.steps
-
-    # the other launch mode, for reference
-    torch.cuda.synchronize()
-    ms_step_other = None
-    if graphs is not None:
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(args.steps):
-            step(i)
-        e1.record()
-        torch.cuda.synchronize()
-        ms_step_other = e0.elapsed_time(e1) / args.steps
 
     # ---- per-kernel durations, live HIP events carried by every library launch --------
     B.cofie_profiler_reset()
@@ -200,61 +197,44 @@ def main():
     torch.cuda.synchronize()
     B.cofie_profiler_enable(False)
     kern = {}
-    for name in ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select", "qer_fold",
-                 "qer_score", "qer_frame_mean", "qer_topk"):
+    for name in NGFF_KERNELS + QER_KERNELS:
         ms, cnt = B.cofie_profiler_read(name)
         if cnt:
-            kern[name] = {"avg_us": 1e3 * ms / cnt, "launches": cnt}
+            kern[name] = {"avg_us": 1e3 * ms / cnt, "per_step": cnt / args.steps,
+                          "us_per_step": 1e3 * ms / args.steps}
     B.cofie_profiler_reset()
 
     # attainable streaming bandwidth: a plain read and a plain copy of 1 GiB
-    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-    dst = torch.empty_like(src)
-    sink = torch.empty(1 << 20, dtype=torch.int32, device="cuda")
+    read_gbs = read_probe_gbs(torch, B)
+    copy_gbs = copy_probe_gbs(torch, B)
 
-    def timed(fn, reps=10):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        c0 = torch.cuda.Event(enable_timing=True)
-        c1 = torch.cuda.Event(enable_timing=True)
-        c0.record()
-        for _ in range(reps):
-            fn()
-        c1.record()
-        torch.cuda.synchronize()
-        return c0.elapsed_time(c1) * 1e-3 / reps
-
-    read_gbs = (1 << 30) / timed(lambda: B.cofie_diag_stream_read(src, sink)) / 1e9
-    copy_gbs = 2 * (1 << 30) / timed(lambda: B.cofie_diag_stream_copy(src, dst)) / 1e9
-    del src, dst, sink
-
-    # ---- algorithmic work per launch -------------------------------------------------------
-    ngff_bytes = n * H * W * C                                   # every frame byte read once
-    qer_bytes = n_vis * wl.H_kv * wl.d * 2 + wl.n_q * wl.H_q * wl.d * 2   # K once + Q
-    qer_flops = 2.0 * wl.n_q * n_vis * wl.H_q * wl.d
-    hist_us = kern["ngff_hist"]["avg_us"]
-    score_us = kern["qer_score"]["avg_us"]
-    ngff_gbs = ngff_bytes / (hist_us * 1e-6) / 1e9
-    qer_gbs = qer_bytes / (score_us * 1e-6) / 1e9
-    qer_tflops = qer_flops / (score_us * 1e-6) / 1e12
-    ngff_stage_us = sum(v["avg_us"] for k, v in kern.items() if k.startswith("ngff"))
-    qer_stage_us = sum(v["avg_us"] for k, v in kern.items() if k.startswith("qer"))
-    if score_us >= hist_us:
+    # ---- algorithmic work ------------------------------------------------------------------
+    ngff_bytes = n * H * W * C                  # every frame byte read once
+    qer_bytes = k_bytes + q_bytes               # keys once + queries
+    hist = kern["ngff_hist"]
+    score = kern["qer_score"]
+    ngff_gbs = ngff_bytes / (hist["us_per_step"] * 1e-6) / 1e9
+    qer_gbs = qer_bytes / (score["us_per_step"] * 1e-6) / 1e9
+    qer_tflops = qer_flops / (score["us_per_step"] * 1e-6) / 1e12
+    ngff_stage_us = sum(v["us_per_step"] for k, v in kern.items() if k.startswith("ngff"))
+    qer_stage_us = sum(v["us_per_step"] for k, v in kern.items() if k.startswith("qer"))
+    # the dominant kernel: the largest share of the step's GPU time
+    if score["us_per_step"] >= hist["us_per_step"]:
+        per = score["per_step"]
         roof = {"kernel": "qer_score", "bound": "hbm", "achieved": round(qer_gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(qer_gbs / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic("qer_score_kernel"), "algorithmic_bytes": qer_bytes,
-                "avg_us": round(score_us, 2)}
+                "traffic": measured_traffic("qer_score_kernel"), "algorithmic_bytes": round(qer_bytes / per),
+                "launches_per_step": per, "avg_us": round(score["avg_us"], 2)}
     else:
         roof = {"kernel": "ngff_hist", "bound": "hbm", "achieved": round(ngff_gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ngff_gbs / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic("ngff_hist_kernel"), "algorithmic_bytes": ngff_bytes,
-                "avg_us": round(hist_us, 2)}
+                "launches_per_step": hist["per_step"], "avg_us": round(hist["avg_us"], 2)}
 
     # ---- CPU oracle on a bounded sample ------------------------------------------------------
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, frames_np, Q_np, K_np, offs_np, float(tau[0].item()), args.cpu_seconds)
+        cpu = cpu_baseline_multistream(wl, cfg, host_frames, args.cpu_seconds)
 
     value = n / (ms_step * 1e-3)
     out = {
@@ -270,33 +250,100 @@ def main():
         "vs_baseline": None,
         "dtype": "u8+bf16",
         "data": "synthetic",
-        "config": {"workload": "1fps_stream", "frames": n, "H": H, "W": W, "hist_mode": wl.hist_mode,
-                   "bins": wl.bins, "retain": wl.retain, "L_max": 30, "M_min": 4,
-                   "qer": {"n_q": wl.n_q, "H_q": wl.H_q, "H_kv": wl.H_kv, "d": wl.d,
-                           "candidates": n_frames, "tokens_per_frame": wl.tokens,
-                           "k_top": wl.k_top, "dtype": "bf16", "score_mode": "logit"},
-                   "step": args.mode, "overlap": args.overlap, "rotated_copies": args.rotate},
+        "config": {"workload": "multistream", "streams": S, "frames_per_stream": T, "frames": n, "H": H, "W": W,
+                   "hist_mode": wl.hist_mode, "bins": wl.bins, "retain": wl.retain, "L_max": 30, "M_min": 4,
+                   "qer": {"queries": n_queries, "n_q": wl.n_q, "H_q": wl.H_q, "H_kv": wl.H_kv, "d": wl.d,
+                           "tokens_per_frame": wl.tokens, "k_top": wl.k_top, "dtype": "bf16",
+                           "score_mode": "logit", "candidates_ranked": ranked,
+                           "calls": "one cofie_qer_rank_batched per stream"}},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages": {
             "ngff_frames_per_s": round(n / (ngff_stage_us * 1e-6), 1),
+            "ngff_us": round(ngff_stage_us, 1),
             "ngff_hist_GBps": round(ngff_gbs, 1),
             "ngff_hist_frac_hbm": round(ngff_gbs / HBM_PEAK_GBS, 4),
             "ngff_hist_traffic": measured_traffic("ngff_hist_kernel"),
-            "qer_candidates_per_s": round(n_frames / (qer_stage_us * 1e-6), 1),
+            "qer_us": round(qer_stage_us, 1),
+            "qer_candidates_ranked_per_s": round(ranked / (qer_stage_us * 1e-6), 1),
+            "qer_key_bytes": k_bytes,
             "qer_score_GBps": round(qer_gbs, 1),
             "qer_score_frac_hbm": round(qer_gbs / HBM_PEAK_GBS, 4),
             "qer_score_TFLOPs": round(qer_tflops, 2),
             "qer_mfma_util": round(qer_tflops / BF16_PEAK_TFLOPS, 4),
-            "kernels_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
+            "kernels_us_per_step": {k: round(v["us_per_step"], 2) for k, v in kern.items()},
+            "kernels_avg_us": {k: round(v["avg_us"], 2) for k, v in kern.items()},
+            "kernel_launches_per_step": {k: v["per_step"] for k, v in kern.items()},
             "kept_frames": kept,
-            "ms_per_step_eager_when_graph": None if ms_step_other is None else round(ms_step_other, 5),
             "copy_probe_GBps": round(copy_gbs, 1),
             "read_probe_GBps": round(read_gbs, 1),
             "wall_s": round(wall, 3),
         },
     }
     print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_multistream(wl, cfg, host_frames, target_s):
+    """The oracle, as it stands, on this host's cores: whole streams of the
+    same workload (NGFF with the stream's calibrated threshold, then the fp64
+    QER of the stream's 4 queries over its candidates), as many as fit the
+    time budget, on all threads; then one stream on one thread.  Rates are
+    frames per second of oracle time (threshold calibration and input
+    generation untimed)."""
+    import oracle
+    from paper_2609_03675_amd import synth
+
+    M = oracle.mass(oracle.PER_CHANNEL, wl.H, wl.W)
+
+    def stream_s(s, frames):
+        h = oracle.histogram(frames, wl.bins, oracle.PER_CHANNEL)
+        t_ngff = time.perf_counter()
+        _, tau = oracle.ngff_calibrate(h, M, wl.target, 30, 4)          # untimed
+        t_cal = time.perf_counter() - t_ngff
+        _, mask, _ = oracle.ngff_select(h, M, tau[0], 30, 4)
+        kept = np.flatnonzero(mask)
+        stamps = synth.multistream_queries(cfg, s)
+        cand = kept[kept <= stamps.max()]
+        t_gen = time.perf_counter()
+        K = synth.multistream_k(cfg, s, cand)                            # untimed
+        Qs = [synth.multistream_q(cfg, s, g) for g in range(len(stamps))]
+        t_gen = time.perf_counter() - t_gen
+        for g, ts in enumerate(stamps):
+            nc = int((kept <= ts).sum())
+            offs = synth.frame_offsets(np.full(nc, wl.tokens))
+            oracle.topk(oracle.qer_scores(Qs[g], K[:nc * wl.tokens], offs, wl.H_q, wl.H_kv, wl.d), wl.k_top)
+        return t_cal + t_gen
+
+    def run(streams, frames_of):
+        t = 0.0
+        for s in streams:
+            fr = frames_of(s)
+            t0 = time.perf_counter()
+            untimed = stream_s(s, fr)
+            t += time.perf_counter() - t0 - untimed
+        return t
+
+    def frames_of(s):
+        return host_frames[s] if s < len(host_frames) else synth.StreamPlan(cfg, s).frames()
+
+    threads = oracle.num_threads()
+    t_all, done = 0.0, 0
+    while done < wl.n_streams and (done == 0 or t_all < target_s):
+        t_all += run([done], frames_of)
+        done += 1
+    oracle.set_num_threads(1)
+    try:
+        t_one = run([0], frames_of)
+    finally:
+        oracle.set_num_threads(threads)
+    return {"value": round(done * wl.T / t_all, 3), "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"the first {done} of the 32 streams (each: NGFF over its {wl.T} frames, then the fp64 QER "
+                      f"of its 4 queries over their candidate prefixes, top-{wl.k_top}); rate = frames / oracle "
+                      f"time on {threads} threads (threshold calibration and input generation untimed)",
+            "seconds": round(t_all, 3),
+            "single_core": {"value": round(wl.T / t_one, 3), "unit": "frames/s", "cores": 1,
+                            "sample": "stream 0 alone on one thread", "seconds": round(t_one, 3)}}
+
 
 
 def measured_traffic(kernel: str):
@@ -824,45 +871,6 @@ def write_report(args, rows, probe):
         lines.append(f"- {r['workload']}: NGFF {r['ngff']['kernels_us']}; QER {r['qer']['kernels_us_per_call']}")
     with open(args.report, "w") as f:
         f.write("\n".join(lines) + "\n")
-
-
-def cpu_baseline(wl, frames_np, Q_np, K_np, offs_np, tau, target_s):
-    """The oracle, as it stands, on this host's cores: whole NGFF passes over
-    the 256-frame stream and whole QER passes over the 128 candidates, each
-    repeated for about half of the time budget; the step rate is the inverse
-    of the two mean times added."""
-    import oracle
-
-    threads = oracle.num_threads()
-    n = frames_np.shape[0]
-    M = oracle.mass(oracle.PER_CHANNEL, wl.H, wl.W)
-
-    def repeat(fn, budget):
-        t0 = time.perf_counter()
-        reps = 0
-        while True:
-            fn()
-            reps += 1
-            el = time.perf_counter() - t0
-            if el >= budget or reps >= 200:
-                return el / reps, reps
-
-    def ngff():
-        h = oracle.histogram(frames_np, wl.bins, oracle.PER_CHANNEL)
-        oracle.ngff_select(h, M, tau, 30, 4)
-
-    def qer():
-        w = oracle.qer_scores(Q_np, K_np, offs_np, wl.H_q, wl.H_kv, wl.d)
-        oracle.topk(w, wl.k_top)
-
-    ngff_s, r1 = repeat(ngff, 0.5 * target_s)
-    qer_s, r2 = repeat(qer, 0.5 * target_s)
-    step_s = ngff_s + qer_s
-    return {"value": round(n / step_s, 3), "unit": "frames/s", "cores": threads, "kind": "oracle",
-            "sample": f"full workload step: NGFF oracle on the {n}-frame stream x{r1} and the fp64 "
-                      f"QER oracle on all {wl.n_frames} candidates x{r2}; rate = {n} frames / "
-                      f"(mean NGFF time + mean QER time)",
-            "ngff_s": round(ngff_s, 5), "qer_s": round(qer_s, 5)}
 
 
 if __name__ == "__main__":

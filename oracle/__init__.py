@@ -67,6 +67,8 @@ def _load():
     P = ctypes.c_void_p
     i32, i64, f32, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
     lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_set_num_threads.argtypes = [ctypes.c_int]
+    lib.orc_set_num_threads.restype = None
     lib.orc_nbins.argtypes = [i32, i32]
     lib.orc_nbins.restype = i64
     lib.orc_mass.argtypes = [i32, i32, i32]
@@ -106,6 +108,11 @@ def _ptr(a: np.ndarray):
 def num_threads() -> int:
     """OpenMP threads the oracle uses."""
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's later calls (timing; results do not depend on it)."""
+    _load().orc_set_num_threads(int(n))
 
 
 def nbins(mode: int, bins: int) -> int:

@@ -46,6 +46,15 @@ int orc_num_threads(void) {
 #endif
 }
 
+/* Threads of the parallel loops that follow (n >= 1); timing only. */
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* NGFF: histograms (Sec. 3.2, "Lightweight histogram-based novelty")       */
 /* ------------------------------------------------------------------------ */

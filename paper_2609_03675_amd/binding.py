@@ -294,6 +294,10 @@ def qer_workspace_bytes(desc: QerDesc, k_top: int) -> int:
     return int(lib().cofie_qer_workspace_bytes(ctypes.byref(desc), k_top))
 
 
+def qer_batched_workspace_bytes(desc: QerDesc, n_queries: int, k_top: int) -> int:
+    return int(lib().cofie_qer_batched_workspace_bytes(ctypes.byref(desc), n_queries, k_top))
+
+
 def cofie_qer_rank(Q, K, frame_offsets, k_top: int, score_mode=LOGIT, scale: float = 0.0,
                    out_scores=None, out_idx=None, workspace=None, stream=None):
     """QER frame scores w_f (float32 [n_frames]) and chronological top-k (int32 [k_top]).

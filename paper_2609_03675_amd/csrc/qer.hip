@@ -4,9 +4,11 @@
 //   a_ij = (scale / H_q) * <q~_i, k~_j>, q~/k~ = all heads side by side,
 // so the text-by-vision scores are one GEMM S^T = K Q^T with contraction
 // length Lc = H_kv * d.  With grouped-query attention the query heads of a
-// group are summed first (q^_g = sum_{h in g} q_h, exact in fp32) and q^ is
-// carried as three bf16 terms hi + mid + lo that reproduce the fp32 value, so
-// the bf16 MFMA still multiplies exact operands.
+// group are summed first, in fp32 and in head order (q^_g = sum_{h in g} q_h,
+// rounded once per addition: exact only while the heads' exponents stay
+// within fp32's 24 bits of each other), and that rounded fp32 q^ is carried
+// as three bf16 terms hi + mid + lo whose sum is exactly it, so the bf16 MFMA
+// multiplies exact representations of the fp32 sum.
 //
 // qer_score: one 8-wave workgroup per CU; each wave owns MB x 16 visual tokens
 //   and all (<= 64, or 128 in eight blocks) query rows of one chunk, over the

@@ -15,7 +15,7 @@ from paper_2609_03675_amd import synth
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
-from gpu_util import bf16_dev, check_topk, hist_np, rel_err, require_gpu, to_dev  # noqa: E402
+from gpu_util import BF16_REGRESSION, bf16_dev, check_topk, hist_np, rel_err, require_gpu, to_dev  # noqa: E402
 
 MODES = {"gray": oracle.GRAY, "per_channel": oracle.PER_CHANNEL, "joint3d": oracle.JOINT3D}
 CHUNK = 128  # frames generated, uploaded and histogrammed on the host at a time
@@ -89,6 +89,7 @@ def test_qer_full_size(cfg):
     err = rel_err(w, ref)
     print(f"workload {cfg}: QER max rel err {err:.3e}", flush=True)
     assert err <= 2e-2
+    assert err <= BF16_REGRESSION  # exact MFMA operands (three-term folded query at high-res)
     check_topk(idx.cpu().numpy(), ref, wl.k_top)
 
 
@@ -106,6 +107,7 @@ def test_qer_softmax_full_size(cfg):
     err = rel_err(w, ref)
     print(f"workload {cfg}: SOFTMAX max rel err {err:.3e}", flush=True)
     assert err <= 2e-2
+    assert err <= BF16_REGRESSION
     check_topk(idx.cpu().numpy(), ref, wl.k_top)
 
 
