@@ -274,6 +274,24 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
                    const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
                    int32_t* out_idx, void* stream);
 
+/* cofie_qer_rank for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, kernels and results, but the scratch is a static
+ * device array of the library (COFIE_QER_NOALLOC_SCRATCH_BYTES, one copy per
+ * device, held until the process ends) instead of a workspace or an
+ * allocation; the call makes no hipMalloc/hipFree and no allocating library
+ * call.  heads->workspace must be NULL (EINVAL).  A call needing more scratch
+ * than the array (cofie_qer_workspace_bytes() above the maximum) returns
+ * EUNSUPPORTED before anything is enqueued.  Every call on a device shares
+ * that device's array: calls that overlap on one device (two streams, or two
+ * host threads) race and must be serialised by the caller; calls in one
+ * stream order are safe.  The array keeps the last call's contents; everything
+ * a call reads is written or cleared by that call's own kernels first. */
+#define COFIE_QER_NOALLOC_SCRATCH_BYTES (32u << 20)
+int cofie_qer_rank_noalloc(const void* Q, const void* K, const int32_t* frame_offsets,
+                           const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
+                           int32_t* out_idx, void* stream);
+
 /* Several queries sharing one key sequence, K read once for all of them
  * (the multi-stream workload: a stream's queries rank prefixes of its
  * candidates).  Query g has heads->n_q rows of Q (device

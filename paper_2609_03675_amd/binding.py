@@ -111,6 +111,7 @@ def lib() -> ctypes.CDLL:
         "cofie_ngff_calibrate": (ctypes.c_int, [P, i64, i32, i32, i32, i32, ctypes.POINTER(KeepRule), i64, P, P]),
         "cofie_qer_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32]),
         "cofie_qer_rank": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
+        "cofie_qer_rank_noalloc": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P]),
         "cofie_ngff_stream_create": (ctypes.c_int, [i32, i32, i32, i32, i32, ctypes.POINTER(KeepRule),
                                                     ctypes.POINTER(P)]),
         "cofie_ngff_stream_push": (ctypes.c_int, [P, P, i64, i32, P, P, i64, P]),
@@ -292,6 +293,28 @@ def qer_desc(n_q: int, n_vis: int, n_frames: int, H_q: int, H_kv: int, d: int, d
 
 def qer_workspace_bytes(desc: QerDesc, k_top: int) -> int:
     return int(lib().cofie_qer_workspace_bytes(ctypes.byref(desc), k_top))
+
+
+def cofie_qer_rank_noalloc(Q, K, frame_offsets, k_top: int, out_scores, out_idx, score_mode=LOGIT,
+                           scale: float = 0.0, stream=None):
+    """cofie_qer_rank with the library's static scratch instead of a workspace
+    or an allocation: the outputs (float32 [n_frames], int32 [k_top]) must be
+    given, and the call allocates nothing."""
+    import torch
+    n_q, H_q, d = Q.shape
+    n_vis, H_kv, d2 = K.shape
+    if d2 != d:
+        raise ValueError("Q and K head dimensions differ")
+    if Q.dtype != K.dtype or Q.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("Q and K must both be bfloat16 or both float32")
+    dtype = BF16 if Q.dtype == torch.bfloat16 else F32
+    n_frames = frame_offsets.numel() - 1
+    desc = qer_desc(n_q, n_vis, n_frames, H_q, H_kv, d, dtype, score_mode, scale)
+    _check(lib().cofie_qer_rank_noalloc(_dev(Q, "Q"), _dev(K, "K") if n_vis > 0 else None,
+                                        _dev(frame_offsets, "frame_offsets"), ctypes.byref(desc), k_top,
+                                        _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
+                                        _stream(stream)))
+    return out_scores[:n_frames], out_idx[:k_top]
 
 
 def qer_batched_workspace_bytes(desc: QerDesc, n_queries: int, k_top: int) -> int:

@@ -34,6 +34,7 @@
 //   order, grouped heads reading their key head through a segment map);
 //   other head sizes take per-head kernels of their own.
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 
@@ -1710,6 +1711,41 @@ int qer_rank_from_m(const float* m, int32_t n_vis, const int32_t* offs, int32_t 
 
 }  // namespace cofie
 
+// ---- scratch of the entry point that allocates nothing ------------------------------
+// cofie_qer_rank_noalloc's scratch: a file-scope device array, one copy per
+// device the library runs on, held until the process ends.  Host code never
+// passes the array's name to a kernel or a copy (on the host it is only a
+// stand-in for the symbol): it uses the device address hipGetSymbolAddress
+// returns, taken once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[COFIE_QER_NOALLOC_SCRATCH_BYTES];
+
+namespace cofie {
+namespace {
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on each device, then cached).
+int noalloc_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return set_error(COFIE_EHIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= 64) return set_error(COFIE_EUNSUPPORTED, "device ordinal %d beyond 63", dev);
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return set_error(COFIE_EHIP, "hipGetSymbolAddress of the static scratch failed on device %d: %s", dev,
+                       hipGetErrorString(e));
+    addr[dev] = ptr;
+  }
+  *out = addr[dev];
+  return COFIE_OK;
+}
+
+}  // namespace
+}  // namespace cofie
+
 using namespace cofie;
 
 extern "C" {
@@ -1732,6 +1768,29 @@ int cofie_qer_rank(const void* Q, const void* K, const int32_t* frame_offsets,
   int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
   if (rc) return rc;
   return rank_impl(Q, K, frame_offsets, *heads, 1, nullptr, k_top, out_scores, out_idx,
+                   static_cast<hipStream_t>(stream));
+}
+
+int cofie_qer_rank_noalloc(const void* Q, const void* K, const int32_t* frame_offsets,
+                           const cofie_qer_desc* heads, int32_t k_top, float* out_scores,
+                           int32_t* out_idx, void* stream) {
+  clear_error();
+  int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
+  if (rc) return rc;
+  if (heads->workspace)
+    return set_error(COFIE_EINVAL, "heads->workspace must be NULL: this call uses the library's static scratch");
+  Arena ar;
+  carve_qer(ar, *heads, plan_qer(*heads));
+  if (ar.bytes() > (size_t)COFIE_QER_NOALLOC_SCRATCH_BYTES)
+    return set_error(COFIE_EUNSUPPORTED, "needs %zu bytes of scratch, more than the static %zu", ar.bytes(),
+                     (size_t)COFIE_QER_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  rc = noalloc_scratch(&ws);
+  if (rc) return rc;
+  cofie_qer_desc h = *heads;
+  h.workspace = ws;
+  h.workspace_bytes = COFIE_QER_NOALLOC_SCRATCH_BYTES;
+  return rank_impl(Q, K, frame_offsets, h, 1, nullptr, k_top, out_scores, out_idx,
                    static_cast<hipStream_t>(stream));
 }
 
