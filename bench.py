@@ -6,7 +6,8 @@ largest one: NGFF (histograms, novelty scores, keep rule with a calibrated
 threshold per stream) over 32 streams x 512 RGB frames of 448x448 (9.87 GB),
 then QER for the 4 queries of every stream (128 queries of 32 text tokens,
 28 heads, head dim 128, bf16): each query ranks its stream's NGFF candidates
-up to its timestamp, 144 visual tokens per frame, top-16.  Inputs are seeded
+up to its timestamp, 144 visual tokens per frame, top-16, all streams in one
+cofie_qer_rank_streams call (every stream's keys read once).  Inputs are seeded
 synthetic data resident in HBM (far larger than the 256 MiB last-level
 cache, so no step is served from the previous one).
 
@@ -40,6 +41,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--qer", choices=["one-launch", "per-stream"], default="one-launch",
+                    help="QER of the step: every stream's queries in one cofie_qer_rank_streams call, or one "
+                         "cofie_qer_rank_batched call per stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the CPU oracle sample (all host threads)")
@@ -165,11 +169,35 @@ def headline(args):
     q_bytes = sum(q.Q.numel() for q in qs) * 2
     # flops of the contraction as issued: every query of a stream against all its keys
     qer_flops = sum(2.0 * len(q.nf) * wl.n_q * q.n_vis * wl.H_q * wl.d for q in qs)
+    if args.qer == "one-launch":
+        # every stream's keys, candidates and queries side by side: one call
+        Kall = torch.cat([q.K for q in qs])
+        Qall = torch.cat([q.Q for q in qs])
+        base = np.concatenate([[0], np.cumsum([q.n_vis for q in qs])])
+        offs_all = torch.from_numpy(np.concatenate(
+            [[0]] + [synth.frame_offsets(np.full(q.n_cand, wl.tokens))[1:] + base[i] for i, q in enumerate(qs)]
+        ).astype(np.int32)).cuda()
+        lay = B.StreamsLayout([q.n_vis for q in qs], [q.n_cand for q in qs], [len(q.nf) for q in qs],
+                              np.concatenate([q.nf for q in qs]))
+        sdesc = B.qer_desc(wl.n_q, int(base[-1]), int(sum(q.n_cand for q in qs)), wl.H_q, wl.H_kv, wl.d)
+        sws = torch.empty(B.qer_streams_workspace_bytes(sdesc, lay, wl.k_top), dtype=torch.uint8, device="cuda")
+        w_all = torch.empty((n_queries, lay.max_frames), dtype=torch.float32, device="cuda")
+        idx_all = torch.empty((n_queries, wl.k_top), dtype=torch.int32, device="cuda")
+        for q in qs:  # the per-stream copies are not needed any more
+            q.K = q.Q = None
+        torch.cuda.empty_cache()
+
+        def qer_step():
+            B.cofie_qer_rank_streams(Qall, Kall, offs_all, lay, wl.k_top, out_scores=w_all, out_idx=idx_all,
+                                     workspace=sws)
+    else:
+        def qer_step():
+            for q in qs:
+                q.rank(B)
 
     def step(i):
         B.cofie_ngff_filter(frames, wl.bins, rule, out_scores=scores, out_mask=mask)
-        for q in qs:
-            q.rank(B)
+        qer_step()
 
     for i in range(args.warmup):
         step(i)
@@ -255,7 +283,8 @@ def headline(args):
                    "qer": {"queries": n_queries, "n_q": wl.n_q, "H_q": wl.H_q, "H_kv": wl.H_kv, "d": wl.d,
                            "tokens_per_frame": wl.tokens, "k_top": wl.k_top, "dtype": "bf16",
                            "score_mode": "logit", "candidates_ranked": ranked,
-                           "calls": "one cofie_qer_rank_batched per stream"}},
+                           "calls": ("one cofie_qer_rank_streams over all streams" if args.qer == "one-launch"
+                                     else "one cofie_qer_rank_batched per stream")}},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages": {

@@ -311,6 +311,45 @@ int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_of
                            const cofie_qer_desc* heads, int32_t n_queries, const int32_t* n_frames_per_query,
                            int32_t k_top, float* out_scores, int32_t* out_idx, void* stream);
 
+/* Several independent key sequences ranked in one launch (the multi-stream
+ * workload: every stream's queries rank prefixes of that stream's
+ * candidates, Sec. 3.1's streaming setting, Eqs. 6-8 per query).
+ *   K              device [n_vis][H_kv][d]: the sequences' keys one after the
+ *                  other; sequence s owns rows [stream_keys[s], stream_keys[s+1])
+ *   frame_offsets  device int32 [n_frames+1], one CSR over all sequences'
+ *                  frames (absolute key rows); sequence s owns frames
+ *                  [stream_frames[s], stream_frames[s+1]), whose key ranges are
+ *                  clamped to its own rows
+ *   Q              device [n_queries][n_q][H_q][d]; queries are grouped by
+ *                  sequence: sequence s owns queries [stream_queries[s],
+ *                  stream_queries[s+1]), n_queries = stream_queries[n_streams]
+ *   stream_keys    host int64 [n_streams+1], stream_frames and stream_queries
+ *                  host int32 [n_streams+1]: non-decreasing, starting at 0,
+ *                  ending at heads->n_vis, heads->n_frames and n_queries
+ *   n_frames_per_query  host int32 [n_queries]: query g ranks the first
+ *                  n_frames_per_query[g] frames of its sequence
+ *   out_scores     device float [n_queries][F], F = max(1, the largest
+ *                  sequence's frame count): row g holds w_f of its sequence's
+ *                  frames (-inf past its prefix)
+ *   out_idx        device int32 [n_queries][k_top]: each query's top-k as in
+ *                  cofie_qer_rank, as frame indices within its sequence.
+ * Each query's scores equal cofie_qer_rank given its sequence's keys and the
+ * CSR of its prefix, to rounding (the contraction order is the same; only
+ * the fp32 additions' grouping follows the work split).  LOGIT mode only,
+ * n_q a multiple of 16 and at most 128 (64 with grouped-query heads), else
+ * EUNSUPPORTED.  A sequence's queries are scored in chunks of at most 128
+ * rows (64 grouped), each chunk reading the sequence's keys once; the keys of
+ * all sequences stream in one score-kernel launch and the frame means and
+ * top-k of all queries in one more.  Workspace: the descriptor's, of
+ * cofie_qer_streams_workspace_bytes() bytes (0 for invalid arguments). */
+size_t cofie_qer_streams_workspace_bytes(const cofie_qer_desc* heads, int32_t n_streams, const int64_t* stream_keys,
+                                         const int32_t* stream_frames, const int32_t* stream_queries,
+                                         const int32_t* n_frames_per_query, int32_t k_top);
+int cofie_qer_rank_streams(const void* Q, const void* K, const int32_t* frame_offsets, const cofie_qer_desc* heads,
+                           int32_t n_streams, const int64_t* stream_keys, const int32_t* stream_frames,
+                           const int32_t* stream_queries, const int32_t* n_frames_per_query, int32_t k_top,
+                           float* out_scores, int32_t* out_idx, void* stream);
+
 /* ---- last-layer prefill attention with QER from its QK^T tiles ------------ */
 
 typedef struct cofie_attn_desc {

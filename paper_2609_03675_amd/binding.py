@@ -127,6 +127,8 @@ def lib() -> ctypes.CDLL:
         "cofie_gather_frames": (ctypes.c_int, [P, i64, i64, P, i32, P, i32, P, i64, P, P, P]),
         "cofie_qer_batched_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32, i32]),
         "cofie_qer_rank_batched": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, i32, P, P, P]),
+        "cofie_qer_streams_workspace_bytes": (sz, [ctypes.POINTER(QerDesc), i32, P, P, P, P, i32]),
+        "cofie_qer_rank_streams": (ctypes.c_int, [P, P, P, ctypes.POINTER(QerDesc), i32, P, P, P, P, i32, P, P, P]),
         "cofie_attn_qer_workspace_bytes": (sz, [ctypes.POINTER(AttnDesc)]),
         "cofie_attn_qer": (ctypes.c_int, [P, P, P, P, ctypes.POINTER(AttnDesc), i32, P, P, P, P]),
         "cofie_qer_k_from_ratio": (i64, [f64, i64]),
@@ -519,6 +521,52 @@ def cofie_qer_rank_batched(Q, K, frame_offsets, n_frames_per_query, k_top: int, 
                                         _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
                                         _stream(stream)))
     return out_scores[:, :n_frames], out_idx[:, :k_top]
+
+
+class StreamsLayout:
+    """Host arrays of cofie_qer_rank_streams: key rows, frames and queries of
+    each sequence (cumulative, int64 / int32 [n_streams + 1]) and each
+    query's prefix length (int32 [n_queries])."""
+
+    def __init__(self, keys_per_stream, frames_per_stream, queries_per_stream, n_frames_per_query):
+        import numpy as np
+        self.keys = np.concatenate([[0], np.cumsum(keys_per_stream)]).astype(np.int64)
+        self.frames = np.concatenate([[0], np.cumsum(frames_per_stream)]).astype(np.int32)
+        self.queries = np.concatenate([[0], np.cumsum(queries_per_stream)]).astype(np.int32)
+        self.nf = np.ascontiguousarray(n_frames_per_query, dtype=np.int32)
+        self.n_streams = len(keys_per_stream)
+        self.max_frames = max(1, int(np.max(frames_per_stream)) if len(frames_per_stream) else 1)
+
+    def args(self):
+        vp = ctypes.c_void_p
+        return (self.n_streams, self.keys.ctypes.data_as(vp), self.frames.ctypes.data_as(vp),
+                self.queries.ctypes.data_as(vp), self.nf.ctypes.data_as(vp))
+
+
+def qer_streams_workspace_bytes(desc: QerDesc, layout: StreamsLayout, k_top: int) -> int:
+    return int(lib().cofie_qer_streams_workspace_bytes(ctypes.byref(desc), *layout.args(), k_top))
+
+
+def cofie_qer_rank_streams(Q, K, frame_offsets, layout: StreamsLayout, k_top: int, scale: float = 0.0,
+                           out_scores=None, out_idx=None, workspace=None, stream=None):
+    """Q [n_queries][n_q][H_q][d] and K [n_vis][H_kv][d] of several key
+    sequences (layout), LOGIT mode.  Returns (w [n_queries][F], idx
+    [n_queries][k_top]) with F the largest sequence's frame count."""
+    import torch
+    n_queries, n_q, H_q, d = Q.shape
+    n_vis, H_kv, _ = K.shape
+    n_frames = frame_offsets.numel() - 1
+    dtype = BF16 if Q.dtype == torch.bfloat16 else F32
+    desc = qer_desc(n_q, n_vis, n_frames, H_q, H_kv, d, dtype, LOGIT, scale, workspace)
+    if out_scores is None:
+        out_scores = torch.empty((n_queries, layout.max_frames), dtype=torch.float32, device=Q.device)
+    if out_idx is None:
+        out_idx = torch.empty((n_queries, max(k_top, 1)), dtype=torch.int32, device=Q.device)
+    _check(lib().cofie_qer_rank_streams(_dev(Q, "Q"), _dev(K, "K") if n_vis > 0 else None,
+                                        _dev(frame_offsets, "frame_offsets"), ctypes.byref(desc), *layout.args(),
+                                        k_top, _dev(out_scores, "out_scores"), _dev(out_idx, "out_idx"),
+                                        _stream(stream)))
+    return out_scores, out_idx[:, :k_top]
 
 
 def attn_desc(L: int, H_q: int, H_kv: int, d: int, vis_begin: int, vis_end: int, n_frames: int,

@@ -34,7 +34,9 @@
 //   order, grouped heads reading their key head through a segment map);
 //   other head sizes take per-head kernels of their own.
 #include <cmath>
+#include <cstring>
 #include <mutex>
+#include <vector>
 
 #include "common.h"
 
@@ -102,6 +104,19 @@ struct Mma<float> {
 // conflict-free 16-byte LDS loads), double buffered: the fragments of phase
 // i+1 are fetched into registers at the start of phase i and written to LDS
 // one batch later.
+// One key sequence of a launch over several (cofie_qer_rank_streams) and the
+// stacked query rows that read it: its tiles sit at [tile0, tile0 + ntiles)
+// of the launch's tile space, side by side with the other sequences'.
+struct QerStreamDesc {
+  int64_t key0;    // first key row
+  int32_t n_keys;  // key rows
+  int32_t tile0;   // first tile
+  int32_t ntiles;  // ceil(n_keys / 16)
+  int32_t q0;      // first stacked query row (of each query term)
+  int32_t n_rows;  // query rows (whole queries, at most 16 NB)
+  int32_t pad;
+};
+
 struct ScoreLdsArgs {
   const uint8_t* K;   // [n_vis][Lc] elements
   const uint8_t* Qp;  // [P][nq_total][Lc] elements
@@ -144,12 +159,19 @@ struct ScoreLdsArgs {
   // keys of its first soft_nf[g] frames, [0, soft_offs[soft_nf[g]]); null: all
   const int32_t* soft_offs;
   const int32_t* soft_nf;
+  // several key sequences (LOGIT, one contraction slice; null: one): tiles is
+  // the total over them, and a workgroup's share is taken one sequence at a
+  // time, with that sequence's keys, token count and query rows
+  const QerStreamDesc* streams;
+  int32_t n_streams;
+  int32_t xcd_order;   // shares in XCD order: consecutive shares to the workgroups of one XCD
 };
 
 constexpr int kModeLogit = 0;     // Eq. 6-7: m_j = max_i a_ij
 constexpr int kModeSoftStats = 1; // SOFTMAX pass 1: per-head row statistics
 constexpr int kModeSoftProb = 2;  // SOFTMAX pass 2: m_j = max_i mean_h P^h_ij
 constexpr int kModeGqa = 4;       // flag: grouped query heads read their key head through a segment map
+constexpr int kModeSeq = 8;       // flag (LOGIT): several key sequences, each with its own query rows
 
 constexpr int kLdsWaves = 8;
 constexpr int kLdsThreads = kLdsWaves * 64;
@@ -222,6 +244,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   using M = Mma<T>;
   constexpr int BASE = MODE & 3;  // kModeLogit, kModeSoftStats or kModeSoftProb
   constexpr bool GQA = (MODE & kModeGqa) != 0;
+  constexpr bool SEQ = (MODE & kModeSeq) != 0;
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
@@ -238,6 +261,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   static_assert(NS == 1 || MB == 1, "split contractions take one tile per wave");
   static_assert(BASE == kModeLogit || (NS == 1 && P == 1), "SOFTMAX passes: one query term, no split");
   static_assert(!GQA || BASE != kModeLogit, "the segment map is for the SOFTMAX passes");
+  static_assert(!SEQ || (BASE == kModeLogit && NS == 1), "several key sequences: LOGIT, one slice");
   // [2][kPhaseU4]: [NS][S][P][NB][64] each; with NS > 1 followed by the
   // slice accumulators [NS - 1][TW][MB][NB][4][64] floats
   extern __shared__ uint4 qs[];
@@ -267,10 +291,19 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   const int pfull = VPS * a.nseg;
   const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
   const int64_t krow_u4 = a.k_row_u4;
-  const uint4* Kq = reinterpret_cast<const uint4*>(a.K) + (NS > 1 ? slice * a.split_u4 : 0);
+  const uint4* const K0 = reinterpret_cast<const uint4*>(a.K) + (NS > 1 ? slice * a.split_u4 : 0);
+  const uint4* Kq = K0;
   const uint4* Qq = reinterpret_cast<const uint4*>(a.Qp);
-  const int t_begin = (int)((int64_t)a.tiles * blockIdx.x / a.nwg);
-  const int t_end = (int)((int64_t)a.tiles * (blockIdx.x + 1) / a.nwg);
+  // This workgroup's share of the tiles.  Workgroups are dealt to the XCDs in
+  // turn (workgroup b to XCD b % 8), so with xcd_order the shares are ordered
+  // by XCD: the workgroups of one XCD take consecutive shares, and a key
+  // sequence's query rows are read into few XCDs' L2.
+  const int wg = a.xcd_order ? (int)((blockIdx.x & 7) * (a.nwg >> 3) + (blockIdx.x >> 3)) : (int)blockIdx.x;
+  const int f_begin = (int)((int64_t)a.tiles * wg / a.nwg);
+  const int f_end = (int)((int64_t)a.tiles * (wg + 1) / a.nwg);
+  int sidx = 0;  // several sequences: the first one whose tiles reach f_begin
+  if constexpr (SEQ)
+    while (sidx + 1 < a.n_streams && a.streams[sidx].tile0 + a.streams[sidx].ntiles <= f_begin) ++sidx;
   if (blockIdx.x == 0 && a.clear)
     for (int i = tid; i < a.nclear; i += kLdsThreads) a.clear[i] = 0;
 
@@ -364,6 +397,9 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   };
 
+  bool staged = false;  // an earlier round of this workgroup has used the phase buffers
+  // the rounds over tiles [t_begin, t_end) of the current key sequence
+  auto rounds = [&](const int t_begin, const int t_end) __attribute__((always_inline)) {
   for (int rb = t_begin; rb < t_end; rb += TW * MB) {
     // this wave's tiles: rb + tw + TW j.  Missing ones repeat tile rb (the
     // first tile of wave 0 in this round): their loads hit the cache and their
@@ -481,7 +517,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 
     uint4 fa[U][MB], fb[U][MB];
     if (a.nseg > 0) k_load(fa, 0);
-    if (rb != t_begin) barrier_lds();  // previous round's readers are done
+    if (staged) barrier_lds();  // previous round's readers are done
+    staged = true;
     uint4 qr[kQRegs];
     q_load(0, qr);
     q_store(0, qr);
@@ -667,7 +704,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t tok = tile * 16 + g4 * 4 + r;
-          if (a.group_rows == 0) {
+          if (!SEQ && a.group_rows == 0) {
             float v = -INFINITY;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
@@ -690,7 +727,11 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
             int gcur = -1;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
-              float v = qok[nb] ? acc[j][nb][r] : -INFINITY;
+              // blocks past the chunk's rows belong to no query of it: they
+              // are skipped (their g would be a row past m or another
+              // sequence's query)
+              if (nb * 16 >= a.n_q) break;
+              float v = acc[j][nb][r];
 #pragma unroll
               for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
               const int g = (a.q0 + nb * 16) / a.group_rows;
@@ -702,16 +743,34 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
                 vg = fmaxf(vg, v);
               }
             }
-            store(gcur, vg);
+            if (gcur >= 0) store(gcur, vg);
           }
         }
       }
     }
   }
+  };
+  if constexpr (SEQ) {
+    // the share, one key sequence at a time
+    for (int fb = f_begin; fb < f_end && sidx < a.n_streams;) {
+      const QerStreamDesc sd = a.streams[sidx++];
+      const int s_end = sd.tile0 + sd.ntiles;
+      if (s_end <= fb || sd.ntiles <= 0) continue;
+      const int tb = fb - sd.tile0, te = (s_end < f_end ? s_end : f_end) - sd.tile0;
+      fb = sd.tile0 + te;
+      Kq = K0 + sd.key0 * krow_u4;
+      a.n_vis = sd.n_keys;
+      a.q0 = sd.q0;
+      a.n_q = sd.n_rows;  // whole 16-row blocks (the epilogue skips the others)
+      rounds(tb, te);
+    }
+  } else {
+    rounds(f_begin, f_end);
+  }
   if constexpr (BASE == kModeSoftStats) {
     // the rounds this workgroup does not run leave empty statistics (a zero
     // sum), which the merge skips
-    const int nr = (t_end - t_begin + TW * MB - 1) / (TW * MB);
+    const int nr = (f_end - f_begin + TW * MB - 1) / (TW * MB);
     for (int rr = nr; rr < a.rounds; ++rr) {
       const int64_t slot = ((int64_t)blockIdx.x * kLdsWaves + wave) * a.rounds + rr;
       for (int i = lane; i < a.H * a.n_q; i += 64) {
@@ -915,6 +974,17 @@ __device__ void topk_block(const uint32_t* keys_g, int32_t n_frames, int32_t k_t
   for (int i = k + tid; i < k_top; i += nthr) out_idx[i] = -1;
 }
 
+// One query of a launch over several key sequences: its sequence's frames
+// are [frame0, frame0 + n_frames) of the launch's CSR, whose key rows start
+// at key0 (n_keys rows), and it ranks the first nf of them.
+struct QerQueryDesc {
+  int64_t key0;
+  int32_t n_keys;
+  int32_t frame0;
+  int32_t n_frames;
+  int32_t nf;
+};
+
 // Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
 // fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
 // Several queries (blockIdx.y): query g reads row g of m, covers its first
@@ -923,28 +993,42 @@ __device__ void topk_block(const uint32_t* keys_g, int32_t n_frames, int32_t k_t
 // trees != null (1024 threads; one zeroed arrival tree of tree_ints ints per
 // query): the last workgroup of query g to finish also selects its top k
 // (Eq. 8) into row g of out_idx, so the selection needs no launch of its own.
+// qd != null (several key sequences): query g takes its frames, key rows and
+// prefix from qd[g]; n_vis and n_frames are then only the row strides of m
+// and of the scores and keys.
 __global__ __launch_bounds__(1024) void qer_frame_mean_kernel(const float* m, int32_t n_vis,
                                                               const int32_t* offs, int32_t n_frames,
                                                               float* out_scores, uint32_t* keys,
                                                               const int32_t* nf_q, int32_t* trees,
                                                               int32_t tree_ints, int32_t tree_stride,
-                                                              int32_t k_top, int32_t* out_idx) {
+                                                              int32_t k_top, int32_t* out_idx,
+                                                              const QerQueryDesc* qd) {
   const int lane = threadIdx.x & 63;
   const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   const int64_t g = blockIdx.y;
-  const int32_t nf = nf_q ? nf_q[g] : n_frames;
+  int32_t nf = nf_q ? nf_q[g] : n_frames;
+  int32_t nfr = n_frames, nv = n_vis;
+  int64_t key0 = 0;
   m += g * n_vis;
   out_scores += g * n_frames;
   keys += g * n_frames;
-  if (f < n_frames && f >= nf) {
+  if (qd) {
+    const QerQueryDesc q = qd[g];
+    offs += q.frame0;
+    key0 = q.key0;
+    nv = q.n_keys;
+    nfr = q.n_frames;
+    nf = q.nf;
+  }
+  if (f < nfr && f >= nf) {
     if (lane == 0) {
       out_scores[f] = -INFINITY;
       st_agent(keys + f, order_key(-INFINITY));
     }
-  } else if (f < n_frames) {
-    int lo = offs[f], hi = offs[f + 1];
-    lo = lo < 0 ? 0 : (lo > n_vis ? n_vis : lo);
-    hi = hi < lo ? lo : (hi > n_vis ? n_vis : hi);
+  } else if (f < nfr) {
+    int64_t lo64 = (int64_t)offs[f] - key0, hi64 = (int64_t)offs[f + 1] - key0;
+    const int lo = (int)(lo64 < 0 ? 0 : (lo64 > nv ? nv : lo64));
+    const int hi = (int)(hi64 < lo ? lo : (hi64 > nv ? nv : hi64));
     // four loads in flight per lane (clamped indices, masked adds)
     double s = 0.0;
     for (int j0 = lo + lane; j0 < hi; j0 += 256) {
@@ -1417,7 +1501,7 @@ template <typename T, int MB, int P, int NS, int MODE>
 int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, size_t lds, hipStream_t s) {
   // 128 query rows in one pass: LOGIT, one query term, one tile per wave
   // (two spill)
-  if constexpr (MB == 1 && P == 1 && MODE == kModeLogit) {
+  if constexpr (MB == 1 && P == 1 && NS == 1 && MODE == kModeLogit) {
     if (NB == 8) return launch_lds_t<T, 1, 8, 1, NS, MODE>(sa, L, lds, s);
   }
   switch (NB) {
@@ -1679,17 +1763,199 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
     const QerTrees tr = qer_trees(h.n_frames);
     return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, n_queries), dim3(1024), 0, s,
                   (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores, w.keys, (const int32_t*)w.nf,
-                  w.done, tr.ints, tr.stride, k_top, out_idx);
+                  w.done, tr.ints, tr.stride, k_top, out_idx, (const QerQueryDesc*)nullptr);
   }
   if (h.n_frames > 0) {
     rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4), n_queries),
                 dim3(256), 0, s, (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores,
-                w.keys, (const int32_t*)w.nf, (int32_t*)nullptr, 0, 0, k_top, out_idx);
+                w.keys, (const int32_t*)w.nf, (int32_t*)nullptr, 0, 0, k_top, out_idx, (const QerQueryDesc*)nullptr);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
   return launch("qer_topk", qer_topk_kernel, dim3(n_queries), dim3(1024), 0, s, (const uint32_t*)w.keys,
                 h.n_frames, k_top, out_idx, (const int32_t*)w.nf);
+}
+
+// ---- several key sequences in one launch (cofie_qer_rank_streams) -------------------
+// The sequences' stacked query rows are cut into chunks of whole queries, at
+// most 128 rows (64 with the three query terms of a folded grouped-query
+// contraction), each chunk a QerStreamDesc that reads its sequence's keys;
+// every query gets a QerQueryDesc for the frame means.  Both tables are
+// copied to the device with one copy per call.
+struct StreamsPlan {
+  std::vector<QerStreamDesc> seq;
+  std::vector<QerQueryDesc> qry;
+  int64_t max_keys = 0;    // row stride of m
+  int32_t max_frames = 0;  // row stride of the scores and their sort keys
+  int64_t tiles = 0;       // over all chunks
+  int NB = 1;              // 16-row blocks of the widest chunk (1-4, or 8)
+  int32_t n_queries = 0;
+};
+
+int plan_streams(const cofie_qer_desc& h, const QerPlan& p, int32_t n_streams, const int64_t* stream_keys,
+                 const int32_t* stream_frames, const int32_t* stream_queries, const int32_t* nf, StreamsPlan& sp) {
+  if (n_streams < 1) return set_error(COFIE_EINVAL, "n_streams = %d must be >= 1", n_streams);
+  if (!stream_keys || !stream_frames || !stream_queries)
+    return set_error(COFIE_EINVAL, "stream_keys, stream_frames and stream_queries must not be NULL");
+  if (stream_keys[0] != 0 || stream_frames[0] != 0 || stream_queries[0] != 0)
+    return set_error(COFIE_EINVAL, "stream_keys, stream_frames and stream_queries must start at 0");
+  if (stream_keys[n_streams] != h.n_vis || stream_frames[n_streams] != h.n_frames)
+    return set_error(COFIE_EINVAL, "stream_keys[n_streams] = %lld and stream_frames[n_streams] = %d must equal "
+                     "n_vis = %d and n_frames = %d", (long long)stream_keys[n_streams], stream_frames[n_streams],
+                     h.n_vis, h.n_frames);
+  if (h.score_mode != COFIE_SCORE_LOGIT)
+    return set_error(COFIE_EUNSUPPORTED, "several key sequences are ranked in LOGIT mode only");
+  const int rows_max = p.P == 1 ? 128 : 64;
+  if (h.n_q % 16 != 0 || h.n_q > rows_max)
+    return set_error(COFIE_EUNSUPPORTED, "several key sequences need n_q (%d) a multiple of 16 and at most %d",
+                     h.n_q, rows_max);
+  const int32_t nq = stream_queries[n_streams];
+  if (nq < 1) return set_error(COFIE_EINVAL, "no queries");
+  if (!nf) return set_error(COFIE_EINVAL, "n_frames_per_query is NULL");
+  if ((int64_t)nq * h.n_q * h.H_q * h.d >= (int64_t(1) << 31)) return set_error(COFIE_EUNSUPPORTED, "queries too large");
+  const int32_t per_chunk = rows_max / h.n_q;  // queries per chunk
+  sp = StreamsPlan();
+  sp.n_queries = nq;
+  int widest = 0;
+  for (int32_t st = 0; st < n_streams; ++st) {
+    const int64_t k0 = stream_keys[st], nk = stream_keys[st + 1] - k0;
+    const int32_t f0 = stream_frames[st], nfr = stream_frames[st + 1] - f0;
+    const int32_t g0 = stream_queries[st], ng = stream_queries[st + 1] - g0;
+    if (nk < 0 || nfr < 0 || ng < 0) return set_error(COFIE_EINVAL, "sequence %d: decreasing stream arrays", st);
+    if (nk >= (int64_t(1) << 31) - 16) return set_error(COFIE_EUNSUPPORTED, "sequence %d: too many keys", st);
+    sp.max_keys = std::max(sp.max_keys, nk);
+    sp.max_frames = std::max(sp.max_frames, nfr);
+    for (int32_t g = g0; g < g0 + ng; ++g) {
+      if (nf[g] < 0 || nf[g] > nfr)
+        return set_error(COFIE_EINVAL, "query %d: %d frames outside [0, %d] (its sequence's frames)", g, nf[g], nfr);
+      sp.qry.push_back(QerQueryDesc{k0, (int32_t)nk, f0, nfr, nf[g]});
+    }
+    const int32_t nt = (int32_t)ceil_div(nk, 16);
+    for (int32_t c = 0; c < ng && nt > 0; c += per_chunk) {
+      const int32_t cg = std::min(per_chunk, ng - c);
+      if (sp.tiles + nt >= (int64_t(1) << 31)) return set_error(COFIE_EUNSUPPORTED, "too many tiles");
+      sp.seq.push_back(QerStreamDesc{k0, (int32_t)nk, (int32_t)sp.tiles, nt, (g0 + c) * h.n_q, cg * h.n_q, 0});
+      sp.tiles += nt;
+      widest = std::max(widest, cg * h.n_q);
+    }
+  }
+  const int nb = (widest + 15) / 16;
+  sp.NB = nb > 4 ? 8 : (nb < 1 ? 1 : nb);
+  return COFIE_OK;
+}
+
+struct StreamsScratch {
+  float* m;           // [n_queries][max_keys]
+  uint32_t* keys;     // [n_queries][max_frames]
+  uint8_t* qp;        // folded queries (grouped heads)
+  uint8_t* meta;      // QerStreamDesc[seq] then QerQueryDesc[n_queries]
+  int32_t* done;      // [n_queries][tree ints] arrival trees of the frame-mean kernel
+};
+
+size_t meta_bytes(const StreamsPlan& sp) {
+  return sp.seq.size() * sizeof(QerStreamDesc) + sp.qry.size() * sizeof(QerQueryDesc);
+}
+
+StreamsScratch carve_streams(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, const StreamsPlan& sp) {
+  StreamsScratch w;
+  w.m = ar.take<float>((size_t)sp.n_queries * std::max<int64_t>(sp.max_keys, 1));
+  w.keys = ar.take<uint32_t>((size_t)sp.n_queries * std::max(sp.max_frames, 1));
+  w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * sp.n_queries * h.n_q * p.Lc * p.esize) : nullptr;
+  w.meta = ar.take<uint8_t>(meta_bytes(sp));
+  w.done = ar.take<int32_t>((size_t)sp.n_queries * qer_trees(std::max(sp.max_frames, 1)).ints);
+  return w;
+}
+
+constexpr int kSeqLogit = kModeLogit | kModeSeq;
+
+int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets, const cofie_qer_desc& h,
+                      const QerPlan& p, const StreamsPlan& sp, int32_t k_top, float* out_scores, int32_t* out_idx,
+                      hipStream_t s) {
+  Arena plan;
+  carve_streams(plan, h, p, sp);
+  Scratch scratch;
+  int rc = scratch.acquire(h.workspace, h.workspace_bytes, plan.bytes(), s);
+  if (rc) return rc;
+  Arena ar;
+  ar.base = scratch.ptr();
+  const StreamsScratch w = carve_streams(ar, h, p, sp);
+  std::vector<uint8_t> meta(meta_bytes(sp));
+  std::memcpy(meta.data(), sp.seq.data(), sp.seq.size() * sizeof(QerStreamDesc));
+  std::memcpy(meta.data() + sp.seq.size() * sizeof(QerStreamDesc), sp.qry.data(),
+              sp.qry.size() * sizeof(QerQueryDesc));
+  if (hipMemcpyAsync(w.meta, meta.data(), meta.size(), hipMemcpyHostToDevice, s) != hipSuccess)
+    return set_error(COFIE_EHIP, "copying the sequence tables failed");
+  const auto* seq_d = reinterpret_cast<const QerStreamDesc*>(w.meta);
+  const auto* qry_d = reinterpret_cast<const QerQueryDesc*>(w.meta + sp.seq.size() * sizeof(QerStreamDesc));
+  const bool bf16 = h.dtype == COFIE_BF16;
+  const int32_t R = sp.n_queries * h.n_q;
+  const uint8_t* qp = static_cast<const uint8_t*>(Q);
+  if (p.fold) {
+    const int64_t total = (int64_t)R * p.Lc;
+    const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 8192);
+    rc = bf16 ? launch("qer_fold", qer_fold_kernel<bf16_t>, dim3(grid), dim3(256), 0, s,
+                       static_cast<const bf16_t*>(Q), R, h.H_q, h.H_kv, h.d, (void*)w.qp)
+              : launch("qer_fold", qer_fold_kernel<float>, dim3(grid), dim3(256), 0, s,
+                       static_cast<const float*>(Q), R, h.H_q, h.H_kv, h.d, (void*)w.qp);
+    if (rc) return rc;
+    qp = w.qp;
+  }
+  const QerTrees tr = qer_trees(std::max(sp.max_frames, 1));
+  // the score kernel: one launch over every chunk's tiles (its workgroup 0
+  // clears the frame-mean kernel's arrival trees, so it runs even without keys)
+  const int cus = device_cu_count();
+  LdsPlan L = plan_score_lds(std::max<int64_t>(sp.tiles, 1) * 16, p.Lc, p.esize, p.P, p.P * sp.NB, cus, false);
+  if (sp.NB == 8 && L.MB != 1) {  // eight blocks take one tile per wave (two spill)
+    L = plan_score_lds(std::min<int64_t>(sp.tiles, (int64_t)cus * kLdsWaves) * 16, p.Lc, p.esize, p.P,
+                       p.P * sp.NB, cus, false);
+  }
+  ScoreLdsArgs sa{};
+  sa.K = static_cast<const uint8_t*>(K);
+  sa.Qp = qp;
+  sa.n_vis = 0;  // per sequence
+  sa.nq_total = R;
+  sa.group_rows = h.n_q;
+  sa.m_stride = std::max<int64_t>(sp.max_keys, 1);
+  sa.Lc = (int32_t)p.Lc;
+  sa.tiles = (int32_t)sp.tiles;
+  const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
+  sa.scale = (float)((double)base_scale / (double)h.H_q);
+  sa.m = w.m;
+  sa.clear = w.done;
+  sa.nclear = sp.n_queries * tr.ints;
+  sa.accumulate = 0;
+  sa.nseg = L.nseg;
+  sa.ksteps = L.ksteps;
+  sa.S = L.S;
+  sa.lgS = L.lgS;
+  sa.nphase = L.nphase;
+  sa.nwg = std::max(1, (L.nwg >= 8 ? L.nwg & ~7 : L.nwg));
+  sa.xcd_order = sa.nwg % 8 == 0 ? 1 : 0;
+  sa.split_u4 = L.split_u4;
+  sa.k_row_u4 = (int32_t)(p.Lc * (int64_t)p.esize / 16);
+  sa.streams = seq_d;
+  sa.n_streams = (int32_t)sp.seq.size();
+  L.nwg = sa.nwg;
+  if (bf16) {
+    if (sp.NB == 8)
+      rc = launch_lds_t<bf16_t, 1, 8, 1, 1, kSeqLogit>(sa, L, L.lds, s);
+    else if (p.P == 3)
+      rc = L.MB == 1 ? launch_lds_nb<bf16_t, 1, 3, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s)
+                     : launch_lds_nb<bf16_t, 2, 3, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s);
+    else
+      rc = L.MB == 1 ? launch_lds_nb<bf16_t, 1, 1, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s)
+                     : launch_lds_nb<bf16_t, 2, 1, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s);
+  } else {
+    if (sp.NB == 8)
+      rc = launch_lds_t<float, 1, 8, 1, 1, kSeqLogit>(sa, L, L.lds, s);
+    else
+      rc = L.MB == 1 ? launch_lds_nb<float, 1, 1, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s)
+                     : launch_lds_nb<float, 2, 1, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s);
+  }
+  if (rc) return rc;
+  return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, sp.n_queries), dim3(1024), 0, s,
+                (const float*)w.m, (int32_t)sa.m_stride, frame_offsets, std::max(sp.max_frames, 1), out_scores,
+                w.keys, (const int32_t*)nullptr, w.done, tr.ints, tr.stride, k_top, out_idx, qry_d);
 }
 
 }  // namespace
@@ -1701,7 +1967,7 @@ int qer_rank_from_m(const float* m, int32_t n_vis, const int32_t* offs, int32_t 
   if (n_frames > 0) {
     int rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(n_frames, 4), 1), dim3(256),
                     0, s, m, n_vis, offs, n_frames, out_scores, keys, (const int32_t*)nullptr, (int32_t*)nullptr,
-                    0, 0, k_top, out_idx);
+                    0, 0, k_top, out_idx, (const QerQueryDesc*)nullptr);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
@@ -1828,6 +2094,38 @@ int cofie_qer_rank_batched(const void* Q, const void* K, const int32_t* frame_of
     return set_error(COFIE_EUNSUPPORTED, "queries too large");
   return rank_impl(Q, K, frame_offsets, h, n_queries, n_frames_per_query, k_top, out_scores, out_idx,
                    static_cast<hipStream_t>(stream));
+}
+
+size_t cofie_qer_streams_workspace_bytes(const cofie_qer_desc* heads, int32_t n_streams, const int64_t* stream_keys,
+                                         const int32_t* stream_frames, const int32_t* stream_queries,
+                                         const int32_t* n_frames_per_query, int32_t k_top) {
+  static const uint64_t dummy[4] = {0, 0, 0, 0};
+  static const int32_t doffs = 0;
+  float dscore;
+  int32_t didx;
+  if (validate_qer(dummy, dummy, &doffs, heads, k_top, &dscore, &didx)) return 0;
+  const QerPlan p = plan_qer(*heads);
+  StreamsPlan sp;
+  if (plan_streams(*heads, p, n_streams, stream_keys, stream_frames, stream_queries, n_frames_per_query, sp)) return 0;
+  Arena ar;
+  carve_streams(ar, *heads, p, sp);
+  return ar.bytes();
+}
+
+int cofie_qer_rank_streams(const void* Q, const void* K, const int32_t* frame_offsets, const cofie_qer_desc* heads,
+                           int32_t n_streams, const int64_t* stream_keys, const int32_t* stream_frames,
+                           const int32_t* stream_queries, const int32_t* n_frames_per_query, int32_t k_top,
+                           float* out_scores, int32_t* out_idx, void* stream) {
+  clear_error();
+  int rc = validate_qer(Q, K, frame_offsets, heads, k_top, out_scores, out_idx);
+  if (rc) return rc;
+  if (!out_scores) return set_error(COFIE_EINVAL, "out_scores is NULL");
+  const QerPlan p = plan_qer(*heads);
+  StreamsPlan sp;
+  rc = plan_streams(*heads, p, n_streams, stream_keys, stream_frames, stream_queries, n_frames_per_query, sp);
+  if (rc) return rc;
+  return rank_streams_impl(Q, K, frame_offsets, *heads, p, sp, k_top, out_scores, out_idx,
+                           static_cast<hipStream_t>(stream));
 }
 
 int64_t cofie_qer_k_from_ratio(double rho, int64_t n) {

@@ -226,3 +226,33 @@ def test_batched_qer_validation(L):
                                     None) == B.COFIE_EUNSUPPORTED
     assert B.lib().cofie_qer_batched_workspace_bytes(ctypes.byref(d), 3, 2) > \
         B.lib().cofie_qer_workspace_bytes(ctypes.byref(d), 2)
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="host-only validation checks")
+def test_streams_qer_validation(L):
+    """cofie_qer_rank_streams refuses inconsistent sequence tables, prefixes
+    past a sequence's frames, SOFTMAX and query widths it does not tile, all
+    before any GPU work; its workspace holds one m row per query as long as
+    the longest sequence."""
+    lay = B.StreamsLayout([40, 0, 24], [3, 0, 2], [2, 1, 1], [3, 1, 0, 2])
+    d = B.qer_desc(16, 64, 5, 2, 2, 32)
+
+    def call(desc, layout, k=2):
+        return L.cofie_qer_rank_streams(FAKE, FAKE, FAKE, ctypes.byref(desc), *layout.args(), k, FAKE, FAKE, None)
+
+    ws = B.qer_streams_workspace_bytes(d, lay, 2)
+    assert ws >= 4 * 40 * 4
+    bad = B.StreamsLayout([40, 0, 24], [3, 0, 2], [2, 1, 1], [3, 1, 0, 3])   # 3 > the third sequence's 2 frames
+    assert call(d, bad) == B.COFIE_EINVAL
+    assert B.qer_streams_workspace_bytes(d, bad, 2) == 0
+    short = B.StreamsLayout([40, 0, 20], [3, 0, 2], [2, 1, 1], [3, 1, 0, 2])  # keys end at 60 != n_vis 64
+    assert call(d, short) == B.COFIE_EINVAL
+    none = B.StreamsLayout([40, 0, 24], [3, 0, 2], [0, 0, 0], [])
+    assert call(d, none) == B.COFIE_EINVAL
+    soft = B.qer_desc(16, 64, 5, 2, 2, 32, score_mode=B.SOFTMAX)
+    assert call(soft, lay) == B.COFIE_EUNSUPPORTED
+    assert call(B.qer_desc(20, 64, 5, 2, 2, 32), lay) == B.COFIE_EUNSUPPORTED   # n_q not a multiple of 16
+    assert call(B.qer_desc(144, 64, 5, 2, 2, 32), lay) == B.COFIE_EUNSUPPORTED  # more than 128 rows
+    assert call(B.qer_desc(80, 64, 5, 4, 2, 32), lay) == B.COFIE_EUNSUPPORTED   # grouped heads: at most 64
+    assert L.cofie_qer_rank_streams(FAKE, FAKE, FAKE, ctypes.byref(d), 0, None, None, None, None, 2, FAKE, FAKE,
+                                    None) == B.COFIE_EINVAL
