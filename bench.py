@@ -87,7 +87,7 @@ def main():
 
 
 NGFF_KERNELS = ("ngff_fill", "ngff_hist", "ngff_keep", "ngff_band", "ngff_next", "ngff_select")
-QER_KERNELS = ("qer_fold", "qer_score", "qer_frame_mean", "qer_topk")
+QER_KERNELS = ("qer_fold", "qer_qop", "qer_score", "qer_frame_mean", "qer_topk")
 
 
 class MsQuery:

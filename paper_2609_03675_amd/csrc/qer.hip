@@ -782,6 +782,364 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   }
 }
 
+// ---- several key sequences, up to 128 query rows per chunk: qer_seq_kernel ----------
+// The multi-stream workload stacks 4 queries of 32 rows per stream: 128 rows
+// per key tile.  There the general score kernel (one tile per wave, query
+// fragments restaged through registers with a bank swizzle every round)
+// reads 1 KiB of query fragments from LDS per MFMA and stalls at every round
+// boundary.  This kernel instead:
+//  * takes the query side from a copy in MFMA operand order, written once per
+//    call by qer_qop_kernel ([chunk][virtual step][16-row block][lane] x 16 B,
+//    rows past the chunk zero), so a phase of query fragments is a contiguous
+//    copy, global to registers to LDS, 2 x 16 B per thread and batch, and every
+//    fragment read is 1 KiB of consecutive LDS;
+//  * gives each wave two tiles of 16 keys (MB = 2): every fragment read from
+//    LDS feeds two MFMAs, half the LDS traffic per key byte;
+//  * runs one pipeline over all the rounds of the workgroup's share: the key
+//    loads of the next round's first batch and the query fragments of its
+//    first phase are in flight while the current round finishes, so a round
+//    boundary costs only the epilogue.
+// Key rows stream in 128-byte segments of 8 rows per load, turned into MFMA
+// operands by a lane select and a DPP rotation as in qer_score_kernel.
+struct SeqArgs {
+  const uint8_t* K;          // [n_vis][Lc] bf16
+  const uint4* Qop;          // [chunks][ksteps][8][64] operand-order query fragments
+  const QerStreamDesc* seq;  // one per chunk
+  int32_t n_seq;
+  int32_t tiles;             // over all chunks
+  int32_t nwg;
+  int32_t xcd_order;
+  int32_t nseg;              // segments (1024 / R bytes) per key row: ksteps = (16 / R) nseg, a multiple of kSeqS
+  int32_t k_row_u4;          // 16-byte chunks per key row
+  float scale;
+  float* m;                  // [n_queries][m_stride]
+  int64_t m_stride;
+  int32_t group_rows;        // rows per query (a multiple of 16)
+  int32_t* clear;            // workgroup 0 zeroes clear[0, nclear)
+  int32_t nclear;
+};
+
+constexpr int kSeqNB = 8;                         // 16-row blocks: 128 query rows
+constexpr int kSeqS = 8;                          // virtual steps per phase
+constexpr int kSeqPhaseU4 = kSeqS * kSeqNB * 64;  // uint4 per phase (64 KiB)
+constexpr int kSeqTab = 64;                       // chunks a workgroup's share may span
+constexpr size_t kSeqLds = 2 * (size_t)kSeqPhaseU4 * 16 + kSeqTab * sizeof(QerStreamDesc);
+
+// Operand-order copy of the stacked queries: chunk c (rows [q0, q0 + n_rows)
+// of the stacked query rows), virtual step v = 2 m + k, block nb, lane l: the
+// 16 bytes of row q0 + 16 nb + l % 16 at 16-byte column 8 m + 2 (l / 16) + k
+// (zero past n_rows).  With keys read R rows per load (segments of 64 / R
+// 16-byte columns, VPS = 16 / R virtual steps each) step v = VPS m + k takes
+// column (64 / R) m + VPS (l / 16) + k.
+__global__ void qer_qop_kernel(const uint4* Q, int64_t row_u4, const QerStreamDesc* seq, int32_t n_seq,
+                               int32_t ksteps, int32_t R, uint4* out) {
+  const int vps = 16 / R, segc = 64 / R;
+  const int64_t per = (int64_t)ksteps * kSeqNB * 64;
+  const int64_t total = per * n_seq;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(e / per);
+    const int64_t r = e - c * per;
+    const int v = (int)(r / (kSeqNB * 64)), nb = (int)((r / 64) % kSeqNB), l = (int)(r & 63);
+    const int row = 16 * nb + (l & 15);
+    const int col = segc * (v / vps) + vps * (l >> 4) + v % vps;
+    const QerStreamDesc sd = seq[c];
+    out[e] = row < sd.n_rows ? Q[(int64_t)(sd.q0 + row) * row_u4 + col] : uint4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int U, int R>
+__global__ __launch_bounds__(kLdsThreads) void qer_seq_kernel(SeqArgs a) {
+  constexpr int MB = 2, NB = kSeqNB, TW = kLdsWaves;
+  constexpr int VPS = 16 / R, SEGC = 64 / R;  // virtual steps (loads per tile) and 16-byte columns per segment
+  constexpr int BPP = kSeqS / U;                    // batches per phase
+  constexpr int CP = kSeqPhaseU4 / kLdsThreads / BPP;  // uint4 each thread copies per batch
+  static_assert(U % VPS == 0 && kSeqS % U == 0 && CP >= 1, "whole segments per batch, whole batches per phase");
+  extern __shared__ uint4 qs[];  // [2][kSeqPhaseU4]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4, own = r16 / R;  // own: the load holding this lane's row
+  const int ksteps = VPS * a.nseg, bpr = ksteps / U;  // batches per round
+  const int wg = a.xcd_order ? (int)((blockIdx.x & 7) * (a.nwg >> 3) + (blockIdx.x >> 3)) : (int)blockIdx.x;
+  const int f_begin = (int)((int64_t)a.tiles * wg / a.nwg);
+  const int f_end = (int)((int64_t)a.tiles * (wg + 1) / a.nwg);
+  if (blockIdx.x == 0 && a.clear)
+    for (int i = tid; i < a.nclear; i += kLdsThreads) a.clear[i] = 0;
+
+  // rounds of the share: RoundDesc of the current and of the next round
+  struct Rnd {
+    int sidx;      // chunk
+    int tb, te;    // first tile of the round, end of the chunk's part of the share (chunk tiles)
+    int nmb;       // this wave's valid tiles
+  };
+  int sidx0 = 0;
+  while (sidx0 + 1 < a.n_seq && a.seq[sidx0].tile0 + a.seq[sidx0].ntiles <= f_begin) ++sidx0;
+  // the chunks of the share, in LDS past the phase buffers (at most kSeqTab:
+  // the host plans shares that span no more), so that a round change reads
+  // its descriptors without a memory-counter wait behind the loads in flight
+  QerStreamDesc* tab = reinterpret_cast<QerStreamDesc*>(qs + 2 * kSeqPhaseU4);
+  for (int i = tid; i < kSeqTab && sidx0 + i < a.n_seq; i += kLdsThreads) tab[i] = a.seq[sidx0 + i];
+  __syncthreads();
+  const int tab_end = sidx0 + kSeqTab < a.n_seq ? sidx0 + kSeqTab : a.n_seq;
+  auto seq_at = [&](int i) __attribute__((always_inline)) { return tab[i - sidx0]; };
+  // the round after r (or r.sidx < 0 at the end of the share)
+  auto first_of = [&](int si, int from) __attribute__((always_inline)) {
+    Rnd r{-1, 0, 0, 0};
+    for (; si < tab_end; ++si) {
+      const QerStreamDesc sd = seq_at(si);
+      const int s_end = sd.tile0 + sd.ntiles;
+      if (sd.ntiles <= 0 || s_end <= from) continue;
+      if (sd.tile0 >= f_end) break;
+      r.sidx = si;
+      r.tb = (from > sd.tile0 ? from : sd.tile0) - sd.tile0;
+      r.te = (s_end < f_end ? s_end : f_end) - sd.tile0;
+      break;
+    }
+    return r;
+  };
+  auto next_of = [&](const Rnd& r) __attribute__((always_inline)) {
+    if (r.tb + TW * MB < r.te) return Rnd{r.sidx, r.tb + TW * MB, r.te, 0};
+    const QerStreamDesc sd = seq_at(r.sidx);
+    return first_of(r.sidx + 1, sd.tile0 + r.te);
+  };
+  auto fill = [&](Rnd& r) __attribute__((always_inline)) {
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) n += (r.tb + wave + TW * j < r.te) ? 1 : 0;
+    r.nmb = n;
+  };
+  Rnd cur = first_of(sidx0, f_begin);
+  if (cur.sidx < 0) return;
+  fill(cur);
+  Rnd nxt = next_of(cur);
+  if (nxt.sidx >= 0) fill(nxt);
+
+  // key load offsets (16-byte units from the chunk's first key row) of this
+  // lane for tile j and load q of a segment: row 8 q + lane % 8 of the tile
+  // (clamped to the sequence), chunk 2 g4 + (lane % 16 / 8 - q) mod 2
+  const uint4* const K0 = reinterpret_cast<const uint4*>(a.K);
+  // key load offsets (16-byte units from the chunk's first key row) of this
+  // lane for tile j and load q of a segment: row 8 q + lane % 8 of the tile
+  // (clamped to the sequence), chunk 2 g4 + (lane % 16 / 8 - q) mod 2; for
+  // the current round (c) and the next (n)
+  const uint4* kc_base = K0;
+  const uint4* kn_base = K0;
+  int32_t kc_off[MB * VPS], kn_off[MB * VPS];
+  auto koff = [&](const Rnd& r, const uint4*& base, int32_t (&off)[MB * VPS]) __attribute__((always_inline)) {
+    const QerStreamDesc sd = seq_at(r.sidx);
+    base = K0 + sd.key0 * a.k_row_u4;
+    const int last = sd.n_keys - 1;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      const int t = j < r.nmb ? r.tb + wave + TW * j : r.tb;  // missing tiles repeat the round's first
+#pragma unroll
+      for (int q = 0; q < VPS; ++q) {
+        const int tok = min(t * 16 + R * q + lane % R, last);
+        off[VPS * j + q] = tok * a.k_row_u4 + VPS * g4 + ((own - q) & (VPS - 1));
+      }
+    }
+  };
+  koff(cur, kc_base, kc_off);
+  koff(nxt.sidx >= 0 ? nxt : cur, kn_base, kn_off);  // without a next round: a harmless repeat
+
+  // batch loads: U virtual steps = U / VPS segments, from segment ms / VPS
+  auto k_load = [&](uint4 (&f)[U][MB], const uint4* base, const int32_t (&off)[MB * VPS], int ms)
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int h = 0; h < U / VPS; ++h)
+#pragma unroll
+      for (int q = 0; q < VPS; ++q)
+#pragma unroll
+        for (int j = 0; j < MB; ++j) {
+          const u32x4v t = __builtin_nontemporal_load(
+              reinterpret_cast<const u32x4v*>(base + off[VPS * j + q] + SEGC * (ms / VPS + h)));
+          f[VPS * h + q][j] = uint4{t.x, t.y, t.z, t.w};
+        }
+  };
+  // query fragments: phase ph of chunk si is kSeqPhaseU4 contiguous uint4
+  auto q_src = [&](int si, int ph) __attribute__((always_inline)) {
+    return a.Qop + ((int64_t)si * ksteps + (int64_t)ph * kSeqS) * NB * 64;
+  };
+  auto barrier_lds = []() __attribute__((always_inline)) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
+
+  // Query fragments move two batches ahead of their store, in two register
+  // groups that alternate with the batches: in batch (ph, bp) group bp % 2,
+  // loaded two batches before, is stored as slice bp of phase ph + 1, and is
+  // loaded again with slice bp + 2 of phase ph + 1 (or slice bp - 2 of phase
+  // ph + 2).  (Waiting for a slice then never waits for keys newer than the
+  // batch's own.)  Phases count on across rounds: ph + 1 and ph + 2 lie in
+  // this round or in the next (a round has at least two phases).
+  const int nph = ksteps / kSeqS;
+  // (a phase past the share reads the current chunk's data, never used)
+  auto phase_src = [&](int pir) __attribute__((always_inline)) {
+    const bool next = pir >= nph;
+    const int si = next && nxt.sidx >= 0 ? nxt.sidx : cur.sidx;
+    return q_src(si, next ? pir - nph : pir);
+  };
+  // phase 0 of the first round into buffer 0
+  {
+    const uint4* src = q_src(cur.sidx, 0);
+#pragma unroll
+    for (int i = 0; i < kSeqPhaseU4 / kLdsThreads; ++i) qs[tid + kLdsThreads * i] = src[tid + kLdsThreads * i];
+  }
+  // the slices in flight: CP (2 or 4) uint4 per thread and group, in named
+  // registers (an array here is placed in scratch memory by the compiler)
+  static_assert(CP == 2 || CP == 4, "two or four query uint4 per thread and batch");
+  uint4 ca0, ca1, ca2, ca3, cb0, cb1, cb2, cb3;
+  auto cp_load = [&](int grp, const uint4* src) __attribute__((always_inline)) {
+    uint4 &c0 = grp ? cb0 : ca0, &c1 = grp ? cb1 : ca1, &c2 = grp ? cb2 : ca2, &c3 = grp ? cb3 : ca3;
+    c0 = src[0];
+    c1 = src[kLdsThreads];
+    if constexpr (CP == 4) {
+      c2 = src[2 * kLdsThreads];
+      c3 = src[3 * kLdsThreads];
+    }
+  };
+  auto cp_store = [&](int grp, uint4* dst) __attribute__((always_inline)) {
+    const uint4 &c0 = grp ? cb0 : ca0, &c1 = grp ? cb1 : ca1, &c2 = grp ? cb2 : ca2, &c3 = grp ? cb3 : ca3;
+    dst[0] = c0;
+    dst[kLdsThreads] = c1;
+    if constexpr (CP == 4) {
+      dst[2 * kLdsThreads] = c2;
+      dst[3 * kLdsThreads] = c3;
+    }
+  };
+  cp_load(0, phase_src(1) + tid);
+  cp_load(1, phase_src(1) + CP * kLdsThreads + tid);
+  // keys three batches ahead, four register sets rotating with the batches of
+  // a phase (BPP = 4): batches 0-2 in flight before the first (a round has at
+  // least two phases)
+  static_assert(BPP == 4, "four batches per phase: the rotation of the key register sets");
+  uint4 fa[U][MB], fb[U][MB], fc[U][MB], fd[U][MB];
+  k_load(fa, kc_base, kc_off, 0);
+  k_load(fb, kc_base, kc_off, U);
+  k_load(fc, kc_base, kc_off, 2 * U);
+  barrier_lds();
+
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int j = 0; j < MB; ++j)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  int gph = 0;  // phases finished (the current phase's buffer is gph & 1)
+  // batch bp (a constant after inlining) of phase ph of the current round: the
+  // query slice loaded two batches ago stored, the slice two ahead and the keys
+  // three batches ahead loaded, this batch's MFMAs
+  auto batch = [&](int ph, const int bp, const uint4 (&cur_k)[U][MB], uint4 (&nxt_k)[U][MB])
+      __attribute__((always_inline)) {
+    // (unconditional, so that the memory-counter waits stay exact: a slice of
+    // a phase past the share lands in a buffer no later phase reads)
+    cp_store(bp & 1, qs + ((gph + 1) & 1) * kSeqPhaseU4 + bp * CP * kLdsThreads + tid);
+    {
+      const bool wrap = bp + 2 >= BPP;
+      cp_load(bp & 1, phase_src(ph + (wrap ? 2 : 1)) + (wrap ? bp + 2 - BPP : bp + 2) * CP * kLdsThreads + tid);
+    }
+    // the keys of the batch three ahead: this round's, or one of the next
+    // round's first three (unconditional loads: past the last round they
+    // repeat its first batches)
+    {
+      const int ahead = BPP * ph + bp + 3;
+      const bool from_next = ahead >= bpr;
+      int32_t off[MB * VPS];
+#pragma unroll
+      for (int i = 0; i < MB * VPS; ++i) off[i] = from_next ? kn_off[i] : kc_off[i];
+      k_load(nxt_k, from_next ? kn_base : kc_base, off, (from_next ? ahead - bpr : ahead) * U);
+    }
+    // keep the loads ahead of this batch's multiplies (the scheduler would
+    // otherwise sink them to the batch end, leaving nothing in flight)
+    __builtin_amdgcn_sched_barrier(0);
+    const uint4* qb = qs + (gph & 1) * kSeqPhaseU4 + (bp * U) * NB * 64 + lane;
+#pragma unroll
+    for (int v = 0; v < U; ++v) {
+      const int h = v / VPS, k = v % VPS;
+      uint4 fk[MB];
+#pragma unroll
+      for (int j = 0; j < MB; ++j) {
+        // operand k: load (lane % 16 / R - k) mod VPS of lane + R k within its
+        // 16-lane row (a bit-mask blend, then a DPP rotation; a select between
+        // the array's elements would be folded into an indexed scratch load)
+        uint4 send = uint4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int q = 0; q < VPS; ++q) {
+          const uint32_t pick = ((own - k) & (VPS - 1)) == q ? ~0u : 0u;
+          const uint4 c = cur_k[VPS * h + q][j];
+          send.x |= c.x & pick;
+          send.y |= c.y & pick;
+          send.z |= c.z & pick;
+          send.w |= c.w & pick;
+        }
+        if constexpr (VPS == 2)
+          fk[j] = k == 0 ? send : row_ror4<8>(send);
+        else
+          fk[j] = k == 0 ? send : (k == 1 ? row_ror4<12>(send) : (k == 2 ? row_ror4<8>(send) : row_ror4<4>(send)));
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint4 qf = qb[(v * NB + nb) * 64];
+#pragma unroll
+        for (int j = 0; j < MB; ++j) Mma<bf16_t>::mac(acc[j][nb], fk[j], qf);
+      }
+    }
+  };
+
+  while (cur.sidx >= 0) {
+    for (int ph = 0; ph < nph; ++ph) {
+      batch(ph, 0, fa, fd);
+      batch(ph, 1, fb, fa);
+      batch(ph, 2, fc, fb);
+      batch(ph, 3, fd, fc);
+      barrier_lds();  // phase end: the next phase is in place, this buffer free
+      ++gph;
+    }
+    // m_j = scale * max over each query's rows, for this wave's tiles
+    const QerStreamDesc sd = seq_at(cur.sidx);
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+      if (j < cur.nmb) {
+        const int tile = cur.tb + wave + TW * j;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tok = tile * 16 + g4 * 4 + r;
+          float vg = -INFINITY;
+          int gcur = -1;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            if (nb * 16 >= sd.n_rows) break;
+            float v = acc[j][nb][r];
+#pragma unroll
+            for (int o = 8; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 16));
+            const int g = (sd.q0 + nb * 16) / a.group_rows;
+            if (g != gcur) {
+              if (gcur >= 0 && r16 == 0 && tok < sd.n_keys) a.m[(int64_t)gcur * a.m_stride + tok] = vg * a.scale;
+              gcur = g;
+              vg = v;
+            } else {
+              vg = fmaxf(vg, v);
+            }
+          }
+          if (gcur >= 0 && r16 == 0 && tok < sd.n_keys) a.m[(int64_t)gcur * a.m_stride + tok] = vg * a.scale;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < MB; ++j)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[j][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    cur = nxt;
+    kc_base = kn_base;
+#pragma unroll
+    for (int i = 0; i < MB * VPS; ++i) kc_off[i] = kn_off[i];
+    if (cur.sidx >= 0) {
+      nxt = next_of(cur);
+      if (nxt.sidx >= 0) fill(nxt);
+      koff(nxt.sidx >= 0 ? nxt : cur, kn_base, kn_off);
+    }
+  }
+}
+
 // ---- GQA query fold ---------------------------------------------------------------
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -1844,10 +2202,47 @@ int plan_streams(const cofie_qer_desc& h, const QerPlan& p, int32_t n_streams, c
   return COFIE_OK;
 }
 
+// qer_seq_kernel's shape: virtual steps per batch, key rows per load
+constexpr int kSeqU = 2;
+constexpr int kSeqR = 8;
+constexpr int kSeqSegBytes = 1024 / kSeqR;  // a segment of a key row (16 / kSeqR virtual steps)
+
+// Whether the chunks take qer_seq_kernel: bf16 heads of one query term, a
+// chunk wider than 64 rows, key rows of whole segments, at least two phases
+// per round.
+bool seq_fast(const cofie_qer_desc& h, const QerPlan& p, const StreamsPlan& sp) {
+  const int64_t row_bytes = p.Lc * (int64_t)p.esize, ksteps = row_bytes / 64;
+  return h.dtype == COFIE_BF16 && p.P == 1 && sp.NB == 8 && row_bytes % kSeqSegBytes == 0 &&
+         ksteps % kSeqS == 0 && ksteps >= 2 * kSeqS &&
+         sp.max_keys * (row_bytes / 16) < (int64_t(1) << 31);  // 32-bit key offsets within a sequence
+}
+
+// qer_seq_kernel's workgroups: one per CU (whole XCD groups), at most one per
+// round of 16 tiles
+int seq_nwg(const StreamsPlan& sp, int cus) {
+  int n = (int)std::min<int64_t>(cus, ceil_div(sp.tiles, (int64_t)kLdsWaves * 2));
+  if (n >= 8) n &= ~7;
+  return std::max(n, 1);
+}
+// the most chunks one workgroup's share of the tiles reaches
+int seq_span(const StreamsPlan& sp, int nwg) {
+  int worst = 0;
+  size_t c = 0;
+  for (int b = 0; b < nwg; ++b) {
+    const int64_t fb = sp.tiles * b / nwg, fe = sp.tiles * (b + 1) / nwg;
+    while (c + 1 < sp.seq.size() && sp.seq[c].tile0 + sp.seq[c].ntiles <= fb) ++c;
+    size_t e = c;
+    while (e < sp.seq.size() && sp.seq[e].tile0 < fe) ++e;
+    worst = std::max(worst, (int)(e - c));
+  }
+  return worst;
+}
+
 struct StreamsScratch {
   float* m;           // [n_queries][max_keys]
   uint32_t* keys;     // [n_queries][max_frames]
   uint8_t* qp;        // folded queries (grouped heads)
+  uint4* qop;         // operand-order query fragments of each chunk (qer_seq_kernel)
   uint8_t* meta;      // QerStreamDesc[seq] then QerQueryDesc[n_queries]
   int32_t* done;      // [n_queries][tree ints] arrival trees of the frame-mean kernel
 };
@@ -1861,6 +2256,7 @@ StreamsScratch carve_streams(Arena& ar, const cofie_qer_desc& h, const QerPlan& 
   w.m = ar.take<float>((size_t)sp.n_queries * std::max<int64_t>(sp.max_keys, 1));
   w.keys = ar.take<uint32_t>((size_t)sp.n_queries * std::max(sp.max_frames, 1));
   w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * sp.n_queries * h.n_q * p.Lc * p.esize) : nullptr;
+  w.qop = seq_fast(h, p, sp) ? ar.take<uint4>(sp.seq.size() * (size_t)(p.Lc * p.esize / 64) * kSeqNB * 64) : nullptr;
   w.meta = ar.take<uint8_t>(meta_bytes(sp));
   w.done = ar.take<int32_t>((size_t)sp.n_queries * qer_trees(std::max(sp.max_frames, 1)).ints);
   return w;
@@ -1901,9 +2297,44 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
     qp = w.qp;
   }
   const QerTrees tr = qer_trees(std::max(sp.max_frames, 1));
+  const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
+  const int cus = device_cu_count();
+  if (w.qop && sp.tiles > 0 && seq_span(sp, seq_nwg(sp, cus)) <= kSeqTab) {
+    // the query side in operand order, then qer_seq_kernel
+    const int32_t ksteps = (int32_t)(p.Lc * p.esize / 64);
+    const int64_t total = (int64_t)sp.seq.size() * ksteps * kSeqNB * 64;
+    rc = launch("qer_qop", qer_qop_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), dim3(256),
+                0, s, static_cast<const uint4*>(Q), (int64_t)(p.Lc * p.esize / 16), seq_d, (int32_t)sp.seq.size(),
+                ksteps, (int32_t)kSeqR, w.qop);
+    if (rc) return rc;
+    SeqArgs qa{};
+    qa.K = static_cast<const uint8_t*>(K);
+    qa.Qop = w.qop;
+    qa.seq = seq_d;
+    qa.n_seq = (int32_t)sp.seq.size();
+    qa.tiles = (int32_t)sp.tiles;
+    qa.nwg = seq_nwg(sp, cus);
+    qa.xcd_order = qa.nwg % 8 == 0 ? 1 : 0;
+    qa.nseg = (int32_t)(p.Lc * p.esize / kSeqSegBytes);
+    qa.k_row_u4 = (int32_t)(p.Lc * p.esize / 16);
+    qa.scale = (float)((double)base_scale / (double)h.H_q);
+    qa.m = w.m;
+    qa.m_stride = std::max<int64_t>(sp.max_keys, 1);
+    qa.group_rows = h.n_q;
+    qa.clear = w.done;
+    qa.nclear = sp.n_queries * tr.ints;
+    auto kern = qer_seq_kernel<kSeqU, kSeqR>;
+    const size_t lds = kSeqLds;
+    rc = allow_lds(kern, lds);
+    if (rc) return rc;
+    rc = launch("qer_score", kern, dim3((unsigned)qa.nwg), dim3(kLdsThreads), lds, s, qa);
+    if (rc) return rc;
+    return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, sp.n_queries), dim3(1024), 0, s,
+                  (const float*)w.m, (int32_t)qa.m_stride, frame_offsets, std::max(sp.max_frames, 1), out_scores,
+                  w.keys, (const int32_t*)nullptr, w.done, tr.ints, tr.stride, k_top, out_idx, qry_d);
+  }
   // the score kernel: one launch over every chunk's tiles (its workgroup 0
   // clears the frame-mean kernel's arrival trees, so it runs even without keys)
-  const int cus = device_cu_count();
   LdsPlan L = plan_score_lds(std::max<int64_t>(sp.tiles, 1) * 16, p.Lc, p.esize, p.P, p.P * sp.NB, cus, false);
   if (sp.NB == 8 && L.MB != 1) {  // eight blocks take one tile per wave (two spill)
     L = plan_score_lds(std::min<int64_t>(sp.tiles, (int64_t)cus * kLdsWaves) * 16, p.Lc, p.esize, p.P,
@@ -1918,7 +2349,6 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
   sa.m_stride = std::max<int64_t>(sp.max_keys, 1);
   sa.Lc = (int32_t)p.Lc;
   sa.tiles = (int32_t)sp.tiles;
-  const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
   sa.scale = (float)((double)base_scale / (double)h.H_q);
   sa.m = w.m;
   sa.clear = w.done;
