@@ -41,6 +41,7 @@ _SRC = os.path.join(_HERE, "cofie_oracle.c")
 _LIB = os.path.join(_HERE, "libcofie_oracle.so")
 
 GRAY, PER_CHANNEL, JOINT3D = 0, 1, 2
+FRAMEDIFF, DHASH = 3, 4  # alternative pre-encoder signals (Table 5)
 F32, BF16 = 0, 1
 LOGIT, SOFTMAX = 0, 1
 
@@ -75,6 +76,10 @@ def _load():
     lib.orc_mass.restype = i64
     lib.orc_histogram.argtypes = [P, i64, i32, i32, i32, i32, i32, P]
     lib.orc_histogram.restype = ctypes.c_int
+    lib.orc_signature.argtypes = [P, i64, i32, i32, i32, i32, i32, P]
+    lib.orc_signature.restype = i64
+    lib.orc_signal_two_m.argtypes = [i32, i32]
+    lib.orc_signal_two_m.restype = i64
     lib.orc_l1.argtypes = [P, P, i64]
     lib.orc_l1.restype = i64
     lib.orc_ngff_select.argtypes = [P, i64, i64, i64, P, i64, i32, i32, i64, P, P, P]
@@ -135,6 +140,28 @@ def histogram(frames: np.ndarray, bins: int, mode: int) -> np.ndarray:
     if rc != 0:
         raise ValueError(f"oracle histogram rejected C={C} mode={mode}")
     return out
+
+
+def signature(frames: np.ndarray, kind: int, grid: int = 32) -> np.ndarray:
+    """Rows [n][nsig] uint32 of an alternative signal (Table 5): the G x G
+    low-resolution luma image (FRAMEDIFF, G = grid) or the 64 dHash bits
+    (DHASH, grid unused); the L1 distance of two rows over signal_two_m() is
+    the signal's distance in [0, 1]."""
+    f = np.ascontiguousarray(frames, dtype=np.uint8)
+    if f.ndim == 3:
+        f = f[..., None]
+    n, H, W, C = f.shape
+    nsig = grid * grid if kind == FRAMEDIFF else 64
+    out = np.zeros((n, nsig), dtype=np.uint32)
+    got = _load().orc_signature(_ptr(f), n, H, W, C, kind, grid, _ptr(out))
+    if got != nsig:
+        raise ValueError(f"oracle signature rejected shape {f.shape} kind={kind} grid={grid}")
+    return out
+
+
+def signal_two_m(kind: int, grid: int = 32) -> int:
+    """2M of a signal: 255 G^2 (frame difference) or 64 (dHash)."""
+    return int(_load().orc_signal_two_m(kind, grid))
 
 
 def l1(ci: np.ndarray, cj: np.ndarray) -> int:

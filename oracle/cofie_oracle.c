@@ -113,6 +113,87 @@ int orc_histogram(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_
   return 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Alternative pre-encoder signals (Table 5, filtering-signal ablation)      */
+/* ------------------------------------------------------------------------ */
+/* The paper names them by citation only; the readings taken here:
+ *   low-res frame difference: the luma image (gray_of, or the value for C = 1)
+ *     box-averaged to a G x G grid, each cell's mean rounded half up to an
+ *     integer in [0, 255]; the distance of two frames is the sum of the
+ *     cells' absolute differences over 255 G^2 (the mean absolute difference
+ *     of the low-resolution images, normalised to [0, 1]);
+ *   dHash: the luma image box-averaged to 8 rows x 9 columns the same way;
+ *     bit (r, c), c < 8, is set when cell (r, c + 1) is brighter than cell
+ *     (r, c); the distance is the Hamming distance over 64.
+ * Row y of an H-row image belongs to grid row (y * gh) div H (column x to
+ * grid column (x * gw) div W), so the cells tile the image without overlap.
+ * Each signal is written as a row of small integers whose L1 distance is the
+ * numerator above (cell means for the frame difference, one 0/1 entry per
+ * hash bit), so the keep rule of Eqs. 3-5 runs on them unchanged with
+ * 2M = 255 G^2 or 64. */
+enum { ORC_SIG_FRAMEDIFF = 3, ORC_SIG_DHASH = 4 };
+
+/* Cell means (rounded half up) of the luma image on a gh x gw grid. */
+static void cell_means(const uint8_t* f, int32_t H, int32_t W, int32_t C, int32_t gh, int32_t gw,
+                       uint32_t* sum, uint32_t* area, uint32_t* mean) {
+  for (int32_t i = 0; i < gh * gw; ++i) {
+    sum[i] = 0;
+    area[i] = 0;
+  }
+  for (int32_t y = 0; y < H; ++y) {
+    const int32_t cy = (int32_t)(((int64_t)y * gh) / H);
+    for (int32_t x = 0; x < W; ++x) {
+      const int32_t cx = (int32_t)(((int64_t)x * gw) / W);
+      const uint8_t* px = f + ((int64_t)y * W + x) * C;
+      const int v = (C == 3) ? gray_of(px[0], px[1], px[2]) : px[0];
+      sum[cy * gw + cx] += (uint32_t)v;
+      area[cy * gw + cx] += 1;
+    }
+  }
+  for (int32_t i = 0; i < gh * gw; ++i) mean[i] = (sum[i] + area[i] / 2) / area[i];
+}
+
+/* Signal rows [n][nsig] of n frames [n][H][W][C]: G^2 cell means (frame
+ * difference, grid G) or 64 hash bits (dHash).  Returns nsig, or -1 for
+ * shapes the signal does not define (a grid finer than the image). */
+int64_t orc_signature(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C, int32_t kind,
+                      int32_t G, uint32_t* out) {
+  if (C != 1 && C != 3) return -1;
+  int32_t gh, gw;
+  int64_t nsig;
+  if (kind == ORC_SIG_FRAMEDIFF) {
+    if (G < 1 || G > H || G > W) return -1;
+    gh = gw = G;
+    nsig = (int64_t)G * G;
+  } else if (kind == ORC_SIG_DHASH) {
+    if (H < 8 || W < 9) return -1;
+    gh = 8;
+    gw = 9;
+    nsig = 64;
+  } else {
+    return -1;
+  }
+  const int64_t fb = (int64_t)H * W * C;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < n; ++t) {
+    uint32_t sum[4096], area[4096], mean[4096];
+    cell_means(frames + t * fb, H, W, C, gh, gw, sum, area, mean);
+    uint32_t* o = out + t * nsig;
+    if (kind == ORC_SIG_FRAMEDIFF) {
+      for (int64_t i = 0; i < nsig; ++i) o[i] = mean[i];
+    } else {
+      for (int r = 0; r < 8; ++r)
+        for (int c = 0; c < 8; ++c) o[r * 8 + c] = mean[r * 9 + c + 1] > mean[r * 9 + c] ? 1u : 0u;
+    }
+  }
+  return nsig;
+}
+
+/* The normaliser 2M of a signal's L1 distance: 255 G^2 or 64. */
+int64_t orc_signal_two_m(int32_t kind, int32_t G) {
+  return kind == ORC_SIG_FRAMEDIFF ? 255 * (int64_t)G * G : 64;
+}
+
 /* 2M * d(h_i,h_j) = sum_b |c_i[b] - c_j[b]| : the exact integer numerator of the
  * total-variation distance between two normalised histograms (Eq. 2). */
 int64_t orc_l1(const uint32_t* ci, const uint32_t* cj, int64_t nbins) {
