@@ -55,6 +55,9 @@ def parse():
                     help="with --configs 5: streams whose queries are ranked (of 32)")
     ap.add_argument("--push-batch", type=int, default=64,
                     help="with --configs: frames per stream and push of the online NGFF pass")
+    ap.add_argument("--signals", default="",
+                    help="comma-separated workload ids (1-5): time NGFF with the Table 5 alternative signals "
+                         "(low-res frame difference, dHash) on the workload's frames (one JSON line each)")
     ap.add_argument("--attn-qer", default="",
                     help="comma-separated workload ids (2-4): time the last-layer prefill attention "
                          "with QER from its QK^T tiles (one JSON line each) instead of the headline step")
@@ -82,6 +85,9 @@ def main():
         return
     if args.attn_qer:
         attn_qer_report(args, [int(c) for c in args.attn_qer.split(",")])
+        return
+    if args.signals:
+        signals_report(args, [int(c) for c in args.signals.split(",")])
         return
     headline(args)
 
@@ -814,6 +820,60 @@ def attn_qer_report(args, cfgs):
                          "algorithmic_flops": flops},
             "separate_qer_rank_us": round(sep_us, 1)}), flush=True)
         del Q, K, V, out, ws, Qt, Kv
+        torch.cuda.empty_cache()
+
+
+def signals_report(args, cfgs):
+    """NGFF with the alternative pre-encoder signals of the filtering-signal
+    ablation (Table 5: low-res frame difference on a 32 x 32 grid, dHash) in
+    place of the histogram, on a workload's frames: thresholds calibrated for
+    the workload's retention, then the whole filter timed; the signature
+    kernel's rate against the HBM peak (algorithmic bytes: every frame byte
+    read once)."""
+    import torch
+
+    from paper_2609_03675_amd import binding as B
+    from paper_2609_03675_amd import synth
+
+    probe = read_probe_gbs(torch, B)
+    for cfg in cfgs:
+        wl = synth.WORKLOADS[cfg]
+        frames, _ = upload_frames(torch, synth, cfg)
+        n = wl.n
+        seg = wl.T if wl.n_streams > 1 else 0
+        fbytes = n * wl.H * wl.W * 3
+        out = {"workload": wl.name, "frames": n, "read_probe_GBps": round(probe, 1)}
+        for name, mode, G in (("framediff", B.FRAMEDIFF, 32), ("dhash", B.DHASH, 8)):
+            rule0 = B.keep_rule(mode, 0.3, 30, 4, seg)
+            tau = B.cofie_ngff_calibrate(frames, G, rule0, wl.target)
+            count = torch.empty(wl.n_streams, dtype=torch.int32, device="cuda")
+            ws = torch.empty(B.ngff_workspace_bytes(n, wl.H, wl.W, 3, G, rule0), dtype=torch.uint8, device="cuda")
+            rule = B.keep_rule(mode, 0.3, 30, 4, seg, tau_per_segment=tau, out_count=count, workspace=ws)
+            scores = torch.empty(n, dtype=torch.float32, device="cuda")
+            mask = torch.empty(n, dtype=torch.uint8, device="cuda")
+
+            def call(i, rule=rule, G=G, scores=scores, mask=mask):
+                B.cofie_ngff_filter(frames, G, rule, out_scores=scores, out_mask=mask)
+
+            reps = 10 if fbytes > (1 << 30) else 30
+            us = median_call_us(torch, call, reps)
+            B.cofie_profiler_reset()
+            B.cofie_profiler_enable(True)
+            for i in range(reps):
+                call(i)
+            torch.cuda.synchronize()
+            B.cofie_profiler_enable(False)
+            ms, cnt = B.cofie_profiler_read("ngff_sig")
+            B.cofie_profiler_reset()
+            sig_us = 1e3 * ms / max(cnt, 1)
+            gbs = fbytes / (sig_us * 1e-6) / 1e9
+            out[name] = {"grid": G if name == "framediff" else "8x9", "us_per_call": round(us, 1),
+                         "frames_per_s": round(n / (us * 1e-6), 1), "signature_us": round(sig_us, 1),
+                         "signature_GBps": round(gbs, 1), "signature_frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                         "kept": int(count.sum().item()), "target_retention": wl.retain}
+            del ws
+        print(json.dumps(out), flush=True)
+        del frames
         torch.cuda.empty_cache()
 
 

@@ -57,7 +57,27 @@ extern "C" {
  *                per-channel distances.  C = 3.
  *   JOINT3D      B^3 bins indexed (bin(R)*B + bin(G))*B + bin(B).  Mass M = H*W.
  *                C = 3, B^3 <= 4096.                                          */
-enum cofie_hist_mode { COFIE_HIST_GRAY = 0, COFIE_HIST_PER_CHANNEL = 1, COFIE_HIST_JOINT3D = 2 };
+/* The novelty signal can also be one of the alternative pre-encoder signals
+ * of the paper's filtering-signal ablation (Table 5, defined there only by
+ * citation; readings):
+ *   FRAMEDIFF    low-resolution frame difference: the luma image (BT.601 in
+ *                integers as for GRAY; the value itself when C = 1) box-
+ *                averaged on a G x G grid, G = `bins` (a power of two in
+ *                [2, 64], G <= H and G <= W), each cell mean rounded half up;
+ *                row = the G^2 means; distance = L1 / (255 G^2) (2M = 255 G^2).
+ *   DHASH        difference hash: luma box means on 8 rows x 9 columns (H >= 8,
+ *                W >= 9; `bins` unused); row = 64 entries, 1 where cell
+ *                (r, c+1) is brighter than cell (r, c); distance = Hamming / 64.
+ * Row y belongs to grid row (y * rows) div H, column x to (x * cols) div W.
+ * W <= 16384.  The keep rule, calibration and histogram outputs work on these
+ * rows unchanged; the online state (cofie_ngff_stream_*) does not take them. */
+enum cofie_hist_mode {
+  COFIE_HIST_GRAY = 0,
+  COFIE_HIST_PER_CHANNEL = 1,
+  COFIE_HIST_JOINT3D = 2,
+  COFIE_SIGNAL_FRAMEDIFF = 3,
+  COFIE_SIGNAL_DHASH = 4
+};
 
 /* Element type of Q and K. */
 enum cofie_dtype { COFIE_F32 = 0, COFIE_BF16 = 1 };
@@ -105,7 +125,8 @@ typedef struct cofie_keep_rule {
  * optional outputs, library-managed scratch. */
 void cofie_keep_rule_default(cofie_keep_rule* rule);
 
-/* Number of histogram bins for a mode and `bins` (B, 3B or B^3); 0 if invalid. */
+/* Number of histogram bins (row entries) for a mode and `bins` (B, 3B, B^3;
+ * G^2 for FRAMEDIFF, 64 for DHASH); 0 if invalid. */
 int64_t cofie_ngff_nbins(int32_t hist_mode, int32_t bins);
 
 /* Bytes of device scratch cofie_ngff_filter / cofie_ngff_calibrate need for

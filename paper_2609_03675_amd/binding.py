@@ -21,7 +21,9 @@ COFIE_OK, COFIE_EINVAL, COFIE_EUNSUPPORTED, COFIE_EHIP, COFIE_ENOMEM = 0, -1, -2
 GRAY, PER_CHANNEL, JOINT3D = 0, 1, 2
 F32, BF16 = 0, 1
 LOGIT, SOFTMAX = 0, 1
-HIST_MODES = {"gray": GRAY, "per_channel": PER_CHANNEL, "joint3d": JOINT3D}
+FRAMEDIFF, DHASH = 3, 4  # alternative pre-encoder signals (Table 5)
+HIST_MODES = {"gray": GRAY, "per_channel": PER_CHANNEL, "joint3d": JOINT3D, "framediff": FRAMEDIFF,
+              "dhash": DHASH}
 
 
 class CofieError(RuntimeError):

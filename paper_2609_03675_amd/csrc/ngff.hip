@@ -232,6 +232,105 @@ __global__ void fill_u32_kernel(uint32_t* p, uint32_t v, int64_t count) {
     p[i] = v;
 }
 
+// ---- alternative signals (Table 5): low-res frame difference, dHash -----------------
+// The luma image box-averaged on a gh x gw grid (row y in grid row
+// (y gh) div H, column x in (x gw) div W), each cell's mean rounded half up;
+// the frame difference emits the gh gw means, dHash the 64 bits "cell
+// (r, c+1) brighter than cell (r, c)" of an 8 x 9 grid.  The rows' L1 distance
+// over 255 gh gw (or 64) is the signal's distance, so the keep rule runs on
+// them like on histogram rows.  One workgroup per frame: each wave takes whole
+// image rows, each lane 4 consecutive pixels per load (12 contiguous bytes:
+// 768 per wave instruction when the frame allows it), sums a run of pixels of
+// one cell in registers and adds it to the cell's LDS counter.
+struct SigArgs {
+  const uint8_t* frames;
+  int64_t frame_bytes;
+  int32_t H, W, C;
+  int32_t gh, gw;
+  int32_t dhash;  // 1: the 64 hash bits, 0: the gh gw cell means
+  int32_t nsig;
+  int32_t vec;    // 1: 4-pixel loads (4-byte aligned frames, W a multiple of 4)
+  uint32_t* out;  // [n][nsig]
+};
+
+constexpr int kSigThreads = 256;
+constexpr int kSigMaxW = 16384;  // the column -> grid column table (uint16, LDS)
+
+__global__ __launch_bounds__(kSigThreads) void ngff_sig_kernel(SigArgs a) {
+  __shared__ uint32_t cell[4096];
+  __shared__ uint16_t gcol[kSigMaxW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = kSigThreads / 64;
+  const int ncell = a.gh * a.gw;
+  for (int i = tid; i < ncell; i += kSigThreads) cell[i] = 0;
+  for (int x = tid; x < a.W; x += kSigThreads) gcol[x] = (uint16_t)(((int64_t)x * a.gw) / a.W);
+  __syncthreads();
+  const uint8_t* f = a.frames + (int64_t)blockIdx.x * a.frame_bytes;
+  auto luma = [&](uint32_t r, uint32_t g, uint32_t b) __attribute__((always_inline)) {
+    return a.C == 3 ? luma_bt601(r, g, b) : r;
+  };
+  for (int y = wave; y < a.H; y += nw) {
+    const int cy = (int)(((int64_t)y * a.gh) / a.H) * a.gw;
+    const uint8_t* row = f + (int64_t)y * a.W * a.C;
+    if (a.vec) {
+      // lane: pixels x0 .. x0 + 3 (12 bytes of RGB or 4 bytes of gray)
+      for (int x0 = 4 * lane; x0 < a.W; x0 += 256) {
+        uint32_t v[4];
+        if (a.C == 3) {
+          const U3 w = *reinterpret_cast<const U3*>(row + 3 * x0);
+          v[0] = luma(w.x & 255u, (w.x >> 8) & 255u, (w.x >> 16) & 255u);
+          v[1] = luma(w.x >> 24, w.y & 255u, (w.y >> 8) & 255u);
+          v[2] = luma((w.y >> 16) & 255u, w.y >> 24, w.z & 255u);
+          v[3] = luma((w.z >> 8) & 255u, (w.z >> 16) & 255u, w.z >> 24);
+        } else {
+          const uint32_t w = *reinterpret_cast<const uint32_t*>(row + x0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = (w >> (8 * i)) & 255u;
+        }
+        // runs of one cell: one LDS add per run
+        int c = gcol[x0];
+        uint32_t run = v[0];
+#pragma unroll
+        for (int i = 1; i < 4; ++i) {
+          const int ci = gcol[x0 + i];
+          if (ci != c) {
+            atomicAdd(&cell[cy + c], run);
+            c = ci;
+            run = 0;
+          }
+          run += v[i];
+        }
+        atomicAdd(&cell[cy + c], run);
+      }
+    } else {
+      for (int x = lane; x < a.W; x += 64) {
+        const uint8_t* px = row + (int64_t)x * a.C;
+        const uint32_t v = a.C == 3 ? luma_bt601(px[0], px[1], px[2]) : px[0];
+        atomicAdd(&cell[cy + gcol[x]], v);
+      }
+    }
+  }
+  __syncthreads();
+  // cell means, rounded half up: grid row i spans rows [ceil(i H / gh),
+  // ceil((i + 1) H / gh)), grid column j likewise
+  auto first = [](int64_t i, int64_t len, int64_t g) __attribute__((always_inline)) { return (i * len + g - 1) / g; };
+  for (int i = tid; i < ncell; i += kSigThreads) {
+    const int r = i / a.gw, c = i - r * a.gw;
+    const uint32_t area = (uint32_t)((first(r + 1, a.H, a.gh) - first(r, a.H, a.gh)) *
+                                     (first(c + 1, a.W, a.gw) - first(c, a.W, a.gw)));
+    cell[i] = (cell[i] + area / 2) / area;
+  }
+  __syncthreads();
+  uint32_t* o = a.out + (int64_t)blockIdx.x * a.nsig;
+  if (a.dhash) {
+    if (tid < 64) {
+      const int r = tid >> 3, c = tid & 7;
+      o[tid] = cell[r * 9 + c + 1] > cell[r * 9 + c] ? 1u : 0u;
+    }
+  } else {
+    for (int i = tid; i < ncell; i += kSigThreads) o[i] = cell[i];
+  }
+}
+
 // ---- band of distances ----------------------------------------------------------
 struct BandArgs {
   const uint32_t* hist;
@@ -853,6 +952,31 @@ int validate_frames(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int3
   if (n > 0 && !frames) return set_error(COFIE_EINVAL, "frames is NULL");
   if (H <= 0 || W <= 0) return set_error(COFIE_EINVAL, "H = %d, W = %d must be positive", H, W);
   if (C != 1 && C != 3) return set_error(COFIE_EINVAL, "C = %d must be 1 or 3", C);
+  if (mode == COFIE_SIGNAL_FRAMEDIFF || mode == COFIE_SIGNAL_DHASH) {
+    // the alternative signals: rows of G^2 cell means or 64 hash bits, 2M =
+    // 255 G^2 or 64 (G a power of two, so that M is an integer)
+    if (W > kSigMaxW) return set_error(COFIE_EUNSUPPORTED, "W = %d exceeds %d for this signal", W, kSigMaxW);
+    if ((int64_t)H * W * 255 >= (int64_t(1) << 32))  // 32-bit cell sums
+      return set_error(COFIE_EUNSUPPORTED, "%d x %d frames exceed the signal's 32-bit cell sums", H, W);
+    if (mode == COFIE_SIGNAL_FRAMEDIFF) {
+      if (bins < 2 || bins > 64 || !is_pow2(bins))
+        return set_error(COFIE_EUNSUPPORTED, "frame-difference grid %d is not a power of two in [2, 64]", bins);
+      if (bins > H || bins > W) return set_error(COFIE_EINVAL, "grid %d finer than the %d x %d image", bins, H, W);
+    } else if (H < 8 || W < 9) {
+      return set_error(COFIE_EINVAL, "dHash needs H >= 8 and W >= 9 (got %d x %d)", H, W);
+    }
+    sh->n = n;
+    sh->H = H;
+    sh->W = W;
+    sh->C = C;
+    sh->B = bins;
+    sh->mode = mode;
+    sh->nbins = cofie_ngff_nbins(mode, bins);
+    sh->npix = (int64_t)H * W;
+    sh->frame_bytes = sh->npix * C;
+    sh->mass = mode == COFIE_SIGNAL_FRAMEDIFF ? 255 * (int64_t)bins * bins / 2 : 32;
+    return COFIE_OK;
+  }
   if (mode != COFIE_HIST_GRAY && mode != COFIE_HIST_PER_CHANNEL && mode != COFIE_HIST_JOINT3D)
     return set_error(COFIE_EINVAL, "unknown hist_mode %d", mode);
   if (C == 1 && mode != COFIE_HIST_GRAY)
@@ -948,9 +1072,26 @@ struct HistMap {  // see HistArgs: group = 0 is the identity
   bool zeroed = false;   // the output rows are known zero: no fill before accumulating
 };
 
+int run_signature(const uint8_t* frames, const NgffShape& sh, uint32_t* out, hipStream_t s) {
+  SigArgs a;
+  a.frames = frames;
+  a.frame_bytes = sh.frame_bytes;
+  a.H = sh.H;
+  a.W = sh.W;
+  a.C = sh.C;
+  a.dhash = sh.mode == COFIE_SIGNAL_DHASH;
+  a.gh = a.dhash ? 8 : sh.B;
+  a.gw = a.dhash ? 9 : sh.B;
+  a.nsig = (int32_t)sh.nbins;
+  a.vec = (reinterpret_cast<uintptr_t>(frames) % 4 == 0) && sh.W % 4 == 0 ? 1 : 0;
+  a.out = out;
+  return launch("ngff_sig", ngff_sig_kernel, dim3((unsigned)sh.n), dim3(kSigThreads), 0, s, a);
+}
+
 int run_histogram(const uint8_t* frames, const NgffShape& sh, uint32_t* hist, hipStream_t s,
                   const HistMap& map = HistMap()) {
   if (sh.n == 0) return COFIE_OK;
+  if (sh.mode == COFIE_SIGNAL_FRAMEDIFF || sh.mode == COFIE_SIGNAL_DHASH) return run_signature(frames, sh, hist, s);
   const HistPlan p = plan_hist(sh, frames);
   HistArgs a;
   a.group = map.group;
@@ -1461,6 +1602,8 @@ int64_t cofie_ngff_nbins(int32_t mode, int32_t bins) {
   if (mode == COFIE_HIST_GRAY) return bins;
   if (mode == COFIE_HIST_PER_CHANNEL) return 3 * (int64_t)bins;
   if (mode == COFIE_HIST_JOINT3D) return (int64_t)bins * bins * bins;
+  if (mode == COFIE_SIGNAL_FRAMEDIFF) return (int64_t)bins * bins;
+  if (mode == COFIE_SIGNAL_DHASH) return 64;
   return 0;
 }
 
@@ -1569,6 +1712,8 @@ int cofie_ngff_stream_create(int32_t n_streams, int32_t H, int32_t W, int32_t C,
   NgffShape sh;
   int rc = validate_frames(nullptr, 0, H, W, C, bins, rule->hist_mode, &sh);
   if (rc) return rc;
+  if (rule->hist_mode == COFIE_SIGNAL_FRAMEDIFF || rule->hist_mode == COFIE_SIGNAL_DHASH)
+    return set_error(COFIE_EUNSUPPORTED, "the online state keeps histograms only (not the Table 5 signals)");
   if (rule->L_max < 1) return set_error(COFIE_EUNSUPPORTED, "the streaming keep rule needs L_max >= 1");
   if (rule->M_min < 0) return set_error(COFIE_EINVAL, "M_min is negative");
   if (!rule->tau_per_segment && !(rule->tau_h == rule->tau_h)) return set_error(COFIE_EINVAL, "tau_h is NaN");

@@ -74,6 +74,8 @@ def test_nbins():
     assert B.cofie_ngff_nbins("joint3d", 8) == 512
     assert B.cofie_ngff_nbins("gray", 32) == 32
     assert B.cofie_ngff_nbins(7, 32) == 0
+    assert B.cofie_ngff_nbins("framediff", 32) == 1024   # G x G cell means
+    assert B.cofie_ngff_nbins("dhash", 8) == 64           # 64 hash bits
 
 
 def test_workspace_sizes_are_host_only():
@@ -108,6 +110,12 @@ FAKE = 0x1000
     ((FAKE, 4, 8, 8, 3, 32, B.JOINT3D, FAKE), B.COFIE_EUNSUPPORTED),      # 32^3 bins
     ((FAKE, 4, 2000, 2000, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # 2M >= 2^24
     ((FAKE, 4, 8, 8, 3, 32, B.PER_CHANNEL, None), B.COFIE_EINVAL),        # out NULL
+    ((FAKE, 4, 64, 64, 3, 24, B.FRAMEDIFF, FAKE), B.COFIE_EUNSUPPORTED),  # grid not a power of two
+    ((FAKE, 4, 64, 64, 3, 128, B.FRAMEDIFF, FAKE), B.COFIE_EUNSUPPORTED), # grid above 64
+    ((FAKE, 4, 16, 64, 3, 32, B.FRAMEDIFF, FAKE), B.COFIE_EINVAL),        # grid finer than H
+    ((FAKE, 4, 7, 64, 3, 8, B.DHASH, FAKE), B.COFIE_EINVAL),              # dHash needs H >= 8
+    ((FAKE, 4, 64, 8, 3, 8, B.DHASH, FAKE), B.COFIE_EINVAL),              # and W >= 9
+    ((FAKE, 4, 64, 20000, 3, 8, B.DHASH, FAKE), B.COFIE_EUNSUPPORTED),    # W above 16384
 ])
 def test_histogram_validation(L, args, code):
     assert L.cofie_ngff_histogram(*args, None) == code
@@ -256,3 +264,12 @@ def test_streams_qer_validation(L):
     assert call(B.qer_desc(80, 64, 5, 4, 2, 32), lay) == B.COFIE_EUNSUPPORTED   # grouped heads: at most 64
     assert L.cofie_qer_rank_streams(FAKE, FAKE, FAKE, ctypes.byref(d), 0, None, None, None, None, 2, FAKE, FAKE,
                                     None) == B.COFIE_EINVAL
+
+
+def test_online_state_refuses_the_table5_signals(L):
+    """The online NGFF state keeps histogram rows only."""
+    st = ctypes.c_void_p()
+    for mode in (B.FRAMEDIFF, B.DHASH):
+        r = B.keep_rule(mode, 0.3, 30, 4)
+        assert L.cofie_ngff_stream_create(2, 64, 64, 3, 8, ctypes.byref(r), ctypes.byref(st)) == \
+            B.COFIE_EUNSUPPORTED
