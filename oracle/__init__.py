@@ -80,6 +80,8 @@ def _load():
     lib.orc_signature.restype = i64
     lib.orc_signal_two_m.argtypes = [i32, i32]
     lib.orc_signal_two_m.restype = i64
+    lib.orc_score.argtypes = [i64, i64]
+    lib.orc_score.restype = f32
     lib.orc_l1.argtypes = [P, P, i64]
     lib.orc_l1.restype = i64
     lib.orc_ngff_select.argtypes = [P, i64, i64, i64, P, i64, i32, i32, i64, P, P, P]
@@ -162,6 +164,12 @@ def signature(frames: np.ndarray, kind: int, grid: int = 32) -> np.ndarray:
 def signal_two_m(kind: int, grid: int = 32) -> int:
     """2M of a signal: 255 G^2 (frame difference) or 64 (dHash)."""
     return int(_load().orc_signal_two_m(kind, grid))
+
+
+def score(D: int, two_m: int) -> np.float32:
+    """The novelty score of an integer distance: D / 2M rounded once to the
+    nearest fp32, ties to even (Eq. 2's total variation)."""
+    return np.float32(_load().orc_score(int(D), int(two_m)))
 
 
 def l1(ci: np.ndarray, cj: np.ndarray) -> int:

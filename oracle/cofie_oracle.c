@@ -205,10 +205,30 @@ int64_t orc_l1(const uint32_t* ci, const uint32_t* cj, int64_t nbins) {
   return D;
 }
 
-/* d = D / (2M), rounded once to fp32.  Both operands are integers below 2^24,
- * so each is exact in fp32 and one IEEE single division gives the correctly
- * rounded total-variation distance. */
-static float tv_of(int64_t D, int64_t mass) { return (float)D / (float)(2 * mass); }
+/* d = D / (2M), the exact quotient rounded once to the nearest fp32 (ties to
+ * even).  Written from that definition in integers: with 2^-k <= D/N < 2^(1-k)
+ * (N = 2M; D <= N + 1 and N < 2^31, so 0 <= k <= 31) the 24-bit significand
+ * is floor(D 2^(23+k) / N), rounded up when twice the remainder exceeds N (or
+ * equals it and the significand is odd).  While N < 2^24 this is what one IEEE
+ * single division of the (then exact) operands returns. */
+static float tv_q(int64_t D, int64_t N) {
+  if (D <= 0) return 0.0f;
+  int k = 0;
+  while (((__int128)D << k) < N) ++k;
+  const __int128 num = (__int128)D << (23 + k);
+  int64_t m = (int64_t)(num / N);
+  const __int128 twice_rem = 2 * (num - (__int128)m * N);
+  if (twice_rem > N || (twice_rem == N && (m & 1))) ++m;
+  if (m == (int64_t)1 << 24) {
+    m >>= 1;
+    --k;
+  }
+  return ldexpf((float)m, -(23 + k));
+}
+static float tv_of(int64_t D, int64_t mass) { return tv_q(D, 2 * mass); }
+
+/* D / N correctly rounded to fp32 (for the pins of the rounding above). */
+float orc_score(int64_t D, int64_t N) { return tv_q(D, N); }
 
 /* ------------------------------------------------------------------------ */
 /* NGFF: novelty score and gap-aware retention (Sec. 3.2, Eqs. 3-5)         */

@@ -393,3 +393,40 @@ def test_count_not_monotone_in_threshold_exists():
 
 def test_workload_targets():
     assert [synth.WORKLOADS[i].target for i in range(1, 6)] == [26, 128, 720, 307, 128]
+
+
+def _rn32_exact(D, N):
+    """D/N rounded to the nearest fp32, ties to even, decided with exact
+    rationals among the float32 neighbours of a first guess."""
+    from fractions import Fraction
+    x = Fraction(D, N)
+    g = np.float32(D / N)
+    cands = [np.nextafter(g, np.float32(-np.inf)), g, np.nextafter(g, np.float32(np.inf))]
+    best = min(cands, key=lambda c: (abs(Fraction(float(c)) - x), int(np.float32(c).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def test_score_is_the_correctly_rounded_quotient():
+    """The novelty score D / 2M (Eq. 2) rounded once to fp32, for 2M below
+    and far above 2^24 (4K frames per channel: 2M = 6 * 3840 * 2160), against
+    exact rational rounding; below 2^24 it equals one IEEE division of the
+    exact operands."""
+    rng = np.random.default_rng([2609, 3675, 66])
+    for N in (2 * 64 * 64, 2 * 3 * 448 * 448, (1 << 24) - 2, 1 << 24, 6 * 3840 * 2160, (1 << 31) - 2, 12345679):
+        Ds = list(rng.integers(0, N + 2, 300)) + [0, 1, 2, N - 1, N, N + 1]
+        for D in Ds:
+            got = oracle.score(int(D), N)
+            assert got.view(np.uint32) == _rn32_exact(int(D), N).view(np.uint32), (D, N)
+            if N < (1 << 24):
+                assert got == np.float32(np.float32(D) / np.float32(N))
+
+
+def test_score_ties_round_to_even():
+    """Quotients exactly halfway between two fp32 values: the fp32 spacing in
+    [2^-2, 2^-1) is 2^-25, so D / 2^26 with D odd in [2^24, 2^25) lies on a
+    midpoint; ties go to the even significand."""
+    N = 1 << 26
+    for D in ((1 << 24) + 1, (1 << 24) + 3, (1 << 25) - 1):
+        got = oracle.score(D, N)
+        assert got.view(np.uint32) == _rn32_exact(D, N).view(np.uint32)
+        assert got.view(np.uint32) & 1 == 0
