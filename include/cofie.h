@@ -142,7 +142,7 @@ size_t cofie_ngff_workspace_bytes(int64_t n, int32_t H, int32_t W, int32_t C, in
  *   bins      B, a power of two in [2, 256]
  *   out_hist  device uint32 [n][nbins], fully overwritten
  * Errors: EINVAL for null pointers, negative/zero sizes, bad enums or C;
- * EUNSUPPORTED for B not a power of two, B^3 > 4096, or 2M >= 2^24.       */
+ * EUNSUPPORTED for B not a power of two, B^3 > 4096, or 2M >= 2^31.       */
 int cofie_ngff_histogram(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int32_t C,
                          int32_t bins, int32_t hist_mode, uint32_t* out_hist, void* stream);
 

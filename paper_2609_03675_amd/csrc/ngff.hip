@@ -21,9 +21,11 @@
 // Without the gap rule (L_max <= 0) a sequential kernel per stream measures
 // D(t, r(t)) directly.
 // Novelty comparisons run on integers: s >= tau  <=>  max(D) >= theta with
-// theta = min{D : fl32(D)/fl32(2M) >= tau}, exact because fl32(D)/fl32(2M) is
-// strictly increasing in D for 2M < 2^24.  Scores are fl32(D)/fl32(2M), one
-// IEEE division, so they are bit-identical to any correct implementation.
+// theta = min{D : score(D) >= tau}, exact because the score, D / 2M rounded
+// once to fp32, never decreases in D.  Scores are that correctly rounded
+// quotient (one IEEE division of exact operands for 2M < 2^24; an fp64
+// quotient and an exact midpoint test beyond), so they are bit-identical to
+// any correct implementation.
 #include <cstring>
 #include <vector>
 #include "common.h"
@@ -417,16 +419,50 @@ __global__ __launch_bounds__(256) void ngff_band_kernel(BandArgs a) {
   }
 }
 
-// Smallest integer D in [0, 2M+1] with fl32(D)/fl32(2M) >= tau, or 2M+2 if
-// none (NaN tau, or tau above fl32(2M+1)/fl32(2M)).  With y = tau * 2M (exact
-// in fp64: a 24-bit mantissa times an integer below 2^24) every D >= y passes
-// and, because 1/2M exceeds half an fp32 ulp of tau, every D <= y - 1 fails;
-// so the answer is ceil(y) or ceil(y) - 1 and one exact IEEE test decides.
-// Straight-line code: no data-dependent loop for the compiler to expand.
+// The score of an integer distance D: D / 2M rounded once to the nearest
+// fp32 (ties to even).  For 2M < 2^24 both operands are exact in fp32 and one
+// IEEE division gives it.  Beyond (frames above ~2.8 MP per channel, up to
+// 2M < 2^31): q = D / 2M in fp64 (exact operands, one rounding) rounded to
+// fp32 is within one fp32 ulp of the answer; the answer is decided by the
+// exact sign of (midpoint * 2M - D) for the midpoints between q's fp32 value
+// and its neighbours (one FMA each: the product of a 25-bit midpoint and a
+// 31-bit integer is exact before FMA's single rounding, which keeps the sign).
+__device__ __forceinline__ float score_of(int64_t D, int64_t twoM) {
+  if (twoM < (int64_t(1) << 24)) return (float)(int32_t)D / (float)(int32_t)twoM;
+  if (D <= 0) return 0.f;
+  const double N = (double)twoM, x = (double)D;
+  const float f = (float)(x / N);
+  const uint32_t b = __float_as_uint(f);
+  const float lo = __uint_as_float(b - 1), hi = __uint_as_float(b + 1);
+  const double s_hi = fma(0.5 * ((double)f + (double)hi), N, -x);  // > 0: D/2M below the upper midpoint
+  if (s_hi < 0) return hi;
+  if (s_hi == 0) return (b & 1u) ? hi : f;
+  const double s_lo = fma(0.5 * ((double)lo + (double)f), N, -x);
+  if (s_lo > 0) return lo;
+  if (s_lo == 0) return (b & 1u) ? lo : f;
+  return f;
+}
+
+// Smallest integer D in [0, 2M+1] with score_of(D) >= tau, or 2M+2 if none
+// (NaN tau, or tau above the score of 2M+1).  For 2M < 2^24: with y = tau * 2M
+// (exact in fp64: a 24-bit mantissa times an integer below 2^24) every D >= y
+// passes and, because 1/2M exceeds half an fp32 ulp of tau, every D <= y - 1
+// fails; so the answer is ceil(y) or ceil(y) - 1 and one exact IEEE test
+// decides (straight-line code).  Beyond, a binary search: score_of never
+// decreases in D.
 __device__ int64_t theta_of(float tau, int64_t twoM) {
   const float den = (float)twoM;
   if (!(tau == tau)) return twoM + 2;
   if (tau <= 0.f) return 0;
+  if (twoM >= (int64_t(1) << 24)) {
+    int64_t lo = 0, hi = twoM + 2;  // answer in [lo, hi]; hi = none
+    while (lo < hi) {
+      const int64_t mid = lo + (hi - lo) / 2;
+      if (score_of(mid, twoM) >= tau) hi = mid;
+      else lo = mid + 1;
+    }
+    return lo;
+  }
   const double y = (double)tau * (double)twoM;
   if (y > (double)(twoM + 1))
     return ((float)(int32_t)(twoM + 1) / den >= tau) ? twoM + 1 : twoM + 2;
@@ -530,7 +566,6 @@ __device__ void select_walk(const RuleArgs& a, int64_t seg, int C, StageFn stage
   const int64_t s0 = seg * a.seg_len;
   const int T = (int)(a.n - s0 < a.seg_len ? a.n - s0 : a.seg_len);
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
-  const float den = (float)a.twoM;
   const int32_t* band = a.band + s0 * a.L;
   const int32_t* adj = adj_g ? adj_g + s0 : nullptr;  // D(t, t-1), contiguous
   if (tid == 0) {
@@ -606,7 +641,7 @@ __device__ void select_walk(const RuleArgs& a, int64_t seg, int C, StageFn stage
         const int t = base + u * nthr + tid;
         if (t < c1) {
           mask[s0 + t] = kp[u];
-          scores[s0 + t] = t > 0 ? (float)(Da[u] > Dr[u] ? Da[u] : Dr[u]) / den : 1.0f;
+          scores[s0 + t] = t > 0 ? score_of(Da[u] > Dr[u] ? Da[u] : Dr[u], a.twoM) : 1.0f;
         }
       }
     }
@@ -811,7 +846,6 @@ __global__ __launch_bounds__(256) void ngff_select_seq_kernel(RuleArgs a, const 
   uint8_t* fl = flag_g + s0;
   for (int64_t i = tid; i < T; i += nthr) fl[i] = 0;
   const int64_t theta = theta_of(tau_of_segment(a, seg), a.twoM);
-  const float den = (float)a.twoM;
   __syncthreads();
   if (tid == 0) {
     fl[0] = 1;
@@ -831,7 +865,7 @@ __global__ __launch_bounds__(256) void ngff_select_seq_kernel(RuleArgs a, const 
     const int64_t D = Dadj > Dref ? Dadj : Dref;
     const bool keep = (t == T - 1) || D >= theta;
     if (tid == 0) {
-      scores[s0 + t] = (float)D / den;
+      scores[s0 + t] = score_of(D, a.twoM);
       fl[t] = keep ? 1 : 0;
     }
     if (keep) {
@@ -933,7 +967,7 @@ __global__ void calib_kernel(RuleArgs a, int64_t nseg, int64_t target, int32_t* 
 
 __global__ void calib_final_kernel(const int32_t* best, int64_t nseg, int64_t twoM, float* tau) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (i < nseg) tau[i] = (float)best[i] / (float)twoM;
+  if (i < nseg) tau[i] = score_of(best[i], twoM);
 }
 
 // ---- host side ------------------------------------------------------------------------
@@ -989,9 +1023,9 @@ int validate_frames(const uint8_t* frames, int64_t n, int32_t H, int32_t W, int3
     return set_error(COFIE_EUNSUPPORTED, "%lld bins exceed 4096", (long long)nbins);
   const int64_t npix = (int64_t)H * W;
   const int64_t mass = mode == COFIE_HIST_PER_CHANNEL ? 3 * npix : npix;
-  if (2 * mass >= (int64_t(1) << 24))
-    return set_error(COFIE_EUNSUPPORTED,
-                     "2M = %lld >= 2^24: distances would not be exact in fp32", (long long)(2 * mass));
+  if (2 * mass >= (int64_t(1) << 31))
+    return set_error(COFIE_EUNSUPPORTED, "2M = %lld >= 2^31: distances would not fit the int32 band",
+                     (long long)(2 * mass));
   sh->n = n;
   sh->H = H;
   sh->W = W;
@@ -1353,7 +1387,6 @@ __global__ __launch_bounds__(1024) void ngff_push_kernel(PushArgs a) {
     if (j < nb) incl_sh[j] = x;
   }
   __syncthreads();
-  const float den = (float)a.twoM;
   for (int j = tid; j < nb; j += nthr) {
     const int64_t t = t0 + j;
     float score = 1.0f;
@@ -1363,7 +1396,7 @@ __global__ __launch_bounds__(1024) void ngff_push_kernel(PushArgs a) {
       const int32_t* row = bandL + j * L;
       const int64_t k = t - rt;  // 1 <= k <= L by the gap rule
       const int32_t Dadj = row[0], Dref = row[k < 1 ? 0 : (k > L ? L - 1 : k - 1)];
-      score = (float)(Dadj > Dref ? Dadj : Dref) / den;
+      score = score_of(Dadj > Dref ? Dadj : Dref, a.twoM);
     }
     a.out_scores[s * a.ld + j] = score;
     a.out_mask[s * a.ld + j] = (uint8_t)keep_sh[j];

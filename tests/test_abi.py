@@ -108,7 +108,7 @@ FAKE = 0x1000
     ((FAKE, 4, 8, 8, 3, 512, B.PER_CHANNEL, FAKE), B.COFIE_EINVAL),       # bins > 256
     ((FAKE, 4, 8, 8, 3, 24, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # not a power of two
     ((FAKE, 4, 8, 8, 3, 32, B.JOINT3D, FAKE), B.COFIE_EUNSUPPORTED),      # 32^3 bins
-    ((FAKE, 4, 2000, 2000, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # 2M >= 2^24
+    ((FAKE, 4, 20000, 20000, 3, 32, B.PER_CHANNEL, FAKE), B.COFIE_EUNSUPPORTED),  # 2M >= 2^31
     ((FAKE, 4, 8, 8, 3, 32, B.PER_CHANNEL, None), B.COFIE_EINVAL),        # out NULL
     ((FAKE, 4, 64, 64, 3, 24, B.FRAMEDIFF, FAKE), B.COFIE_EUNSUPPORTED),  # grid not a power of two
     ((FAKE, 4, 64, 64, 3, 128, B.FRAMEDIFF, FAKE), B.COFIE_EUNSUPPORTED), # grid above 64

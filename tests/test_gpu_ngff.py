@@ -288,3 +288,26 @@ def test_calibration_matches_oracle(case):
     rule = B.keep_rule(mode, 0.3, L, 4, seg)
     tau_g = B.cofie_ngff_calibrate(to_dev(f), bins, rule, target).cpu().numpy()
     assert np.array_equal(tau_g.view(np.uint32), tau_o.view(np.uint32))
+
+
+@pytest.mark.parametrize("H,W,mode,bins", [(2160, 3840, "per_channel", 32),   # 4K: 2M = 4.98e7
+                                           (1464, 1920, "per_channel", 16),   # 2M just above 2^24
+                                           (2160, 3840, "gray", 32)])         # 2M just below 2^24
+def test_filter_frames_beyond_2_24(H, W, mode, bins):
+    """Frames whose 2M reaches past 2^24 (Eq. 2 with the score the correctly
+    rounded D / 2M): histograms, a threshold calibrated for 50 % retention
+    (the binary-search threshold path), scores, masks and counts equal to the
+    oracle's, bit for bit."""
+    f = synth.random_frames(4242 + H, 24, H, W, 3, scenes=6)
+    print(f"4K-class frames {f.shape} {mode} {bins}: 2M = {2 * oracle.mass(MODES[mode], H, W)}", flush=True)
+    h = oracle.histogram(f, bins, MODES[mode])
+    M = oracle.mass(MODES[mode], H, W)
+    theta, tau = oracle.ngff_calibrate(h, M, 12, 30, 4)
+    fd = to_dev(f)
+    tau_g = B.cofie_ngff_calibrate(fd, bins, B.keep_rule(mode, 0.3, 30, 4), 12)
+    torch.cuda.synchronize()
+    assert np.array_equal(tau_g.cpu().numpy().view(np.uint32), tau.view(np.uint32))
+    for t in (float(tau[0]), 0.011, 0.3):
+        g = run_filter(f, bins, mode, t)
+        o = oracle_filter(f, bins, mode, t)
+        assert_filter_equal(g, o)
