@@ -437,12 +437,14 @@ int cofie_mask_compact(const uint8_t* mask, int64_t n, int64_t segment_len, int3
  *                      written
  *   out_offsets        device int32 [k+1]: CSR of the kept rows per entry of
  *                      sel, counted in full (out_offsets[k] > capacity reports
- *                      a short dst); the total must stay below 2^31
+ *                      a short dst); a running count past 2^31 - 1 (sel may
+ *                      repeat frames) is stored as 2^31 - 1, and the frames
+ *                      from there on are not copied
  *   out_rows           optional device int32 [dst_capacity_rows]: the source
  *                      row of every written dst row (e.g. to gather positions)
  * 16-byte accesses when src, dst and row_bytes are 16-byte aligned.  Errors:
- * EINVAL for NULL pointers, n_rows outside [0, 2^31), row_bytes <= 0 or a
- * negative n_frames, k or capacity. */
+ * EINVAL for NULL pointers, n_rows outside [0, 2^31), row_bytes <= 0, a
+ * negative n_frames or k, or a capacity outside [0, 2^31). */
 int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, const int32_t* frame_offsets,
                         int32_t n_frames, const int32_t* sel, int32_t k, void* dst,
                         int64_t dst_capacity_rows, int32_t* out_offsets, int32_t* out_rows,
@@ -493,6 +495,29 @@ const char* cofie_version(void);
 int cofie_profiler_enable(int on);
 int cofie_profiler_reset(void);
 int cofie_profiler_read(const char* name_substr, double* total_ms, int64_t* launches);
+
+/* Host-side address check, for tests without a GPU.  cofie_debug_dry_run(1)
+ * (per host thread; it also clears earlier results and buffers) makes the
+ * entry points validate and plan as usual but launch nothing and make no HIP
+ * call; instead every kernel with an address model walks each global and LDS
+ * address its threads would touch, computed by the kernel's own index
+ * functions, and checks it against the buffers registered with
+ * cofie_debug_buffer (fake device addresses and their sizes: the caller's
+ * inputs, outputs and workspace; the library allocates nothing in a dry run
+ * when a workspace is given) and the launch's LDS.  Kernels with a model:
+ * the QER score kernels (every mode), the operand-order query copy, the frame
+ * means, the NGFF histograms and the frame gather; other launches are
+ * skipped unchecked.
+ * cofie_debug_dry_run_result returns the number of violations, the number of
+ * accesses checked, and a description of the first violation.
+ * cofie_debug_dry_run(0) ends the dry run. */
+int cofie_debug_dry_run(int on);
+int cofie_debug_buffer(const void* base, size_t bytes, const char* name);
+/* As cofie_debug_buffer, for an input whose values decide addresses (frame
+ * indices, frame offsets): `data` (host, `bytes` long, copied) is what the
+ * fake buffer holds for the address models. */
+int cofie_debug_buffer_data(const void* base, const void* data, size_t bytes, const char* name);
+int64_t cofie_debug_dry_run_result(int64_t* checked, char* msg, size_t msg_bytes);
 
 /* Streaming copy of `bytes` device bytes (16-byte aligned pointers): a plain
  * HBM read+write kernel used as a bandwidth and hardware-counter reference

@@ -140,6 +140,10 @@ def lib() -> ctypes.CDLL:
         "cofie_profiler_enable": (ctypes.c_int, [ctypes.c_int]),
         "cofie_profiler_reset": (ctypes.c_int, []),
         "cofie_profiler_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(f64), ctypes.POINTER(i64)]),
+        "cofie_debug_dry_run": (ctypes.c_int, [ctypes.c_int]),
+        "cofie_debug_buffer": (ctypes.c_int, [P, sz, ctypes.c_char_p]),
+        "cofie_debug_buffer_data": (ctypes.c_int, [P, P, sz, ctypes.c_char_p]),
+        "cofie_debug_dry_run_result": (i64, [ctypes.POINTER(i64), ctypes.c_char_p, sz]),
         "cofie_diag_stream_copy": (ctypes.c_int, [P, P, sz, P]),
         "cofie_diag_stream_read": (ctypes.c_int, [P, sz, P, sz, P]),
     }
@@ -367,6 +371,84 @@ def cofie_profiler_read(name_substr: str = ""):
     cnt = ctypes.c_int64()
     _check(lib().cofie_profiler_read(name_substr.encode(), ctypes.byref(ms), ctypes.byref(cnt)))
     return ms.value, cnt.value
+
+
+# ---- host-side address check (dry run) ----------------------------------------------
+
+class DryBuffer:
+    """A fake device buffer of a dry run: what the wrappers above read from a
+    tensor (shape, dtype, sizes, address), at an address no device holds."""
+    is_cuda = True
+    device = "cuda:0"
+
+    def __init__(self, addr: int, shape: tuple, dtype, esize: int):
+        self.addr, self.shape, self.dtype, self._esize = addr, shape, dtype, esize
+
+    def dim(self) -> int:
+        return len(self.shape)
+
+    def numel(self) -> int:
+        n = 1
+        for s in self.shape:
+            n *= s
+        return n
+
+    def element_size(self) -> int:
+        return self._esize
+
+    def is_contiguous(self) -> bool:
+        return True
+
+    def data_ptr(self) -> int:
+        return self.addr
+
+    def __getitem__(self, key):  # the wrappers return views of their outputs
+        return self
+
+
+class DryRun:
+    """cofie_debug_dry_run as a context: entry points called inside, with
+    DryBuffer arguments, a workspace and every output given and stream 0,
+    validate and plan as usual, launch nothing, and check every address of
+    the kernels that have an address model against the buffers."""
+
+    def __init__(self):
+        self._next = 1 << 44
+
+    def __enter__(self):
+        _check(lib().cofie_debug_dry_run(1))
+        return self
+
+    def __exit__(self, *exc):
+        lib().cofie_debug_dry_run(0)
+
+    def buffer(self, shape, dtype, name: str = "buffer", data=None, misalign: int = 0, trim: int = 0) -> DryBuffer:
+        """A fake buffer of `shape` and torch `dtype`; `data` (numpy, same
+        bytes) is what it holds where its values decide addresses; `misalign`
+        bytes shift its start off the 4 KiB page; `trim` bytes are cut from
+        its registered end (a buffer shorter than its shape claims)."""
+        import numpy as np
+        import torch
+        shape = tuple(int(x) for x in (shape if isinstance(shape, (tuple, list)) else (shape,)))
+        esize = torch.empty((), dtype=dtype).element_size()
+        nbytes = int(np.prod(shape, dtype=np.int64)) * esize
+        addr = self._next + misalign
+        self._next += (misalign + nbytes + 4095) // 4096 * 4096 + 4096  # an unregistered page between buffers
+        if data is None:
+            _check(lib().cofie_debug_buffer(addr, max(nbytes - trim, 0), name.encode()))
+        else:
+            arr = np.ascontiguousarray(data)
+            if arr.nbytes != nbytes:
+                raise ValueError(f"{name}: {arr.nbytes} data bytes for a buffer of {nbytes}")
+            _check(lib().cofie_debug_buffer_data(addr, arr.ctypes.data, max(nbytes - trim, 0), name.encode()))
+        return DryBuffer(addr, shape, dtype, esize)
+
+    def result(self):
+        """(violations, accesses checked, the first violation)."""
+        checked = ctypes.c_int64()
+        msg = ctypes.create_string_buffer(512)
+        v = lib().cofie_debug_dry_run_result(ctypes.byref(checked), msg, 512)
+        return int(v), int(checked.value), msg.value.decode()
 
 
 def cofie_diag_stream_copy(src, dst, stream=None) -> None:

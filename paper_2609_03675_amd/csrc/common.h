@@ -32,12 +32,35 @@ void clear_error();
 // without the latency of separate event packets on the stream.
 bool prof_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 
+// ---- host-side address check (dry run) ------------------------------------------
+// With the dry run on (cofie_debug_dry_run, for tests on the host: no GPU is
+// touched), the entry points validate and plan as usual but launch nothing and
+// make no HIP call; the kernels that have an address model walk instead every
+// global and LDS address their threads would touch, computed by the same
+// index functions the kernels use, and check each against the buffers the
+// caller registered (fake device addresses with their sizes) or the launch's
+// LDS size.  A violation records the first offending access.
+bool dry_run();
+// [base + off, base + off + bytes) must lie in the registered buffer that
+// holds `base` (the kernel's base pointer for this access)
+void dry_access(const void* base, int64_t off, int64_t bytes, const char* what);
+void dry_lds(int64_t off, int64_t bytes, int64_t lds_bytes, const char* what);
+// lo <= v < hi (an index that stays inside its buffer but would read or write
+// another row's or slot's data)
+void dry_range(int64_t v, int64_t lo, int64_t hi, const char* what);
+// Host-to-device copy of a plan table: in a dry run the bytes are kept on the
+// host as the shadow of `dst`, where the address models read them back with
+// dry_shadow (null for an address that no copy wrote).
+int copy_to_device(void* dst, const void* src, size_t bytes, hipStream_t s, const char* what);
+const void* dry_shadow(const void* dst);
+
 // Launch `kernel` on `s` (timed when profiling is on) and turn a launch failure
-// into COFIE_EHIP.
+// into COFIE_EHIP.  In a dry run nothing is launched.
 template <typename... KArgs, typename... Args>
 int launch(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds,
            hipStream_t s, Args... args) {
   if (grid.x == 0 || grid.y == 0 || grid.z == 0) return COFIE_OK;
+  if (dry_run()) return COFIE_OK;
   (void)hipGetLastError();
   hipEvent_t start = nullptr, stop = nullptr;
   if (prof_slot(name, &start, &stop))
@@ -58,7 +81,7 @@ void lds_attr_mark(const void* kernel, size_t bytes);
 
 template <typename... KArgs>
 int allow_lds(void (*kernel)(KArgs...), size_t bytes) {
-  if (bytes <= 65536) return COFIE_OK;
+  if (bytes <= 65536 || dry_run()) return COFIE_OK;
   const void* k = reinterpret_cast<const void*>(kernel);
   if (lds_attr_done(k, bytes)) return COFIE_OK;
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);

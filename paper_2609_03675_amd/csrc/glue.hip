@@ -12,6 +12,7 @@
 //   the output CSR; a copy kernel then streams every selected frame's
 //   contiguous byte range with 16-byte lanes (4-byte or byte lanes when the
 //   pointers or the row size are not aligned), bounded by the capacity.
+#include <climits>
 #include <type_traits>
 
 #include "common.h"
@@ -78,8 +79,10 @@ __global__ __launch_bounds__(kGlueThreads) void mask_compact_kernel(const uint8_
   }
 }
 
-__device__ __forceinline__ void frame_rows(const int32_t* offs, int32_t n_frames, int64_t n_rows,
-                                           int32_t f, int64_t* lo, int64_t* hi) {
+// Rows [lo, hi) of frame f: its CSR range clamped to [0, n_rows) (empty for
+// a frame index outside [0, n_frames) or a decreasing range).
+__host__ __device__ __forceinline__ void frame_rows(const int32_t* offs, int32_t n_frames, int64_t n_rows,
+                                                    int32_t f, int64_t* lo, int64_t* hi) {
   if (f < 0 || f >= n_frames) {
     *lo = *hi = 0;
     return;
@@ -89,6 +92,13 @@ __device__ __forceinline__ void frame_rows(const int32_t* offs, int32_t n_frames
   b = b < 0 ? 0 : (b > n_rows ? n_rows : b);
   *lo = a;
   *hi = b < a ? a : b;
+}
+
+// An output offset as stored: a running row count saturated at 2^31 - 1, so
+// that a total past the int32 range never wraps to a negative offset (the
+// capacity is below 2^31, so every frame placed past it is skipped).
+__host__ __device__ __forceinline__ int32_t out_offset(int64_t rows) {
+  return (int32_t)(rows < INT32_MAX ? rows : INT32_MAX);
 }
 
 // out_offs[0..k]: exclusive scan of the selected frames' clamped row counts
@@ -108,7 +118,7 @@ __global__ __launch_bounds__(kGlueThreads) void gather_offsets_kernel(const int3
     }
     int64_t total;
     const int64_t ex = block_exscan64(len, &total, wsum);
-    if (i < k) out_offs[i + 1] = (int32_t)(base + ex + len);
+    if (i < k) out_offs[i + 1] = out_offset(base + ex + len);
     base += total;
   }
   if (tid == 0) out_offs[0] = 0;
@@ -188,7 +198,7 @@ __global__ __launch_bounds__(256) void gather_copy_kernel(const uint8_t* src, in
       }
       int64_t total;
       const int64_t ex = block_exscan64(len, &total, wsum);
-      if (i < k) offs_out[i + 1] = (int32_t)(base + ex + len);
+      if (i < k) offs_out[i + 1] = out_offset(base + ex + len);
       base += total;
     }
     if (threadIdx.x == 0) offs_out[0] = 0;
@@ -198,6 +208,41 @@ __global__ __launch_bounds__(256) void gather_copy_kernel(const uint8_t* src, in
 // at most this many frames take the one-kernel gather (each workgroup sums
 // the row counts before its frame)
 constexpr int32_t kGatherFused = 4096;
+
+// Address model of gather_copy_kernel<V> (dry run): the frames' row ranges
+// through frame_rows on the host copies of sel and the frame offsets (given
+// with cofie_debug_buffer_data), each frame's output position as the kernel
+// takes it (the saturated offsets, or the exact prefix when it scans itself),
+// the source and destination bytes, the source-row output.
+void model_gather(int V, const uint8_t* src, int64_t n_rows, int64_t row_bytes, const int32_t* offs, int32_t n_frames,
+                  const int32_t* sel, int32_t k, const uint8_t* dst, int64_t capacity, bool scanned,
+                  const int32_t* offs_out, const int32_t* out_rows) {
+  const int32_t* sel_h = static_cast<const int32_t*>(dry_shadow(sel));
+  const int32_t* offs_h = static_cast<const int32_t*>(dry_shadow(offs));
+  if (!sel_h || !offs_h) {
+    dry_range(0, 0, 0, "gather: sel or the frame offsets without host contents");
+    return;
+  }
+  dry_range(row_bytes % V, 0, 1, "gather: row size not a multiple of the access");
+  dry_access(offs_out, 0, 4 * ((int64_t)k + 1), "gather: output offsets");
+  int64_t pre = 0;  // the exact prefix of the clamped row counts
+  for (int32_t i = 0; i < k; ++i) {
+    dry_access(sel, 4 * (int64_t)i, 4, "gather: sel");
+    const int32_t f = sel_h[i];
+    if (f >= 0 && f < n_frames) dry_access(offs, 4 * (int64_t)f, 8, "gather: frame offsets");
+    int64_t lo, hi;
+    frame_rows(offs_h, n_frames, n_rows, f, &lo, &hi);
+    const int64_t o = scanned ? out_offset(pre) : pre;
+    pre += hi - lo;
+    int64_t rows = hi - lo;
+    const int64_t room = capacity - o;
+    rows = rows < room ? rows : (room > 0 ? room : 0);
+    if (rows <= 0) continue;
+    dry_access(src, lo * row_bytes, rows * row_bytes, "gather: source rows");
+    dry_access(dst, o * row_bytes, rows * row_bytes, "gather: destination rows");
+    if (out_rows) dry_access(out_rows, 4 * o, 4 * rows, "gather: source row indices");
+  }
+}
 
 }  // namespace
 }  // namespace cofie
@@ -226,6 +271,9 @@ int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, cons
   if (row_bytes <= 0) return set_error(COFIE_EINVAL, "row_bytes must be positive");
   if (n_frames < 0 || k < 0 || dst_capacity_rows < 0)
     return set_error(COFIE_EINVAL, "negative n_frames, k or capacity");
+  if (dst_capacity_rows >= (int64_t(1) << 31))
+    return set_error(COFIE_EINVAL, "dst_capacity_rows = %lld: the output rows are int32 offsets, below 2^31",
+                     (long long)dst_capacity_rows);
   if (!out_offsets) return set_error(COFIE_EINVAL, "out_offsets is NULL");
   if (k > 0 && (!sel || !frame_offsets)) return set_error(COFIE_EINVAL, "sel or frame_offsets is NULL");
   if (k > 0 && n_rows > 0 && (!src || (dst_capacity_rows > 0 && !dst)))
@@ -244,6 +292,11 @@ int cofie_gather_frames(const void* src, int64_t n_rows, int64_t row_bytes, cons
   const uintptr_t al = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)row_bytes;
   const uint8_t* sp = static_cast<const uint8_t*>(src);
   uint8_t* dp = static_cast<uint8_t*>(dst);
+  if (dry_run()) {
+    model_gather(al % 16 == 0 ? 16 : (al % 4 == 0 ? 4 : 1), sp, n_rows, row_bytes, frame_offsets, n_frames, sel, k, dp,
+                 dst_capacity_rows, !fused, out_offsets, out_rows);
+    return COFIE_OK;
+  }
   if (al % 16 == 0)
     return launch("glue_gather_copy", gather_copy_kernel<16>, dim3(gx, gy), dim3(256), 0, s, sp, n_rows, row_bytes,
                   frame_offsets, n_frames, sel, k, dp, dst_capacity_rows, offs_in, out_offsets, out_rows);

@@ -139,6 +139,17 @@ __device__ __forceinline__ void count_pixel(uint32_t* cnt, const uint8_t* px, ui
   }
 }
 
+// Frame (or histogram row) of launch frame t under the map of HistArgs.
+__host__ __device__ __forceinline__ int64_t hist_map(int64_t t, int64_t group, int64_t stride, int64_t off) {
+  return group ? (t / group) * stride + off + t % group : t;
+}
+// Unit that wave g (of G sharing a frame) loads as the i-th of its batches'
+// units: g + i G, clamped to the last whole unit.
+__host__ __device__ __forceinline__ int hist_unit(int g, int i, int G, int units) {
+  const int u = g + i * G;
+  return u < units ? u : units - 1;
+}
+
 // grid: n * splits workgroups; workgroup (t, s) counts its share of frame t.
 template <int KIND, int P, int BC>
 __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
@@ -148,8 +159,8 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
   const int wave = tid >> 6, nw = nthr >> 6;
   const int64_t t = blockIdx.x / a.splits;
   const int s = (int)(blockIdx.x - t * a.splits);
-  const int64_t src_frame = a.group ? (t / a.group) * a.in_stride + a.in_off + t % a.group : t;
-  const int64_t dst_row = a.group ? (t / a.group) * a.out_stride + a.out_off + t % a.group : t;
+  const int64_t src_frame = hist_map(t, a.group, a.in_stride, a.in_off);
+  const int64_t dst_row = hist_map(t, a.group, a.out_stride, a.out_off);
   const uint8_t* f = a.frames + src_frame * a.frame_bytes;
   const int G = a.splits * nw;  // waves sharing this frame
   const int g = s * nw + wave;
@@ -161,8 +172,7 @@ __global__ __launch_bounds__(512) void ngff_hist_kernel(HistArgs a) {
   auto load_batch = [&](U3 (&v)[kUnroll], int b) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < kUnroll; ++j) {
-      int u = g + (b * kUnroll + j) * G;
-      u = u < a.units ? u : a.units - 1;
+      const int u = hist_unit(g, b * kUnroll + j, G, a.units);
       // frames are read once: non-temporal loads (1 fps stream 28.0 -> 26.4 us,
       // high-res 1031 -> 938 us)
       const uint32_t* src = reinterpret_cast<const uint32_t*>(f + (int64_t)u * kUnitBytes + lane * 12);
@@ -1075,11 +1085,46 @@ HistPlan plan_hist(const NgffShape& sh, const uint8_t* frames) {
   return p;
 }
 
+// Address model of ngff_hist_kernel (dry run): every unit load of every wave
+// through the kernel's own index functions, the byte-wise pixels after the
+// units, the LDS counters of every bin a pixel can reach, the output row.
+template <int KIND, int P, int BC>
+void model_hist(const HistArgs& a, int64_t n, int threads, size_t lds) {
+  const int nw = threads / 64, G = a.splits * nw;
+  const int C = KIND == K_GRAY1 ? 1 : 3;
+  dry_range(a.npix * C, 0, a.frame_bytes + 1, "hist: pixels past the frame");
+  dry_range((int64_t)a.units * kUnitBytes, 0, a.npix * C + 1, "hist: units past the pixels");
+  const int64_t top_bin = KIND == K_PC ? 3 * (int64_t)a.B - 1
+                        : (KIND == K_JOINT ? (int64_t)a.B * a.B * a.B - 1 : (int64_t)a.B - 1);
+  dry_range(top_bin, 0, a.nbins, "hist: a pixel's bin past the counters");
+  if (BC) dry_range(BC, a.B, a.B + 1, "hist: compiled bin count differs");
+  dry_lds(0, (int64_t)a.nbins * P * 4, (int64_t)lds, "hist: counters");
+  for (int64_t t = 0; t < n; ++t) {
+    const int64_t fb = hist_map(t, a.group, a.in_stride, a.in_off) * a.frame_bytes;
+    for (int g = 0; g < G; ++g) {
+      const int nbatch = g < a.units ? (a.units - g + G * kUnroll - 1) / (G * kUnroll) : 0;
+      const int last_b = nbatch > 0 ? 2 * (nbatch / 2) : -1;  // the pipeline loads one batch past an even count
+      for (int b = 0; b <= last_b; ++b)
+        for (int j = 0; j < kUnroll; ++j)
+          dry_access(a.frames, fb + (int64_t)hist_unit(g, b * kUnroll + j, G, a.units) * kUnitBytes, kUnitBytes,
+                     "hist: unit load");
+    }
+    const int64_t p0 = (int64_t)a.units * (kUnitBytes / C);
+    if (p0 < a.npix) dry_access(a.frames, fb + p0 * C, (a.npix - p0) * C, "hist: pixels after the units");
+    dry_access(a.hist, hist_map(t, a.group, a.out_stride, a.out_off) * a.nbins * 4, (int64_t)a.nbins * 4,
+               "hist: histogram row");
+  }
+}
+
 template <int KIND, int P, int BC>
 int launch_hist_t(const HistArgs& args, const HistPlan& p, int64_t n, hipStream_t s) {
   auto k = ngff_hist_kernel<KIND, P, BC>;
   int rc = allow_lds(k, p.lds);
   if (rc) return rc;
+  if (dry_run()) {
+    if (n * p.splits > 0) model_hist<KIND, P, BC>(args, n, p.threads, p.lds);
+    return COFIE_OK;
+  }
   return launch("ngff_hist", k, dim3((unsigned)(n * p.splits)), dim3(p.threads), p.lds, s, args);
 }
 
@@ -1740,6 +1785,7 @@ int cofie_ngff_stream_create(int32_t n_streams, int32_t H, int32_t W, int32_t C,
   clear_error();
   if (!out_state) return set_error(COFIE_EINVAL, "out_state is NULL");
   *out_state = nullptr;
+  if (dry_run()) return set_error(COFIE_EUNSUPPORTED, "the online filter allocates its state: no dry run");
   if (!rule) return set_error(COFIE_EINVAL, "keep_rule is NULL");
   if (n_streams < 1) return set_error(COFIE_EINVAL, "n_streams = %d must be >= 1", n_streams);
   NgffShape sh;

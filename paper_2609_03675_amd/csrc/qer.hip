@@ -33,6 +33,8 @@
 //   with a per-head epilogue (the contraction runs over the query heads in
 //   order, grouped heads reading their key head through a segment map);
 //   other head sizes take per-head kernels of their own.
+#include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <mutex>
@@ -228,6 +230,73 @@ __device__ __forceinline__ float sum_x32(float v) {
 // segments) in this kernel on the 1 fps stream workload (48.9 vs 51.1 us).
 __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 
+// ---- address arithmetic of qer_score_kernel, shared with its address model ---------
+// Key load q (of 16 / R per segment) of lane `lane` for the tile whose first
+// token is t0: 16-byte index from the key base of its load in segment 0
+// (segment m adds 64 / R m).  Rows past the last key repeat the last.
+template <int R>
+__host__ __device__ __forceinline__ int64_t score_key_u4(int64_t t0, int q, int lane, int64_t last, int64_t krow_u4) {
+  constexpr int VPS = 16 / R;
+  const int64_t t = t0 + R * q + lane % R;
+  const int64_t tok = t < last ? t : last;
+  return tok * krow_u4 + VPS * (lane >> 4) + ((((lane & 15) / R) - q) & (VPS - 1));
+}
+// Plain MFMA-shaped key load of the contraction tail (lane: row lane % 16,
+// 16-byte column col + lane / 16 of that row, or two columns back where that
+// column is past the row: the value is then multiplied by zero).
+__host__ __device__ __forceinline__ int64_t score_tail_u4(int64_t t0, int lane, int64_t last, int64_t krow_u4, int col,
+                                                          bool in) {
+  const int64_t t = t0 + (lane & 15);
+  return (t < last ? t : last) * krow_u4 + (lane >> 4) + col + (in ? 0 : -2);
+}
+// Query fragment load: element e of phase ph (16-byte units): the query row
+// (of term p) and column it takes, and whether it is real (else it loads row
+// q0 of term 0, column 0, and stores zero).
+template <int NB, int NS, int FPS, int EPL>
+__host__ __device__ __forceinline__ int64_t score_q_u4(int32_t n_q, int32_t q0, int32_t nq_total, int32_t Lc,
+                                                       int32_t split_u4, int e, int ph, int lgC, int64_t row_u4,
+                                                       bool& ok) {
+  constexpr int LGNS = NS == 4 ? 2 : (NS == 2 ? 1 : 0);
+  const int row = e >> (lgC + LGNS), f = row >> 4;
+  const int p = f / NB, nb = f - p * NB;
+  const int q = nb * 16 + (row & 15);
+  const int sl = (e >> lgC) & (NS - 1);
+  const int col = sl * split_u4 + (ph << lgC) + (e & ((1 << lgC) - 1));
+  ok = f < FPS && q < n_q && col * EPL < Lc;
+  const int64_t grow = ok ? (int64_t)p * nq_total + q0 + q : (int64_t)q0;
+  return grow * row_u4 + (ok ? col : 0);
+}
+// Query fragments in LDS, one phase buffer: [slice][step][fragment][lane],
+// 16 bytes per lane.  Phase column c of a query row (a 16-byte chunk) belongs
+// to virtual step ls = VPS (c / SEGC) + c % VPS and lane group
+// g = (c % SEGC) / VPS, the order in which the key segments are read; row r
+// of fragment f sits at lane 16 g + (r ^ score_swz(ls, g)).  The swizzle
+// (step mod the batch length U, a power of two <= 8, and g: 16 values)
+// spreads the 64 stores of a contiguous query-row load over the banks.
+template <int U>
+__host__ __device__ __forceinline__ int score_swz(int ls, int g) {
+  constexpr int LOGU = U >= 8 ? 3 : (U >= 4 ? 2 : 1);
+  return ((ls & (U - 1)) | (g << LOGU)) & 15;
+}
+// slot of column c, fragment f, row r within a slice's steps
+template <int U, int VPS, int SEGC, int FPS>
+__host__ __device__ __forceinline__ int score_q_slot_c(int c, int f, int r) {
+  const int ls = VPS * (c / SEGC) + c % VPS, g = (c % SEGC) / VPS;
+  return ((ls * FPS + f) << 6) + (g << 4) + (r ^ score_swz<U>(ls, g));
+}
+// The slot element e of a phase's row-major query load is stored to: slice
+// (e >> lgC) % NS, row (e >> lgC) / NS (fragment row / 16, row row % 16),
+// column e % 2^lgC; spare elements past the fragments keep slot e (their value
+// is zero and never read).
+template <int U, int VPS, int SEGC, int FPS, int NS>
+__host__ __device__ __forceinline__ int score_q_slot(int e, int lgC, int lgS) {
+  constexpr int LGNS = NS == 4 ? 2 : (NS == 2 ? 1 : 0);
+  const int row = e >> (lgC + LGNS), f = row >> 4;
+  const int sl = (e >> lgC) & (NS - 1);
+  if (f >= FPS) return e;
+  return ((sl * FPS) << (lgS + 6)) + score_q_slot_c<U, VPS, SEGC, FPS>(e & ((1 << lgC) - 1), f, row & 15);
+}
+
 // NS > 1 splits the contraction inside the workgroup: wave w multiplies slice
 // w % NS (a.split_u4 columns from the previous one) of the tiles of wave group
 // w / NS, and the slices' accumulators are added in slice order through LDS
@@ -270,24 +339,12 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   const int slice = wave & (NS - 1), tw = wave >> LGNS;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int qs_lane = r16 / R;  // load index holding this lane's own row
-  // Query fragments in LDS: [step][term][block][lane] (16 bytes per lane, a
-  // phase of S steps), lane = 16 g + (r ^ swz(step, g)) for the row r and
-  // lane group g of the fragment.  The swizzle (step mod the batch length U,
-  // a power of two <= 8, and g give 16 values) spreads the 64 stores of a
-  // contiguous query-row load over the banks; readers undo it.  Phase column
-  // c (a 16-byte chunk of a query row) belongs to virtual step
-  // VPS (c / SEGC) + c % VPS and lane group (c % SEGC) / VPS, the order in
-  // which the key segments are read (phases hold whole segments); the tail
-  // steps past the whole segments use the same order.
-  constexpr int LOGU = U >= 8 ? 3 : (U >= 4 ? 2 : 1);
-  auto swz = [](int ls, int g) __attribute__((always_inline)) { return ((ls & (U - 1)) | (g << LOGU)) & 15; };
-  auto q_slot = [&](int c, int f, int r) __attribute__((always_inline)) {
-    const int ls = VPS * (c / SEGC) + c % VPS, g = (c % SEGC) / VPS;
-    return ((ls * FPS + f) << 6) + (g << 4) + (r ^ swz(ls, g));
-  };
+  // Query fragments in LDS: a phase of S steps per buffer in the layout of
+  // score_q_slot_c (the tail steps past the whole segments use the same
+  // order); readers undo the swizzle.
   int lsw[U];  // this lane's swizzled slot for steps congruent to u mod U
 #pragma unroll
-  for (int u = 0; u < U; ++u) lsw[u] = lane ^ swz(u, g4);
+  for (int u = 0; u < U; ++u) lsw[u] = lane ^ score_swz<U>(u, g4);
   const int pfull = VPS * a.nseg;
   const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
   const int64_t krow_u4 = a.k_row_u4;
@@ -365,17 +422,12 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     qmask = 0;
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
-      const int e = tid + kLdsThreads * i;
-      const int row = e >> (lgC + LGNS), f = row >> 4;
-      const int p = f / NB, nb = f - p * NB;
-      const int q = nb * 16 + (row & 15);
-      const int sl = (e >> lgC) & (NS - 1);
-      const int col = sl * a.split_u4 + (ph << lgC) + (e & ((1 << lgC) - 1));
-      const bool ok = f < FPS && q < a.n_q && col * M::EPL < a.Lc;
       // slots past the P NB fragments (f >= FPS, so p >= P) and masked rows
       // load row q0 of term 0, which every chunk has
-      const int64_t grow = ok ? (int64_t)p * a.nq_total + a.q0 + q : (int64_t)a.q0;
-      qr[i] = Qq[grow * row_u4 + (ok ? col : 0)];
+      bool ok;
+      const int64_t src = score_q_u4<NB, NS, FPS, M::EPL>(a.n_q, a.q0, a.nq_total, a.Lc, a.split_u4,
+                                                          tid + kLdsThreads * i, ph, lgC, row_u4, ok);
+      qr[i] = Qq[src];
       qmask |= ok ? 1u << i : 0u;
     }
   };
@@ -383,11 +435,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     uint4* dst = qs + (ph & 1) * kPhaseU4;
 #pragma unroll
     for (int i = 0; i < kQRegs; ++i) {
-      const int e = tid + kLdsThreads * i;
-      const int row = e >> (lgC + LGNS), f = row >> 4;
-      const int sl = (e >> lgC) & (NS - 1);
       const bool ok = (qmask >> i) & 1u;
-      dst[f < FPS ? (((sl * FPS) << (a.lgS + 6)) + q_slot(e & ((1 << lgC) - 1), f, row & 15)) : e] =
+      dst[score_q_slot<U, VPS, SEGC, FPS, NS>(tid + kLdsThreads * i, lgC, a.lgS)] =
           uint4{ok ? qr[i].x : 0u, ok ? qr[i].y : 0u, ok ? qr[i].z : 0u, ok ? qr[i].w : 0u};
     }
   };
@@ -414,12 +463,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       const int64_t t0 = (int64_t)(j < nmb ? rb + tw + TW * j : rb) * 16;
       const int64_t last = a.n_vis - 1;
 #pragma unroll
-      for (int q = 0; q < VPS; ++q) {
-        const int64_t tok = min(t0 + R * q + (lane % R), last);
-        const int chunk = VPS * g4 + ((((lane & 15) / R) - q) & (VPS - 1));
-        kq[j][q] = Kq + tok * krow_u4 + chunk;
-      }
-      k16[j] = Kq + min(t0 + r16, last) * krow_u4 + g4;
+      for (int q = 0; q < VPS; ++q) kq[j][q] = Kq + score_key_u4<R>(t0, q, lane, last, krow_u4);
+      k16[j] = Kq + score_tail_u4(t0, lane, last, krow_u4, 0, true);
     }
     f32x4 acc[MB][NB];
 #pragma unroll
@@ -642,7 +687,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       const int col = SEGC * a.nseg + 4 * (v - pfull);  // 16-byte column of lane group 0
       const bool in = (col + g4) * M::EPL < a.Lc;
       const int cph = (col + g4) - (ph << lgC);  // this lane's column within the phase
-      const uint4* qb = qs + (ph & 1) * kPhaseU4 + (((slice * FPS) << (a.lgS + 6)) + q_slot(cph, 0, r16));
+      const uint4* qb =
+          qs + (ph & 1) * kPhaseU4 + (((slice * FPS) << (a.lgS + 6)) + score_q_slot_c<U, VPS, SEGC, FPS>(cph, 0, r16));
       uint4 kf[MB];
 #pragma unroll
       for (int j = 0; j < MB; ++j) {
@@ -825,6 +871,26 @@ constexpr int kSeqPhaseU4 = kSeqS * kSeqNB * 64;  // uint4 per phase (64 KiB)
 constexpr int kSeqTab = 64;                       // chunks a workgroup's share may span
 constexpr size_t kSeqLds = 2 * (size_t)kSeqPhaseU4 * 16 + kSeqTab * sizeof(QerStreamDesc);
 
+// Key load q of lane `lane` for tile t of a chunk whose keys end at row last:
+// 16-byte offset from the chunk's first key row (32-bit: the host keeps a
+// sequence's keys under 2^31 16-byte units).  Row R q + lane % R of the tile,
+// clamped; chunk VPS (lane / 16) + ((lane % 16) / R - q) mod VPS.
+template <int R>
+__host__ __device__ __forceinline__ int32_t seq_key_off(int t, int q, int lane, int last, int32_t k_row_u4) {
+  constexpr int VPS = 16 / R;
+  const int t16 = t * 16 + R * q + lane % R;
+  const int tok = t16 < last ? t16 : last;
+  return (int32_t)((int64_t)tok * k_row_u4 + VPS * (lane >> 4) + ((((lane & 15) / R) - q) & (VPS - 1)));
+}
+// Operand-order query copy: element r of a chunk's copy (virtual step v, block
+// nb, lane l) holds the 16 bytes of chunk row `row` at 16-byte column `col`.
+__host__ __device__ __forceinline__ void qop_source(int64_t r, int R, int& row, int& col) {
+  const int vps = 16 / R, segc = 64 / R;
+  const int v = (int)(r / (kSeqNB * 64)), nb = (int)((r / 64) % kSeqNB), l = (int)(r & 63);
+  row = 16 * nb + (l & 15);
+  col = segc * (v / vps) + vps * (l >> 4) + v % vps;
+}
+
 // Operand-order copy of the stacked queries: chunk c (rows [q0, q0 + n_rows)
 // of the stacked query rows), virtual step v = 2 m + k, block nb, lane l: the
 // 16 bytes of row q0 + 16 nb + l % 16 at 16-byte column 8 m + 2 (l / 16) + k
@@ -833,15 +899,12 @@ constexpr size_t kSeqLds = 2 * (size_t)kSeqPhaseU4 * 16 + kSeqTab * sizeof(QerSt
 // column (64 / R) m + VPS (l / 16) + k.
 __global__ void qer_qop_kernel(const uint4* Q, int64_t row_u4, const QerStreamDesc* seq, int32_t n_seq,
                                int32_t ksteps, int32_t R, uint4* out) {
-  const int vps = 16 / R, segc = 64 / R;
   const int64_t per = (int64_t)ksteps * kSeqNB * 64;
   const int64_t total = per * n_seq;
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
     const int c = (int)(e / per);
-    const int64_t r = e - c * per;
-    const int v = (int)(r / (kSeqNB * 64)), nb = (int)((r / 64) % kSeqNB), l = (int)(r & 63);
-    const int row = 16 * nb + (l & 15);
-    const int col = segc * (v / vps) + vps * (l >> 4) + v % vps;
+    int row, col;
+    qop_source(e - c * per, R, row, col);
     const QerStreamDesc sd = seq[c];
     out[e] = row < sd.n_rows ? Q[(int64_t)(sd.q0 + row) * row_u4 + col] : uint4{0u, 0u, 0u, 0u};
   }
@@ -931,10 +994,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_seq_kernel(SeqArgs a) {
     for (int j = 0; j < MB; ++j) {
       const int t = j < r.nmb ? r.tb + wave + TW * j : r.tb;  // missing tiles repeat the round's first
 #pragma unroll
-      for (int q = 0; q < VPS; ++q) {
-        const int tok = min(t * 16 + R * q + lane % R, last);
-        off[VPS * j + q] = tok * a.k_row_u4 + VPS * g4 + ((own - q) & (VPS - 1));
-      }
+      for (int q = 0; q < VPS; ++q) off[VPS * j + q] = seq_key_off<R>(t, q, lane, last, a.k_row_u4);
     }
   };
   koff(cur, kc_base, kc_off);
@@ -1845,11 +1905,300 @@ LdsPlan plan_score_lds(int64_t n_vis, int64_t Lc, size_t esize, int P, int PNB, 
   return L;
 }
 
+// ---- address models (dry run) -------------------------------------------------------
+// Host walks of the addresses that a kernel's threads touch, computed by the
+// index functions the kernel itself uses, each checked against the registered
+// buffers or the launch's LDS.  An address affine in a loop counter (the key
+// segments of a row) is checked at both ends of the loop, which bounds every
+// address between them.  Values that decide an index and lie in device
+// memory are read from the host copies of the plan tables (dry_shadow).
+
+template <typename T>
+const T* shadow_of(const T* dev, const char* what) {
+  const T* p = static_cast<const T*>(dry_shadow(dev));
+  if (!p && dev) dry_range(0, 0, 0, what);  // a table no copy wrote: reported as a violation
+  return p;
+}
+
+// qer_score_kernel with grid `grid` and `lds` bytes of LDS
+template <typename T, int MB, int NB, int P, int NS, int MODE>
+void model_score(ScoreLdsArgs a, int grid, size_t lds) {
+  constexpr int BASE = MODE & 3;
+  constexpr bool GQA = (MODE & kModeGqa) != 0;
+  constexpr bool SEQ = (MODE & kModeSeq) != 0;
+  constexpr int R = lds_rows(MB, P * NB);
+  constexpr int VPS = 16 / R, SEGC = 64 / R;
+  constexpr int U = lds_batch(MB, P * NB, R, NS) / (BASE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
+  constexpr int FPS = P * NB;
+  constexpr int kQRegs = lds_q_regs(FPS, NS);
+  constexpr int kPhaseU4 = kQRegs * kLdsThreads;
+  constexpr int TW = kLdsWaves / NS;
+  const int64_t L = (int64_t)lds;
+  const int lgC = a.lgS + 2;
+  const int pfull = VPS * a.nseg;
+  const int64_t row_u4 = (int64_t)a.Lc * sizeof(T) / 16;
+  const int64_t krow_u4 = a.k_row_u4;
+  dry_range(grid, a.nwg, a.nwg + 1, "score: grid and planned workgroups differ");
+  if (a.xcd_order) dry_range(a.nwg % 8, 0, 1, "score: XCD order needs whole groups of 8 workgroups");
+  if (a.clear && a.nclear > 0) dry_access(a.clear, 0, 4 * (int64_t)a.nclear, "score: arrival counters");
+  // LDS past the phase buffers
+  const int64_t extra = (int64_t)(a.nphase > 1 ? 2 : 1) * kPhaseU4 * 16;
+  if constexpr (BASE == kModeSoftProb) dry_lds(extra, (int64_t)a.H * a.n_q * 8, L, "score: row statistics in LDS");
+  int seg_lo = 0, seg_hi = a.nseg - 1;  // the key segments read (mapped for grouped heads)
+  if constexpr (GQA) {
+    dry_lds(extra + (BASE == kModeSoftProb ? (int64_t)a.H * a.n_q * 8 : 0), 4 * (int64_t)a.nseg, L,
+            "score: segment map");
+    seg_lo = INT32_MAX;
+    seg_hi = -1;
+    for (int v = 0; v < a.nseg; ++v) {
+      const int sm = (v / a.sph / a.G) * a.sph + v % a.sph;
+      seg_lo = std::min(seg_lo, sm);
+      seg_hi = std::max(seg_hi, sm);
+    }
+  }
+  if constexpr (NS > 1) dry_lds(extra, (int64_t)(NS - 1) * TW * MB * NB * 4 * 64 * 4, L, "score: slice sums");
+  if constexpr (BASE == kModeSoftProb)
+    if (a.H * a.n_q > 0) {
+      dry_access(a.stats, ((int64_t)a.q0) * 8, 8, "score: pass-2 statistics");
+      dry_access(a.stats, ((int64_t)(a.H - 1) * a.nq_total + a.q0 + a.n_q - 1) * 8, 8, "score: pass-2 statistics");
+    }
+
+  // query fragment stores: slots inside the phase buffer, both buffers
+  for (int par = 0; par < (a.nphase > 1 ? 2 : 1); ++par)
+    for (int e = 0; e < kPhaseU4; ++e) {
+      const int slot = score_q_slot<U, VPS, SEGC, FPS, NS>(e, lgC, a.lgS);
+      dry_range(slot, 0, kPhaseU4, "score: query slot outside its phase buffer");
+      dry_lds(((int64_t)par * kPhaseU4 + slot) * 16, 16, L, "score: query fragment store");
+    }
+  // fragment reads of the batches and the tail, following the kernel's phase
+  // counter; phase ph's buffer is ph % 2
+  for (int slice = 0; slice < NS; ++slice) {
+    int ph = 0;
+    bool pending = a.nphase > 1;
+    for (int ms = 0; ms < pfull; ms += U) {
+      if (pending && ms > ph * a.S) pending = false;
+      const int64_t qb = ((int64_t)slice * a.S + ms - (int64_t)ph * a.S) * FPS * 64;
+      for (int h = 0; h < U / VPS; ++h) {
+        if (ms + VPS * h >= pfull) continue;
+        for (int k = 0; k < VPS; ++k) {
+          const int64_t lo = qb + (int64_t)((VPS * h + k) * FPS) * 64, hi = lo + (int64_t)(FPS - 1) * 64 + 63;
+          dry_range(lo, 0, kPhaseU4, "score: batch fragment read outside its phase buffer");
+          dry_range(hi, 0, kPhaseU4, "score: batch fragment read outside its phase buffer");
+          dry_lds(((ph & 1) * (int64_t)kPhaseU4 + lo) * 16, (hi - lo + 1) * 16, L, "score: batch fragment read");
+        }
+      }
+      if (ms + U == (ph + 1) * a.S && ph + 1 < a.nphase) {
+        pending = false;
+        ++ph;
+        if (ph + 1 < a.nphase) pending = true;
+      }
+    }
+    if (pfull < a.ksteps && pending) ++ph;
+    for (int v = pfull; v < a.ksteps; ++v) {
+      const int col = SEGC * a.nseg + 4 * (v - pfull);
+      for (int lane = 0; lane < 64; ++lane) {
+        const int cph = col + (lane >> 4) - (ph << lgC);
+        dry_range(cph, 0, 1 << lgC, "score: tail column outside its phase");
+        const int64_t slot = ((int64_t)(slice * FPS) << (a.lgS + 6)) + score_q_slot_c<U, VPS, SEGC, FPS>(cph, 0, lane & 15);
+        for (int f = 0; f < FPS; ++f) {
+          dry_range(slot + f * 64, 0, kPhaseU4, "score: tail fragment read outside its phase buffer");
+          dry_lds(((ph & 1) * (int64_t)kPhaseU4 + slot + f * 64) * 16, 16, L, "score: tail fragment read");
+        }
+      }
+    }
+  }
+
+  // the chunk's query rows (q0, n_q): every phase's loads
+  auto q_loads = [&](int q0, int n_q) {
+    for (int ph = 0; ph < a.nphase; ++ph)
+      for (int e = 0; e < kPhaseU4; ++e) {
+        bool ok;
+        const int64_t src = score_q_u4<NB, NS, FPS, Mma<T>::EPL>(n_q, q0, a.nq_total, a.Lc, a.split_u4, e, ph, lgC,
+                                                                 row_u4, ok);
+        dry_access(a.Qp, src * 16, 16, "score: query load");
+      }
+  };
+  std::vector<std::pair<int, int>> q_done;
+  const int32_t* nf_h = nullptr;
+  if constexpr (BASE == kModeSoftStats)
+    if (a.soft_nf) nf_h = shadow_of(a.soft_nf, "score: per-query frame counts without a host copy");
+  // tiles [t_begin, t_end) of one key sequence for workgroup b
+  auto share = [&](int b, int t_begin, int t_end, int64_t kbase_u4, int64_t n_vis, int q0, int n_q) {
+    if (std::find(q_done.begin(), q_done.end(), std::make_pair(q0, n_q)) == q_done.end()) {
+      q_done.push_back({q0, n_q});
+      q_loads(q0, n_q);
+    }
+    if constexpr (BASE == kModeSoftStats) {
+      if (a.soft_nf)
+        for (int nb = 0; nb < NB; ++nb)
+          if (nb * 16 < n_q) {
+            const int gi = (q0 + nb * 16) / a.group_rows;
+            dry_access(a.soft_nf, 4 * (int64_t)gi, 4, "score: per-query frame count");
+            if (nf_h) dry_access(a.soft_offs, 4 * (int64_t)nf_h[gi], 4, "score: the query's key limit");
+          }
+    }
+    const int64_t last = n_vis - 1;
+    for (int rb = t_begin; rb < t_end; rb += TW * MB) {
+      const int rr = (rb - t_begin) / (TW * MB);
+      if constexpr (BASE == kModeSoftStats) dry_range(rr, 0, a.rounds, "score: round past the statistics slots");
+      for (int tw = 0; tw < TW; ++tw) {
+        int nmb = 0;
+        for (int j = 0; j < MB; ++j) nmb += (rb + tw + TW * j < t_end) ? 1 : 0;
+        for (int slice = 0; slice < NS; ++slice) {
+          const int64_t k0 = kbase_u4 + (NS > 1 ? (int64_t)slice * a.split_u4 : 0);
+          for (int j = 0; j < MB; ++j) {
+            const int64_t t0 = (int64_t)(j < nmb ? rb + tw + TW * j : rb) * 16;
+            for (int lane = 0; lane < 64; ++lane) {
+              if (a.nseg > 0)
+                for (int q = 0; q < VPS; ++q) {
+                  const int64_t off = k0 + score_key_u4<R>(t0, q, lane, last, krow_u4);
+                  dry_access(a.K, (off + (int64_t)SEGC * seg_lo) * 16, 16, "score: key load");
+                  dry_access(a.K, (off + (int64_t)SEGC * seg_hi) * 16, 16, "score: key load");
+                }
+              for (int v = pfull; v < a.ksteps; ++v) {
+                const int col = SEGC * a.nseg + 4 * (v - pfull);
+                const bool in = (col + (lane >> 4)) * Mma<T>::EPL < a.Lc;
+                dry_access(a.K, (k0 + score_tail_u4(t0, lane, last, krow_u4, col, in)) * 16, 16, "score: key tail load");
+              }
+            }
+          }
+        }
+        if constexpr (BASE == kModeSoftStats) {
+          // (max, sum) of every head and query row of this wave and round
+          const int heads = a.sph > 0 ? a.nseg / a.sph : 0;
+          const int64_t slot = ((int64_t)b * kLdsWaves + tw) * a.rounds + rr;
+          if (heads > 0 && n_q > 0)
+            for (int64_t row : {(int64_t)q0, (int64_t)(heads - 1) * a.nq_total + q0 + n_q - 1})
+              dry_access(a.stats_part, (((row >> 4) * a.nparts + slot) * 16 + (row & 15)) * 8, 8,
+                         "score: pass-1 statistics");
+          continue;
+        }
+        // the maxima of this wave's tiles (slice 0 of the wave group)
+        for (int j = 0; j < nmb; ++j) {
+          const int64_t tile = rb + tw + TW * j;
+          for (int64_t tok : {tile * 16, std::min(tile * 16 + 15, n_vis - 1)}) {
+            if (tok < tile * 16 || tok >= n_vis) continue;
+            if (!SEQ && a.group_rows == 0) {
+              dry_access(a.m, tok * 4, 4, "score: m");
+              continue;
+            }
+            dry_range(tok, 0, a.m_stride, "score: token past the row of m");
+            for (int nb = 0; nb < NB; ++nb) {
+              if (nb * 16 >= n_q) break;
+              const int64_t g = (q0 + nb * 16) / a.group_rows;
+              dry_access(a.m, (g * a.m_stride + tok) * 4, 4, "score: m of a query");
+            }
+          }
+        }
+      }
+    }
+  };
+  const QerStreamDesc* sd_h = nullptr;
+  if constexpr (SEQ) sd_h = shadow_of(a.streams, "score: sequence table without a host copy");
+  for (int blk = 0; blk < grid; ++blk) {
+    const int wg = a.xcd_order ? (blk & 7) * (a.nwg >> 3) + (blk >> 3) : blk;
+    dry_range(wg, 0, a.nwg, "score: workgroup share");
+    const int f_begin = (int)((int64_t)a.tiles * wg / a.nwg);
+    const int f_end = (int)((int64_t)a.tiles * (wg + 1) / a.nwg);
+    int nr = 0;  // rounds run (pass 1: the rest are filled with empty statistics)
+    if constexpr (SEQ) {
+      if (!sd_h) return;
+      int sidx = 0;
+      while (sidx + 1 < a.n_streams && sd_h[sidx].tile0 + sd_h[sidx].ntiles <= f_begin) ++sidx;
+      for (int fb = f_begin; fb < f_end && sidx < a.n_streams;) {
+        dry_access(a.streams, (int64_t)sidx * sizeof(QerStreamDesc), sizeof(QerStreamDesc), "score: sequence table");
+        const QerStreamDesc sd = sd_h[sidx++];
+        const int s_end = sd.tile0 + sd.ntiles;
+        if (s_end <= fb || sd.ntiles <= 0) continue;
+        const int tb = fb - sd.tile0, te = (s_end < f_end ? s_end : f_end) - sd.tile0;
+        fb = sd.tile0 + te;
+        share(blk, tb, te, sd.key0 * krow_u4, sd.n_keys, sd.q0, sd.n_rows);
+      }
+    } else {
+      share(blk, f_begin, f_end, 0, a.n_vis, a.q0, a.n_q);
+      nr = (f_end - f_begin + TW * MB - 1) / (TW * MB);
+    }
+    if constexpr (BASE == kModeSoftStats) {
+      for (int tw = 0; tw < kLdsWaves; ++tw)
+        for (int rr = nr; rr < a.rounds; ++rr) {
+          const int64_t slot = ((int64_t)blk * kLdsWaves + tw) * a.rounds + rr;
+          if (a.H * a.n_q > 0)
+            for (int64_t row : {(int64_t)a.q0, (int64_t)(a.H - 1) * a.nq_total + a.q0 + a.n_q - 1})
+              dry_access(a.stats_part, (((row >> 4) * a.nparts + slot) * 16 + (row & 15)) * 8, 8,
+                         "score: empty pass-1 statistics");
+        }
+    }
+  }
+}
+
+// Address model of qer_frame_mean_kernel (grid x gy workgroups of `threads`)
+void model_frame_mean(int gx, int gy, int threads, const float* m, int32_t n_vis, const int32_t* offs,
+                      int32_t n_frames, const float* out_scores, const uint32_t* keys, const int32_t* nf_q,
+                      const int32_t* trees, int32_t tree_ints, int32_t tree_stride, int32_t k_top,
+                      const int32_t* out_idx, const QerQueryDesc* qd) {
+  const int32_t* nf_h = nf_q ? shadow_of(nf_q, "frame mean: per-query frame counts without a host copy") : nullptr;
+  const QerQueryDesc* qd_h = qd ? shadow_of(qd, "frame mean: query table without a host copy") : nullptr;
+  if ((nf_q && !nf_h) || (qd && !qd_h)) return;
+  const int64_t nfw = (int64_t)gx * (threads / 64);  // frames the grid covers
+  for (int64_t g = 0; g < gy; ++g) {
+    int32_t nf = nf_q ? nf_h[g] : n_frames, nfr = n_frames, nv = n_vis, frame0 = 0;
+    if (nf_q) dry_access(nf_q, 4 * g, 4, "frame mean: frame count");
+    if (qd) {
+      dry_access(qd, g * (int64_t)sizeof(QerQueryDesc), sizeof(QerQueryDesc), "frame mean: query table");
+      frame0 = qd_h[g].frame0;
+      nv = qd_h[g].n_keys;
+      nfr = qd_h[g].n_frames;
+      nf = qd_h[g].nf;
+    }
+    dry_range(nv, 0, (int64_t)n_vis + 1, "frame mean: keys past the row of m");
+    dry_range(nfr, 0, (int64_t)n_frames + 1, "frame mean: frames past the row of scores");
+    dry_range(nf, 0, (int64_t)nfr + 1, "frame mean: prefix past the frames");
+    dry_range(std::min<int64_t>(nfr, 1), 0, nfw + 1, "frame mean: frames past the grid");
+    if (nfr > nfw) dry_range(nfr, 0, nfw + 1, "frame mean: frames past the grid");
+    const int32_t fr = std::min<int64_t>(nfr, nfw);
+    if (fr > 0) {
+      dry_access(out_scores, (g * n_frames) * 4, 4 * (int64_t)fr, "frame mean: scores");
+      dry_access(keys, (g * n_frames) * 4, 4 * (int64_t)fr, "frame mean: sort keys");
+    }
+    const int32_t nread = std::min(nf, fr);  // frames whose tokens are read
+    if (nread > 0) {
+      dry_access(offs, 4 * (int64_t)frame0, 4 * ((int64_t)nread + 1), "frame mean: frame offsets");
+      if (nv > 0) dry_access(m, (g * n_vis) * 4, 4 * (int64_t)nv, "frame mean: m");
+    }
+    if (k_top > 0 && nf > 0) dry_access(keys, (g * n_frames) * 4, 4 * (int64_t)std::min(nf, fr), "frame mean: top-k keys");
+    if (trees) {
+      const int32_t G = arrive_fan(gx);
+      dry_range((int64_t)G * tree_stride, 0, tree_ints, "frame mean: arrival tree");
+      dry_access(trees, (g * tree_ints) * 4, ((int64_t)G * tree_stride + 1) * 4, "frame mean: arrival tree");
+      if (k_top > 0) dry_access(out_idx, (g * k_top) * 4, 4 * (int64_t)k_top, "frame mean: top-k");
+    }
+  }
+}
+
+// qer_frame_mean_kernel on grid (gx, gy) of `threads` (its model in a dry run)
+int launch_frame_mean(int gx, int gy, int threads, hipStream_t s, const float* m, int32_t n_vis, const int32_t* offs,
+                      int32_t n_frames, float* out_scores, uint32_t* keys, const int32_t* nf_q, int32_t* trees,
+                      int32_t tree_ints, int32_t tree_stride, int32_t k_top, int32_t* out_idx, const QerQueryDesc* qd) {
+  if (dry_run()) {
+    if (gx > 0 && gy > 0)
+      model_frame_mean(gx, gy, threads, m, n_vis, offs, n_frames, out_scores, keys, nf_q, trees, tree_ints,
+                       tree_stride, k_top, out_idx, qd);
+    return COFIE_OK;
+  }
+  return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)gx, (unsigned)gy), dim3((unsigned)threads), 0,
+                s, m, n_vis, offs, n_frames, out_scores, keys, nf_q, trees, tree_ints, tree_stride, k_top, out_idx, qd);
+}
+
 template <typename T, int MB, int NB, int P, int NS, int MODE>
 int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, size_t lds, hipStream_t s) {
   auto k = qer_score_kernel<T, MB, NB, P, NS, MODE>;
   int rc = allow_lds(k, lds);
   if (rc) return rc;
+  if (dry_run()) {
+    dry_range((int64_t)lds, 0, 160 * 1024 + 1, "score: LDS beyond a CU's 160 KiB");
+    if (L.nwg > 0) model_score<T, MB, NB, P, NS, MODE>(sa, L.nwg, lds);
+    return COFIE_OK;
+  }
   const int base = MODE & 3;
   const char* name = base == kModeLogit ? "qer_score" : (base == kModeSoftStats ? "qer_soft_stats" : "qer_soft_score");
   return launch(name, k, dim3((unsigned)L.nwg), dim3(kLdsThreads), lds, s, sa);
@@ -1948,8 +2297,10 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
   Arena ar;
   ar.base = scratch.ptr();
   QerScratch w = carve_qer(ar, h, p, n_queries);
-  if (multi && hipMemcpyAsync(w.nf, nf_host, n_queries * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess)
-    return set_error(COFIE_EHIP, "copying the per-query frame counts failed");
+  if (multi) {
+    rc = copy_to_device(w.nf, nf_host, n_queries * sizeof(int32_t), s, "the per-query frame counts");
+    if (rc) return rc;
+  }
   const bool bf16 = h.dtype == COFIE_BF16;
   const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
   // the top-k runs in the frame-mean kernel's last workgroup when the score
@@ -2119,14 +2470,14 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
   }
   if (fused_tail) {
     const QerTrees tr = qer_trees(h.n_frames);
-    return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, n_queries), dim3(1024), 0, s,
+    return launch_frame_mean(tr.nwg, n_queries, 1024, s,
                   (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores, w.keys, (const int32_t*)w.nf,
                   w.done, tr.ints, tr.stride, k_top, out_idx, (const QerQueryDesc*)nullptr);
   }
   if (h.n_frames > 0) {
-    rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(h.n_frames, 4), n_queries),
-                dim3(256), 0, s, (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores,
-                w.keys, (const int32_t*)w.nf, (int32_t*)nullptr, 0, 0, k_top, out_idx, (const QerQueryDesc*)nullptr);
+    rc = launch_frame_mean(ceil_div(h.n_frames, 4), n_queries, 256, s, (const float*)w.m, h.n_vis, frame_offsets,
+                           h.n_frames, out_scores, w.keys, (const int32_t*)w.nf, (int32_t*)nullptr, 0, 0, k_top,
+                           out_idx, (const QerQueryDesc*)nullptr);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
@@ -2264,6 +2615,148 @@ StreamsScratch carve_streams(Arena& ar, const cofie_qer_desc& h, const QerPlan& 
 
 constexpr int kSeqLogit = kModeLogit | kModeSeq;
 
+// Address model of qer_qop_kernel: every element of the copy
+void model_qop(const uint4* Q, int64_t row_u4, const QerStreamDesc* seq, int32_t n_seq, int32_t ksteps, int32_t R,
+               const uint4* out) {
+  const QerStreamDesc* sd_h = shadow_of(seq, "qop: sequence table without a host copy");
+  if (!sd_h) return;
+  const int64_t per = (int64_t)ksteps * kSeqNB * 64;
+  for (int32_t c = 0; c < n_seq; ++c) {
+    dry_access(seq, (int64_t)c * sizeof(QerStreamDesc), sizeof(QerStreamDesc), "qop: sequence table");
+    dry_access(out, (int64_t)c * per * 16, per * 16, "qop: copy");
+    for (int64_t r = 0; r < per; ++r) {
+      int row, col;
+      qop_source(r, R, row, col);
+      dry_range(col, 0, row_u4, "qop: column past the query row");
+      if (row < sd_h[c].n_rows) dry_access(Q, ((int64_t)(sd_h[c].q0 + row) * row_u4 + col) * 16, 16, "qop: query load");
+    }
+  }
+}
+
+// Address model of qer_seq_kernel<U, R> (grid a.nwg, `lds` bytes of LDS): the
+// round sequence of every workgroup as the kernel walks it, its key loads at
+// both ends of each round's segments, its query-fragment copies and LDS
+// traffic, and its stores of m.
+template <int U, int R>
+void model_seq(const SeqArgs& a, size_t lds) {
+  constexpr int MB = 2, NB = kSeqNB, TW = kLdsWaves;
+  constexpr int VPS = 16 / R, SEGC = 64 / R;
+  constexpr int BPP = kSeqS / U;
+  constexpr int CP = kSeqPhaseU4 / kLdsThreads / BPP;
+  const int64_t L = (int64_t)lds;
+  const int ksteps = VPS * a.nseg, bpr = ksteps / U, nph = ksteps / kSeqS;
+  dry_range(nph, 2, INT32_MAX, "seq: a round needs two phases");
+  dry_range(ksteps % kSeqS, 0, 1, "seq: whole phases per round");
+  if (a.xcd_order) dry_range(a.nwg % 8, 0, 1, "seq: XCD order needs whole groups of 8 workgroups");
+  if (a.clear && a.nclear > 0) dry_access(a.clear, 0, 4 * (int64_t)a.nclear, "seq: arrival counters");
+  const QerStreamDesc* seq = shadow_of(a.seq, "seq: sequence table without a host copy");
+  if (!seq) return;
+  // LDS: the two phase buffers, then the table
+  for (int bp = 0; bp < BPP; ++bp) {
+    const int64_t hi = (int64_t)bp * CP * kLdsThreads + (CP - 1) * kLdsThreads + kLdsThreads - 1;
+    dry_range(hi, 0, kSeqPhaseU4, "seq: query slice past its phase buffer");
+    const int64_t rd = (int64_t)bp * U * NB * 64 + ((U - 1) * NB + NB - 1) * 64 + 63;
+    dry_range(rd, 0, kSeqPhaseU4, "seq: fragment read past its phase buffer");
+    dry_lds((kSeqPhaseU4 + rd) * 16, 16, L, "seq: fragment read");
+  }
+  dry_lds(2 * (int64_t)kSeqPhaseU4 * 16, kSeqTab * (int64_t)sizeof(QerStreamDesc), L, "seq: chunk table");
+  auto q_src = [&](int si, int ph) { return ((int64_t)si * ksteps + (int64_t)ph * kSeqS) * NB * 64; };
+  struct Rnd {
+    int sidx, tb, te;
+  };
+  for (int blk = 0; blk < a.nwg; ++blk) {
+    const int wg = a.xcd_order ? (blk & 7) * (a.nwg >> 3) + (blk >> 3) : blk;
+    const int f_begin = (int)((int64_t)a.tiles * wg / a.nwg);
+    const int f_end = (int)((int64_t)a.tiles * (wg + 1) / a.nwg);
+    int sidx0 = 0;
+    while (sidx0 + 1 < a.n_seq && seq[sidx0].tile0 + seq[sidx0].ntiles <= f_begin) ++sidx0;
+    const int tab_end = std::min(sidx0 + kSeqTab, a.n_seq);
+    dry_access(a.seq, (int64_t)sidx0 * sizeof(QerStreamDesc), (int64_t)(tab_end - sidx0) * sizeof(QerStreamDesc),
+               "seq: chunk table load");
+    auto first_of = [&](int si, int from) {
+      Rnd r{-1, 0, 0};
+      for (; si < tab_end; ++si) {
+        const QerStreamDesc sd = seq[si];
+        const int s_end = sd.tile0 + sd.ntiles;
+        if (sd.ntiles <= 0 || s_end <= from) continue;
+        if (sd.tile0 >= f_end) break;
+        r = Rnd{si, std::max(from, sd.tile0) - sd.tile0, std::min(s_end, f_end) - sd.tile0};
+        break;
+      }
+      return r;
+    };
+    auto next_of = [&](const Rnd& r) {
+      if (r.tb + TW * MB < r.te) return Rnd{r.sidx, r.tb + TW * MB, r.te};
+      return first_of(r.sidx + 1, seq[r.sidx].tile0 + r.te);
+    };
+    // a round's key offsets, lane by lane, at its first and last segment
+    auto keys = [&](const Rnd& r) {
+      const QerStreamDesc sd = seq[r.sidx];
+      const int64_t base = sd.key0 * a.k_row_u4;
+      for (int wave = 0; wave < TW; ++wave) {
+        int nmb = 0;
+        for (int j = 0; j < MB; ++j) nmb += (r.tb + wave + TW * j < r.te) ? 1 : 0;
+        for (int j = 0; j < MB; ++j) {
+          const int t = j < nmb ? r.tb + wave + TW * j : r.tb;
+          for (int lane = 0; lane < 64; ++lane)
+            for (int q = 0; q < VPS; ++q) {
+              const int32_t off = seq_key_off<R>(t, q, lane, sd.n_keys - 1, a.k_row_u4);
+              dry_range(off, 0, (int64_t)sd.n_keys * a.k_row_u4, "seq: key offset outside its sequence");
+              dry_access(a.K, (base + off) * 16, 16, "seq: key load");
+              dry_access(a.K, (base + off + (int64_t)SEGC * (a.nseg - 1)) * 16, 16, "seq: key load");
+            }
+        }
+      }
+    };
+    Rnd cur = first_of(sidx0, f_begin);
+    if (cur.sidx < 0) continue;
+    Rnd nxt = next_of(cur);
+    keys(cur);
+    dry_access(a.Qop, q_src(cur.sidx, 0) * 16, (int64_t)kSeqPhaseU4 * 16, "seq: first phase");
+    auto phase_src = [&](int pir) {
+      const bool next = pir >= nph;
+      const int si = next && nxt.sidx >= 0 ? nxt.sidx : cur.sidx;
+      dry_range(next ? pir - nph : pir, 0, nph, "seq: phase past its chunk");
+      return q_src(si, next ? pir - nph : pir);
+    };
+    dry_access(a.Qop, phase_src(1) * 16, 2 * (int64_t)CP * kLdsThreads * 16, "seq: query slices");
+    while (cur.sidx >= 0) {
+      dry_range(cur.sidx - sidx0, 0, kSeqTab, "seq: chunk past the LDS table");
+      for (int ph = 0; ph < nph; ++ph)
+        for (int bp = 0; bp < BPP; ++bp) {
+          const bool wrap = bp + 2 >= BPP;
+          const int64_t src = phase_src(ph + (wrap ? 2 : 1)) + (int64_t)(wrap ? bp + 2 - BPP : bp + 2) * CP * kLdsThreads;
+          dry_access(a.Qop, src * 16, (int64_t)CP * kLdsThreads * 16, "seq: query slice");
+          const int ahead = BPP * ph + bp + 3;
+          const int ms = (ahead >= bpr ? ahead - bpr : ahead) * U;
+          dry_range(ms / VPS, 0, a.nseg, "seq: key segment");
+          dry_range(ms / VPS + U / VPS - 1, 0, a.nseg, "seq: key segment");
+        }
+      const QerStreamDesc sd = seq[cur.sidx];
+      for (int wave = 0; wave < TW; ++wave)
+        for (int j = 0; j < MB; ++j) {
+          const int tile = cur.tb + wave + TW * j;
+          if (tile >= cur.te) continue;
+          for (int tok : {tile * 16, std::min(tile * 16 + 15, sd.n_keys - 1)}) {
+            if (tok < tile * 16 || tok >= sd.n_keys) continue;
+            dry_range(tok, 0, a.m_stride, "seq: token past the row of m");
+            for (int nb = 0; nb < NB && nb * 16 < sd.n_rows; ++nb) {
+              const int64_t g = (sd.q0 + nb * 16) / a.group_rows;
+              dry_access(a.m, (g * a.m_stride + tok) * 4, 4, "seq: m of a query");
+            }
+          }
+        }
+      cur = nxt;
+      if (cur.sidx >= 0) {
+        keys(cur);
+        nxt = next_of(cur);
+      }
+    }
+  }
+}
+
+
+
 int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets, const cofie_qer_desc& h,
                       const QerPlan& p, const StreamsPlan& sp, int32_t k_top, float* out_scores, int32_t* out_idx,
                       hipStream_t s) {
@@ -2279,8 +2772,8 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
   std::memcpy(meta.data(), sp.seq.data(), sp.seq.size() * sizeof(QerStreamDesc));
   std::memcpy(meta.data() + sp.seq.size() * sizeof(QerStreamDesc), sp.qry.data(),
               sp.qry.size() * sizeof(QerQueryDesc));
-  if (hipMemcpyAsync(w.meta, meta.data(), meta.size(), hipMemcpyHostToDevice, s) != hipSuccess)
-    return set_error(COFIE_EHIP, "copying the sequence tables failed");
+  rc = copy_to_device(w.meta, meta.data(), meta.size(), s, "the sequence tables");
+  if (rc) return rc;
   const auto* seq_d = reinterpret_cast<const QerStreamDesc*>(w.meta);
   const auto* qry_d = reinterpret_cast<const QerQueryDesc*>(w.meta + sp.seq.size() * sizeof(QerStreamDesc));
   const bool bf16 = h.dtype == COFIE_BF16;
@@ -2303,6 +2796,9 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
     // the query side in operand order, then qer_seq_kernel
     const int32_t ksteps = (int32_t)(p.Lc * p.esize / 64);
     const int64_t total = (int64_t)sp.seq.size() * ksteps * kSeqNB * 64;
+    if (dry_run())
+      model_qop(static_cast<const uint4*>(Q), (int64_t)(p.Lc * p.esize / 16), seq_d, (int32_t)sp.seq.size(), ksteps,
+                (int32_t)kSeqR, w.qop);
     rc = launch("qer_qop", qer_qop_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(total, 256), 8192)), dim3(256),
                 0, s, static_cast<const uint4*>(Q), (int64_t)(p.Lc * p.esize / 16), seq_d, (int32_t)sp.seq.size(),
                 ksteps, (int32_t)kSeqR, w.qop);
@@ -2327,9 +2823,10 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
     const size_t lds = kSeqLds;
     rc = allow_lds(kern, lds);
     if (rc) return rc;
+    if (dry_run()) model_seq<kSeqU, kSeqR>(qa, lds);
     rc = launch("qer_score", kern, dim3((unsigned)qa.nwg), dim3(kLdsThreads), lds, s, qa);
     if (rc) return rc;
-    return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, sp.n_queries), dim3(1024), 0, s,
+    return launch_frame_mean(tr.nwg, sp.n_queries, 1024, s,
                   (const float*)w.m, (int32_t)qa.m_stride, frame_offsets, std::max(sp.max_frames, 1), out_scores,
                   w.keys, (const int32_t*)nullptr, w.done, tr.ints, tr.stride, k_top, out_idx, qry_d);
   }
@@ -2383,7 +2880,7 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
                      : launch_lds_nb<float, 2, 1, 1, kSeqLogit>(sa, L, sp.NB, L.lds, s);
   }
   if (rc) return rc;
-  return launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)tr.nwg, sp.n_queries), dim3(1024), 0, s,
+  return launch_frame_mean(tr.nwg, sp.n_queries, 1024, s,
                 (const float*)w.m, (int32_t)sa.m_stride, frame_offsets, std::max(sp.max_frames, 1), out_scores,
                 w.keys, (const int32_t*)nullptr, w.done, tr.ints, tr.stride, k_top, out_idx, qry_d);
 }
@@ -2395,9 +2892,9 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
 int qer_rank_from_m(const float* m, int32_t n_vis, const int32_t* offs, int32_t n_frames, int32_t k_top,
                     float* out_scores, uint32_t* keys, int32_t* out_idx, hipStream_t s) {
   if (n_frames > 0) {
-    int rc = launch("qer_frame_mean", qer_frame_mean_kernel, dim3((unsigned)ceil_div(n_frames, 4), 1), dim3(256),
-                    0, s, m, n_vis, offs, n_frames, out_scores, keys, (const int32_t*)nullptr, (int32_t*)nullptr,
-                    0, 0, k_top, out_idx, (const QerQueryDesc*)nullptr);
+    int rc = launch_frame_mean(ceil_div(n_frames, 4), 1, 256, s, m, n_vis, offs, n_frames, out_scores, keys,
+                               (const int32_t*)nullptr, (int32_t*)nullptr, 0, 0, k_top, out_idx,
+                               (const QerQueryDesc*)nullptr);
     if (rc) return rc;
   }
   if (k_top == 0) return COFIE_OK;
@@ -2423,6 +2920,11 @@ namespace {
 int noalloc_scratch(void** out) {
   static std::mutex mu;
   static void* addr[64] = {};
+  if (dry_run()) {  // a fake address of the array's size, checked like the caller's buffers
+    static const uintptr_t kDryScratch = uintptr_t(0x7e) << 40;
+    *out = reinterpret_cast<void*>(kDryScratch);
+    return cofie_debug_buffer(*out, COFIE_QER_NOALLOC_SCRATCH_BYTES, "static scratch");
+  }
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(COFIE_EHIP, "hipGetDevice failed");
   if (dev < 0 || dev >= 64) return set_error(COFIE_EUNSUPPORTED, "device ordinal %d beyond 63", dev);
