@@ -379,7 +379,7 @@ typedef struct cofie_attn_desc {
                       /*   h / (H_q / H_kv)                                         */
   int32_t d;          /* head dimension: 128 (others EUNSUPPORTED)                   */
   int32_t vis_begin;  /* visual tokens are [vis_begin, vis_end); every other token   */
-  int32_t vis_end;    /*   is text (the scoring set of Sec. 3.3), 1 to 64 of them    */
+  int32_t vis_end;    /*   is text (the scoring set of Sec. 3.3), at least one       */
   int32_t n_frames;   /* frames of the visual tokens, >= 0                           */
   float scale;        /* softmax and QER scale; <= 0 selects 1/sqrt(d)               */
   void* workspace;    /* optional device scratch of                                  */
@@ -399,8 +399,8 @@ size_t cofie_attn_qer_workspace_bytes(const cofie_attn_desc* desc);
  *   out          device bf16 [L][H_q][128]
  *   frame_offsets device int32 [n_frames+1] (clamped as in cofie_qer_rank)
  * 16-byte aligned tensors.  Errors: EINVAL for NULL pointers or an invalid
- * descriptor, EUNSUPPORTED for d != 128 or a text count outside 1..64,
- * ENOMEM for a short workspace. */
+ * descriptor (no text token included), EUNSUPPORTED for d != 128, ENOMEM for
+ * a short workspace. */
 int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* frame_offsets,
                    const cofie_attn_desc* desc, int32_t k_top, void* out, float* out_scores, int32_t* out_idx,
                    void* stream);

@@ -17,17 +17,19 @@
 //    in LDS in the same order).  Heaviest query blocks first; the blocks of
 //    one head are kept on one XCD so that its L2 serves their key reads.
 //  * text-row workgroups (first in the grid): one per 256-token chunk of the
-//    key sequence, all text rows (<= 64, one 16-row tile per wave), looping
-//    over every head.  The per-head S^T tiles serve both the text rows'
-//    attention (a partial softmax over the chunk, merged afterwards) and QER:
-//    their sum over heads, kept in registers for the chunk's keys, is the
-//    head-mean logit of Eq. 6 up to the factor scale / H; its max over the
-//    text rows is m_j (Eq. 7) for the chunk's visual keys.
+//    key sequence and group of 128 text rows (one 16-row tile per wave),
+//    looping over every head.  The per-head S^T tiles serve both the text
+//    rows' attention (a partial softmax over the chunk, merged afterwards)
+//    and QER: their sum over heads, kept in registers for the chunk's keys,
+//    is the head-mean logit of Eq. 6 up to the factor scale / H; its max over
+//    the group's text rows is m_j (Eq. 7) for the chunk's visual keys (with
+//    several groups, a partial that attn_m_max reduces).
 //
 // attn_vt first writes V transposed (d-major rows of tokens, in the operand
 // order of the value product) into the workspace; attn_merge combines the
-// text rows' chunk partials; qer_rank_from_m then takes the frame means and
-// the top-k (Eqs. 7-8).
+// text rows' chunk partials (and attn_m_max the row groups' m_j);
+// qer_rank_from_m then takes the frame means and the top-k (Eqs. 7-8).
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -52,7 +54,7 @@ constexpr int kBM = kWaves * kRowsA;  // visual rows per workgroup
 constexpr int kBN = 64;          // tokens per LDS stage
 constexpr int kChunk = 256;      // tokens per text-row workgroup
 constexpr int kStages = kChunk / kBN;
-constexpr int kMaxText = 64;
+constexpr int kTextRows = 16 * kWaves;  // text rows per text workgroup
 
 struct AttnArgs {
   const uint16_t* Q;  // [L][H_q][128]
@@ -60,10 +62,10 @@ struct AttnArgs {
   const uint16_t* Vt; // [H_kv][128][Lp]: V transposed, tokens permuted (vpos32) in 32-token groups
   uint16_t* O;        // [L][H_q][128]
   int32_t L, Lp, H_q, H_kv, vb, ve, n_text, ntp;  // Lp: L rounded up to 64; ntp: text rows to 16
-  int32_t n_chunks, nb_pad, qb;               // text workgroups (padded to 8), query blocks per head
+  int32_t n_chunks, n_rg, nb_pad, qb;  // chunks, text row groups, text workgroups (padded to 8), query blocks per head
   float c2;          // scale * log2(e)
   float qer_scale;   // scale / H_q
-  float* m;          // [ve - vb]
+  float* m;          // [n_rg][ve - vb]: each row group's max (one group: m_j itself)
   float* part_o;     // [n_chunks][H_q][ntp][128]
   float2* part_ml;   // [n_chunks][H_q][ntp]: (row max, base 2; row sum)
 };
@@ -446,14 +448,14 @@ __device__ void visual_block(const AttnArgs& a, int b, char* lds) {
 }
 
 // ---- text rows: chunk partials of their attention, and QER's m_j --------------------------
-__device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
+__device__ void text_block(const AttnArgs& a, int c, int rg, char* lds, float* red) {
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int c0 = c * kChunk;
   const int nst = min(kStages, (a.L - c0 + kBN - 1) / kBN);
-  const int tr = 16 * wave + (l & 15);  // text row of this lane
+  const int tr = kTextRows * rg + 16 * wave + (l & 15);  // text row of this lane
   const bool valid = tr < a.n_text;
   const int pos = tr < a.vb ? tr : a.ve + (tr - a.vb);
-  const bool active = 16 * wave < a.n_text;
+  const bool active = kTextRows * rg + 16 * wave < a.n_text;
   int row[1] = {valid ? pos : -1};      // an invalid row sees no token
 
   f32x4 acc[kStages][4];                // sum over heads of S^T, the chunk's tokens
@@ -516,7 +518,7 @@ __device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
 
   dma_wait();
   // m_j: max over the text rows of the head sum, the chunk's visual tokens
-  for (int i = threadIdx.x; i < 4 * kChunk; i += kThreads) red[i] = -INFINITY;
+  for (int i = threadIdx.x; i < kWaves * kChunk; i += kThreads) red[i] = -INFINITY;
   __syncthreads();
   if (active) {
 #pragma unroll
@@ -539,12 +541,24 @@ __device__ void text_block(const AttnArgs& a, int c, char* lds, float* red) {
         }
   }
   __syncthreads();
+  float* m = a.m + (int64_t)rg * (a.ve - a.vb);
   for (int i = threadIdx.x; i < kChunk; i += kThreads) {
     const int tok = c0 + i;
     if (tok >= a.vb && tok < a.ve) {
-      const float v = fmaxf(fmaxf(red[i], red[kChunk + i]), fmaxf(red[2 * kChunk + i], red[3 * kChunk + i]));
-      a.m[tok - a.vb] = v * a.qer_scale;
+      float v = red[i];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) v = fmaxf(v, red[w * kChunk + i]);
+      m[tok - a.vb] = v * a.qer_scale;
     }
+  }
+}
+
+// m_j over several text row groups: the max of their partial maxima.
+__global__ void attn_m_max_kernel(const float* part, int32_t n_vis, int32_t n_rg, float* m) {
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n_vis; j += (int64_t)gridDim.x * blockDim.x) {
+    float v = part[j];
+    for (int r = 1; r < n_rg; ++r) v = fmaxf(v, part[(int64_t)r * n_vis + j]);
+    m[j] = v;
   }
 }
 
@@ -552,7 +566,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_qer_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char lds[];
   const int b = blockIdx.x;
   if (b < a.nb_pad) {
-    if (b < a.n_chunks) text_block(a, b, lds, reinterpret_cast<float*>(lds + 2 * kStageBytes));
+    if (b < a.n_chunks * a.n_rg)
+      text_block(a, b % a.n_chunks, b / a.n_chunks, lds, reinterpret_cast<float*>(lds + 2 * kStageBytes));
     return;
   }
   visual_block(a, b - a.nb_pad, lds);
@@ -615,7 +630,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(AttnArgs a) {
 }
 
 struct AttnPlan {
-  int32_t n_vis, n_text, ntp, n_chunks, nb_pad, qb, Lp;
+  int32_t n_vis, n_text, ntp, n_chunks, n_rg, nb_pad, qb, Lp;
 };
 
 AttnPlan plan_attn(const cofie_attn_desc& h) {
@@ -624,16 +639,18 @@ AttnPlan plan_attn(const cofie_attn_desc& h) {
   p.n_text = h.L - p.n_vis;
   p.ntp = (p.n_text + 15) / 16 * 16;
   p.n_chunks = ceil_div(h.L, kChunk);
-  p.nb_pad = (p.n_chunks + 7) / 8 * 8;
+  p.n_rg = ceil_div(p.n_text, kTextRows);
+  p.nb_pad = (p.n_chunks * p.n_rg + 7) / 8 * 8;
   p.qb = ceil_div(p.n_vis, kBM);
   p.Lp = ceil_div(h.L, kBN) * kBN;
   return p;
 }
 
-void carve_attn(Arena& ar, const cofie_attn_desc& h, const AttnPlan& p, float** m, uint32_t** keys, float** po,
-                float2** pml, uint16_t** vt) {
+void carve_attn(Arena& ar, const cofie_attn_desc& h, const AttnPlan& p, float** m, float** mpart, uint32_t** keys,
+                float** po, float2** pml, uint16_t** vt) {
   *vt = ar.take<uint16_t>((size_t)h.H_kv * kD * p.Lp);
   *m = ar.take<float>((size_t)(p.n_vis > 0 ? p.n_vis : 1));
+  *mpart = p.n_rg > 1 ? ar.take<float>((size_t)p.n_rg * (p.n_vis > 0 ? p.n_vis : 1)) : *m;
   *keys = ar.take<uint32_t>((size_t)(h.n_frames > 0 ? h.n_frames : 1));
   *po = ar.take<float>((size_t)p.n_chunks * h.H_q * p.ntp * kD);
   *pml = ar.take<float2>((size_t)p.n_chunks * h.H_q * p.ntp);
@@ -649,8 +666,7 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
   if (h->vis_begin < 0 || h->vis_end < h->vis_begin || h->vis_end > h->L)
     return set_error(COFIE_EINVAL, "visual range [%d, %d) outside [0, L = %d]", h->vis_begin, h->vis_end, h->L);
   const int32_t n_text = h->L - (h->vis_end - h->vis_begin);
-  if (n_text < 1 || n_text > kMaxText)
-    return set_error(COFIE_EUNSUPPORTED, "%d text tokens (1 to %d supported)", n_text, kMaxText);
+  if (n_text < 1) return set_error(COFIE_EINVAL, "no text token outside the visual range");
   if (h->n_frames < 0) return set_error(COFIE_EINVAL, "n_frames is negative");
   if (k_top < 0) return set_error(COFIE_EINVAL, "k_top is negative");
   if (!Q || !K || !V || !out) return set_error(COFIE_EINVAL, "Q, K, V or out is NULL");
@@ -664,7 +680,8 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
   return COFIE_OK;
 }
 
-constexpr size_t kLdsBytes = 3 * kStageBytes;  // 96 KiB (the text rows use 2 stages + 4 KiB)
+constexpr size_t kLdsBytes = 3 * kStageBytes;  // 96 KiB (the text rows use 2 stages + 8 KiB)
+static_assert(2 * kStageBytes + kWaves * kChunk * sizeof(float) <= kLdsBytes, "text rows' LDS");
 
 }  // namespace
 }  // namespace cofie
@@ -680,11 +697,11 @@ size_t cofie_attn_qer_workspace_bytes(const cofie_attn_desc* desc) {
   int32_t di;
   if (validate_attn(dummy, dummy, dummy, &doffs, desc, 0, dummy, &ds, &di)) return 0;
   Arena ar;
-  float *m, *po;
+  float *m, *mpart, *po;
   uint32_t* keys;
   float2* pml;
   uint16_t* vt;
-  carve_attn(ar, *desc, plan_attn(*desc), &m, &keys, &po, &pml, &vt);
+  carve_attn(ar, *desc, plan_attn(*desc), &m, &mpart, &keys, &po, &pml, &vt);
   return ar.bytes();
 }
 
@@ -698,17 +715,17 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   const AttnPlan p = plan_attn(h);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Arena plan;
-  float *m, *po;
+  float *m, *mpart, *po;
   uint32_t* keys;
   float2* pml;
   uint16_t* vt;
-  carve_attn(plan, h, p, &m, &keys, &po, &pml, &vt);
+  carve_attn(plan, h, p, &m, &mpart, &keys, &po, &pml, &vt);
   Scratch scratch;
   rc = scratch.acquire(h.workspace, h.workspace_bytes, plan.bytes(), s);
   if (rc) return rc;
   Arena ar;
   ar.base = scratch.ptr();
-  carve_attn(ar, h, p, &m, &keys, &po, &pml, &vt);
+  carve_attn(ar, h, p, &m, &mpart, &keys, &po, &pml, &vt);
 
   AttnArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
@@ -724,12 +741,13 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   a.n_text = p.n_text;
   a.ntp = p.ntp;
   a.n_chunks = p.n_chunks;
+  a.n_rg = p.n_rg;
   a.nb_pad = p.nb_pad;
   a.qb = p.qb;
   const double scale = h.scale > 0.f ? (double)h.scale : 1.0 / std::sqrt((double)kD);
   a.c2 = (float)(scale * 1.4426950408889634);
   a.qer_scale = (float)(scale / (double)h.H_q);
-  a.m = m;
+  a.m = mpart;
   a.part_o = po;
   a.part_ml = pml;
   rc = launch("attn_vt", attn_vt_kernel, dim3((unsigned)(p.Lp / kBN), (unsigned)h.H_kv), dim3(kThreads), 0, s,
@@ -742,6 +760,11 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   if (rc) return rc;
   rc = launch("attn_merge", attn_merge_kernel, dim3((unsigned)p.n_text, (unsigned)h.H_q), dim3(kD), 0, s, a);
   if (rc) return rc;
+  if (p.n_rg > 1 && p.n_vis > 0) {
+    rc = launch("attn_m_max", attn_m_max_kernel, dim3((unsigned)std::min(ceil_div(p.n_vis, 256), 1024)), dim3(256), 0,
+                s, (const float*)mpart, p.n_vis, p.n_rg, m);
+    if (rc) return rc;
+  }
   return qer_rank_from_m(m, p.n_vis, frame_offsets, h.n_frames, k_top, out_scores, keys, out_idx, s);
 }
 

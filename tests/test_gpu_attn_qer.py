@@ -78,11 +78,15 @@ def check(Q, K, V, offs, vb, ve, k_top, rows=None, scale=0.0):
 @pytest.mark.parametrize("n_pre,n_vis,n_post,H_q,H_kv,n_frames", [
     (5, 30, 5, 2, 2, 3),        # one block, one chunk, partial tiles
     (7, 650, 43, 4, 2, 9),      # 3 query blocks (ragged), 2 chunks, grouped heads
-    (0, 536, 64, 3, 1, 5),      # 64 text rows (the maximum), all after the video
+    (0, 536, 64, 3, 1, 5),      # 64 text rows, all after the video
     (64, 300, 0, 2, 1, 4),      # all text before the video
     (0, 1000, 1, 2, 2, 7),      # a single text token
     (3, 256, 2, 1, 1, 1),       # exactly one query block
     (1, 1, 1, 2, 2, 1),         # one visual token
+    (40, 100, 40, 2, 2, 3),     # 80 text rows: one text workgroup's 128 rows
+    (100, 700, 100, 4, 2, 9),   # 200 text rows: two row groups, their m_j maxima combined
+    (0, 300, 300, 2, 1, 4),     # 300 text rows, all after the video: three row groups
+    (129, 520, 0, 2, 2, 5),     # 129 text rows before the video: a group of one row
 ])
 def test_shapes_against_oracle(n_pre, n_vis, n_post, H_q, H_kv, n_frames):
     Q, K, V, offs = make_case(n_pre * 1000 + n_vis + n_post, n_pre, n_vis, n_post, H_q, H_kv, n_frames)
@@ -145,7 +149,11 @@ def test_workspace_and_determinism():
 
 
 def test_rejects_unsupported():
-    Q, K, V, offs = make_case(5, 40, 100, 40, 2, 2, 3)   # 80 text tokens
-    with pytest.raises(B.CofieError) as e:
-        B.cofie_attn_qer(bf16_dev(Q), bf16_dev(K), bf16_dev(V), to_dev(offs), 40, 140, 3)
+    Q, K, V, offs = make_case(5, 4, 100, 4, 2, 2, 3)
+    with pytest.raises(B.CofieError) as e:  # head dimension 64: only 128 is built
+        B.cofie_attn_qer(bf16_dev(Q[..., :64]).contiguous(), bf16_dev(K[..., :64]).contiguous(),
+                         bf16_dev(V[..., :64]).contiguous(), to_dev(offs), 4, 104, 3)
     assert e.value.code == B.COFIE_EUNSUPPORTED
+    with pytest.raises(B.CofieError) as e:  # no text token: nothing to score with
+        B.cofie_attn_qer(bf16_dev(Q[4:104]), bf16_dev(K[4:104]), bf16_dev(V[4:104]), to_dev(offs), 0, 100, 3)
+    assert e.value.code == B.COFIE_EINVAL
