@@ -230,6 +230,17 @@ __device__ __forceinline__ float sum_x32(float v) {
 // segments) in this kernel on the 1 fps stream workload (48.9 vs 51.1 us).
 __host__ __device__ constexpr int lds_rows(int, int) { return 8; }
 
+// The score kernel's batch (virtual steps per key batch): the host plan's,
+// halved for SOFTMAX pass 1 with three or more query blocks and for pass 2
+// (MHA heads) with eight, one tile per wave: the full batch would spill (the
+// grouped-head pass 2 spills with the half batch instead).  S, the phase
+// length, stays a multiple of it.
+__host__ __device__ constexpr int score_batch(int MB, int NB, int P, int NS, int mode) {
+  return lds_batch(MB, P * NB, lds_rows(MB, P * NB), NS) /
+         (MB == 1 && (((mode & 3) == kModeSoftStats && P * NB >= 3) || (mode == kModeSoftProb && P * NB >= 8)) ? 2
+                                                                                                            : 1);
+}
+
 // ---- address arithmetic of qer_score_kernel, shared with its address model ---------
 // Key load q (of 16 / R per segment) of lane `lane` for the tile whose first
 // token is t0: 16-byte index from the key base of its load in segment 0
@@ -317,9 +328,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R;   // virtual steps (= loads per tile) per segment
   constexpr int SEGC = 64 / R;  // 16-byte chunks per segment
-  // (SOFTMAX pass 1 with three or four query blocks and one tile per wave
-  // halves the host's batch, which would spill: S stays a multiple of it)
-  constexpr int U = lds_batch(MB, P * NB, R, NS) / (BASE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
+  constexpr int U = score_batch(MB, NB, P, NS, MODE);
   constexpr int FPS = P * NB;   // fragments per virtual step
   constexpr int kQRegs = lds_q_regs(FPS, NS);
   constexpr int kPhaseU4 = kQRegs * kLdsThreads;
@@ -1759,6 +1768,7 @@ struct QerPlan {
   // SOFTMAX through the LDS-staged score kernel: heads of whole 128-byte
   // segments, the pass-2 statistics and the segment map within the LDS budget
   bool soft_fast;
+  bool soft_wide;       // 128 query rows per pass (else 64)
   int64_t soft_nwg;     // workgroups of the score kernel
   int64_t soft_rounds;  // their rounds
 };
@@ -1928,7 +1938,7 @@ void model_score(ScoreLdsArgs a, int grid, size_t lds) {
   constexpr bool SEQ = (MODE & kModeSeq) != 0;
   constexpr int R = lds_rows(MB, P * NB);
   constexpr int VPS = 16 / R, SEGC = 64 / R;
-  constexpr int U = lds_batch(MB, P * NB, R, NS) / (BASE == kModeSoftStats && MB == 1 && P * NB >= 3 ? 2 : 1);
+  constexpr int U = score_batch(MB, NB, P, NS, MODE);
   constexpr int FPS = P * NB;
   constexpr int kQRegs = lds_q_regs(FPS, NS);
   constexpr int kPhaseU4 = kQRegs * kLdsThreads;
@@ -2206,9 +2216,9 @@ int launch_lds_t(const ScoreLdsArgs& sa, const LdsPlan& L, size_t lds, hipStream
 
 template <typename T, int MB, int P, int NS, int MODE>
 int launch_lds_nb(const ScoreLdsArgs& sa, const LdsPlan& L, int NB, size_t lds, hipStream_t s) {
-  // 128 query rows in one pass: LOGIT, one query term, one tile per wave
-  // (two spill)
-  if constexpr (MB == 1 && P == 1 && NS == 1 && MODE == kModeLogit) {
+  // 128 query rows in one pass: one query term, one tile per wave (two
+  // spill), no contraction split (LOGIT, and both SOFTMAX passes)
+  if constexpr (MB == 1 && P == 1 && NS == 1) {
     if (NB == 8) return launch_lds_t<T, 1, 8, 1, NS, MODE>(sa, L, lds, s);
   }
   switch (NB) {
@@ -2250,13 +2260,23 @@ constexpr size_t kLdsMax = 160 * 1024;
 // of a key row, the widest query chunk's LDS within the CU's), and its
 // pass-1 statistics count.
 void plan_soft(const cofie_qer_desc& h, int32_t n_queries, QerPlan& p) {
-  p.soft_fast = false;
+  p.soft_fast = p.soft_wide = false;
   p.soft_nwg = p.soft_rounds = 0;
   if (h.score_mode != COFIE_SCORE_SOFTMAX || h.n_vis <= 0) return;
   const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)p.esize;
   if (h.d % seg_el != 0) return;
-  const int nq = (int)std::min<int64_t>(64, (int64_t)h.n_q * n_queries), NB = (nq + 15) / 16;
-  const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, device_cu_count(), false);
+  const int cus = device_cu_count();
+  const int64_t rows = (int64_t)h.n_q * n_queries;
+  // 128 query rows per pass (K read twice for up to 128 stacked rows) where
+  // the plan takes one tile per wave and the LDS holds the pass-2 statistics
+  // of 128 rows; else 64
+  p.soft_wide = false;
+  if (rows > 64) {
+    const LdsPlan W = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, 8, cus, false);
+    p.soft_wide = W.MB == 1 && soft_lds(W, kModeSoftProb, h.H_q, 128, h.H_q / h.H_kv, p.Lc / seg_el) <= kLdsMax;
+  }
+  const int nq = (int)std::min<int64_t>(p.soft_wide ? 128 : 64, rows), NB = nq > 64 ? 8 : (nq + 15) / 16;
+  const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, cus, false);
   if (soft_lds(L, kModeSoftProb, h.H_q, nq, h.H_q / h.H_kv, p.Lc / seg_el) > kLdsMax) return;
   p.soft_fast = true;
   p.soft_nwg = L.nwg;
@@ -2388,14 +2408,15 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.stats = w.stats;
       sa.nclear = n_queries * qer_trees(h.n_frames).ints;
       const int cus = device_cu_count();
+      const int chunk = p.soft_wide ? 128 : 64;
       for (int pass = 1; pass <= 2; ++pass) {
-        for (int q0 = 0; q0 < R; q0 += 64) {
+        for (int q0 = 0; q0 < R; q0 += chunk) {
           sa.q0 = q0;
-          sa.n_q = std::min(64, R - q0);
+          sa.n_q = std::min(chunk, R - q0);
           sa.accumulate = pass == 2 && q0 > 0;
           sa.clear = (pass == 2 && q0 == 0 && fused_tail) ? w.done : nullptr;
           sa.scale = 1.0f / (float)h.H_q;  // pass 2: the head mean
-          const int NB = (sa.n_q + 15) / 16;
+          const int NB = sa.n_q > 64 ? 8 : (sa.n_q + 15) / 16;
           const LdsPlan L = plan_score_lds(h.n_vis, p.Lc, p.esize, 1, NB, cus, false);
           sa.nseg = L.nseg;
           sa.ksteps = L.ksteps;
