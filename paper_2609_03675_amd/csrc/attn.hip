@@ -104,22 +104,34 @@ typedef __attribute__((address_space(1))) void global_void;
 // values: 8 rows of V^T each, k0 clamped to its last stage).
 constexpr int kDma = 32 / kWaves;
 
+// Source element (from the tensor's base) of lane l in DMA instruction i of
+// stage k0 of head g: keys (i < 16) token 4 i + l / 16 of the stage (row
+// clamped to the sequence), swizzled 16-byte chunk; V^T (i >= 16) row d of
+// the head's transposed values, 8 tokens at the stage start (clamped to its
+// last stage) plus the swizzled chunk.  The LDS destination of instruction i
+// is 1 KiB at st + 1024 i (keys) or st + kKBytes + 1024 (i - 16) (values).
+__host__ __device__ __forceinline__ int64_t dma_src(int i, int l, int k0, int g, int L, int Lp, int H_kv) {
+  if (i < 16) {
+    const int tok = 4 * i + (l >> 4), c = (l & 15) ^ (tok & 15);
+    const int row = k0 + tok < L - 1 ? k0 + tok : L - 1;
+    return ((int64_t)row * H_kv + g) * kD + 8 * c;
+  }
+  const int kv = k0 < Lp - kBN ? k0 : Lp - kBN;
+  const int d = 8 * (i - 16) + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
+  return ((int64_t)g * kD + d) * Lp + kv + 8 * c;
+}
+
 __device__ __forceinline__ void stage_dma(const AttnArgs& a, int g, int k0, char* st) {
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int kv = min(k0, a.Lp - kBN);
 #pragma unroll
   for (int j = 0; j < kDma; ++j) {
     const int i = wave + kWaves * j;  // instruction 0..31
-    if (i < 16) {
-      const int tok = 4 * i + (l >> 4), c = (l & 15) ^ (tok & 15);
-      const int row = min(k0 + tok, a.L - 1);
-      __builtin_amdgcn_global_load_lds((global_void*)(a.K + ((int64_t)row * a.H_kv + g) * kD + 8 * c),
+    if (i < 16)
+      __builtin_amdgcn_global_load_lds((global_void*)(a.K + dma_src(i, l, k0, g, a.L, a.Lp, a.H_kv)),
                                        (lds_void*)(st + 1024 * i), 16, 0, 0);
-    } else {
-      const int d = 8 * (i - 16) + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
-      __builtin_amdgcn_global_load_lds((global_void*)(a.Vt + ((int64_t)g * kD + d) * a.Lp + kv + 8 * c),
+    else
+      __builtin_amdgcn_global_load_lds((global_void*)(a.Vt + dma_src(i, l, k0, g, a.L, a.Lp, a.H_kv)),
                                        (lds_void*)(st + kKBytes + 1024 * (i - 16)), 16, 0, 0);
-    }
   }
 }
 
@@ -132,8 +144,8 @@ struct FragBase {
   int ka[4];
   int va[2];
 };
-__device__ __forceinline__ FragBase frag_base() {
-  const int l = threadIdx.x & 63, g = l >> 4, r = l & 15;
+__host__ __device__ __forceinline__ FragBase frag_base_of(int l) {
+  const int g = l >> 4, r = l & 15;
   FragBase f;
 #pragma unroll
   for (int s = 0; s < 4; ++s) f.ka[s] = r * 256 + 16 * ((4 * s + g) ^ r);
@@ -141,6 +153,7 @@ __device__ __forceinline__ FragBase frag_base() {
   for (int sub = 0; sub < 2; ++sub) f.va[sub] = kKBytes + r * 128 + 16 * ((4 * sub + g) ^ ((r >> 1) & 7));
   return f;
 }
+__device__ __forceinline__ FragBase frag_base() { return frag_base_of(threadIdx.x & 63); }
 // A operand of S^T for key tile kt (16 tokens) and contraction step s (32 d)
 __device__ __forceinline__ uint4 k_frag(const char* st, const FragBase& f, int kt, int s) {
   return *reinterpret_cast<const uint4*>(st + f.ka[s] + kt * 4096);
@@ -348,10 +361,18 @@ __device__ __forceinline__ void pv_half(const char* st, const FragBase& f, int h
   }
 }
 
+// Visual workgroup b: its head and query block (the blocks of one XCD take
+// consecutive work; heaviest, i.e. latest, blocks first within a head).
+__host__ __device__ __forceinline__ void visual_map(int b, int n_qb, int H_q, int& h, int& qb) {
+  const int total = n_qb * H_q, t8 = total / 8;
+  const int w = b < 8 * t8 ? (b % 8) * t8 + b / 8 : b;
+  h = w / n_qb;
+  qb = n_qb - 1 - w % n_qb;
+}
+
 __device__ void visual_block(const AttnArgs& a, int b, char* lds) {
-  const int total = a.qb * a.H_q, t8 = total / 8;
-  const int w = b < 8 * t8 ? (b % 8) * t8 + b / 8 : b;  // the blocks of one XCD: consecutive work
-  const int h = w / a.qb, qb = a.qb - 1 - w % a.qb;        // heaviest first within a head
+  int h, qb;
+  visual_map(b, a.qb, a.H_q, h, qb);
   const int g = h / (a.H_q / a.H_kv);
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const bool lag = wave >= kWaves / 2;  // one interval behind
@@ -683,6 +704,103 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
 constexpr size_t kLdsBytes = 3 * kStageBytes;  // 96 KiB (the text rows use 2 stages + 8 KiB)
 static_assert(2 * kStageBytes + kWaves * kChunk * sizeof(float) <= kLdsBytes, "text rows' LDS");
 
+// Address model of the fused call (dry run): the transpose pre-pass, every
+// visual and text workgroup's DMA stages (at both ends of their affine
+// ranges), fragment reads, query loads and stores, the merge and the
+// row-group maximum, through the kernels' own index functions.
+void model_attn(const AttnArgs& a, const uint16_t* V, int H_q) {
+  const int64_t lds = (int64_t)kLdsBytes;
+  // fragment reads: inside one stage, for every lane
+  for (int l = 0; l < 64; ++l) {
+    const FragBase f = frag_base_of(l);
+    for (int s = 0; s < 4; ++s) {
+      dry_range(f.ka[s] + 3 * 4096 + 16, 0, kKBytes + 1, "attn: key fragment past the stage's keys");
+      dry_range(f.ka[s], 0, kKBytes, "attn: key fragment");
+    }
+    for (int sub = 0; sub < 2; ++sub) {
+      dry_range(f.va[sub] + 7 * 2048 + 16, kKBytes, kStageBytes + 1, "attn: value fragment past the stage");
+      dry_range(f.va[sub], kKBytes, kStageBytes, "attn: value fragment");
+    }
+  }
+  // one DMA stage: the extreme lanes of each instruction (rows and columns
+  // are monotone in the token, the swizzled chunk stays in its row)
+  auto dma = [&](int g, int k0, int64_t st) {
+    for (int i = 0; i < 32; ++i) {
+      dry_lds(st + (i < 16 ? 1024 * i : kKBytes + 1024 * (i - 16)), 1024, lds, "attn: DMA destination");
+      for (int l : {0, 15, 48, 63}) {
+        const int64_t e = dma_src(i, l, k0, g, a.L, a.Lp, a.H_kv);
+        dry_access(i < 16 ? (const void*)a.K : (const void*)a.Vt, 2 * e, 16, "attn: DMA source");
+      }
+    }
+  };
+  // V^T pre-pass: token tiles of 64 for every key head
+  for (int g = 0; g < a.H_kv; ++g)
+    for (int k0 = 0; k0 < a.Lp; k0 += kBN) {
+      const int last = k0 + kBN - 1 < a.L - 1 ? k0 + kBN - 1 : a.L - 1;
+      if (k0 < a.L) dry_access(V, 2 * (((int64_t)last * a.H_kv + g) * kD + 8 * 15), 16, "attn: V load");
+      dry_access(a.Vt, 2 * (((int64_t)g * kD + kD - 1) * a.Lp + k0 + 56), 16, "attn: V^T store");
+    }
+  const int per = a.H_q / a.H_kv;
+  // text workgroups: chunk c, row group rg, every head
+  for (int b = 0; b < a.n_chunks * a.n_rg; ++b) {
+    const int c = b % a.n_chunks, rg = b / a.n_chunks, c0 = c * kChunk;
+    const int nst = (a.L - c0 + kBN - 1) / kBN < kStages ? (a.L - c0 + kBN - 1) / kBN : kStages;
+    int buf = 0;
+    dma(0, c0, 0);
+    for (int h = 0; h < a.H_q; ++h)
+      for (int st = 0; st < nst; ++st) {
+        const int k0 = c0 + st * kBN;
+        if (st + 1 < nst || h + 1 < a.H_q)
+          dma((st + 1 < nst ? h : h + 1) / per, st + 1 < nst ? k0 + kBN : c0, (buf ^ 1) * (int64_t)kStageBytes);
+        buf ^= 1;
+      }
+    for (int wave = 0; wave < kWaves; ++wave) {
+      const int tr_hi = kTextRows * rg + 16 * wave + 15, tr_lo = kTextRows * rg + 16 * wave;
+      if (tr_lo >= a.n_text) continue;
+      const int tr = tr_hi < a.n_text ? tr_hi : a.n_text - 1;
+      const int pos = tr < a.vb ? tr : a.ve + (tr - a.vb);
+      dry_range(pos, 0, a.L, "attn: text row position");
+      dry_access(a.Q, 2 * (((int64_t)pos * a.H_q + H_q - 1) * kD + 32 * 3 + 8 * 3), 16, "attn: text query load");
+      const int64_t pr = ((int64_t)c * a.H_q + H_q - 1) * a.ntp + tr;
+      dry_access(a.part_ml, 8 * pr, 8, "attn: text row statistics");
+      dry_access(a.part_o, 4 * (pr * kD + 4 * 3 + 16 * 7), 16, "attn: text row partial");
+      dry_lds(2 * (int64_t)kStageBytes + 4 * (wave * kChunk + kChunk - 1), 4, lds, "attn: row-group maxima");
+    }
+    const int lo = c0 > a.vb ? c0 : a.vb, hi = c0 + kChunk < a.ve ? c0 + kChunk : a.ve;
+    if (hi > lo) dry_access(a.m, 4 * ((int64_t)rg * (a.ve - a.vb) + lo - a.vb), 4 * (int64_t)(hi - lo), "attn: m_j");
+  }
+  // visual workgroups
+  for (int b = 0; b < a.qb * a.H_q; ++b) {
+    int h, qb;
+    visual_map(b, a.qb, a.H_q, h, qb);
+    dry_range(h, 0, a.H_q, "attn: visual head");
+    const int g = h / per;
+    const int r0 = a.vb + kBM * qb;
+    const int last = (r0 + kBM < a.ve ? r0 + kBM : a.ve) - 1;
+    const int nst = last / kBN + 1;
+    dma(g, 0, 0);
+    dma(g, kBN, kStageBytes);
+    for (int st = 0; st < nst; ++st) dma(g, (st + 2) * kBN, ((st + 2) % 3) * (int64_t)kStageBytes);
+    const int pos_lo = r0 < a.L - 1 ? r0 : a.L - 1;
+    const int pos_hi = r0 + kBM - 1 < a.L - 1 ? r0 + kBM - 1 : a.L - 1;
+    dry_access(a.Q, 2 * (((int64_t)pos_lo * a.H_q + h) * kD), 16, "attn: visual query load");
+    dry_access(a.Q, 2 * (((int64_t)pos_hi * a.H_q + h) * kD + 32 * 3 + 8 * 3), 16, "attn: visual query load");
+    if (last >= r0) {
+      dry_access(a.O, 2 * (((int64_t)r0 * a.H_q + h) * kD), 8, "attn: output row");
+      dry_access(a.O, 2 * (((int64_t)last * a.H_q + h) * kD + 4 * 3 + 16 * 7), 8, "attn: output row");
+    }
+  }
+  // merge of the text rows (every chunk's partials) and their outputs
+  if (a.n_text > 0) {
+    const int tr = a.n_text - 1, pos = tr < a.vb ? tr : a.ve + (tr - a.vb);
+    const int64_t pr = ((int64_t)(a.n_chunks - 1) * a.H_q + a.H_q - 1) * a.ntp + tr;
+    dry_access(a.part_ml, 8 * pr, 8, "attn: merge statistics");
+    dry_access(a.part_o, 4 * (pr * kD + kD - 1), 4, "attn: merge partial");
+    dry_access(a.O, 2 * (((int64_t)pos * a.H_q + a.H_q - 1) * kD + kD - 1), 2, "attn: merged output");
+  }
+}
+
+
 }  // namespace
 }  // namespace cofie
 
@@ -750,6 +868,7 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   a.m = mpart;
   a.part_o = po;
   a.part_ml = pml;
+  if (dry_run()) model_attn(a, static_cast<const uint16_t*>(V), h.H_q);
   rc = launch("attn_vt", attn_vt_kernel, dim3((unsigned)(p.Lp / kBN), (unsigned)h.H_kv), dim3(kThreads), 0, s,
               static_cast<const uint16_t*>(V), h.L, h.H_kv, p.Lp, vt);
   if (rc) return rc;
@@ -761,6 +880,10 @@ int cofie_attn_qer(const void* Q, const void* K, const void* V, const int32_t* f
   rc = launch("attn_merge", attn_merge_kernel, dim3((unsigned)p.n_text, (unsigned)h.H_q), dim3(kD), 0, s, a);
   if (rc) return rc;
   if (p.n_rg > 1 && p.n_vis > 0) {
+    if (dry_run()) {
+      dry_access(mpart, 0, 4 * (int64_t)p.n_rg * p.n_vis, "attn: row-group maxima");
+      dry_access(m, 0, 4 * (int64_t)p.n_vis, "attn: m_j");
+    }
     rc = launch("attn_m_max", attn_m_max_kernel, dim3((unsigned)std::min(ceil_div(p.n_vis, 256), 1024)), dim3(256), 0,
                 s, (const float*)mpart, p.n_vis, p.n_rg, m);
     if (rc) return rc;

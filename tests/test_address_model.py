@@ -6,8 +6,9 @@ and LDS address of the kernels that have an address model: the QER score
 kernels (LOGIT and both SOFTMAX passes, grouped-query folds, split
 contractions, several key sequences), the operand-order query copy and the
 sequence kernel of the multi-stream step, the frame means and their top-k
-trees, the NGFF histogram kernel's clamped unit loads and pixel tails, and
-the frame gather.  The addresses come from the same __host__ __device__
+trees, the fused prefill attention (its DMA stages, fragments, text row
+groups and merge), the NGFF histogram kernel's clamped unit loads and pixel
+tails, and the frame gather.  The addresses come from the same __host__ __device__
 index functions the kernels call, and each is checked against fake device
 buffers of the sizes a caller passes (the inputs, the outputs and the
 workspace the library asks for).
@@ -243,6 +244,54 @@ def test_short_keys_reported_in_score_kernel():
         qer_single(dr, 33, 28, 28, 128, [17, 0, 40, 1, 33, 64, 5, 0, 29], "bf16", 4, trim_k=16)
         v, _, msg = dr.result()
     assert v > 0 and "score: key" in msg, msg
+
+
+# ---- fused attention -------------------------------------------------------------------
+
+def attn_call(dr, n_pre, n_vis, n_post, H_q, H_kv, n_frames, k=4, trim_v=0):
+    L = n_pre + n_vis + n_post
+    Q = dr.buffer((L, H_q, 128), torch.bfloat16, "Q")
+    K = dr.buffer((L, H_kv, 128), torch.bfloat16, "K")
+    V = dr.buffer((L, H_kv, 128), torch.bfloat16, "V", trim=trim_v)
+    offs = np.linspace(0, n_vis, n_frames + 1).astype(np.int32)
+    od = dr.buffer(n_frames + 1, torch.int32, "frame offsets", data=offs)
+    out = dr.buffer((L, H_q, 128), torch.bfloat16, "out")
+    w = dr.buffer(max(n_frames, 1), torch.float32, "scores")
+    idx = dr.buffer(max(k, 1), torch.int32, "top-k")
+    ws = dr.buffer(B.attn_qer_workspace_bytes(B.attn_desc(L, H_q, H_kv, 128, n_pre, n_pre + n_vis, n_frames)),
+                   torch.uint8, "workspace")
+    B.cofie_attn_qer(Q, K, V, od, n_pre, n_pre + n_vis, k, out=out, out_scores=w, out_idx=idx, workspace=ws,
+                     stream=0)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_attention_workloads(cfg):
+    """The last-layer prefill of the 1 fps, hour and high-res workloads."""
+    wl = synth.WORKLOADS[cfg]
+    L, vb, ve = synth.attn_layout(cfg)
+    with B.DryRun() as dr:
+        attn_call(dr, vb, ve - vb, L - ve, wl.H_q, wl.H_kv, wl.n_frames, wl.k_top)
+        clean(dr, f"attention C{cfg}")
+
+
+@pytest.mark.parametrize("n_pre,n_vis,n_post,H_q,H_kv,n_frames", [
+    (5, 30, 5, 2, 2, 3), (7, 650, 43, 4, 2, 9), (0, 536, 64, 3, 1, 5), (64, 300, 0, 2, 1, 4), (0, 1000, 1, 2, 2, 7),
+    (3, 256, 2, 1, 1, 1), (1, 1, 1, 2, 2, 1), (40, 100, 40, 2, 2, 3), (100, 700, 100, 4, 2, 9),
+    (0, 300, 300, 2, 1, 4), (129, 520, 0, 2, 2, 5), (20, 0, 0, 2, 2, 3),
+])
+def test_attention_shapes(n_pre, n_vis, n_post, H_q, H_kv, n_frames):
+    """The attention parity tests' shapes (ragged blocks and chunks, text
+    rows before and after the video, several row groups, no visual token)."""
+    with B.DryRun() as dr:
+        attn_call(dr, n_pre, n_vis, n_post, H_q, H_kv, n_frames)
+        clean(dr, "attention shapes")
+
+
+def test_attention_short_values_reported():
+    with B.DryRun() as dr:
+        attn_call(dr, 7, 650, 43, 4, 2, 9, trim_v=16)
+        v, _, msg = dr.result()
+    assert v > 0 and "V" in msg, msg
 
 
 # ---- NGFF ---------------------------------------------------------------------------
