@@ -1151,6 +1151,56 @@ struct HistMap {  // see HistArgs: group = 0 is the identity
   bool zeroed = false;   // the output rows are known zero: no fill before accumulating
 };
 
+// Address model of ngff_sig_kernel (dry run): each frame's rows as the
+// vector or byte path reads them, the LDS column table and cell counters,
+// the output row.
+void model_sig(const SigArgs& a, int64_t n) {
+  dry_range(a.W, 1, kSigMaxW + 1, "sig: columns past the column table");
+  dry_range((int64_t)a.gh * a.gw, 1, 4097, "sig: cells past the counters");
+  dry_range((int64_t)a.H * a.W * a.C, 1, a.frame_bytes + 1, "sig: pixels past the frame");
+  const int64_t top_cell = (int64_t)((((int64_t)(a.H - 1) * a.gh) / a.H) * a.gw) + ((int64_t)(a.W - 1) * a.gw) / a.W;
+  dry_range(top_cell, 0, (int64_t)a.gh * a.gw, "sig: a pixel's cell");
+  for (int64_t b = 0; b < n; ++b) {
+    const int64_t f = b * a.frame_bytes;
+    const int64_t last_row = f + (int64_t)(a.H - 1) * a.W * a.C;
+    if (a.vec) {
+      const int x0 = (a.W - 1) / 4 * 4;  // the last 4-pixel group a lane reads
+      dry_range(a.W % 4, 0, 1, "sig: 4-pixel loads need W a multiple of 4");
+      dry_access(a.frames, f, a.C == 3 ? 12 : 4, "sig: first pixels");
+      dry_access(a.frames, last_row + (a.C == 3 ? 3 * (int64_t)x0 : x0), a.C == 3 ? 12 : 4, "sig: last pixels");
+    } else {
+      dry_access(a.frames, f, a.C, "sig: first pixel");
+      dry_access(a.frames, last_row + (int64_t)(a.W - 1) * a.C, a.C, "sig: last pixel");
+    }
+    dry_access(a.out, 4 * b * a.nsig, 4 * (int64_t)a.nsig, "sig: signature row");
+  }
+}
+
+// Address model of ngff_band_keep_kernel (dry run): each workgroup's
+// histogram rows, its LDS rows (transposed, stride RS) and band block, and
+// the band, adjacent-distance and keep-word outputs of its frames.
+void model_band_keep(const BandKeepArgs& a, int64_t nwg, int64_t lds) {
+  const int L = a.rule.L;
+  dry_lds(0, 4 * ((int64_t)a.nbins * a.RS + (int64_t)a.TB * L), lds, "keep: LDS rows and band block");
+  for (int64_t b = 0; b < nwg; ++b) {
+    const int64_t t0 = b * a.TB, t1 = t0 + a.TB < a.n ? t0 + a.TB : a.n;
+    const int64_t r0 = t0 - L > 0 ? t0 - L : 0;
+    dry_range(t1 - r0, 1, (int64_t)a.RS + 1, "keep: staged rows past the LDS row stride");
+    dry_access(a.hist, 4 * r0 * a.nbins, 4 * (t1 - r0) * a.nbins, "keep: histogram rows");
+    // the earliest row a pair reads: t - k >= the stream's first frame and >= r0
+    const int64_t seg0 = (t0 / a.rule.seg_len) * a.rule.seg_len;
+    const int64_t lo = t0 - L > seg0 ? t0 - L : seg0;
+    dry_range(lo - r0, 0, a.RS, "keep: a pair's reference row before the staged rows");
+    dry_access(a.band, 4 * t0 * L, 4 * (t1 - t0) * L, "keep: band rows");
+    dry_access(a.adj, 4 * t0, 4 * (t1 - t0), "keep: adjacent distances");
+    dry_access(a.G, 4 * t0, 4 * (t1 - t0), "keep: keep words");
+    if (a.rule.tau_seg) {
+      const int64_t s_lo = t0 / a.rule.seg_len, s_hi = (t1 - 1) / a.rule.seg_len;
+      dry_access(a.rule.tau_seg, 4 * s_lo, 4 * (s_hi - s_lo + 1), "keep: per-stream thresholds");
+    }
+  }
+}
+
 int run_signature(const uint8_t* frames, const NgffShape& sh, uint32_t* out, hipStream_t s) {
   SigArgs a;
   a.frames = frames;
@@ -1164,6 +1214,7 @@ int run_signature(const uint8_t* frames, const NgffShape& sh, uint32_t* out, hip
   a.nsig = (int32_t)sh.nbins;
   a.vec = (reinterpret_cast<uintptr_t>(frames) % 4 == 0) && sh.W % 4 == 0 ? 1 : 0;
   a.out = out;
+  if (dry_run()) model_sig(a, sh.n);
   return launch("ngff_sig", ngff_sig_kernel, dim3((unsigned)sh.n), dim3(kSigThreads), 0, s, a);
 }
 
@@ -1565,6 +1616,7 @@ int filter_impl(const uint8_t* frames, const uint32_t* hist_in, const NgffShape&
     bk.G = w.G;
     rc = allow_lds(ngff_band_keep_kernel, bp.lds);
     if (rc) return rc;
+    if (dry_run()) model_band_keep(bk, ceil_div(sh.n, bp.TB), (int64_t)bp.lds);
     rc = launch("ngff_keep", ngff_band_keep_kernel, dim3((unsigned)ceil_div(sh.n, bp.TB)), dim3(kKeepThreads),
                 bp.lds, s, bk);
     if (rc) return rc;

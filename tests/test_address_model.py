@@ -8,7 +8,8 @@ contractions, several key sequences), the operand-order query copy and the
 sequence kernel of the multi-stream step, the frame means and their top-k
 trees, the fused prefill attention (its DMA stages, fragments, text row
 groups and merge), the NGFF histogram kernel's clamped unit loads and pixel
-tails, and the frame gather.  The addresses come from the same __host__ __device__
+tails, the signature kernel of the alternative signals, the keep-rule
+kernel's staged rows, and the frame gather.  The addresses come from the same __host__ __device__
 index functions the kernels call, and each is checked against fake device
 buffers of the sizes a caller passes (the inputs, the outputs and the
 workspace the library asks for).
@@ -330,6 +331,24 @@ def test_ngff_shapes(shape, mode, bins):
         ngff_filter(dr, n, H, W, C, mode, bins)
         ngff_filter(dr, n, H, W, C, mode, bins, misalign=1)  # byte path of a frame at an odd address
         clean(dr, "NGFF shapes")
+
+
+@pytest.mark.parametrize("name", ["framediff", "dhash"])
+@pytest.mark.parametrize("shape,G", [((5, 33, 47, 3), 4), ((3, 64, 64, 1), 16), ((2, 90, 160, 3), 32),
+                                     ((3, 37, 29, 3), 2), ((2, 64, 64, 3), 64), ((4, 448, 448, 3), 32),
+                                     ((2, 1080, 1920, 3), 32), ((200, 448, 448, 3), 32)])
+def test_signal_shapes(name, shape, G):
+    """The alternative signals (Table 5) with the signal tests' shapes: the
+    signature kernel's vector and byte paths (W not a multiple of 4, a frame
+    at an odd address), then the keep rule on their rows."""
+    n, H, W, C = shape
+    if name == "dhash" and (H < 8 or W < 9):
+        pytest.skip("dHash needs an 8 x 9 grid")
+    with B.DryRun() as dr:
+        ngff_filter(dr, n, H, W, C, name, G)
+        ngff_filter(dr, n, H, W, C, name, G, misalign=1)
+        ngff_filter(dr, n, H, W, C, name, G, seg=100 if n >= 200 else 0)
+        clean(dr, "signals")
 
 
 def test_short_frames_reported():
