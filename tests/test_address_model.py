@@ -415,3 +415,24 @@ def test_gather_capacity_beyond_int32_refused():
     with B.DryRun() as dr:
         with pytest.raises(B.CofieError):
             gather(dr, 4, 16, np.array([0, 4]), np.array([0]), 1 << 31)
+
+
+def test_dry_run_allocates_nothing():
+    """A dry run makes no HIP call: a call that would allocate its scratch is
+    refused (a workspace must be given), the online filter (device state) is
+    refused, and the dry run ends cleanly."""
+    with B.DryRun() as dr:
+        Q = dr.buffer((16, 2, 32), torch.bfloat16, "Q")
+        K = dr.buffer((64, 2, 32), torch.bfloat16, "K")
+        od = dr.buffer(5, torch.int32, "frame offsets", data=np.arange(0, 80, 16, dtype=np.int32))
+        out = dr.buffer(4, torch.float32, "scores")
+        idx = dr.buffer(2, torch.int32, "top-k")
+        with pytest.raises(B.CofieError) as e:
+            B.cofie_qer_rank(Q, K, od, 2, out_scores=out, out_idx=idx, stream=0)
+        assert e.value.code == B.COFIE_EINVAL and "workspace" in str(e.value)
+        with pytest.raises(B.CofieError) as e:
+            B.cofie_ngff_stream_create(2, 16, 16, 3, 32, B.keep_rule("per_channel"))
+        assert e.value.code == B.COFIE_EUNSUPPORTED
+    # outside the dry run the refusals are gone (no GPU here: the sizing call works)
+    assert B.qer_workspace_bytes(B.qer_desc(16, 64, 4, 2, 2, 32), 2) > 0
+
