@@ -287,14 +287,23 @@ __device__ __forceinline__ void qk_half(const char* st, const FragBase& f, int h
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int rt = 0; rt < kNT; ++rt) s[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 a = k_frag(st, f, 2 * half, 0), b = k_frag(st, f, 2 * half + 1, 0);
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint4 kf = k_frag(st, f, 2 * half + j, ks);
-#pragma unroll
-      for (int rt = 0; rt < kNT; ++rt) mfma(s[j][rt], kf, q[ks][rt]);
+  for (int ks = 0; ks < 4; ++ks) {
+    uint4 c = a, d = b;
+    if (ks + 1 < 4) {
+      c = k_frag(st, f, 2 * half, ks + 1);
+      d = k_frag(st, f, 2 * half + 1, ks + 1);
     }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) mfma(s[0][rt], a, q[ks][rt]);
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) mfma(s[1][rt], b, q[ks][rt]);
+    __builtin_amdgcn_sched_barrier(0);
+    a = c;
+    b = d;
+  }
 }
 
 // softmax of one 32-token step -> P (B operand of O^T), lazy max
@@ -353,11 +362,24 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
 
 __device__ __forceinline__ void pv_half(const char* st, const FragBase& f, int half, f32x4 (&o)[8][kNT],
                                         const uint4 (&p)[kNT]) {
+  // fragment reads one pair ahead of the pair being multiplied (the order is
+  // pinned: by itself the scheduler waits for each pair right after its reads)
+  uint4 a = v_frag(st, f, 0, half), b = v_frag(st, f, 1, half);
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    const uint4 vf = v_frag(st, f, dt, half);
+  for (int dt = 0; dt < 8; dt += 2) {
+    uint4 c = a, d = b;
+    if (dt + 2 < 8) {
+      c = v_frag(st, f, dt + 2, half);
+      d = v_frag(st, f, dt + 3, half);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int rt = 0; rt < kNT; ++rt) mfma(o[dt][rt], vf, p[rt]);
+    for (int rt = 0; rt < kNT; ++rt) mfma(o[dt][rt], a, p[rt]);
+#pragma unroll
+    for (int rt = 0; rt < kNT; ++rt) mfma(o[dt + 1][rt], b, p[rt]);
+    __builtin_amdgcn_sched_barrier(0);
+    a = c;
+    b = d;
   }
 }
 
