@@ -411,6 +411,20 @@ def test_gather_malformed_offsets_and_short_dst():
     assert v > 0 and "gather: destination" in msg, msg
 
 
+def test_gather_offsets_saturate_past_int32():
+    """A selection that repeats a frame until its running row count passes
+    2^31 (5000 entries of a 2^20-row frame: the offsets kernel path): every
+    copy stays inside dst, because the stored offsets saturate at 2^31 - 1
+    and the frames placed past the capacity are skipped (int32 offsets that
+    wrapped would have placed them before dst)."""
+    rows = 1 << 20
+    offs = np.array([0, rows])
+    sel = np.zeros(5000, np.int32)
+    with B.DryRun() as dr:
+        gather(dr, rows, 16, offs, sel, (1 << 31) - 1)
+        clean(dr, "saturated offsets")
+
+
 def test_gather_capacity_beyond_int32_refused():
     with B.DryRun() as dr:
         with pytest.raises(B.CofieError):
