@@ -229,6 +229,21 @@ def test_streams_shapes(dtype, n_q, H_q, H_kv, d, streams):
         clean(dr, "streams")
 
 
+@pytest.mark.parametrize("frames", [33288, 33289])
+def test_streams_keys_near_int32_offsets(frames):
+    """A sequence whose keys reach the 32-bit 16-byte offsets of the sequence
+    kernel (2^31 units = 4 793 490.3 rows of 7168 bytes): 33 288 frames of
+    144 keys stay below, the sequence kernel runs with every offset inside
+    its sequence; 33 289 frames pass it, the call takes the general score
+    kernel (64-bit offsets).  Both walk clean."""
+    tokens = 144
+    nk = frames * tokens
+    with B.DryRun() as dr:
+        streams_call(dr, [nk, 2880], [frames, 20], [4, 4], [frames, frames // 2, 7, frames, 20, 10, 1, 0],
+                     32, 28, 28, 128, "bf16", 16)
+        clean(dr, "keys near 2^31 units")
+
+
 @pytest.mark.parametrize("short", ["K", "Q", "offs"])
 def test_short_buffers_are_reported(short):
     """Negative control: the same multi-stream step with one buffer 16 (4)
