@@ -366,6 +366,14 @@ def test_signal_shapes(name, shape, G):
         clean(dr, "signals")
 
 
+def test_ngff_million_frames():
+    """2^20 small frames in streams of 4096: frame and histogram offsets past
+    2^31 bytes, 256 streams of keep words."""
+    with B.DryRun() as dr:
+        ngff_filter(dr, 1 << 20, 40, 48, 3, "per_channel", 32, seg=4096)
+        clean(dr, "a million frames")
+
+
 def test_short_frames_reported():
     with B.DryRun() as dr:
         ngff_filter(dr, 5, 448, 448, 3, "per_channel", 32, trim=1)
