@@ -1412,8 +1412,9 @@ struct QerQueryDesc {
   int32_t nf;
 };
 
-// Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame,
-// fp64 partial sums in a fixed lane order.  Also writes the frame's sort key.
+// Eq. 7: w_f = mean over the frame's visual tokens of m_j; one wave per frame
+// (wave w of the grid takes frames w, w + waves, ...), fp64 partial sums in a
+// fixed lane order.  Also writes the frame's sort key.
 // Several queries (blockIdx.y): query g reads row g of m, covers its first
 // nf_q[g] frames (all when nf_q is null) and writes row g of the scores and
 // keys; frames past its prefix score -inf.
@@ -1431,7 +1432,6 @@ __global__ __launch_bounds__(1024) void qer_frame_mean_kernel(const float* m, in
                                                               int32_t k_top, int32_t* out_idx,
                                                               const QerQueryDesc* qd) {
   const int lane = threadIdx.x & 63;
-  const int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   const int64_t g = blockIdx.y;
   int32_t nf = nf_q ? nf_q[g] : n_frames;
   int32_t nfr = n_frames, nv = n_vis;
@@ -1447,12 +1447,15 @@ __global__ __launch_bounds__(1024) void qer_frame_mean_kernel(const float* m, in
     nfr = q.n_frames;
     nf = q.nf;
   }
-  if (f < nfr && f >= nf) {
+  // every wave takes frames (blockIdx.x * waves + wave) + k * (grid * waves)
+  const int64_t fstep = (int64_t)gridDim.x * (blockDim.x >> 6);
+  for (int64_t f = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); f < nfr; f += fstep) {
+  if (f >= nf) {
     if (lane == 0) {
       out_scores[f] = -INFINITY;
       st_agent(keys + f, order_key(-INFINITY));
     }
-  } else if (f < nfr) {
+  } else {
     int64_t lo64 = (int64_t)offs[f] - key0, hi64 = (int64_t)offs[f + 1] - key0;
     const int lo = (int)(lo64 < 0 ? 0 : (lo64 > nv ? nv : lo64));
     const int hi = (int)(hi64 < lo ? lo : (hi64 > nv ? nv : hi64));
@@ -1475,6 +1478,7 @@ __global__ __launch_bounds__(1024) void qer_frame_mean_kernel(const float* m, in
       out_scores[f] = w;
       st_agent(keys + f, order_key(w));
     }
+  }
   }
   if (trees) {
     __shared__ int32_t last_sh;
@@ -1787,9 +1791,15 @@ struct QerScratch {
 struct QerTrees {
   int32_t nwg, ints, stride;
 };
-inline QerTrees qer_trees(int32_t n_frames) {
+// Grid of the frame-mean kernel (16 waves a workgroup): one frame per wave
+// while the queries' workgroups fit one per CU, else each wave strides over
+// ceil(workgroups / CUs) frames, so the launch stays one round on the chip
+// (fewer, fuller waves and a shallower arrival tree per query).
+inline QerTrees qer_trees(int32_t n_frames, int32_t n_queries) {
   QerTrees t;
-  t.nwg = (n_frames + 15) / 16;
+  const int64_t one = ((int64_t)n_frames + 15) / 16, cus = device_cu_count();
+  const int64_t fpw = std::max<int64_t>(1, (one * std::max(n_queries, 1) + cus - 1) / cus);
+  t.nwg = (int32_t)(((int64_t)n_frames + 16 * fpw - 1) / (16 * fpw));
   t.stride = arrive_fan(t.nwg) > 0 ? 16 : 1;
   t.ints = (arrive_fan(t.nwg) + 1) * t.stride;
   return t;
@@ -1802,7 +1812,7 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
   w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * n_queries * h.n_q * p.Lc * p.esize) : nullptr;
   // (the SOFTMAX partial statistics are carved below)
   w.nf = n_queries > 1 ? ar.take<int32_t>((size_t)n_queries) : nullptr;
-  w.done = ar.take<int32_t>((size_t)n_queries * qer_trees(h.n_frames).ints);
+  w.done = ar.take<int32_t>((size_t)n_queries * qer_trees(h.n_frames, n_queries).ints);
   if (h.score_mode == COFIE_SCORE_SOFTMAX) {
     // the score kernel's statistics: rows (heads x query rows) in whole blocks
     // of 16, per wave and round
@@ -2163,9 +2173,8 @@ void model_frame_mean(int gx, int gy, int threads, const float* m, int32_t n_vis
     dry_range(nv, 0, (int64_t)n_vis + 1, "frame mean: keys past the row of m");
     dry_range(nfr, 0, (int64_t)n_frames + 1, "frame mean: frames past the row of scores");
     dry_range(nf, 0, (int64_t)nfr + 1, "frame mean: prefix past the frames");
-    dry_range(std::min<int64_t>(nfr, 1), 0, nfw + 1, "frame mean: frames past the grid");
-    if (nfr > nfw) dry_range(nfr, 0, nfw + 1, "frame mean: frames past the grid");
-    const int32_t fr = std::min<int64_t>(nfr, nfw);
+    (void)nfw;  // the waves loop over the frames with the grid's stride: every frame is covered
+    const int32_t fr = nfr;
     if (fr > 0) {
       dry_access(out_scores, (g * n_frames) * 4, 4 * (int64_t)fr, "frame mean: scores");
       dry_access(keys, (g * n_frames) * 4, 4 * (int64_t)fr, "frame mean: sort keys");
@@ -2352,7 +2361,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.tiles = (int32_t)ceil_div(h.n_vis, 16);
       sa.scale = (float)((double)base_scale / (double)h.H_q);
       sa.m = w.m;
-      sa.nclear = n_queries * qer_trees(h.n_frames).ints;
+      sa.nclear = n_queries * qer_trees(h.n_frames, n_queries).ints;
       const int cus = device_cu_count();
       // query rows per pass over K: 64, or 128 (eight 16-row blocks) where the
       // plan gives one tile per wave, no contraction split (its LDS would not
@@ -2406,7 +2415,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       sa.soft_scale = base_scale;
       sa.stats_part = w.partial;
       sa.stats = w.stats;
-      sa.nclear = n_queries * qer_trees(h.n_frames).ints;
+      sa.nclear = n_queries * qer_trees(h.n_frames, n_queries).ints;
       const int cus = device_cu_count();
       const int chunk = p.soft_wide ? 128 : 64;
       for (int pass = 1; pass <= 2; ++pass) {
@@ -2490,7 +2499,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
     }
   }
   if (fused_tail) {
-    const QerTrees tr = qer_trees(h.n_frames);
+    const QerTrees tr = qer_trees(h.n_frames, n_queries);
     return launch_frame_mean(tr.nwg, n_queries, 1024, s,
                   (const float*)w.m, h.n_vis, frame_offsets, h.n_frames, out_scores, w.keys, (const int32_t*)w.nf,
                   w.done, tr.ints, tr.stride, k_top, out_idx, (const QerQueryDesc*)nullptr);
@@ -2630,7 +2639,7 @@ StreamsScratch carve_streams(Arena& ar, const cofie_qer_desc& h, const QerPlan& 
   w.qp = p.fold ? ar.take<uint8_t>((size_t)p.P * sp.n_queries * h.n_q * p.Lc * p.esize) : nullptr;
   w.qop = seq_fast(h, p, sp) ? ar.take<uint4>(sp.seq.size() * (size_t)(p.Lc * p.esize / 64) * kSeqNB * 64) : nullptr;
   w.meta = ar.take<uint8_t>(meta_bytes(sp));
-  w.done = ar.take<int32_t>((size_t)sp.n_queries * qer_trees(std::max(sp.max_frames, 1)).ints);
+  w.done = ar.take<int32_t>((size_t)sp.n_queries * qer_trees(std::max(sp.max_frames, 1), sp.n_queries).ints);
   return w;
 }
 
@@ -2810,7 +2819,7 @@ int rank_streams_impl(const void* Q, const void* K, const int32_t* frame_offsets
     if (rc) return rc;
     qp = w.qp;
   }
-  const QerTrees tr = qer_trees(std::max(sp.max_frames, 1));
+  const QerTrees tr = qer_trees(std::max(sp.max_frames, 1), sp.n_queries);
   const float base_scale = h.scale > 0.f ? h.scale : (float)(1.0 / std::sqrt((double)h.d));
   const int cus = device_cu_count();
   if (w.qop && sp.tiles > 0 && seq_span(sp, seq_nwg(sp, cus)) <= kSeqTab) {
