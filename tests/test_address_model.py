@@ -333,15 +333,18 @@ def test_ngff_workloads(cfg):
         clean(dr, f"NGFF C{cfg}")
 
 
-@pytest.mark.parametrize("shape", [(3, 64, 64, 3), (2, 40, 40, 3), (3, 37, 53, 3), (5, 448, 448, 3), (1, 1, 1, 3),
-                                   (4, 64, 64, 1), (3, 37, 53, 1), (2, 448, 448, 1), (2, 2160, 3840, 3),
-                                   (2, 1464, 1920, 3)])
-@pytest.mark.parametrize("mode,bins", [("per_channel", 32), ("per_channel", 2), ("per_channel", 64),
-                                       ("joint3d", 8), ("joint3d", 16), ("gray", 32), ("gray", 256)])
+RGB_SHAPES = [(3, 64, 64, 3), (2, 40, 40, 3), (3, 37, 53, 3), (5, 448, 448, 3), (1, 1, 1, 3), (2, 2160, 3840, 3),
+              (2, 1464, 1920, 3)]
+ONE_CHANNEL_SHAPES = [(4, 64, 64, 1), (3, 37, 53, 1), (2, 448, 448, 1)]
+MODES = [("per_channel", 32), ("per_channel", 2), ("per_channel", 64), ("joint3d", 8), ("joint3d", 16), ("gray", 32),
+         ("gray", 256)]
+
+
+# one-channel frames take the gray mode only
+@pytest.mark.parametrize("shape,mode,bins", [(s, m, b) for s in RGB_SHAPES for m, b in MODES] +
+                         [(s, m, b) for s in ONE_CHANNEL_SHAPES for m, b in MODES if m == "gray"])
 def test_ngff_shapes(shape, mode, bins):
     n, H, W, C = shape
-    if C == 1 and mode != "gray":
-        pytest.skip("one channel: gray only")
     with B.DryRun() as dr:
         ngff_filter(dr, n, H, W, C, mode, bins)
         ngff_filter(dr, n, H, W, C, mode, bins, misalign=1)  # byte path of a frame at an odd address

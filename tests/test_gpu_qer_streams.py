@@ -85,17 +85,21 @@ def run_streams(per, n_q, H_q, H_kv, d, k_top, dtype, regression=False):
     return w, idx
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("n_q,H_q,H_kv,d,streams", [
+STREAM_SHAPES = [
     (32, 4, 4, 64, [(12, 4), (0, 2), (7, 0), (20, 3), (1, 1)]),   # empty sequence, sequence without queries
     (16, 2, 2, 64, [(30, 9), (5, 1)]),                             # 9 x 16 rows: chunks of 128 + 16
     (48, 4, 4, 32, [(25, 3), (9, 2)]),                             # 96-row chunks: two of eight blocks unused
     (32, 8, 2, 64, [(18, 3), (6, 2), (11, 1)]),                    # grouped heads: 64-row chunks
     (16, 28, 28, 128, [(40, 4), (3, 4), (60, 2)]),                 # workload heads, many tiles
-])
+]
+
+
+# the grouped-head shape in bf16 only: in fp32 its fold is one query term,
+# chunked as MHA, which the fp32 MHA shapes cover
+@pytest.mark.parametrize("dtype,n_q,H_q,H_kv,d,streams",
+                         [("bf16",) + c for c in STREAM_SHAPES] +
+                         [("f32",) + c for c in STREAM_SHAPES if not (c[1] != c[2] and c[0] > 16)])
 def test_streams_shapes(dtype, n_q, H_q, H_kv, d, streams):
-    if dtype == "f32" and H_q != H_kv and n_q > 16:
-        pytest.skip("covered in bf16")  # fp32 grouped heads: one query term, same chunking as MHA
     per = make_streams(n_q + 7 * d + len(streams), n_q, H_q, H_kv, d, streams, dtype)
     for k in (0, 3, 50):
         run_streams(per, n_q, H_q, H_kv, d, k, dtype)
