@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcofie.so")
-SOURCES = ["runtime.hip", "ngff.hip", "qer.hip", "glue.hip", "attn.hip", "diag.hip"]
+SOURCES = ["runtime.hip", "ngff.hip", "qer.hip", "soft_grp.hip", "glue.hip", "attn.hip", "diag.hip"]
 ARCH = os.environ.get("COFIE_OFFLOAD_ARCH", "gfx950")
 
 CFLAGS = [

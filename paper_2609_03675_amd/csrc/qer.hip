@@ -41,6 +41,7 @@
 #include <vector>
 
 #include "common.h"
+#include "soft_grp.h"
 
 namespace cofie {
 namespace {
@@ -1773,8 +1774,10 @@ struct QerPlan {
   // segments, the pass-2 statistics and the segment map within the LDS budget
   bool soft_fast;
   bool soft_wide;       // 128 query rows per pass (else 64)
-  int64_t soft_nwg;     // workgroups of the score kernel
-  int64_t soft_rounds;  // their rounds
+  int64_t soft_nwg;     // workgroups of the score kernel (qer_soft_grp_kernel: its key ranges)
+  int64_t soft_rounds;  // their rounds (qer_soft_grp_kernel: 1)
+  // SOFTMAX through qer_soft_grp_kernel (grouped bf16 heads of d = 128, one query)
+  bool soft_grp;
 };
 
 struct QerScratch {
@@ -1817,8 +1820,9 @@ QerScratch carve_qer(Arena& ar, const cofie_qer_desc& h, const QerPlan& p, int32
     // the score kernel's statistics: rows (heads x query rows) in whole blocks
     // of 16, per wave and round
     const size_t rows16 = (size_t)ceil_div((int64_t)h.H_q * h.n_q * n_queries, 16) * 16;
-    w.partial = p.soft_fast ? ar.take<float2>((size_t)p.soft_nwg * kLdsWaves * p.soft_rounds * rows16)
-                            : ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
+    w.partial = p.soft_grp    ? ar.take<float2>((size_t)p.soft_nwg * rows16)
+                : p.soft_fast ? ar.take<float2>((size_t)p.soft_nwg * kLdsWaves * p.soft_rounds * rows16)
+                              : ar.take<float2>((size_t)p.nblk_soft * h.H_q * h.n_q);
     w.stats = ar.take<float2>((size_t)h.H_q * h.n_q * n_queries);
   } else {
     w.partial = nullptr;
@@ -2265,13 +2269,29 @@ int64_t soft_rounds(const LdsPlan& L, int64_t n_vis) {
 }
 constexpr size_t kLdsMax = 160 * 1024;
 
+// SOFTMAX through qer_soft_grp_kernel: bf16 grouped heads of d = 128 with an
+// instance for their shape, one query
+bool soft_grp_ok(const cofie_qer_desc& h, int32_t n_queries) {
+  return h.score_mode == COFIE_SCORE_SOFTMAX && h.dtype == COFIE_BF16 && h.d == 128 && n_queries == 1 &&
+         h.n_vis > 0 && h.H_q % h.H_kv == 0 && grp_has_instance(h.H_kv, h.H_q / h.H_kv);
+}
+int grp_blocks(int32_t n_q) { return (n_q + 15) / 16; }
+// key ranges: a multiple of 8 (whole XCD groups), one workgroup per CU
+int grp_ranges(int nb, int cus) { return 8 * std::max(1, cus / (8 * nb)); }
+
 // Whether SOFTMAX takes the score kernel (each head whole 128-byte segments
 // of a key row, the widest query chunk's LDS within the CU's), and its
 // pass-1 statistics count.
 void plan_soft(const cofie_qer_desc& h, int32_t n_queries, QerPlan& p) {
-  p.soft_fast = p.soft_wide = false;
+  p.soft_fast = p.soft_wide = p.soft_grp = false;
   p.soft_nwg = p.soft_rounds = 0;
   if (h.score_mode != COFIE_SCORE_SOFTMAX || h.n_vis <= 0) return;
+  if (soft_grp_ok(h, n_queries)) {
+    p.soft_grp = true;
+    p.soft_nwg = grp_ranges(grp_blocks(h.n_q), device_cu_count());
+    p.soft_rounds = 1;
+    return;
+  }
   const int64_t seg_el = (1024 / lds_rows(1, 1)) / (int64_t)p.esize;
   if (h.d % seg_el != 0) return;
   const int cus = device_cu_count();
@@ -2335,7 +2355,7 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
   // the top-k runs in the frame-mean kernel's last workgroup when the score
   // kernel (launched first) clears its arrival counters
   const bool fused_tail =
-      (h.score_mode == COFIE_SCORE_LOGIT || p.soft_fast) && h.n_vis > 0 && h.n_frames > 0 && k_top > 0;
+      (h.score_mode == COFIE_SCORE_LOGIT || p.soft_fast || p.soft_grp) && h.n_vis > 0 && h.n_frames > 0 && k_top > 0;
 
   if (h.n_vis > 0) {
     if (h.score_mode == COFIE_SCORE_LOGIT) {
@@ -2392,6 +2412,33 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
           rc = launch_lds<float, 1>(sa, L, NB, s);
         if (rc) return rc;
       }
+    } else if (p.soft_grp) {
+      // grouped heads: per-head statistics, their merge over the key ranges,
+      // then the probabilities
+      SoftGrpArgs ga{};
+      ga.K = static_cast<const uint4*>(K);
+      ga.Q = static_cast<const uint4*>(Q);
+      ga.n_vis = h.n_vis;
+      ga.n_q = h.n_q;
+      ga.tiles = ceil_div(h.n_vis, 16);
+      ga.nb = grp_blocks(h.n_q);
+      ga.ranges = (int32_t)p.soft_nwg;
+      ga.c2 = (float)((double)base_scale * 1.4426950408889634);
+      ga.inv_h = 1.0f / (float)h.H_q;
+      ga.stats_part = w.partial;
+      ga.stats = w.stats;
+      ga.m = w.m;
+      ga.clear = fused_tail ? w.done : nullptr;
+      ga.nclear = qer_trees(h.n_frames, 1).ints;
+      ga.q_gstride = (h.H_q / h.H_kv) * 256;
+      rc = launch_grp(ga, h.H_kv, h.H_q / h.H_kv, 1, s);
+      if (rc) return rc;
+      const int32_t rows = h.H_q * h.n_q;
+      rc = launch("qer_soft_merge", qer_soft_merge_blocked_kernel, dim3((unsigned)ceil_div(rows, 16)), dim3(1024), 0,
+                  s, (const float2*)w.partial, p.soft_nwg, rows, w.stats);
+      if (rc) return rc;
+      rc = launch_grp(ga, h.H_kv, h.H_q / h.H_kv, 2, s);
+      if (rc) return rc;
     } else if (p.soft_fast) {
       // two passes of the score kernel over K (per-head statistics, then the
       // probabilities), the statistics merged in between

@@ -89,6 +89,33 @@ def test_qer_shapes(dtype, n_q, H_q, H_kv, d):
         clean(dr, "shapes")
 
 
+# SOFTMAX with grouped bf16 heads of d = 128 (one query) takes the grouped-head
+# kernel: every instance, ragged rows and tiles, fewer tiles than key ranges
+SOFT_GRP = [(48, 28, 4, [222] * 8 + [224]),   # the high-res heads
+            (40, 28, 4, [17, 0, 40, 1, 33]),   # rows past the last full block, ragged last tile
+            (1, 28, 4, [5]),                   # one row, one partial tile
+            (64, 32, 4, [100] * 7),            # four row blocks
+            (16, 8, 4, [16] * 33),             # 33 whole tiles: one pair short of a full last pair
+            (33, 8, 2, [3001]),                # G = 4
+            (5, 16, 2, [64] * 60)]             # G = 8, many tiles per range
+
+
+@pytest.mark.parametrize("n_q,H_q,H_kv,tokens", SOFT_GRP)
+def test_softmax_grouped_heads(n_q, H_q, H_kv, tokens):
+    with B.DryRun() as dr:
+        for k in (0, 3):
+            qer_single(dr, n_q, H_q, H_kv, 128, tokens, "bf16", k, B.SOFTMAX)
+        qer_single(dr, n_q, H_q, H_kv, 128, tokens, "bf16", 3, B.SOFTMAX, noalloc=True)
+        clean(dr, "grouped SOFTMAX")
+
+
+def test_softmax_grouped_heads_short_keys_reported():
+    with B.DryRun() as dr:
+        qer_single(dr, 48, 28, 4, 128, [222] * 8 + [224], "bf16", 4, B.SOFTMAX, trim_k=16)
+        v, n, msg = dr.result()
+    assert v > 0 and "soft grp: keys" in msg, msg
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n_q,H_q,H_kv,d,tokens", [
     (32, 28, 28, 128, [333] * 8 + [337]),   # ragged last tile

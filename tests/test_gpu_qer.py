@@ -79,19 +79,47 @@ def test_softmax_mode(dtype, n_q, H_q, H_kv, d):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n_q,H_q,H_kv,d,n_tok", [
     (32, 28, 28, 128, 3001),   # the 1 fps stream's heads, ragged last tile
-    (48, 28, 4, 128, 2000),    # the high-res heads: seven query heads per key head
+    (48, 28, 4, 128, 2000),    # the high-res heads (bf16: the grouped-head kernel)
+    (48, 12, 4, 128, 2000),    # three query heads per key head: no grouped-head instance
     (70, 4, 4, 64, 1500),      # two query chunks (> 64 rows)
     (16, 2, 1, 64, 65600),     # > 4096 tiles: two rounds in some workgroups, one in others
 ])
 def test_softmax_through_score_kernel(dtype, n_q, H_q, H_kv, d, n_tok):
     """SOFTMAX mode where every head is whole 128-byte segments of a key row:
     both passes run in the LDS-staged score kernel (per-head statistics per
-    wave, merged, then the head mean of the probabilities)."""
+    wave, merged, then the head mean of the probabilities), or, for bf16
+    grouped heads of d = 128 with an instance, in the grouped-head kernel."""
     per = max(1, n_tok // 9)
     tokens = [per] * 8 + [n_tok - 8 * per]
     offs = synth.frame_offsets(tokens)
     Q, K = synth.random_qk(n_q * 31 + H_q + n_tok, n_q, int(offs[-1]), H_q, H_kv, d, dtype)
     w, idx, ref = run_case(Q, K, offs, H_q, H_kv, d, 4, mode=B.SOFTMAX, dtype=dtype)
+    w2, idx2 = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs.astype(np.int32)), 4, score_mode=B.SOFTMAX)
+    torch.cuda.synchronize()
+    assert np.array_equal(w, w2.cpu().numpy()), "SOFTMAX scores differ between two calls"
+
+
+@pytest.mark.parametrize("n_q,H_q,H_kv,tokens", [
+    (48, 28, 4, [222] * 8 + [224]),    # the high-res heads
+    (40, 28, 4, [17, 0, 40, 1, 33]),   # rows past the last full block, ragged last tile
+    (1, 28, 4, [5]),                   # one row, one partial tile
+    (64, 32, 4, [100] * 7),            # four row blocks
+    (16, 8, 4, [16] * 33),             # 33 whole tiles
+    (33, 8, 2, [3001]),                # G = 4
+    (5, 16, 2, [64] * 60),             # G = 8
+    (48, 28, 4, [196] * 60),           # several pairs per wave
+])
+def test_softmax_grouped_heads(n_q, H_q, H_kv, tokens):
+    """SOFTMAX with bf16 grouped heads of d = 128 through the grouped-head
+    kernel (per-head statistics per lane over its own keys, merged over lanes,
+    waves and key ranges; then the head mean of the probabilities and its max
+    over the rows): every instance, ragged rows and tiles, fewer tiles than key
+    ranges.  Scores within the bf16 regression bound (the products are exact
+    bf16 values, accumulated in fp32), and two calls bit-identical."""
+    offs = synth.frame_offsets(tokens)
+    Q, K = synth.random_qk(n_q * 37 + H_q + len(tokens), n_q, int(offs[-1]), H_q, H_kv, 128, "bf16")
+    for k in (0, 4):
+        w, idx, ref = run_case(Q, K, offs, H_q, H_kv, 128, k, mode=B.SOFTMAX, regression=True)
     w2, idx2 = B.cofie_qer_rank(qk_dev(Q), qk_dev(K), to_dev(offs.astype(np.int32)), 4, score_mode=B.SOFTMAX)
     torch.cuda.synchronize()
     assert np.array_equal(w, w2.cpu().numpy()), "SOFTMAX scores differ between two calls"

@@ -96,7 +96,8 @@ def test_qer_full_size(cfg):
 @pytest.mark.parametrize("cfg", [2, 3, 4])
 def test_qer_softmax_full_size(cfg):
     """SOFTMAX mode at the workloads' full sizes: both passes through the
-    score kernel (grouped heads at the high-res workload)."""
+    score kernel, or at the high-res workload (seven bf16 query heads per key
+    head, d = 128) through the grouped-head kernel."""
     wl = synth.WORKLOADS[cfg]
     Q, K, offs = synth.qer_inputs(cfg)
     print(f"workload {cfg}: SOFTMAX n_q={wl.n_q} n_vis={K.shape[0]} heads {wl.H_q}/{wl.H_kv}", flush=True)
