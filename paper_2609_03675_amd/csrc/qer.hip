@@ -1774,7 +1774,7 @@ struct QerPlan {
   // segments, the pass-2 statistics and the segment map within the LDS budget
   bool soft_fast;
   bool soft_wide;       // 128 query rows per pass (else 64)
-  int64_t soft_nwg;     // workgroups of the score kernel (qer_soft_grp_kernel: its key ranges)
+  int64_t soft_nwg;     // workgroups of the score kernel (qer_soft_grp_kernel: pass 1's key ranges)
   int64_t soft_rounds;  // their rounds (qer_soft_grp_kernel: 1)
   // SOFTMAX through qer_soft_grp_kernel (grouped bf16 heads of d = 128, one query)
   bool soft_grp;
@@ -2276,8 +2276,14 @@ bool soft_grp_ok(const cofie_qer_desc& h, int32_t n_queries) {
          h.n_vis > 0 && h.H_q % h.H_kv == 0 && grp_has_instance(h.H_kv, h.H_q / h.H_kv);
 }
 int grp_blocks(int32_t n_q) { return (n_q + 15) / 16; }
-// key ranges: a multiple of 8 (whole XCD groups), one workgroup per CU
-int grp_ranges(int nb, int cus) { return 8 * std::max(1, cus / (8 * nb)); }
+// key ranges of a pass whose workgroups are `per` per range: a multiple of 8
+// (whole XCD groups), at most one workgroup per CU
+int grp_ranges(int per, int cus) { return 8 * std::max(1, cus / (8 * per)); }
+// pass 1: per range, one workgroup per key head and set of row blocks
+int grp_ranges1(const cofie_qer_desc& h, int cus) {
+  const int nb = grp_blocks(h.n_q), nbw = grp_nbw(h.H_q / h.H_kv, nb);
+  return grp_ranges(h.H_kv * ((nb + nbw - 1) / nbw), cus);
+}
 
 // Whether SOFTMAX takes the score kernel (each head whole 128-byte segments
 // of a key row, the widest query chunk's LDS within the CU's), and its
@@ -2288,7 +2294,7 @@ void plan_soft(const cofie_qer_desc& h, int32_t n_queries, QerPlan& p) {
   if (h.score_mode != COFIE_SCORE_SOFTMAX || h.n_vis <= 0) return;
   if (soft_grp_ok(h, n_queries)) {
     p.soft_grp = true;
-    p.soft_nwg = grp_ranges(grp_blocks(h.n_q), device_cu_count());
+    p.soft_nwg = grp_ranges1(h, device_cu_count());  // pass 1's key ranges: the partial statistics
     p.soft_rounds = 1;
     return;
   }
@@ -2422,7 +2428,10 @@ int rank_impl(const void* Q, const void* K, const int32_t* frame_offsets, const 
       ga.n_q = h.n_q;
       ga.tiles = ceil_div(h.n_vis, 16);
       ga.nb = grp_blocks(h.n_q);
-      ga.ranges = (int32_t)p.soft_nwg;
+      ga.ranges = grp_ranges(ga.nb, device_cu_count());
+      ga.ranges1 = (int32_t)p.soft_nwg;
+      ga.nbw = grp_nbw(h.H_q / h.H_kv, ga.nb);
+      ga.nbs = (ga.nb + ga.nbw - 1) / ga.nbw;
       ga.c2 = (float)((double)base_scale * 1.4426950408889634);
       ga.inv_h = 1.0f / (float)h.H_q;
       ga.stats_part = w.partial;

@@ -6,28 +6,33 @@
 // exponential per score (H_q n_q of them per key), and the general score
 // kernel spends most of its VALU instructions around them (the operand select
 // and rotation of its key rows, reductions across lanes at every head,
-// masks).  Here a workgroup takes one 16-row block of the query rows, all
-// H_q heads of it in LDS in MFMA operand order (4 KiB per head), and a range
-// of key tiles; each wave takes pairs of 16-key tiles, holds the pair's keys
-// of one key head in registers (the A operand, read straight from K) and
-// multiplies them by that key head's G query heads (one LDS fragment feeds
-// both tiles).  A lane holds one query row and four keys of each tile (the
-// accumulator layout), so a score costs one fma, one exp2 and one add:
-//  * pass 1 keeps per head the lane's running (max, sum of exp2) over its own
-//    keys; the max is raised only when a pair's sum leaves [0, 2^64) (the pair
-//    is then summed again against its own max), and lanes and waves are
-//    combined once, at the end (the key ranges by the merge kernel);
-//  * pass 2 adds exp2(s c2 - L) over all heads (L = M log2 e + log2 Z of the
-//    row; +inf for rows past the query, which then add 0), takes the max over
-//    the block's 16 rows with DPP and max-accumulates it into m: the values
-//    are not negative, so their bit patterns order as unsigned integers (pass
-//    1 zeroed m), and the result does not depend on the order.
-// The products run one head ahead of the exponentials (the fragments two
-// heads ahead, the keys one key head ahead, the next pair's first key head
-// during the last), so the matrix core works on head h + 1 while the VALU
-// finishes head h.  Workgroup b runs on XCD b mod 8, and the nb row blocks
-// of one key range are consecutive workgroups of one XCD, so that its L2
-// serves their key reads.
+// masks).  Here the keys are the A operand straight from K (a lane's row and
+// 16 bytes of each 64-byte step), the query fragments sit in LDS in MFMA
+// operand order (4 KiB per head and 16-row block), each wave takes pairs of
+// 16-key tiles (one fragment read feeds both), and a lane holds one query
+// row and four keys of each tile (the accumulator layout), so a score costs
+// one fma, one exp2 and one add:
+//  * pass 1 (per-head statistics) needs no sum over heads, so a workgroup
+//    takes one key head, up to four 16-row blocks and a range of key tiles:
+//    each key byte is read once per launch and each key fragment feeds the
+//    G x blocks products of its query heads.  A lane keeps per (head, block)
+//    its running (max, sum of exp2) over its own keys; the max is raised only
+//    when a pair's sum leaves [0, 2^64) (the pair is then summed again against
+//    its own max), and lanes and waves are combined once, at the end (the key
+//    ranges by the merge kernel);
+//  * pass 2 (the head mean of the probabilities) needs every head of a row,
+//    so a workgroup takes one 16-row block with all H_q heads and a range of
+//    key tiles: it adds exp2(s c2 - L) over all heads (L = M log2 e + log2 Z
+//    of the row; +inf for rows past the query, which then add 0), takes the
+//    max over the block's 16 rows with DPP and max-accumulates it into m: the
+//    values are not negative, so their bit patterns order as unsigned
+//    integers (pass 1 zeroed m), and the result does not depend on the order.
+// The products run one unit (head, or head and block) ahead of the
+// exponentials and the fragments two ahead; the keys one pair ahead (pass 1)
+// or one key head ahead (pass 2), so the matrix core works on unit u + 1
+// while the VALU finishes unit u.
+// Workgroup b runs on XCD b mod 8; consecutive workgroups of one XCD take one
+// key range (pass 2: its row blocks, whose key reads its L2 serves).
 #include <algorithm>
 #include <climits>
 #include <cmath>
@@ -54,6 +59,16 @@ __host__ __device__ __forceinline__ void grp_map(int b, int nb, int ranges, int 
   t_lo = (int)((int64_t)tiles * range / ranges);
   t_hi = (int)((int64_t)tiles * (range + 1) / ranges);
 }
+// Pass-1 workgroup b: its key head, row-block set, key range and tiles.
+__host__ __device__ __forceinline__ void grp_map1(int b, int hkv, int nbs, int ranges, int tiles, int& g, int& rs,
+                                                  int& range, int& t_lo, int& t_hi) {
+  const int s = b >> 3;
+  g = s % hkv;
+  rs = (s / hkv) % nbs;
+  range = (s / (hkv * nbs)) * 8 + (b & 7);
+  t_lo = (int)((int64_t)tiles * range / ranges);
+  t_hi = (int)((int64_t)tiles * (range + 1) / ranges);
+}
 // Key fragment of lane l: tile t, key head g, contraction step ks (16-byte
 // index into K; rows past the last key repeat it).
 __host__ __device__ __forceinline__ int64_t grp_key_u4(int t, int g, int ks, int l, int n_vis, int hkv) {
@@ -72,12 +87,13 @@ __host__ __device__ __forceinline__ int64_t grp_q_src(int rb, int h, int ks, int
 __host__ __device__ __forceinline__ int64_t grp_part(int64_t r, int range, int ranges) {
   return ((r >> 4) * ranges + range) * 16 + (r & 15);
 }
-// LDS: pass 2 first L of hq x 16 rows (hq * 4 uint4), then the fragments
-// (pass 1: from 0, reused at the end for the combine buffer of kGrpWaves x
-// hq x 16 pairs)
+// LDS: pass 2 first L of hq x 16 rows (hq * 4 uint4), then the fragments of
+// all hq heads of one row block; pass 1 the fragments of the g query heads
+// of one key head for nbw row blocks ([block][head][step][lane]), reused at
+// the end for the combine buffer of kGrpWaves x nbw g x 16 pairs
 __host__ __device__ constexpr int grp_frag0(int hq, int pass) { return pass == 2 ? hq * 4 : 0; }
-__host__ __device__ constexpr size_t grp_lds(int hq, int pass) {
-  return (size_t)hq * 4096 + (size_t)grp_frag0(hq, pass) * 16;
+__host__ __device__ constexpr size_t grp_lds(int hq, int g, int nbw, int pass) {
+  return pass == 2 ? (size_t)hq * 4096 + (size_t)grp_frag0(hq, pass) * 16 : (size_t)nbw * g * 4096;
 }
 
 __device__ __forceinline__ float dpp_max16(float v) {  // max over the 16 lanes of a DPP row
@@ -93,68 +109,27 @@ __device__ __forceinline__ void grp_combine(float& m1, float& z1, float m2, floa
   m1 = m;
 }
 
-template <int HKV, int G, int PASS>
+template <int HKV, int G, int PASS, int NBW>
 __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a) {
   constexpr int HQ = HKV * G;
-  static_assert(HKV % 2 == 0 && HQ % 2 == 0, "key heads and query heads alternate between two register sets");
-  extern __shared__ uint4 lds_u4[];  // pass 2: [HQ][16] L; then [HQ][4][64] query fragments
+  static_assert(HQ % 2 == 0, "query heads alternate between two register sets");
+  extern __shared__ uint4 lds_u4[];
   uint4* const qs = lds_u4 + grp_frag0(HQ, PASS);
   const int tid = threadIdx.x, l = tid & 63, wave = tid >> 6;
-  int rb, range, t_lo, t_hi;
-  grp_map((int)blockIdx.x, a.nb, a.ranges, a.tiles, rb, range, t_lo, t_hi);
-  if constexpr (PASS == 1) {
-    for (int64_t i = (int64_t)blockIdx.x * kGrpThreads + tid; i < a.n_vis; i += (int64_t)gridDim.x * kGrpThreads)
-      a.m[i] = 0.f;
-    if (blockIdx.x == 0 && a.clear)
-      for (int i = tid; i < a.nclear; i += kGrpThreads) a.clear[i] = 0;
-  }
-  // the row block's query fragments, zero past the rows
-  for (int e = tid; e < HQ * 256; e += kGrpThreads) {
-    const int h = e >> 8, ks = (e >> 6) & 3, ll = e & 63;
-    const int64_t src = grp_q_src(rb, h, ks, ll, a.n_q, HQ);
-    qs[grp_q_slot(h, ks, ll)] = src >= 0 ? a.Q[src] : uint4{0u, 0u, 0u, 0u};
-  }
-  float* ls = reinterpret_cast<float*>(lds_u4);
-  if constexpr (PASS == 2)
-    for (int i = tid; i < HQ * 16; i += kGrpThreads) {
-      const int h = i >> 4, q = 16 * rb + (i & 15);
-      float L = INFINITY;
-      if (q < a.n_q) {
-        const float2 st = a.stats[(int64_t)h * a.n_q + q];
-        L = st.x * 1.4426950408889634f + __log2f(st.y);
-      }
-      ls[i] = L;
-    }
-  __syncthreads();
-
-  float mh[HQ], zh[HQ];
-#pragma unroll
-  for (int h = 0; h < HQ; ++h) {
-    mh[h] = -INFINITY;
-    zh[h] = 0.f;
-  }
-  const float* lrow = ls + (l & 15);  // pass 2: L of this lane's row, head h at lrow[16 h]
   const float c2 = a.c2;
-  const int npairs = (t_hi - t_lo + 1) >> 1;
-
-  uint4 kf[2][2][4];  // [key head parity][tile][step]
-  uint4 qf[2][4];     // [query head parity][step]
-  float lq[2];        // pass 2: L of the row, [query head parity]
-  f32x4 sc[2][2];     // [query head parity][tile]
+  const uint4* qlane = qs + l;
   auto load_k = [&](uint4 (&f)[2][4], int t0, int g) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) f[j][ks] = a.K[grp_key_u4(t0 + j, g, ks, l, a.n_vis, HKV)];
   };
-  // (a key head's fragments from a base of its own, a runtime multiple of the
-  // head count: each read is then that base plus an immediate, where 112 KiB of
+  // (fragments from a base per G heads, a runtime multiple of the head count:
+  // each read is then that base plus an immediate, where up to 128 KiB of
   // constant offsets from one base would take a register per address)
-  const uint4* qlane = qs + l;
-  auto q_read = [&](int h, uint4 (&f)[4]) __attribute__((always_inline)) {
-    const uint4* qg = qlane + (h / G) * a.q_gstride;
+  auto q_read = [&](const uint4* qg, int hl, uint4 (&f)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) f[ks] = qg[grp_q_slot(h % G, ks, 0)];
+    for (int ks = 0; ks < 4; ++ks) f[ks] = qg[grp_q_slot(hl, ks, 0)];
   };
   auto products = [&](f32x4 (&s)[2], const uint4 (&k)[2][4], const uint4 (&q)[4]) __attribute__((always_inline)) {
     s[0] = s[1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -166,77 +141,210 @@ __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a
                                                        __builtin_bit_cast(bf16x8, q[ks]), s[j], 0, 0, 0);
   };
 
-  // keys of the first pair's first key head, fragments of heads 0 and 1
-  int p = wave;
-  load_k(kf[0], t_lo + 2 * p, 0);
-  q_read(0, qf[0]);
-  q_read(1, qf[1]);
-  for (; p < npairs; p += kGrpWaves) {
-    const int t0 = t_lo + 2 * p;
-    const bool has1 = t0 + 1 < t_hi;
-    const bool full = has1 && 16 * (t0 + 2) <= a.n_vis;
-    // this lane's keys of the pair that exist: bit 4 j + e (tile j, key 4 (l / 16) + e)
-    uint32_t valid = 0xFFu;
-    if (!full)
+  if constexpr (PASS == 1) {
+    // one key head g, row blocks NBW rs + [0, NBW), keys [16 t_lo, 16 t_hi);
+    // unit u = rbw G + hl (block rbw, query head g G + hl)
+    constexpr int U = NBW * G;
+    int g, rs, range, t_lo, t_hi;
+    grp_map1((int)blockIdx.x, HKV, a.nbs, a.ranges1, a.tiles, g, rs, range, t_lo, t_hi);
+    for (int64_t i = (int64_t)blockIdx.x * kGrpThreads + tid; i < a.n_vis; i += (int64_t)gridDim.x * kGrpThreads)
+      a.m[i] = 0.f;
+    if (blockIdx.x == 0 && a.clear)
+      for (int i = tid; i < a.nclear; i += kGrpThreads) a.clear[i] = 0;
+    {
+      // the fragments, zero past the rows: every load before the first store
+      constexpr int NF = (U * 256 + kGrpThreads - 1) / kGrpThreads;
+      uint4 v[NF];
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if ((j == 1 && !has1) || 16 * (t0 + j) + 4 * (l >> 4) + e >= a.n_vis) valid &= ~(1u << (4 * j + e));
-    f32x4 prob[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-    load_k(kf[1], t0, 1);
-    products(sc[0], kf[0], qf[0]);
-    q_read(2 % HQ, qf[0]);
-    if constexpr (PASS == 2) lq[0] = lrow[0];
-#pragma unroll
-    for (int h = 0; h < HQ; ++h) {
-      if (h + 1 < HQ) {
-        const int g1 = (h + 1) / G;
-        // the key head after g1 (the next pair's first after the last) into
-        // the set of g1 - 1, whose last products were issued before this
-        if ((h + 1) % G == 0) {
-          if (g1 + 1 < HKV) load_k(kf[(g1 + 1) & 1], t0, g1 + 1);
-          else load_k(kf[0], t0 + kGrpPairStride, 0);
-        }
-        products(sc[(h + 1) & 1], kf[g1 & 1], qf[(h + 1) & 1]);
-        q_read((h + 3) % HQ, qf[(h + 1) & 1]);
-        if constexpr (PASS == 2) lq[(h + 1) & 1] = lrow[16 * (h + 1)];
+      for (int i = 0; i < NF; ++i) {
+        const int e = tid + i * kGrpThreads, u = e >> 8;
+        const int64_t src = e < U * 256 ? grp_q_src(NBW * rs + u / G, g * G + u % G, (e >> 6) & 3, e & 63, a.n_q, HQ)
+                                        : -1;
+        v[i] = src >= 0 ? a.Q[src] : uint4{0u, 0u, 0u, 0u};
       }
-      __builtin_amdgcn_sched_barrier(0);
-      f32x4 (&s)[2] = sc[h & 1];
-      if constexpr (PASS == 1) {
-        if (!full)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < NF; ++i) {
+        const int e = tid + i * kGrpThreads;
+        if (e < U * 256) qs[grp_q_slot(e >> 8, (e >> 6) & 3, e & 63)] = v[i];
+      }
+    }
+    __syncthreads();
+
+    const int npairs = (t_hi - t_lo + 1) >> 1;
+    auto q_at = [&](int u, uint4 (&f)[4]) __attribute__((always_inline)) {
+      q_read(qlane + (u / G) * a.q_gstride, u % G, f);
+    };
+    float mh[U], zh[U];
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (!((valid >> (4 * j + e)) & 1u)) s[j][e] = -INFINITY;
-        float zt = 0.f;
+    for (int u = 0; u < U; ++u) {
+      mh[u] = -INFINITY;
+      zh[u] = 0.f;
+    }
+    uint4 kb[2][2][4];  // this pair's keys, the next pair's
+    uint4 qf[2][4];
+    f32x4 sc[2][2];
+    int p = wave;
+    load_k(kb[0], t_lo + 2 * p, g);
+    q_at(0, qf[0]);
+    q_at(1 % U, qf[1]);
+    for (; p < npairs; p += 2 * kGrpWaves) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) zt += __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mh[h]));
-        if (zt < 0x1p64f) {
-          zh[h] += zt;
-        } else {
-          // the running max is too low (or not set yet): sum the pair against
-          // its own max and rescale what came before
-          float mx = mh[h];
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[j][e] * c2);
-          if (mx > -INFINITY) {
-            float z = 0.f;
+      for (int v = 0; v < 2; ++v) {
+        const int pv = p + v * kGrpWaves;
+        load_k(kb[v ^ 1], t_lo + 2 * (pv + kGrpWaves), g);
+        if (pv < npairs) {
+          // (with U odd the fragments of unit u alternate sets from pair to pair)
+          const int flip = (U & 1) ? v : 0;
+          const int t0 = t_lo + 2 * pv;
+          const bool has1 = t0 + 1 < t_hi;
+          const bool full = has1 && 16 * (t0 + 2) <= a.n_vis;
+          // this lane's keys of the pair that exist: bit 4 j + e (tile j, key 4 (l / 16) + e)
+          uint32_t valid = 0xFFu;
+          if (!full)
 #pragma unroll
             for (int j = 0; j < 2; ++j)
 #pragma unroll
-              for (int e = 0; e < 4; ++e) z += __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mx));
-            zh[h] = (zh[h] > 0.f ? zh[h] * __builtin_amdgcn_exp2f(mh[h] - mx) : 0.f) + z;
-            mh[h] = mx;
+              for (int e = 0; e < 4; ++e)
+                if ((j == 1 && !has1) || 16 * (t0 + j) + 4 * (l >> 4) + e >= a.n_vis) valid &= ~(1u << (4 * j + e));
+          products(sc[0], kb[v], qf[flip]);
+          q_at(2 % U, qf[flip]);
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (u + 1 < U) {
+              products(sc[(u + 1) & 1], kb[v], qf[(u + 1 + flip) & 1]);
+              q_at((u + 3) % U, qf[(u + 1 + flip) & 1]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            f32x4 (&s)[2] = sc[u & 1];
+            if (!full)
+#pragma unroll
+              for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (!((valid >> (4 * j + e)) & 1u)) s[j][e] = -INFINITY;
+            float zt = 0.f;
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) zt += __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mh[u]));
+            if (zt < 0x1p64f) {
+              zh[u] += zt;
+            } else {
+              // the running max is too low (or not set yet): sum the pair
+              // against its own max and rescale what came before
+              float mx = mh[u];
+#pragma unroll
+              for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[j][e] * c2);
+              if (mx > -INFINITY) {
+                float z = 0.f;
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) z += __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mx));
+                zh[u] = (zh[u] > 0.f ? zh[u] * __builtin_amdgcn_exp2f(mh[u] - mx) : 0.f) + z;
+                mh[u] = mx;
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
         }
-      } else {
+      }
+    }
+    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same row: combine them, then
+    // the waves (in LDS, over the fragments), in a fixed order
+    __syncthreads();
+    float2* comb = reinterpret_cast<float2*>(qs);  // [wave][U][16]
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float m1 = mh[u], z1 = zh[u];
+      grp_combine(m1, z1, __shfl_xor(m1, 16), __shfl_xor(z1, 16));
+      grp_combine(m1, z1, __shfl_xor(m1, 32), __shfl_xor(z1, 32));
+      if (l < 16) comb[(wave * U + u) * 16 + l] = make_float2(m1, z1);
+    }
+    __syncthreads();
+    for (int i = tid; i < U * 16; i += kGrpThreads) {
+      const int u = i >> 4, q = 16 * (NBW * rs + u / G) + (i & 15), h = g * G + u % G;
+      float2 c = comb[i];
+      for (int w = 1; w < kGrpWaves; ++w) {
+        const float2 o = comb[w * U * 16 + i];
+        grp_combine(c.x, c.y, o.x, o.y);
+      }
+      if (q < a.n_q)  // in the natural-log units of the merge: max * scale
+        a.stats_part[grp_part((int64_t)h * a.n_q + q, range, a.ranges1)] =
+            c.y > 0.f ? make_float2(c.x * 0.6931471805599453f, c.y) : make_float2(-INFINITY, 0.f);
+    }
+  } else {
+    // one 16-row block rb with every query head, keys [16 t_lo, 16 t_hi)
+    int rb, range, t_lo, t_hi;
+    grp_map((int)blockIdx.x, a.nb, a.ranges, a.tiles, rb, range, t_lo, t_hi);
+    {
+      constexpr int NF = (HQ * 256 + kGrpThreads - 1) / kGrpThreads;
+      uint4 v[NF];
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        const int e = tid + i * kGrpThreads;
+        const int64_t src = e < HQ * 256 ? grp_q_src(rb, e >> 8, (e >> 6) & 3, e & 63, a.n_q, HQ) : -1;
+        v[i] = src >= 0 ? a.Q[src] : uint4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        const int e = tid + i * kGrpThreads;
+        if (e < HQ * 256) qs[grp_q_slot(e >> 8, (e >> 6) & 3, e & 63)] = v[i];
+      }
+    }
+    float* ls = reinterpret_cast<float*>(lds_u4);
+    for (int i = tid; i < HQ * 16; i += kGrpThreads) {
+      const int h = i >> 4, q = 16 * rb + (i & 15);
+      float L = INFINITY;
+      if (q < a.n_q) {
+        const float2 st = a.stats[(int64_t)h * a.n_q + q];
+        L = st.x * 1.4426950408889634f + __log2f(st.y);
+      }
+      ls[i] = L;
+    }
+    __syncthreads();
+
+    const int npairs = (t_hi - t_lo + 1) >> 1;
+    const float* lrow = ls + (l & 15);  // L of this lane's row, head h at lrow[16 h]
+    auto q_at = [&](int h, uint4 (&f)[4]) __attribute__((always_inline)) {
+      q_read(qlane + (h / G) * a.q_gstride, h % G, f);
+    };
+    // wave w: pairs w + 8 k, every query head; the keys one key head ahead
+    // (the next pair's first during the last), in two register sets
+    uint4 kf[2][2][4];
+    uint4 qf[2][4];
+    float lq[2];
+    f32x4 sc[2][2];
+    int p = wave;
+    load_k(kf[0], t_lo + 2 * p, 0);
+    q_at(0, qf[0]);
+    q_at(1, qf[1]);
+    for (; p < npairs; p += kGrpWaves) {
+      const int t0 = t_lo + 2 * p;
+      const bool has1 = t0 + 1 < t_hi;
+      f32x4 prob[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+      load_k(kf[1], t0, 1);
+      products(sc[0], kf[0], qf[0]);
+      q_at(2 % HQ, qf[0]);
+      lq[0] = lrow[0];
+#pragma unroll
+      for (int h = 0; h < HQ; ++h) {
+        if (h + 1 < HQ) {
+          const int g1 = (h + 1) / G;
+          // the key head after g1 (the next pair's first after the last) into
+          // the set of g1 - 1, whose last products were issued before this
+          if ((h + 1) % G == 0) {
+            if (g1 + 1 < HKV) load_k(kf[(g1 + 1) & 1], t0, g1 + 1);
+            else load_k(kf[0], t0 + kGrpPairStride, 0);
+          }
+          products(sc[(h + 1) & 1], kf[g1 & 1], qf[(h + 1) & 1]);
+          q_at((h + 3) % HQ, qf[(h + 1) & 1]);
+          lq[(h + 1) & 1] = lrow[16 * (h + 1)];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 (&s)[2] = sc[h & 1];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -247,10 +355,8 @@ __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a
         for (int j = 0; j < 2; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e) asm volatile("" : "+v"(prob[j][e]));
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (PASS == 2) {
       // max over the block's 16 rows, then into m (keys that exist only)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
@@ -263,120 +369,129 @@ __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a
         }
     }
   }
-  if constexpr (PASS == 1) {
-    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same row: combine them, then
-    // the waves (in LDS, over the query fragments), in a fixed order
-    __syncthreads();
-    float2* comb = reinterpret_cast<float2*>(qs);  // [wave][HQ][16]
-#pragma unroll
-    for (int h = 0; h < HQ; ++h) {
-      float m1 = mh[h], z1 = zh[h];
-      grp_combine(m1, z1, __shfl_xor(m1, 16), __shfl_xor(z1, 16));
-      grp_combine(m1, z1, __shfl_xor(m1, 32), __shfl_xor(z1, 32));
-      if (l < 16) comb[(wave * HQ + h) * 16 + l] = make_float2(m1, z1);
-    }
-    __syncthreads();
-    for (int i = tid; i < HQ * 16; i += kGrpThreads) {
-      const int h = i >> 4, q = 16 * rb + (i & 15);
-      float2 c = comb[i];
-      for (int w = 1; w < kGrpWaves; ++w) {
-        const float2 o = comb[w * HQ * 16 + i];
-        grp_combine(c.x, c.y, o.x, o.y);
+}
+
+// Address model of qer_soft_grp_kernel<HKV, G, PASS, NBW> (grid nwg, `lds`
+// bytes of LDS): the zeroing, every workgroup's query-fragment loads and LDS
+// slots, the statistics it reads or writes, the keys of every pair it loads
+// (the extreme key heads, steps and lanes of each tile: the index is affine
+// in each, and rows past the last key repeat it) and its stores into m.
+template <int HKV, int G, int PASS, int NBW>
+void model_grp(const SoftGrpArgs& a, int nwg, size_t lds) {
+  constexpr int HQ = HKV * G;
+  dry_range((int64_t)lds, 0, 160 * 1024 + 1, "soft grp: LDS beyond a CU's 160 KiB");
+  dry_range((int64_t)a.nb, (a.n_q + 15) / 16, (a.n_q + 15) / 16 + 1, "soft grp: row blocks");
+  auto keys = [&](int t, int g0, int g1) {
+    for (int g : {g0, g1})
+      for (int ks : {0, 3})
+        for (int l : {0, 63}) dry_access(a.K, grp_key_u4(t, g, ks, l, a.n_vis, HKV) * 16, 16, "soft grp: keys");
+  };
+  auto frag = [&](int rb, int h, int slot_h, int64_t f0) {  // query head h of row block rb at slot head slot_h
+    const int last = std::min(16 * rb + 15, a.n_q - 1) - 16 * rb;  // the block's last row (lane % 16), < 0: none
+    for (int ks = 0; ks < 4; ++ks)
+      for (int l : {0, 63, 48 + std::max(last, 0)}) {
+        const int64_t src = grp_q_src(rb, h, ks, l, a.n_q, HQ);
+        if (src >= 0) dry_access(a.Q, src * 16, 16, "soft grp: query fragment");
+        dry_lds(f0 + (int64_t)grp_q_slot(slot_h, ks, l) * 16, 16, (int64_t)lds, "soft grp: query fragment slot");
       }
-      if (q < a.n_q)  // in the natural-log units of the merge: max * scale
-        a.stats_part[grp_part((int64_t)h * a.n_q + q, range, a.ranges)] =
-            c.y > 0.f ? make_float2(c.x * 0.6931471805599453f, c.y) : make_float2(-INFINITY, 0.f);
+  };
+  if (PASS == 1) {
+    constexpr int U = NBW * G;
+    dry_range(a.ranges1 % 8, 0, 1, "soft grp: key ranges not whole XCD groups");
+    dry_range((int64_t)a.nbw, NBW, NBW + 1, "soft grp: row blocks per workgroup");
+    dry_range((int64_t)a.nbs, (a.nb + NBW - 1) / NBW, (a.nb + NBW - 1) / NBW + 1, "soft grp: row-block sets");
+    dry_range((int64_t)nwg, (int64_t)HKV * a.nbs * a.ranges1, (int64_t)HKV * a.nbs * a.ranges1 + 1, "soft grp: grid");
+    dry_range((int64_t)a.q_gstride, (int64_t)G * 256, (int64_t)G * 256 + 1, "soft grp: fragment stride");
+    dry_access(a.m, 0, 4 * (int64_t)a.n_vis, "soft grp: zeroing m");
+    if (a.clear && a.nclear > 0) dry_access(a.clear, 0, 4 * (int64_t)a.nclear, "soft grp: arrival trees");
+    dry_lds(0, (int64_t)kGrpWaves * U * 16 * 8, (int64_t)lds, "soft grp: combine buffer");
+    for (int b = 0; b < nwg; ++b) {
+      int g, rs, range, t_lo, t_hi;
+      grp_map1(b, HKV, a.nbs, a.ranges1, a.tiles, g, rs, range, t_lo, t_hi);
+      dry_range(g, 0, HKV, "soft grp: key head");
+      dry_range(rs, 0, a.nbs, "soft grp: row-block set");
+      dry_range(range, 0, a.ranges1, "soft grp: key range");
+      dry_range(t_hi, t_lo, (int64_t)a.tiles + 1, "soft grp: tiles");
+      for (int u = 0; u < U; ++u) {
+        // unit u: its fragments at slot head u (block u / G at u / G * q_gstride uint4)
+        frag(NBW * rs + u / G, g * G + u % G, u, 0);
+        const int q0 = 16 * (NBW * rs + u / G), qn = std::min(16, a.n_q - q0);
+        for (int q = q0; q < q0 + qn; ++q)
+          dry_access(a.stats_part, grp_part((int64_t)(g * G + u % G) * a.n_q + q, range, a.ranges1) * 8, 8,
+                     "soft grp: partial statistics");
+      }
+      const int npairs = (t_hi - t_lo + 1) >> 1;
+      for (int w = 0; w < kGrpWaves; ++w) {
+        // the wave's first pair (loaded ahead of the loop, whether or not it
+        // exists), then for each step of two pairs the pair after each
+        keys(t_lo + 2 * w, g, g);
+        keys(t_lo + 2 * w + 1, g, g);
+        for (int p = w; p < npairs; p += 2 * kGrpWaves)
+          for (int v = 0; v < 2; ++v) {
+            const int pn = p + v * kGrpWaves + kGrpWaves;
+            keys(t_lo + 2 * pn, g, g);
+            keys(t_lo + 2 * pn + 1, g, g);
+          }
+      }
+    }
+  } else {
+    dry_range(a.ranges % 8, 0, 1, "soft grp: key ranges not whole XCD groups");
+    dry_range((int64_t)nwg, (int64_t)a.nb * a.ranges, (int64_t)a.nb * a.ranges + 1, "soft grp: grid");
+    dry_range((int64_t)a.q_gstride, (int64_t)G * 256, (int64_t)G * 256 + 1, "soft grp: fragment stride");
+    const int64_t f0 = (int64_t)grp_frag0(HQ, PASS) * 16;  // the fragments' first byte
+    dry_lds(0, (int64_t)HQ * 16 * 4, (int64_t)lds, "soft grp: L");
+    for (int b = 0; b < nwg; ++b) {
+      int rb, range, t_lo, t_hi;
+      grp_map(b, a.nb, a.ranges, a.tiles, rb, range, t_lo, t_hi);
+      dry_range(rb, 0, a.nb, "soft grp: row block");
+      dry_range(range, 0, a.ranges, "soft grp: key range");
+      dry_range(t_hi, t_lo, (int64_t)a.tiles + 1, "soft grp: tiles");
+      for (int h = 0; h < HQ; ++h) frag(rb, h, h, f0);
+      const int q0 = 16 * rb, qn = std::min(16, a.n_q - q0);
+      for (int h = 0; h < HQ; ++h)
+        dry_access(a.stats, ((int64_t)h * a.n_q + q0) * 8, 8 * (int64_t)qn, "soft grp: statistics");
+      const int npairs = (t_hi - t_lo + 1) >> 1;
+      for (int w = 0; w < kGrpWaves; ++w) {
+        // the first pair loaded ahead of the loop, then each pair's successor
+        keys(t_lo + 2 * w, 0, HKV - 1);
+        keys(t_lo + 2 * w + 1, 0, HKV - 1);
+        for (int p = w; p < npairs; p += kGrpWaves) {
+          const int t0 = t_lo + 2 * p;
+          keys(t0 + kGrpPairStride, 0, HKV - 1);
+          keys(t0 + kGrpPairStride + 1, 0, HKV - 1);
+          for (int j = 0; j < 2; ++j)
+            if (j == 0 || t0 + 1 < t_hi) {
+              const int tok0 = 16 * (t0 + j), cnt = std::min(16, a.n_vis - tok0);
+              if (cnt > 0) dry_access(a.m, 4 * (int64_t)tok0, 4 * (int64_t)cnt, "soft grp: m");
+            }
+        }
+      }
     }
   }
 }
 
-// Address model of qer_soft_grp_kernel<HKV, G, PASS> (grid nwg, `lds` bytes of
-// LDS): the zeroing, every workgroup's query-fragment loads and LDS slots, the
-// statistics it reads or writes, the keys of every pair it loads (the extreme
-// key heads, steps and lanes of each tile: the index is affine in each), the
-// next pair's first key head loaded during the last, and its stores into m.
-template <int HKV, int G, int PASS>
-void model_grp(const SoftGrpArgs& a, int nwg, size_t lds) {
-  constexpr int HQ = HKV * G;
-  dry_range((int64_t)lds, 0, 160 * 1024 + 1, "soft grp: LDS beyond a CU's 160 KiB");
-  dry_range(a.ranges % 8, 0, 1, "soft grp: key ranges not whole XCD groups");
-  dry_range((int64_t)nwg, (int64_t)a.nb * a.ranges, (int64_t)a.nb * a.ranges + 1, "soft grp: grid");
-  dry_range((int64_t)a.nb, (a.n_q + 15) / 16, (a.n_q + 15) / 16 + 1, "soft grp: row blocks");
-  if (PASS == 1) {
-    dry_access(a.m, 0, 4 * (int64_t)a.n_vis, "soft grp: zeroing m");
-    if (a.clear && a.nclear > 0) dry_access(a.clear, 0, 4 * (int64_t)a.nclear, "soft grp: arrival trees");
-  }
-  const int64_t f0 = (int64_t)grp_frag0(HQ, PASS) * 16;  // the fragments' first byte
-  dry_lds(f0 + (int64_t)grp_q_slot(HQ - 1, 3, 63) * 16, 16, (int64_t)lds, "soft grp: query fragments");
-  if (PASS == 2) dry_lds(0, (int64_t)HQ * 16 * 4, (int64_t)lds, "soft grp: L");
-  if (PASS == 1) dry_lds(f0, (int64_t)kGrpWaves * HQ * 16 * 8, (int64_t)lds, "soft grp: combine buffer");
-  auto keys = [&](int t) {
-    for (int g : {0, HKV - 1})
-      for (int ks : {0, 3})
-        for (int l : {0, 63}) dry_access(a.K, grp_key_u4(t, g, ks, l, a.n_vis, HKV) * 16, 16, "soft grp: keys");
-  };
-  for (int b = 0; b < nwg; ++b) {
-    int rb, range, t_lo, t_hi;
-    grp_map(b, a.nb, a.ranges, a.tiles, rb, range, t_lo, t_hi);
-    dry_range(rb, 0, a.nb, "soft grp: row block");
-    dry_range(range, 0, a.ranges, "soft grp: key range");
-    dry_range(t_hi, t_lo, (int64_t)a.tiles + 1, "soft grp: tiles");
-    const int last = std::min(16 * rb + 15, a.n_q - 1) - 16 * rb;  // the block's last row (lane % 16)
-    for (int h = 0; h < HQ; ++h)
-      for (int ks = 0; ks < 4; ++ks)
-        for (int l : {0, 48 + last}) {
-          const int64_t src = grp_q_src(rb, h, ks, l, a.n_q, HQ);
-          dry_range(src, 0, INT64_MAX, "soft grp: a row block's last row past the query");
-          if (src >= 0) dry_access(a.Q, src * 16, 16, "soft grp: query fragment");
-          dry_lds(f0 + (int64_t)grp_q_slot(h, ks, l) * 16, 16, (int64_t)lds, "soft grp: query fragment slot");
-        }
-    const int q0 = 16 * rb, qn = std::min(16, a.n_q - q0);
-    for (int h = 0; h < HQ; ++h) {
-      if (PASS == 2) dry_access(a.stats, ((int64_t)h * a.n_q + q0) * 8, 8 * (int64_t)qn, "soft grp: statistics");
-      if (PASS == 1)
-        for (int q = q0; q < q0 + qn; ++q)
-          dry_access(a.stats_part, grp_part((int64_t)h * a.n_q + q, range, a.ranges) * 8, 8,
-                     "soft grp: partial statistics");
-    }
-    const int npairs = (t_hi - t_lo + 1) >> 1;
-    for (int w = 0; w < kGrpWaves; ++w) {
-      // the first key head of the wave's first pair (loaded even without one),
-      // then every pair's tiles and the next pair's first key head
-      keys(t_lo + 2 * w);
-      keys(t_lo + 2 * w + 1);
-      for (int p = w; p < npairs; p += kGrpWaves) {
-        const int t0 = t_lo + 2 * p;
-        const bool has1 = t0 + 1 < t_hi;
-        for (int j = 0; j < 2; ++j) {
-          keys(t0 + j);
-          keys(t0 + kGrpPairStride + j);
-          if (PASS == 2 && (j == 0 || has1)) {
-            const int tok0 = 16 * (t0 + j), cnt = std::min(16, a.n_vis - tok0);
-            if (cnt > 0) dry_access(a.m, 4 * (int64_t)tok0, 4 * (int64_t)cnt, "soft grp: m");
-          }
-        }
-      }
-    }
-  }
+template <int HKV, int G, int PASS, int NBW>
+int launch_grp_k(const SoftGrpArgs& a, int nwg, hipStream_t s) {
+  const size_t lds = grp_lds(HKV * G, G, NBW, PASS);
+  auto k = qer_soft_grp_kernel<HKV, G, PASS, NBW>;
+  if (dry_run()) model_grp<HKV, G, PASS, NBW>(a, nwg, lds);
+  const int rc = allow_lds(k, lds);
+  if (rc) return rc;
+  return launch(PASS == 1 ? "qer_soft_stats_grp" : "qer_soft_score_grp", k, dim3((unsigned)nwg), dim3(kGrpThreads),
+                lds, s, a);
 }
 
 template <int HKV, int G>
 int launch_grp_t(const SoftGrpArgs& a, int pass, hipStream_t s) {
-  constexpr int HQ = HKV * G;
-  const int nwg = a.nb * a.ranges;
-  const size_t lds = grp_lds(HQ, pass);
-  if (pass == 1) {
-    auto k = qer_soft_grp_kernel<HKV, G, 1>;
-    if (dry_run()) model_grp<HKV, G, 1>(a, nwg, lds);
-    const int rc = allow_lds(k, lds);
-    if (rc) return rc;
-    return launch("qer_soft_stats_grp", k, dim3((unsigned)nwg), dim3(kGrpThreads), lds, s, a);
+  if (pass == 2) return launch_grp_k<HKV, G, 2, 1>(a, a.nb * a.ranges, s);
+  const int nwg = HKV * a.nbs * a.ranges1;
+  switch (a.nbw) {
+    case 1: return launch_grp_k<HKV, G, 1, 1>(a, nwg, s);
+    case 2: return launch_grp_k<HKV, G, 1, 2>(a, nwg, s);
+    case 3: return launch_grp_k<HKV, G, 1, 3>(a, nwg, s);
+    case 4: return launch_grp_k<HKV, G, 1, 4>(a, nwg, s);
+    default: return set_error(COFIE_EINVAL, "grouped SOFTMAX: %d row blocks per workgroup", a.nbw);
   }
-  auto k = qer_soft_grp_kernel<HKV, G, 2>;
-  if (dry_run()) model_grp<HKV, G, 2>(a, nwg, lds);
-  const int rc = allow_lds(k, lds);
-  if (rc) return rc;
-  return launch("qer_soft_score_grp", k, dim3((unsigned)nwg), dim3(kGrpThreads), lds, s, a);
 }
 
 }  // namespace
@@ -387,8 +502,11 @@ bool grp_has_instance(int hkv, int g) {
   return (hkv == 4 && (g == 7 || g == 8 || g == 2)) || (hkv == 2 && (g == 4 || g == 8));
 }
 
+int grp_nbw(int g, int nb) { return std::max(1, std::min({nb, 4, 36 / g})); }
+
 int launch_grp(const SoftGrpArgs& a, int hkv, int g, int pass, hipStream_t s) {
-  if (a.nb < 1 || a.ranges < 8 || a.ranges % 8 != 0 || a.n_vis < 1 || a.n_q < 1 || a.q_gstride != g * 256)
+  if (a.nb < 1 || a.ranges < 8 || a.ranges % 8 != 0 || a.ranges1 < 8 || a.ranges1 % 8 != 0 || a.n_vis < 1 ||
+      a.n_q < 1 || a.q_gstride != g * 256 || a.nbw != grp_nbw(g, a.nb) || a.nbs != (a.nb + a.nbw - 1) / a.nbw)
     return set_error(COFIE_EINVAL, "grouped SOFTMAX plan: %d row blocks, %d key ranges", a.nb, a.ranges);
   if (hkv == 4 && g == 7) return launch_grp_t<4, 7>(a, pass, s);
   if (hkv == 4 && g == 8) return launch_grp_t<4, 8>(a, pass, s);
