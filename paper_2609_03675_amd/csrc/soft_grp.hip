@@ -50,7 +50,7 @@ constexpr int kGrpWaves = 8;
 constexpr int kGrpThreads = 64 * kGrpWaves;
 constexpr int kGrpPairStride = 2 * kGrpWaves;  // tiles between a wave's pairs
 
-// Workgroup b: its row block, key range and tiles [t_lo, t_hi).
+// Pass-2 workgroup b: its row block, key range and tiles [t_lo, t_hi).
 __host__ __device__ __forceinline__ void grp_map(int b, int nb, int ranges, int tiles, int& rb, int& range, int& t_lo,
                                                  int& t_hi) {
   const int s = b >> 3;
