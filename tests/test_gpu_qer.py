@@ -125,6 +125,30 @@ def test_softmax_grouped_heads(n_q, H_q, H_kv, tokens):
     assert np.array_equal(w, w2.cpu().numpy()), "SOFTMAX scores differ between two calls"
 
 
+@pytest.mark.parametrize("n_q,H_q,H_kv", [(48, 28, 4), (33, 8, 2), (20, 12, 4)])
+@pytest.mark.parametrize("rising", [True, False])
+def test_softmax_scores_of_very_different_scale(n_q, H_q, H_kv, rising):
+    """Key rows scaled by powers of two that grow (or shrink) along the
+    sequence, up to 2^6: a row's scores later in the keys exceed the running
+    maximum by far more than 2^64 allows (grouped-head kernel: the pair is
+    summed again against its own max and the earlier sum rescaled), or fall
+    far below it (their exponentials underflow).  The scaling is exact in
+    bf16, so the oracle sees the same inputs; the (48, 28, 4) and (33, 8, 2)
+    shapes take the grouped-head kernel, (20, 12, 4) the score kernel."""
+    tokens = [64] * 24 + [37]
+    offs = synth.frame_offsets(tokens)
+    n_vis = int(offs[-1])
+    Q, K = synth.random_qk(n_q * 41 + H_q, n_q, n_vis, H_q, H_kv, 128, "bf16")
+    e = np.floor(np.linspace(0, 6, n_vis)).astype(np.uint16)
+    e = (e if rising else e[::-1])[:, None, None]
+    # times 2^e on the bf16 bits: e added to the exponent field of every normal value
+    normal = (K & 0x7F80) != 0
+    K = np.where(normal, K + (e << 7), K).astype(np.uint16)
+    w, idx, ref = run_case(Q, K, offs, H_q, H_kv, 128, 5, mode=B.SOFTMAX)
+    err = rel_err(w, ref)
+    assert err <= 1e-3, err  # fp32 exponents of scores up to ~2^9 in size
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n_q,H_q,H_kv,d,tokens", [
     (1, 2, 2, 64, [1]),               # one query row, one token
