@@ -97,7 +97,9 @@ SOFT_GRP = [(48, 28, 4, [222] * 8 + [224]),   # the high-res heads
             (64, 32, 4, [100] * 7),            # four row blocks
             (16, 8, 4, [16] * 33),             # 33 whole tiles: one pair short of a full last pair
             (33, 8, 2, [3001]),                # G = 4
-            (5, 16, 2, [64] * 60)]             # G = 8, many tiles per range
+            (5, 16, 2, [64] * 60),             # G = 8, many tiles per range
+            (100, 28, 4, [160] * 9 + [77]),    # 7 row blocks: two sets of four, the last set one block short
+            (70, 8, 4, [300, 1, 299])]         # G = 2: 5 row blocks in two sets
 
 
 @pytest.mark.parametrize("n_q,H_q,H_kv,tokens", SOFT_GRP)

@@ -108,6 +108,8 @@ def test_softmax_through_score_kernel(dtype, n_q, H_q, H_kv, d, n_tok):
     (33, 8, 2, [3001]),                # G = 4
     (5, 16, 2, [64] * 60),             # G = 8
     (48, 28, 4, [196] * 60),           # several pairs per wave
+    (100, 28, 4, [160] * 9 + [77]),    # 7 row blocks: pass 1 in two sets of four, the last one block short
+    (70, 8, 4, [300, 1, 299]),         # G = 2: 5 row blocks in two sets
 ])
 def test_softmax_grouped_heads(n_q, H_q, H_kv, tokens):
     """SOFTMAX with bf16 grouped heads of d = 128 through the grouped-head
