@@ -16,9 +16,10 @@
 //    takes one key head, up to four 16-row blocks and a range of key tiles:
 //    each key byte is read once per launch and each key fragment feeds the
 //    G x blocks products of its query heads.  A lane keeps per (head, block)
-//    its running (max, sum of exp2) over its own keys; the max is raised only
-//    when a pair's sum leaves [0, 2^64) (the pair is then summed again against
-//    its own max), and lanes and waves are combined once, at the end (the key
+//    its sum of exp2 over its own keys against a reference (0 at first); the
+//    reference moves only when a pair's sum leaves (2^-64, 2^64) (the pair is
+//    then summed again against its own max, or the reference if that is
+//    larger), and lanes and waves are combined once, at the end (the key
 //    ranges by the merge kernel);
 //  * pass 2 (the head mean of the probabilities) needs every head of a row,
 //    so a workgroup takes one 16-row block with all H_q heads and a range of
@@ -102,9 +103,10 @@ __device__ __forceinline__ float dpp_max16(float v) {  // max over the 16 lanes 
   v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xF, 0xF, false)));
   return fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xF, 0xF, false)));
 }
-// (m1, z1) and (m2, z2), sums of exp2(x - m): both against max(m1, m2)
+// (m1, z1) and (m2, z2), sums of exp2(x - m): both against max(m1, m2), or
+// the one reference with a sum (an empty side's reference is no max)
 __device__ __forceinline__ void grp_combine(float& m1, float& z1, float m2, float z2) {
-  const float m = fmaxf(m1, m2);
+  const float m = z1 > 0.f ? (z2 > 0.f ? fmaxf(m1, m2) : m1) : m2;
   z1 = (z1 > 0.f ? z1 * __builtin_amdgcn_exp2f(m1 - m) : 0.f) + (z2 > 0.f ? z2 * __builtin_amdgcn_exp2f(m2 - m) : 0.f);
   m1 = m;
 }
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a
     float mh[U], zh[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      mh[u] = -INFINITY;
+      mh[u] = 0.f;  // a reference, not yet a max: most scores' exp2 against 0 is in range
       zh[u] = 0.f;
     }
     uint4 kb[2][2][4];  // this pair's keys, the next pair's
@@ -222,22 +224,26 @@ __global__ __launch_bounds__(kGrpThreads) void qer_soft_grp_kernel(SoftGrpArgs a
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                   if (!((valid >> (4 * j + e)) & 1u)) s[j][e] = -INFINITY;
-            float zt = 0.f;
+            float ex[8];
 #pragma unroll
             for (int j = 0; j < 2; ++j)
 #pragma unroll
-              for (int e = 0; e < 4; ++e) zt += __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mh[u]));
-            if (zt < 0x1p64f) {
+              for (int e = 0; e < 4; ++e) ex[4 * j + e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], c2, -mh[u]));
+            const float zt = ((ex[0] + ex[1]) + (ex[2] + ex[3])) + ((ex[4] + ex[5]) + (ex[6] + ex[7]));
+            if (zt < 0x1p64f && zt > 0x1p-64f) {
               zh[u] += zt;
             } else {
-              // the running max is too low (or not set yet): sum the pair
-              // against its own max and rescale what came before
-              float mx = mh[u];
+              // the reference is too low, or far too high for this pair (or
+              // the pair has no key): sum the pair against the larger of its
+              // own max and the reference (its own max while nothing is
+              // summed), rescaling what came before
+              float pm = -INFINITY;
 #pragma unroll
               for (int j = 0; j < 2; ++j)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[j][e] * c2);
-              if (mx > -INFINITY) {
+                for (int e = 0; e < 4; ++e) pm = fmaxf(pm, s[j][e]);
+              const float mx = zh[u] > 0.f ? fmaxf(mh[u], pm * c2) : pm * c2;
+              if (pm > -INFINITY) {
                 float z = 0.f;
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
