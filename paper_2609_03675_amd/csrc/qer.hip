@@ -407,7 +407,8 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
       for (int i = tid; i < a.H * a.n_q; i += kLdsThreads) {
         const int hh = i / a.n_q, q = i - hh * a.n_q;
         const float2 st = a.stats[(int64_t)hh * a.nq_total + a.q0 + q];
-        st_sh[i] = make_float2(st.x, 1.0f / st.y);
+        // L = M log2 e + log2 Z: p = exp2(s scale log2 e - L)
+        st_sh[i] = make_float2(st.x * 1.44269504088896341f + __log2f(st.y), 0.f);
       }
   }
 
@@ -508,27 +509,41 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
     }
     auto head_close = [&](int hh) __attribute__((always_inline)) {
       if constexpr (BASE == kModeSoftStats) {
-        // (max, sum of exp(s - max)) over this wave's valid tokens, per query
-        // row; a wave without tokens writes (-inf, 0)
+        // (m, sum of exp(s - m)) over this wave's valid tokens, per query row,
+        // m = 0 or, where the sum against 0 is out of range, the max; a wave
+        // without tokens writes (-inf, 0)
         const int64_t slot = ((int64_t)blockIdx.x * kLdsWaves + wave) * a.rounds + (rb - t_begin) / (TW * MB);
         const int64_t row0 = (int64_t)hh * a.nq_total + a.q0;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          float mx = -INFINITY;
-#pragma unroll
-          for (int j = 0; j < MB; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if ((vmask[nb] >> (4 * j + r)) & 1u) mx = fmaxf(mx, acc[j][nb][r]);
-          mx = max_x32(max_x16(mx));
-          const float mc = mx * c2;
+          // the sum against 0 first (no max); the row's four lane groups hold
+          // the same sum, so the exact form below runs for whole rows only,
+          // where that sum leaves (2^-64, 2^64) or the row has no valid token
           float z = 0.f;
 #pragma unroll
           for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if ((vmask[nb] >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
+              if ((vmask[nb] >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(acc[j][nb][r] * c2);
           z = sum_x32(sum_x16(z));
+          float mx = 0.f;
+          if (!(z < 0x1p64f && z > 0x1p-64f)) {
+            mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < MB; ++j)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if ((vmask[nb] >> (4 * j + r)) & 1u) mx = fmaxf(mx, acc[j][nb][r]);
+            mx = max_x32(max_x16(mx));
+            const float mc = mx * c2;
+            z = 0.f;
+#pragma unroll
+            for (int j = 0; j < MB; ++j)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if ((vmask[nb] >> (4 * j + r)) & 1u) z += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -mc));
+            z = sum_x32(sum_x16(z));
+          }
           const int q = nb * 16 + r16;
           if (g4 == 0 && q < a.n_q) {
             const int64_t row = row0 + q;  // 16 lanes: one or two 128-byte runs
@@ -544,7 +559,7 @@ __global__ __launch_bounds__(kLdsThreads) void qer_score_kernel(ScoreLdsArgs a) 
 #pragma unroll
           for (int j = 0; j < MB; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) prob[j][nb][r] += __expf(acc[j][nb][r] * a.soft_scale - st.x) * st.y;
+            for (int r = 0; r < 4; ++r) prob[j][nb][r] += __builtin_amdgcn_exp2f(fmaf(acc[j][nb][r], c2, -st.x));
         }
       }
 #pragma unroll
