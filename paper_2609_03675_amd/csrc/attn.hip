@@ -271,13 +271,16 @@ __device__ __forceinline__ uint4 q_frag(const AttnArgs& a, int pos, int h, int s
 // skip the rescale.
 constexpr float kLazy = 8.f;
 
+// Max over lanes l, l ^ 16, l ^ 32 and l ^ 48: each swap hands every lane
+// its own value and its partner's (one of the two pair elements is the
+// lane's own).  The pair elements are read as values (__uint_as_float), not
+// through __builtin_bit_cast of the vector subscript, which this compiler
+// turns into two reads of element 0, i.e. no exchange at all.
 __device__ __forceinline__ float max_xor16_32(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
-                                                  false, false);
-  x = fmaxf(__builtin_bit_cast(float, a[0]), __builtin_bit_cast(float, a[1]));
-  const auto b = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
-                                                  false, false);
-  return fmaxf(__builtin_bit_cast(float, b[0]), __builtin_bit_cast(float, b[1]));
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(x, fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1])));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(x, fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1])));
 }
 
 // S^T of one 32-token step (key tiles 2 half, 2 half + 1 of the stage)
@@ -306,7 +309,12 @@ __device__ __forceinline__ void qk_half(const char* st, const FragBase& f, int h
   }
 }
 
-// softmax of one 32-token step -> P (B operand of O^T), lazy max
+// softmax of one 32-token step -> P (B operand of O^T), lazy max.  A row's
+// four lanes agree on its running max m, so the max over the step's 32 keys
+// is exchanged across them only when some row of the wave grows: a row's max
+// exceeds m + kLazy exactly when one of its lanes' own maxima does (the
+// product with c2 > 0 is monotone).  The row sums add the probabilities as
+// the value product sees them, rounded to bf16, two per dot product with 1.
 __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT], float (&lsum)[kNT], f32x4 (&o)[8][kNT],
                                              uint4 (&p)[kNT], const int (&row)[kNT], int k0, bool masked, float c2) {
   const int l = threadIdx.x & 63;
@@ -319,7 +327,8 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
         for (int e = 0; e < 4; ++e)
           if (k0 + 16 * j + 4 * (l >> 4) + e > row[rt]) s[j][rt][e] = -INFINITY;
   }
-  float mx[kNT];
+  float mx[kNT];  // this lane's max of the raw scores
+  bool grow = false;
 #pragma unroll
   for (int rt = 0; rt < kNT; ++rt) {
     float v = -INFINITY;
@@ -327,23 +336,23 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) v = fmaxf(v, s[j][rt][e]);
-    mx[rt] = max_xor16_32(v) * c2;
+    mx[rt] = v;
+    grow |= v * c2 > m[rt] + kLazy;
   }
-  bool grow = false;
-#pragma unroll
-  for (int rt = 0; rt < kNT; ++rt) grow |= mx[rt] > m[rt] + kLazy;
   if (__builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
     for (int rt = 0; rt < kNT; ++rt) {
-      if (mx[rt] > m[rt] + kLazy) {
-        const float alpha = __builtin_amdgcn_exp2f(m[rt] - mx[rt]);  // m = -inf: 0
-        m[rt] = mx[rt];
+      const float r = max_xor16_32(mx[rt]) * c2;
+      if (r > m[rt] + kLazy) {
+        const float alpha = __builtin_amdgcn_exp2f(m[rt] - r);  // m = -inf: 0
+        m[rt] = r;
         lsum[rt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) o[dt][rt] *= alpha;
       }
     }
   }
+  constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1, 1)
 #pragma unroll
   for (int rt = 0; rt < kNT; ++rt) {
     float pv[2][4];
@@ -351,12 +360,16 @@ __device__ __forceinline__ void softmax_half(f32x4 (&s)[2][kNT], float (&m)[kNT]
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pv[j][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][rt][e], c2, nm));
-        lsum[rt] += pv[j][e];
-      }
-    p[rt] = make_uint4(pack2(pv[0][0], pv[0][1]), pack2(pv[0][2], pv[0][3]), pack2(pv[1][0], pv[1][1]),
-                       pack2(pv[1][2], pv[1][3]));
+      for (int e = 0; e < 4; ++e) pv[j][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][rt][e], c2, nm));
+    const uint32_t u0 = pack2(pv[0][0], pv[0][1]), u1 = pack2(pv[0][2], pv[0][3]);
+    const uint32_t u2 = pack2(pv[1][0], pv[1][1]), u3 = pack2(pv[1][2], pv[1][3]);
+    float ls = lsum[rt];
+    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u0), __builtin_bit_cast(bf16x2, kOnes), ls, false);
+    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u1), __builtin_bit_cast(bf16x2, kOnes), ls, false);
+    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u2), __builtin_bit_cast(bf16x2, kOnes), ls, false);
+    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u3), __builtin_bit_cast(bf16x2, kOnes), ls, false);
+    lsum[rt] = ls;
+    p[rt] = make_uint4(u0, u1, u2, u3);
   }
 }
 

@@ -5,9 +5,11 @@ QER over the text rows (all non-visual tokens) and the visual rows, the
 top-k exact.
 
 Attention tolerance, from the arithmetic: the probabilities enter the value
-product rounded to bf16 (relative 2^-9 each) while the row sum keeps them in
-fp32, and the output is rounded to bf16 (2^-9 relative); together at most
-3 * 2^-9 of the largest |v| the row attends to, plus the output rounding, so
+product rounded to bf16 (relative 2^-9 each; the visual rows' row sums add
+the same rounded values, the text rows' chunk sums keep them in fp32), so
+the normalised weights are off by at most about 2 * 2^-9 relative, and the
+output is rounded to bf16 (2^-9 relative); together at most 3 * 2^-9 of the
+largest |v| the row attends to, plus the output rounding, so
 |o - o_ref| <= 2^-7 max|v| + 2^-8 |o_ref| per element.  Frame scores within
 2e-2 relative as for cofie_qer_rank (bf16 inputs, fp32 accumulation)."""
 import numpy as np
@@ -103,6 +105,27 @@ def test_peaked_logits_and_explicit_scale():
     # large logits: the running max moves often and the weights are peaked
     Q, K, V, offs = make_case(2, 4, 700, 12, 2, 2, 6, scale=3.0)
     check(Q, K, V, offs, 4, 704, 3, scale=0.2)
+
+
+def test_outlier_keys_beyond_the_first_lane_group():
+    """Keys whose logit exceeds the rest of their 32-key step by about 231
+    in base 2 (exp2 of that overflows fp32): a visual row's running max must
+    see every key of the step; a max over the first lane group's keys only
+    (offsets 0-3 and 16-19 of the step) would leave exp2 to overflow.  The
+    outliers sit at offsets 5, 10, 29, 23, 26 and 21 of their steps, i.e. in
+    lane groups 1, 2, 3, 1, 2 and 1; positive queries and constant outlier
+    keys make every row prefer them."""
+    n_pre, n_vis, n_post, H = 6, 700, 10, 2
+    Q, K, V, offs = make_case(6, n_pre, n_vis, n_post, H, H, 7)
+    rng = np.random.default_rng([2609, 3675, 97])
+    q = np.abs(rng.standard_normal(Q.shape)).astype(np.float32) * 0.5 + 0.5
+    Q = synth.bf16_bits(q)
+    Kf = dec(K).copy()
+    outl = [37, 106, 189, 247, 410, 629]          # offsets 5, 10, 29, 23, 26, 21
+    Kf[outl] = 16.0
+    K = synth.bf16_bits(Kf)
+    rows = np.arange(n_pre + n_vis + n_post, dtype=np.int32)
+    check(Q, K, V, offs, n_pre, n_pre + n_vis, 3, rows=rows)
 
 
 def test_workload_sampled_rows():
