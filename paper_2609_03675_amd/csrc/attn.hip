@@ -7,7 +7,7 @@
 //
 //  * visual-row workgroups: causal flash attention of 384 visual query rows
 //    (48 per wave, two waves per SIMD in a ping-pong) for one head.  Keys and
-//    values stream through LDS in stages of 64 tokens (three buffers); each
+//    values stream through LDS in stages of 64 tokens (four buffers); each
 //    wave
 //    forms S^T = K Q^T with bf16 MFMA 16x16x32 (the queries sit in registers
 //    as the B operand), keeps the running row max and sum in the base-2
@@ -93,6 +93,7 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 // immediate.
 constexpr int kKBytes = kBN * kD * 2;              // 16 KiB
 constexpr int kStageBytes = kKBytes + kD * kBN * 2;  // + 16 KiB
+constexpr int kBufs = 4;                            // stage buffers of a visual-row workgroup
 
 __host__ __device__ constexpr int vpos32(int kk) { return 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3); }
 
@@ -135,8 +136,35 @@ __device__ __forceinline__ void stage_dma(const AttnArgs& a, int g, int k0, char
   }
 }
 
+// The same DMA issued through asm, for the visual rows: the compiler does not
+// see these loads, so it adds no wait for them (vmcnt(0)) before LDS reads it
+// cannot prove disjoint from their destination.  The visual loop orders them
+// itself: each wave waits for its share of a stage before the barrier that
+// publishes it, and for all of them before it ends.  M0 holds the LDS
+// destination (one wait state between its write and the load).
+__device__ __forceinline__ void dma16(const void* src, char* dst) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_void*)dst);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "memory", "m0");
+}
+
+__device__ __forceinline__ void stage_dma_async(const AttnArgs& a, int g, int k0, char* st) {
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < kDma; ++j) {
+    const int i = wave + kWaves * j;  // instruction 0..31
+    if (i < 16)
+      dma16(a.K + dma_src(i, l, k0, g, a.L, a.Lp, a.H_kv), st + 1024 * i);
+    else
+      dma16(a.Vt + dma_src(i, l, k0, g, a.L, a.Lp, a.H_kv), st + kKBytes + 1024 * (i - 16));
+  }
+}
+
 // this wave's DMA has landed in LDS (vmcnt(0); expcnt and lgkmcnt untouched)
 __device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// all of this wave's DMA but its last stage (kDma loads) has landed: vector
+// memory loads count down in issue order
+static_assert(kDma < 16, "vmcnt field");
+__device__ __forceinline__ void dma_wait_but_last() { __builtin_amdgcn_s_waitcnt(0x0F70 | kDma); }
 
 // lane bases of the fragment reads: ka[s] for contraction step s (key tile
 // kt adds kt * 4 KiB), va[sub] for token step sub (d tile dt adds dt * 2 KiB)
@@ -169,6 +197,15 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
+
+// Barrier of the visual-row loop.  Its stage buffers are written only by DMA,
+// and each wave waits for its own share of a stage (dma_wait_but_last) before
+// the barrier that publishes it, so the barrier itself waits only for this
+// wave's LDS reads (a buffer is refilled only after the barrier that follows
+// its last read).  The fences of lds_barrier would add a wait for every DMA
+// still in flight (vmcnt(0)) and expose the DMA latency at each barrier; the
+// asm's memory clobber keeps the compiler from moving LDS reads across it.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 __device__ __forceinline__ float wave_max4(float x) {
   x = fmaxf(x, __shfl_xor(x, 16));
@@ -263,9 +300,10 @@ __device__ __forceinline__ uint4 q_frag(const AttnArgs& a, int pos, int h, int s
 // barrier interval behind waves 0-3, and each wave alternates an interval of
 // matrix work (the value product of one 32-token step and the key product of
 // the next) with an interval of softmax, so in every interval one wave of a
-// SIMD feeds the matrix core while the other uses the VALU.  Three stage
+// SIMD feeds the matrix core while the other uses the VALU.  Four stage
 // buffers: the lagging waves still multiply the values of stage st - 1 while
-// the leading ones start stage st + 1's keys.  The running max is raised
+// the leading ones start stage st + 1's keys, and stages st + 2 and st + 3
+// are in flight (a DMA has two stages to land).  The running max is raised
 // lazily: the accumulators are rescaled only when a row's max grows by more
 // than kLazy (base 2), so probabilities stay below 2^kLazy and most steps
 // skip the rescale.
@@ -437,54 +475,60 @@ __device__ void visual_block(const AttnArgs& a, int b, char* lds) {
   }
   const FragBase fb = frag_base();
 
-  stage_dma(a, g, 0, lds);
-  stage_dma(a, g, kBN, lds + kStageBytes);
+  // the query fragments have arrived: the compiler then tracks no load of
+  // its own into the loop, where its counted waits would also wait for the
+  // stage DMA in flight
   dma_wait();
-  lds_barrier();
-  if (lag) lds_barrier();
+  stage_dma_async(a, g, 0, lds);
+  stage_dma_async(a, g, kBN, lds + kStageBytes);
+  stage_dma_async(a, g, 2 * kBN, lds + 2 * kStageBytes);
+  dma_wait_but_last();  // stages 0 and 1
+  stage_barrier();
+  if (lag) stage_barrier();
 
   f32x4 s[2][kNT];
   uint4 p[kNT];
   for (int st = 0; st <= nst; ++st) {
-    const char* cur = lds + (st % 3) * kStageBytes;
-    const char* prev = lds + ((st + 2) % 3) * kStageBytes;
+    const char* cur = lds + (st % kBufs) * kStageBytes;
+    const char* prev = lds + ((st + kBufs - 1) % kBufs) * kStageBytes;
     const int k0 = st * kBN;
     const bool on = st < nsw, was = st > 0 && st - 1 < nsw;
     const bool masked = k0 + kBN - 1 > rw;
-    // Stage st + 2 goes into the buffer of stage st - 1 in the interval after
+    // Stage st + 3 goes into the buffer of stage st - 1 in the interval after
     // that buffer's last read (a lagging wave's interval 0): the leading waves
     // in their interval 2, the lagging ones in their interval 1 -- the same
     // interval of the workgroup.  Each wave first waits for its share of stage
-    // st + 1, which the following barrier then publishes.
-    char* next = lds + ((st + 2) % 3) * kStageBytes;
+    // st + 1 (stage st + 2's may still be in flight), which the following
+    // barrier then publishes.
+    char* next = lds + ((st + kBufs - 1) % kBufs) * kStageBytes;
     // interval 0: values of the previous stage's second step, keys of this
     // stage's first step
     if (was) pv_half(prev, fb, 1, o, p);
     if (on) qk_half(cur, fb, 0, s, q);
-    lds_barrier();
+    stage_barrier();
     if (st == nst) break;
     // interval 1: softmax of the first step
     if (lag) {
-      dma_wait();
-      stage_dma(a, g, k0 + 2 * kBN, next);
+      dma_wait_but_last();
+      stage_dma_async(a, g, k0 + 3 * kBN, next);
     }
     if (on) softmax_half(s, m, lsum, o, p, row, k0, masked, a.c2);
-    lds_barrier();
+    stage_barrier();
     // interval 2: values of the first step, keys of the second
     if (!lag) {
-      dma_wait();
-      stage_dma(a, g, k0 + 2 * kBN, next);
+      dma_wait_but_last();
+      stage_dma_async(a, g, k0 + 3 * kBN, next);
     }
     if (on) {
       pv_half(cur, fb, 0, o, p);
       qk_half(cur, fb, 1, s, q);
     }
-    lds_barrier();
+    stage_barrier();
     // interval 3: softmax of the second step
     if (on) softmax_half(s, m, lsum, o, p, row, k0 + 32, masked, a.c2);
-    lds_barrier();
+    stage_barrier();
   }
-  if (!lag) lds_barrier();
+  if (!lag) stage_barrier();
   dma_wait();  // no DMA may land in LDS after the workgroup is gone
   if (nsw == 0) return;
 #pragma unroll
@@ -736,7 +780,7 @@ int validate_attn(const void* Q, const void* K, const void* V, const int32_t* of
   return COFIE_OK;
 }
 
-constexpr size_t kLdsBytes = 3 * kStageBytes;  // 96 KiB (the text rows use 2 stages + 8 KiB)
+constexpr size_t kLdsBytes = kBufs * kStageBytes;  // 128 KiB (the text rows use 2 stages + 8 KiB)
 static_assert(2 * kStageBytes + kWaves * kChunk * sizeof(float) <= kLdsBytes, "text rows' LDS");
 
 // Address model of the fused call (dry run): the transpose pre-pass, every
@@ -813,9 +857,8 @@ void model_attn(const AttnArgs& a, const uint16_t* V, int H_q) {
     const int r0 = a.vb + kBM * qb;
     const int last = (r0 + kBM < a.ve ? r0 + kBM : a.ve) - 1;
     const int nst = last / kBN + 1;
-    dma(g, 0, 0);
-    dma(g, kBN, kStageBytes);
-    for (int st = 0; st < nst; ++st) dma(g, (st + 2) * kBN, ((st + 2) % 3) * (int64_t)kStageBytes);
+    for (int st = 0; st < kBufs - 1; ++st) dma(g, st * kBN, st * (int64_t)kStageBytes);
+    for (int st = 0; st < nst; ++st) dma(g, (st + 3) * kBN, ((st + 3) % kBufs) * (int64_t)kStageBytes);
     const int pos_lo = r0 < a.L - 1 ? r0 : a.L - 1;
     const int pos_hi = r0 + kBM - 1 < a.L - 1 ? r0 + kBM - 1 : a.L - 1;
     dry_access(a.Q, 2 * (((int64_t)pos_lo * a.H_q + h) * kD), 16, "attn: visual query load");
