@@ -712,19 +712,50 @@ __global__ __launch_bounds__(kThreads) void attn_vt_kernel(const uint16_t* V, in
 
 // Text rows: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c over the chunks.
 __global__ __launch_bounds__(kD) void attn_merge_kernel(AttnArgs a) {
+  // One workgroup per text row and head, a thread per d.  The chunks' maxima
+  // are read in parallel (a thread per chunk), then the chunks are taken in
+  // blocks of kD: their weights exp2(m_c - M) go through LDS and every thread
+  // accumulates its d over the block with independent loads (a chunk no key
+  // of which the row sees has m_c = -inf, weight 0 and a zero partial).
+  __shared__ float red[kD / 64];
+  __shared__ float wsh[kD];
   const int tr = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
   const int pos = tr < a.vb ? tr : a.ve + (tr - a.vb);
+  const int64_t base = (int64_t)h * a.ntp + tr, cstride = (int64_t)a.H_q * a.ntp;
   float M = -INFINITY;
-  for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[((int64_t)c * a.H_q + h) * a.ntp + tr].x);
-  float lsum = 0.f, acc = 0.f;
-  for (int c = 0; c < a.n_chunks; ++c) {
-    const int64_t pr = ((int64_t)c * a.H_q + h) * a.ntp + tr;
-    const float2 ml = a.part_ml[pr];
-    if (ml.x == -INFINITY) continue;
-    const float wgt = exp2f(ml.x - M);
-    lsum += wgt * ml.y;
-    acc += wgt * a.part_o[pr * kD + d];
+  for (int c = d; c < a.n_chunks; c += kD) M = fmaxf(M, a.part_ml[c * cstride + base].x);
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if ((d & 63) == 0) red[d >> 6] = M;
+  __syncthreads();
+  M = red[0];
+#pragma unroll
+  for (int w = 1; w < kD / 64; ++w) M = fmaxf(M, red[w]);
+  float lpart = 0.f, acc = 0.f;
+  for (int c0 = 0; c0 < a.n_chunks; c0 += kD) {
+    const int c = c0 + d;
+    float wgt = 0.f;
+    if (c < a.n_chunks) {
+      const float2 ml = a.part_ml[c * cstride + base];
+      if (ml.x != -INFINITY) {
+        wgt = exp2f(ml.x - M);
+        lpart += wgt * ml.y;
+      }
+    }
+    __syncthreads();  // the previous block's weights have been read
+    wsh[d] = wgt;
+    __syncthreads();
+    const int n = a.n_chunks - c0 < kD ? a.n_chunks - c0 : kD;
+    const float* po = a.part_o + (c0 * cstride + base) * kD + d;
+#pragma unroll 8
+    for (int j = 0; j < n; ++j) acc = fmaf(wsh[j], po[j * cstride * kD], acc);
   }
+  for (int o = 32; o > 0; o >>= 1) lpart += __shfl_xor(lpart, o);
+  __syncthreads();
+  if ((d & 63) == 0) red[d >> 6] = lpart;
+  __syncthreads();
+  float lsum = 0.f;
+#pragma unroll
+  for (int w = 0; w < kD / 64; ++w) lsum += red[w];
   const __bf16 v = (__bf16)(acc / lsum);
   a.O[((int64_t)pos * a.H_q + h) * kD + d] = __builtin_bit_cast(uint16_t, v);
 }
