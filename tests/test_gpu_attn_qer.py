@@ -107,16 +107,17 @@ def test_peaked_logits_and_explicit_scale():
     check(Q, K, V, offs, 4, 704, 3, scale=0.2)
 
 
-def test_outlier_keys_beyond_the_first_lane_group():
+@pytest.mark.parametrize("H_q,H_kv", [(2, 2), (4, 2)])
+def test_outlier_keys_beyond_the_first_lane_group(H_q, H_kv):
     """Keys whose logit exceeds the rest of their 32-key step by about 231
     in base 2 (exp2 of that overflows fp32): a visual row's running max must
     see every key of the step; a max over the first lane group's keys only
     (offsets 0-3 and 16-19 of the step) would leave exp2 to overflow.  The
     outliers sit at offsets 5, 10, 29, 23, 26 and 21 of their steps, i.e. in
     lane groups 1, 2, 3, 1, 2 and 1; positive queries and constant outlier
-    keys make every row prefer them."""
-    n_pre, n_vis, n_post, H = 6, 700, 10, 2
-    Q, K, V, offs = make_case(6, n_pre, n_vis, n_post, H, H, 7)
+    keys make every row prefer them.  MHA and two query heads per key head."""
+    n_pre, n_vis, n_post = 6, 700, 10
+    Q, K, V, offs = make_case(6, n_pre, n_vis, n_post, H_q, H_kv, 7)
     rng = np.random.default_rng([2609, 3675, 97])
     q = np.abs(rng.standard_normal(Q.shape)).astype(np.float32) * 0.5 + 0.5
     Q = synth.bf16_bits(q)
