@@ -141,10 +141,11 @@ __device__ __forceinline__ void stage_dma(const AttnArgs& a, int g, int k0, char
 // cannot prove disjoint from their destination.  The visual loop orders them
 // itself: each wave waits for its share of a stage before the barrier that
 // publishes it, and for all of them before it ends.  M0 holds the LDS
-// destination (one wait state between its write and the load).
+// destination, bound through the operand constraint so that the compiler
+// writes it and knows it (one wait state between that write and the load).
 __device__ __forceinline__ void dma16(const void* src, char* dst) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_void*)dst);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "memory", "m0");
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
 }
 
 __device__ __forceinline__ void stage_dma_async(const AttnArgs& a, int g, int k0, char* st) {
